@@ -1,0 +1,251 @@
+"""Pins for the oracle's optimizer steps.
+
+* AdamW with FP32 states against torch.optim.AdamW (an independent
+  implementation; the paper aligns its reference path to PyTorch AdamW).
+* Adafactor with FP32 states against Hugging Face's Adafactor (same options
+  the paper's reference path uses), plus the rank-1 closed form.
+* CAME: the official implementation is not available here, so the CAME oracle
+  is pinned by closed forms (beta1 = 0; a uniform gradient; a rank-1
+  gradient) and by its second-moment path against the (HF-pinned) Adafactor
+  oracle at t = 1.
+* Dormant entries (exact zeros) keep code 0 and a pure weight-decay
+  trajectory, as the exact-zero invariant (section 4.2) implies.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import AL8, AL16, FP32, UF8, State
+from paper_2608_22322_amd import synth
+
+
+def _grads(rows, cols, steps, seed, sigma=1e-3, zero_frac=0.0):
+    out = []
+    for t in range(1, steps + 1):
+        g = synth.normal_f32(synth.grad_key(seed, t), rows * cols, sigma,
+                             synth.mask_key(seed), zero_frac)
+        out.append(g)
+    return out
+
+
+def _param(n, seed, sigma=0.02):
+    return synth.normal_f32(synth.param_key(seed), n, sigma)
+
+
+# ----------------------------------------------------------------------- AdamW
+@pytest.mark.parametrize("shape", [(64, 96), (1, 1000)])
+def test_adamw_fp32_matches_torch(shape):
+    rows, cols = shape
+    n = rows * cols
+    steps = 100
+    p0 = _param(n, 1)
+    grads = _grads(rows, cols, steps, 2, zero_frac=0.05)
+    cfg = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.01)
+
+    p = p0.copy()
+    m, v = State(FP32, n), State(FP32, n)
+    for t, g in enumerate(grads, 1):
+        oracle.adamw_step(p, g, m, v, t, **cfg)
+
+    tp = torch.nn.Parameter(torch.from_numpy(p0.copy()))
+    opt = torch.optim.AdamW([tp], lr=cfg["lr"], betas=(cfg["beta1"], cfg["beta2"]), eps=cfg["eps"],
+                            weight_decay=cfg["wd"], foreach=False)
+    for g in grads:
+        tp.grad = torch.from_numpy(g.copy())
+        opt.step()
+    ref = tp.detach().numpy()
+    assert np.abs(p - ref).max() <= 1e-5 * 0.2  # the paper's alignment tolerance is 1e-5
+    assert np.linalg.norm(p - ref) / np.linalg.norm(ref) < 2e-6
+    st = opt.state[tp]
+    np.testing.assert_allclose(m.codes, st["exp_avg"].numpy(), rtol=1e-4, atol=1e-10)
+    np.testing.assert_allclose(v.codes, st["exp_avg_sq"].numpy(), rtol=1e-4, atol=1e-16)
+
+
+def test_adamw_dormant_entries():
+    """Exact-zero gradients from a zero state: codes stay 0 and p follows (1 - lr wd)^t."""
+    rows, cols = 16, 256
+    n = rows * cols
+    p0 = _param(n, 3)
+    mk = synth.mask_key(4)
+    mask = synth.normal_f32(synth.grad_key(4, 1), n, 1e-3, mk, 0.05) == 0
+    p = p0.copy()
+    m = State(UF8, n, 256)
+    v = State(AL8, n, 256, float(np.float32(2 * math.log2(1e-8))))
+    lr, wd = 1e-3, 0.01
+    for t in range(1, 8):
+        g = synth.normal_f32(synth.grad_key(4, t), n, 1e-3)
+        if t <= 5:
+            g[mask] = 0.0
+        oracle.adamw_step(p, g, m, v, t, lr=lr, wd=wd)
+        if t <= 5:
+            assert np.all(m.codes[mask] == 0) and np.all(v.codes[mask] == 0)
+            want = p0[mask].astype(np.float64) * (1 - lr * wd) ** t
+            np.testing.assert_allclose(p[mask], want, rtol=4e-7 * t, atol=0)
+            assert np.all(v.codes[~mask] > 0)
+        else:
+            assert np.all(v.codes > 0)
+
+
+def test_adamw_quantized_close_to_fp32():
+    """AL8 second moment + UF8 momentum stays close to the FP32 trajectory (qualitative)."""
+    n = 256 * 64
+    p0 = _param(n, 5)
+    grads = _grads(64, 256, 50, 6)
+    pf, pq = p0.copy(), p0.copy()
+    mf, vf = State(FP32, n), State(FP32, n)
+    mq, vq = State(UF8, n, 256), State(AL8, n, 256, float(np.float32(2 * math.log2(1e-8))))
+    for t, g in enumerate(grads, 1):
+        oracle.adamw_step(pf, g, mf, vf, t)
+        oracle.adamw_step(pq, g, mq, vq, t)
+    rel = np.linalg.norm(pq - pf) / np.linalg.norm(pf - p0)
+    assert rel < 0.02, rel
+
+
+# ------------------------------------------------------------------- Adafactor
+def _hf_adafactor(p0, rows, cols, grads, lr=1e-3):
+    from transformers.optimization import Adafactor
+
+    shape = (rows, cols) if rows > 1 else (cols,)
+    tp = torch.nn.Parameter(torch.from_numpy(p0.copy().reshape(shape)))
+    opt = Adafactor([tp], lr=lr, eps=(1e-30, 1e-3), clip_threshold=1.0, decay_rate=-0.8, beta1=None,
+                    weight_decay=0.0, scale_parameter=False, relative_step=False, warmup_init=False)
+    for g in grads:
+        tp.grad = torch.from_numpy(g.copy().reshape(shape))
+        opt.step()
+    return tp.detach().numpy().reshape(-1), opt.state[tp]
+
+
+@pytest.mark.parametrize("shape", [(48, 80), (1, 777)])
+def test_adafactor_fp32_matches_hf(shape):
+    rows, cols = shape
+    n = rows * cols
+    steps = 60
+    p0 = _param(n, 7)
+    grads = _grads(rows, cols, steps, 8, zero_frac=0.02)
+    p = p0.copy()
+    if rows > 1:
+        vr, vc, v = State(FP32, rows), State(FP32, cols), None
+    else:
+        vr, vc, v = None, None, State(FP32, n)
+    for t, g in enumerate(grads, 1):
+        oracle.adafactor_step(p, g, rows, cols, vr, vc, v, t)
+    ref, st = _hf_adafactor(p0, rows, cols, grads)
+    assert np.abs(p - ref).max() <= 2e-6
+    assert np.linalg.norm(p - ref) / np.linalg.norm(ref) < 2e-6
+    if rows > 1:
+        np.testing.assert_allclose(vr.codes, st["exp_avg_sq_row"].numpy(), rtol=2e-6)
+        np.testing.assert_allclose(vc.codes, st["exp_avg_sq_col"].numpy(), rtol=2e-6)
+    else:
+        np.testing.assert_allclose(v.codes, st["exp_avg_sq"].numpy(), rtol=2e-6)
+
+
+def test_adafactor_rank1_closed_form():
+    """g_ij = a_i b_j: the factored estimate is exact, so at t = 1 the clipped update is sign(g)."""
+    rng = np.random.default_rng(21)
+    rows, cols = 24, 40
+    # power-of-two factors keep |g| = a_i b_j exact in fp32
+    a = np.exp2(rng.integers(-12, -8, rows)).astype(np.float64)
+    b = np.exp2(rng.integers(-2, 2, cols)).astype(np.float64)
+    sgn = np.where(rng.random(rows * cols) < 0.5, -1.0, 1.0)
+    g = (np.outer(a, b).reshape(-1) * sgn).astype(np.float32)
+    p0 = _param(rows * cols, 9)
+    for codec in (FP32, AL16):
+        p = p0.copy()
+        oracle.adafactor_step(p, g, rows, cols, State(codec, rows, 128, -99.66), State(codec, cols, 128, -99.66),
+                              None, 1, lr=1e-3)
+        upd = (p0.astype(np.float64) - p) / 1e-3
+        tol = 1e-4 if codec == FP32 else 3e-4
+        np.testing.assert_allclose(upd, sgn, rtol=tol, atol=tol)
+
+
+# ------------------------------------------------------------------------ CAME
+def _came_states(rows, cols, codec=FP32, mcodec=FP32):
+    n = rows * cols
+    if rows > 1:
+        return dict(m=State(mcodec, n, 256), vr=State(codec, rows, 128, -99.66), vc=State(codec, cols, 128, -99.66),
+                    v=None, cr=State(codec, rows, 128, -53.15), cc=State(codec, cols, 128, -53.15))
+    return dict(m=State(mcodec, n, 256), vr=None, vc=None, v=State(codec, n, 128, -99.66), cr=None, cc=None)
+
+
+def test_came_beta1_zero_closed_form():
+    """beta1 = 0: m = clipped update, residual == eps2, so from zero confidence
+    R'_t = C'_t = (1 - beta3^t) eps2 and p -= lr * uhat / sqrt((1 - beta3^t) eps2)."""
+    rows, cols = 20, 36
+    n = rows * cols
+    p0 = _param(n, 11)
+    grads = _grads(rows, cols, 5, 12)
+    st = _came_states(rows, cols)
+    beta3, eps2, lr = 0.9999, 1e-16, 1e-4
+    p = p0.copy()
+    # reference clipped update from the Adafactor-pinned factored path: with
+    # beta1 = 0 the CAME update equals the clipped Adafactor-style update
+    # scaled by 1/sqrt((1 - beta3^t) eps2)
+    for t, g in enumerate(grads, 1):
+        before = p.copy()
+        oracle.came_step(p, g, rows, cols, t=t, beta1=0.0, lr=lr, beta3=beta3, eps2=eps2, **st)
+        c_expect = (1 - beta3**t) * eps2
+        np.testing.assert_allclose(st["cr"].codes, np.float32(c_expect), rtol=1e-6)
+        np.testing.assert_allclose(st["cc"].codes, np.float32(c_expect), rtol=1e-6)
+        upd = (before.astype(np.float64) - p) / lr * math.sqrt(c_expect)
+        # |uhat| has RMS <= 1 after clipping; the update is m = uhat exactly
+        np.testing.assert_allclose(upd, st["m"].codes, rtol=2e-3, atol=1e-3 * np.abs(upd).max())
+
+
+def test_came_uniform_gradient_closed_form():
+    """Uniform g = c: uhat = sign(c); m = (1-beta1) sign(c); residual beta1^2 + eps2 everywhere;
+    p -= lr (1-beta1) sign(c) / sqrt((1-beta3)(beta1^2 + eps2))."""
+    for rows, cols in ((16, 32), (1, 300)):
+        n = rows * cols
+        p0 = _param(n, 13)
+        c = np.float32(-3e-4)
+        g = np.full(n, c, np.float32)
+        st = _came_states(rows, cols)
+        p = p0.copy()
+        b1, b3, e2, lr = 0.9, 0.9999, 1e-16, 1e-4
+        oracle.came_step(p, g, rows, cols, t=1, beta1=b1, beta3=b3, eps2=e2, lr=lr, **st)
+        if rows > 1:
+            want = lr * (1 - b1) * -1.0 / math.sqrt((1 - b3) * (b1 * b1 + e2))
+        else:
+            want = lr * (1 - b1) * -1.0  # 1-D tensors: update = momentum, no confidence
+        # p is fp32: the observed step carries one rounding of p
+        ulp_p = float(np.spacing(np.abs(p0)).max())
+        np.testing.assert_allclose(p0.astype(np.float64) - p, want, rtol=1e-5, atol=ulp_p)
+
+
+def test_came_rank1_closed_form():
+    rng = np.random.default_rng(23)
+    rows, cols = 12, 20
+    a = np.exp2(rng.integers(-12, -8, rows)).astype(np.float64)
+    b = np.exp2(rng.integers(-2, 2, cols)).astype(np.float64)
+    sgn = np.where(rng.random(rows * cols) < 0.5, -1.0, 1.0)
+    g = (np.outer(a, b).reshape(-1) * sgn).astype(np.float32)
+    p0 = _param(rows * cols, 15)
+    st = _came_states(rows, cols)
+    p = p0.copy()
+    b1, b3, e2, lr = 0.9, 0.9999, 1e-16, 1e-4
+    oracle.came_step(p, g, rows, cols, t=1, beta1=b1, beta3=b3, eps2=e2, lr=lr, **st)
+    want = lr * (1 - b1) * sgn / math.sqrt((1 - b3) * (b1 * b1 + e2))
+    np.testing.assert_allclose(p0.astype(np.float64) - p, want, rtol=1e-4)
+
+
+def test_came_second_moment_path_matches_adafactor_at_t1():
+    """With beta2 = 0 CAME's factored V equals Adafactor's at t = 1 (beta2_t = 0); with beta1 = 0 its
+    update is that clipped update scaled by 1/sqrt((1 - beta3) eps2)."""
+    for rows, cols in ((30, 44), (1, 500)):
+        n = rows * cols
+        p0 = _param(n, 17)
+        g = _grads(rows, cols, 1, 18, zero_frac=0.02)[0]
+        pa = p0.copy()
+        fac = rows > 1
+        oracle.adafactor_step(pa, g, rows, cols, State(FP32, rows) if fac else None,
+                              State(FP32, cols) if fac else None, None if fac else State(FP32, n), 1, lr=1e-3)
+        ua = (p0.astype(np.float64) - pa) / 1e-3
+        st = _came_states(rows, cols)
+        pc = p0.copy()
+        oracle.came_step(pc, g, rows, cols, t=1, beta1=0.0, beta2=0.0, lr=1e-4, **st)
+        uc = (p0.astype(np.float64) - pc) / 1e-4
+        scale = math.sqrt((1 - 0.9999) * 1e-16) if fac else 1.0
+        np.testing.assert_allclose(uc * scale, ua, rtol=5e-3, atol=5e-3 * np.abs(ua).max())
