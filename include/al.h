@@ -1,0 +1,219 @@
+/*
+ * al.h -- C ABI of the MI355X (gfx950) quantized optimizer-step library
+ * (libal.so).
+ *
+ * The library implements the fused quantized optimizer step of "Beyond Dense
+ * Adam States: Adaptive Log-Space Quantization for Memory-Efficient
+ * Optimizers": each step decodes block-wise optimizer state, applies the
+ * optimizer update and re-encodes the state, for AdamW (dense M, V), Adafactor
+ * (factored V) and CAME (dense M, factored V and factored confidence C),
+ * section 3.1.
+ *
+ * Codes (section 4):
+ *   AL8 / AL16  non-negative states. Per block of B consecutive elements of
+ *               the row-major flattening: l_min = max(l_floor, log2 of the
+ *               smallest positive value), l_max = log2 of the largest,
+ *               capped at 126 (Eq. al_bounds); positive x -> 1 +
+ *               round((L-2) clip((log2 x - l_min)/(l_max - l_min), 0, 1)),
+ *               zero -> 0 (Eq. al_quant); decode 2^(l_min + (q-1)/(L-2) *
+ *               delta) (Eq. al_dequant). L = 256 (AL8, uint8 codes) or
+ *               65,536 (AL16, uint16 codes). q = 0 iff x = 0 (Eq.
+ *               exact_zero). Equal positives widen the interval upward by
+ *               one log2 unit; the width is at least 1e-12.
+ *               Metadata: 2 floats per block, {l_min, delta}.
+ *   UF8         signed momentum (section 4.3): symmetric int8 in
+ *               [-127, 127] with a per-block absmax scale; code =
+ *               round(127 x / absmax), decode code * absmax / 127.
+ *               Metadata: 1 float per block, {absmax}.
+ *   FP32        the state is a plain float array (no metadata).
+ *
+ * Storage (section 4.4, Eq. al_memory): a state of n elements under block B
+ * holds ceil(n/B)*B codes -- padded per tensor; padded codes are written as
+ * 0 -- plus its metadata. al_code_bytes / al_meta_floats / al_state_bytes
+ * give the sizes.
+ *
+ * Numeric contract. State arithmetic (decode, EMA, marginal means, factor
+ * reconstruction, residuals) is binary64, each state rounded once to fp32
+ * per step, sums exact to binary64 rounding; codes are decided from binary64
+ * positions. The parameter update itself is fp32.
+ *
+ * Memory and execution. Every pointer argument is device memory owned by
+ * the caller, except that tensor lists and config structs are host memory
+ * read during the call. The library keeps no pointer after a call returns.
+ * All device work is enqueued on `stream` (a hipStream_t; NULL = the null
+ * stream) in order; calls return without synchronizing. The library never
+ * allocates device memory: Adafactor and CAME take a caller workspace whose
+ * size the *_workspace_bytes query returns. Calls on distinct streams with
+ * distinct buffers may run concurrently; calls that share a workspace or
+ * state buffers must be ordered by the caller.
+ *
+ * Fresh state: all codes and metadata zero (code 0 is exact zero).
+ *
+ * Errors. Every call returns an al_status. All argument checks run on the
+ * host before any HIP call, so a rejected call has enqueued nothing.
+ * al_last_error() returns a thread-local description of the last failure on
+ * the calling thread. Non-finite or negative values in a non-negative state
+ * are not detected; their codes are unspecified.
+ *
+ * Alignment. Every device pointer must be 16-byte aligned (AL_EALIGN).
+ */
+#ifndef AL_H
+#define AL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum al_status {
+    AL_OK = 0,
+    AL_EINVAL = 1,       /* bad argument: NULL, n < 0, bad codec/block/dtype, rows*cols mismatch */
+    AL_EALIGN = 2,       /* a device pointer is not 16-byte aligned */
+    AL_EWORKSPACE = 3,   /* workspace missing or smaller than the query returned */
+    AL_EUNSUPPORTED = 4, /* a valid combination this build does not implement */
+    AL_EHIP = 5          /* a HIP runtime call or launch failed */
+} al_status;
+
+typedef enum al_codec {
+    AL_CODEC_FP32 = 0,
+    AL_CODEC_AL8 = 1,
+    AL_CODEC_AL16 = 2,
+    AL_CODEC_UF8 = 3
+} al_codec;
+
+typedef enum al_dtype { AL_DTYPE_F32 = 0, AL_DTYPE_BF16 = 1 } al_dtype;
+
+/* Which code a state gets ("representation and state policy", section 4.3).
+ * block: 64, 128, 256, 512, 1024 or 2048 (ignored for FP32).
+ * log_floor: l_floor of Eq. al_bounds (AL codecs only); the optimizer path
+ * supplies it, typically log2 of its squared numerical floor (section 4.1). */
+typedef struct al_state_spec {
+    int32_t codec;
+    int32_t block;
+    float log_floor;
+} al_state_spec;
+
+/* One parameter tensor and its optimizer state buffers.
+ * rows, cols: the row-major shape; a 1-D tensor has rows == 1 (such tensors,
+ * and any tensor with rows == 1, keep an unfactored second moment in `v`).
+ * param: rows*cols fp32, updated in place. grad: rows*cols of the call's
+ * grad dtype.
+ * m, m_meta:       momentum (AdamW, CAME).
+ * v, v_meta:       dense second moment (AdamW), or the unfactored second
+ *                  moment of a rows == 1 tensor (Adafactor, CAME).
+ * vr/vc (+meta):   factored second moment, row (len rows) / column (len cols)
+ *                  statistics (Adafactor, CAME; rows > 1 only).
+ * cr/cc (+meta):   CAME factored confidence, row / column (rows > 1 only).
+ * Slots a path does not use must be NULL. Metadata pointers are NULL for
+ * FP32 states. */
+typedef struct al_tensor {
+    float* param;
+    const void* grad;
+    int64_t rows;
+    int64_t cols;
+    void* m;
+    float* m_meta;
+    void* v;
+    float* v_meta;
+    void* vr;
+    float* vr_meta;
+    void* vc;
+    float* vc_meta;
+    void* cr;
+    float* cr_meta;
+    void* cc;
+    float* cc_meta;
+} al_tensor;
+
+/* AdamW (section 3.1, Eq. adam_update; decoupled weight decay and bias
+ * corrections as in PyTorch AdamW). m: UF8 (block 256) or FP32.
+ * v: AL8, AL16 or FP32. */
+typedef struct al_adamw_cfg {
+    double lr, beta1, beta2, eps, weight_decay;
+    int32_t grad_dtype;
+    int32_t reserved;
+    al_state_spec m, v;
+} al_adamw_cfg;
+
+/* Adafactor (factored second moment, section 3.1): beta2_t = 1 - t^decay_rate,
+ * G2 = g^2 + eps1, R/C = EMA of row/column means of G2, update
+ * u = g / sqrt(R_i C_j / mean(R)), clipped by max(1, RMS(u)/clip_threshold);
+ * no first moment, no relative step, no parameter scaling.
+ * v: AL8, AL16 or FP32 for R, C and 1-D v. */
+typedef struct al_adafactor_cfg {
+    double lr, eps1, clip_threshold, decay_rate, weight_decay;
+    int32_t grad_dtype;
+    int32_t reserved;
+    al_state_spec v;
+} al_adafactor_cfg;
+
+/* CAME (confidence-guided factored optimizer, section 3.1): factored V as
+ * Adafactor with a constant beta2 and no bias correction; clipped update
+ * uhat; m = EMA(beta1) of uhat; residual (uhat - m)^2 + eps2 feeds factored
+ * confidence R', C' (EMA beta3); update m / sqrt(R'_i C'_j / mean(R')).
+ * 1-D tensors: unfactored v, update = m, no confidence.
+ * m: UF8 (block 256) or FP32; v and conf: AL8, AL16 or FP32. */
+typedef struct al_came_cfg {
+    double lr, beta1, beta2, beta3, eps1, eps2, clip_threshold, weight_decay;
+    int32_t grad_dtype;
+    int32_t reserved;
+    al_state_spec m, v, conf;
+} al_came_cfg;
+
+/* Library version string, e.g. "0.1.0 gfx950". */
+const char* al_version(void);
+
+/* Thread-local text of the last failure on this thread ("" if none). */
+const char* al_last_error(void);
+
+/* Storage accounting (section 4.4). Bytes of the code array of an n-element
+ * state (padded to whole blocks), metadata floats, and their total in bytes.
+ * Return -1 for an invalid codec, block or n < 0. */
+int64_t al_code_bytes(int32_t codec, int64_t n, int32_t block);
+int64_t al_meta_floats(int32_t codec, int64_t n, int32_t block);
+int64_t al_state_bytes(int32_t codec, int64_t n, int32_t block);
+
+/* Encode n fp32 values x (non-negative for AL codecs) into codes + meta
+ * (Eq. al_bounds and al_quant for AL8/AL16; section 4.3 for UF8).
+ * codec: AL8, AL16 or UF8. codes: al_code_bytes(codec, n, block) bytes;
+ * meta: al_meta_floats(codec, n, block) floats. log_floor is ignored for
+ * UF8. n == 0 is a no-op. */
+al_status al_quantize(int32_t codec, const float* x, int64_t n, int32_t block, float log_floor,
+                      void* codes, float* meta, void* stream);
+
+/* Decode n values (Eq. al_dequant for AL8/AL16; section 4.3 for UF8) into
+ * out (n floats). */
+al_status al_dequantize(int32_t codec, const void* codes, const float* meta, int64_t n,
+                        int32_t block, float* out, void* stream);
+
+/* One fused AdamW step over a list of nt tensors (step = the 1-based step
+ * count after increment). One pass over HBM: read p, g, m, v (+meta), write
+ * p, m, v (+meta). Uses per tensor: param, grad, m, m_meta, v, v_meta. */
+al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg,
+                        int64_t step, void* stream);
+
+/* Workspace size (bytes) that al_adafactor_step / al_came_step need for this
+ * tensor list and config. */
+al_status al_adafactor_workspace_bytes(const al_tensor* tensors, int32_t nt,
+                                       const al_adafactor_cfg* cfg, size_t* bytes);
+al_status al_came_workspace_bytes(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg,
+                                  size_t* bytes);
+
+/* One Adafactor step over nt tensors. Uses per tensor: param, grad and
+ * (rows > 1) vr, vr_meta, vc, vc_meta or (rows == 1) v, v_meta.
+ * ws: device workspace of at least the queried size, 256-byte aligned. */
+al_status al_adafactor_step(const al_tensor* tensors, int32_t nt, const al_adafactor_cfg* cfg,
+                            int64_t step, void* ws, size_t ws_bytes, void* stream);
+
+/* One CAME step over nt tensors. Uses per tensor: param, grad, m, m_meta and
+ * (rows > 1) vr, vc, cr, cc with metadata or (rows == 1) v, v_meta. */
+al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg,
+                       int64_t step, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AL_H */

@@ -1,0 +1,271 @@
+// C ABI of libal.so: argument validation (on the host, before any HIP call),
+// storage accounting, scalar precompute in binary64, and launches on the
+// caller's stream. See include/al.h for the contract of each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/al.h"
+#include "../../include/al_synth.h"
+#include "al_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+al_status fail(al_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+al_status hip_fail(hipError_t e, const char* what) {
+    return fail(AL_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_block(int32_t b) { return b == 64 || b == 128 || b == 256 || b == 512 || b == 1024 || b == 2048; }
+
+bool valid_codec(int32_t c) { return c >= AL_CODEC_FP32 && c <= AL_CODEC_UF8; }
+
+bool is_fin(double x) { return std::isfinite(x); }
+
+int64_t nblocks(int64_t n, int32_t b) { return (n + b - 1) / b; }
+
+// Validate a state spec for a role: `allowed` is a bit mask of codecs.
+al_status check_spec(const al_state_spec& s, unsigned allowed, const char* role) {
+    if (!valid_codec(s.codec) || !((allowed >> s.codec) & 1u))
+        return fail(AL_EINVAL, "%s: codec %d not allowed for this state", role, s.codec);
+    if (s.codec != AL_CODEC_FP32 && !valid_block(s.block))
+        return fail(AL_EINVAL, "%s: block %d must be 64, 128, 256, 512, 1024 or 2048", role, s.block);
+    if ((s.codec == AL_CODEC_AL8 || s.codec == AL_CODEC_AL16) && !std::isfinite(s.log_floor))
+        return fail(AL_EINVAL, "%s: log_floor must be finite", role);
+    return AL_OK;
+}
+
+// A state slot: codes non-NULL and aligned; metadata required iff quantized.
+al_status check_state(const void* codes, const float* meta, const al_state_spec& s, int64_t n, const char* role,
+                      int i) {
+    if (n == 0) return AL_OK;
+    if (!codes) return fail(AL_EINVAL, "tensor %d: %s buffer is NULL", i, role);
+    if (!aligned16(codes)) return fail(AL_EALIGN, "tensor %d: %s buffer not 16-byte aligned", i, role);
+    if (s.codec != AL_CODEC_FP32) {
+        if (!meta) return fail(AL_EINVAL, "tensor %d: %s metadata is NULL", i, role);
+        if (!aligned16(meta)) return fail(AL_EALIGN, "tensor %d: %s metadata not 16-byte aligned", i, role);
+    }
+    return AL_OK;
+}
+
+al_status check_unused(const void* a, const void* b, const char* role, int i) {
+    if (a || b) return fail(AL_EINVAL, "tensor %d: %s must be NULL for this path", i, role);
+    return AL_OK;
+}
+
+al_status check_shape(const al_tensor& t, int i, int64_t* n_out) {
+    if (t.rows < 0 || t.cols < 0) return fail(AL_EINVAL, "tensor %d: negative shape", i);
+    if (t.rows > 0 && t.cols > (int64_t(1) << 62) / t.rows) return fail(AL_EINVAL, "tensor %d: shape overflows", i);
+    const int64_t n = t.rows * t.cols;
+    if (n > 0) {
+        if (!t.param || !t.grad) return fail(AL_EINVAL, "tensor %d: param or grad is NULL", i);
+        if (!aligned16(t.param) || !aligned16(t.grad))
+            return fail(AL_EALIGN, "tensor %d: param or grad not 16-byte aligned", i);
+    }
+    *n_out = n;
+    return AL_OK;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+namespace al {
+
+int device_cu_count() {
+    static std::mutex mu;
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    std::lock_guard<std::mutex> lk(mu);
+    if (cache[dev] == 0) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cache[dev] = v;
+    }
+    return cache[dev];
+}
+
+}  // namespace al
+
+extern "C" {
+
+const char* al_version(void) { return "0.1.0 gfx950"; }
+
+const char* al_last_error(void) { return g_err; }
+
+int64_t al_code_bytes(int32_t codec, int64_t n, int32_t block) {
+    if (n < 0 || !valid_codec(codec)) return -1;
+    if (codec == AL_CODEC_FP32) return 4 * n;
+    if (!valid_block(block)) return -1;
+    const int64_t padded = nblocks(n, block) * block;
+    return codec == AL_CODEC_AL16 ? 2 * padded : padded;
+}
+
+int64_t al_meta_floats(int32_t codec, int64_t n, int32_t block) {
+    if (n < 0 || !valid_codec(codec)) return -1;
+    if (codec == AL_CODEC_FP32) return 0;
+    if (!valid_block(block)) return -1;
+    return nblocks(n, block) * (codec == AL_CODEC_UF8 ? 1 : 2);
+}
+
+int64_t al_state_bytes(int32_t codec, int64_t n, int32_t block) {
+    const int64_t c = al_code_bytes(codec, n, block);
+    const int64_t m = al_meta_floats(codec, n, block);
+    if (c < 0 || m < 0) return -1;
+    return c + 4 * m;
+}
+
+al_status al_quantize(int32_t codec, const float* x, int64_t n, int32_t block, float log_floor, void* codes,
+                      float* meta, void* stream) {
+    g_err[0] = 0;
+    if (codec != AL_CODEC_AL8 && codec != AL_CODEC_AL16 && codec != AL_CODEC_UF8)
+        return fail(AL_EINVAL, "al_quantize: codec %d is not AL8, AL16 or UF8", codec);
+    if (n < 0) return fail(AL_EINVAL, "al_quantize: n < 0");
+    if (!valid_block(block)) return fail(AL_EINVAL, "al_quantize: block %d invalid", block);
+    if (codec != AL_CODEC_UF8 && !std::isfinite(log_floor)) return fail(AL_EINVAL, "al_quantize: log_floor");
+    if (n == 0) return AL_OK;
+    if (!x || !codes || !meta) return fail(AL_EINVAL, "al_quantize: NULL buffer");
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(meta)) return fail(AL_EALIGN, "al_quantize: alignment");
+    hipError_t e = al::launch_quantize(codec, x, n, block, log_floor, codes, meta, al::device_cu_count() * 8,
+                                       as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_quantize launch");
+}
+
+al_status al_dequantize(int32_t codec, const void* codes, const float* meta, int64_t n, int32_t block, float* out,
+                        void* stream) {
+    g_err[0] = 0;
+    if (codec != AL_CODEC_AL8 && codec != AL_CODEC_AL16 && codec != AL_CODEC_UF8)
+        return fail(AL_EINVAL, "al_dequantize: codec %d is not AL8, AL16 or UF8", codec);
+    if (n < 0) return fail(AL_EINVAL, "al_dequantize: n < 0");
+    if (!valid_block(block)) return fail(AL_EINVAL, "al_dequantize: block %d invalid", block);
+    if (n == 0) return AL_OK;
+    if (!codes || !meta || !out) return fail(AL_EINVAL, "al_dequantize: NULL buffer");
+    if (!aligned16(out) || !aligned16(codes) || !aligned16(meta)) return fail(AL_EALIGN, "al_dequantize: alignment");
+    hipError_t e = al::launch_dequantize(codec, codes, meta, n, block, out, al::device_cu_count() * 8,
+                                         as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_dequantize launch");
+}
+
+al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step,
+                        void* stream) {
+    g_err[0] = 0;
+    if (nt < 0) return fail(AL_EINVAL, "al_adamw_step: nt < 0");
+    if (nt > 0 && !tensors) return fail(AL_EINVAL, "al_adamw_step: tensors is NULL");
+    if (!cfg) return fail(AL_EINVAL, "al_adamw_step: cfg is NULL");
+    if (step < 1) return fail(AL_EINVAL, "al_adamw_step: step must be >= 1");
+    if (cfg->grad_dtype != AL_DTYPE_F32 && cfg->grad_dtype != AL_DTYPE_BF16)
+        return fail(AL_EINVAL, "al_adamw_step: grad_dtype %d", cfg->grad_dtype);
+    if (!is_fin(cfg->lr) || cfg->lr < 0 || !is_fin(cfg->eps) || cfg->eps < 0 || !is_fin(cfg->weight_decay) ||
+        cfg->weight_decay < 0 || !(cfg->beta1 >= 0 && cfg->beta1 < 1) || !(cfg->beta2 >= 0 && cfg->beta2 < 1))
+        return fail(AL_EINVAL, "al_adamw_step: hyperparameters out of range");
+    al_status st;
+    if ((st = check_spec(cfg->m, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_UF8), "m")) != AL_OK) return st;
+    if ((st = check_spec(cfg->v, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16), "v")) !=
+        AL_OK)
+        return st;
+    if (cfg->m.codec == AL_CODEC_UF8 && cfg->m.block != 256)
+        return fail(AL_EUNSUPPORTED, "al_adamw_step: UF8 momentum block must be 256 (got %d)", cfg->m.block);
+
+    std::vector<int64_t> ns(nt);
+    for (int i = 0; i < nt; ++i) {
+        const al_tensor& t = tensors[i];
+        if ((st = check_shape(t, i, &ns[i])) != AL_OK) return st;
+        if ((st = check_state(t.m, t.m_meta, cfg->m, ns[i], "m", i)) != AL_OK) return st;
+        if ((st = check_state(t.v, t.v_meta, cfg->v, ns[i], "v", i)) != AL_OK) return st;
+        if ((st = check_unused(t.vr, t.vr_meta, "vr", i)) != AL_OK) return st;
+        if ((st = check_unused(t.vc, t.vc_meta, "vc", i)) != AL_OK) return st;
+        if ((st = check_unused(t.cr, t.cr_meta, "cr", i)) != AL_OK) return st;
+        if ((st = check_unused(t.cc, t.cc_meta, "cc", i)) != AL_OK) return st;
+    }
+
+    al::AdamWLaunch a;
+    std::memset(&a, 0, sizeof(a));
+    const double bc1 = 1.0 - std::pow(cfg->beta1, (double)step);
+    const double bc2 = 1.0 - std::pow(cfg->beta2, (double)step);
+    a.beta1 = cfg->beta1;
+    a.omb1 = 1.0 - cfg->beta1;
+    a.beta2 = cfg->beta2;
+    a.omb2 = 1.0 - cfg->beta2;
+    a.step_size = (float)(cfg->lr / bc1);
+    a.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+    a.eps = (float)cfg->eps;
+    a.decay = (float)(1.0 - cfg->lr * cfg->weight_decay);
+    a.v_floor = cfg->v.log_floor;
+    const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
+    const int grid_cap = al::device_cu_count() * 8;
+    hipStream_t s = as_stream(stream);
+
+    auto flush = [&]() -> al_status {
+        if (a.nt == 0) return AL_OK;
+        const int64_t want = (a.total_tiles + 3) / 4;
+        const int grid = (int)(want < grid_cap ? want : grid_cap);
+        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, grid, s);
+        a.nt = 0;
+        a.total_tiles = 0;
+        return e == hipSuccess ? AL_OK : hip_fail(e, "al_adamw_step launch");
+    };
+    for (int i = 0; i < nt; ++i) {
+        if (ns[i] == 0) continue;
+        const al_tensor& t = tensors[i];
+        al::AdamWDesc& d = a.t[a.nt++];
+        d.p = t.param;
+        d.g = t.grad;
+        d.m = t.m;
+        d.ms = t.m_meta;
+        d.v = t.v;
+        d.vm = t.v_meta;
+        d.n = ns[i];
+        d.tile_begin = a.total_tiles;
+        a.total_tiles += (ns[i] + T - 1) / T;
+        if (a.nt == al::kAdamWMaxTensors)
+            if ((st = flush()) != AL_OK) return st;
+    }
+    return flush();
+}
+
+al_status al_synth_normal(void* out, int32_t out_dtype, int64_t n, uint64_t key, float scale, uint64_t mask_key,
+                          uint64_t mask_threshold, void* stream) {
+    g_err[0] = 0;
+    if (out_dtype != AL_DTYPE_F32 && out_dtype != AL_DTYPE_BF16) return fail(AL_EINVAL, "al_synth_normal: dtype");
+    if (n < 0) return fail(AL_EINVAL, "al_synth_normal: n < 0");
+    if (n == 0) return AL_OK;
+    if (!out) return fail(AL_EINVAL, "al_synth_normal: out is NULL");
+    if (!aligned16(out)) return fail(AL_EALIGN, "al_synth_normal: alignment");
+    hipError_t e = al::launch_synth_normal(out, out_dtype == AL_DTYPE_BF16, n, key, scale, mask_key, mask_threshold,
+                                           al::device_cu_count() * 16, as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_synth_normal launch");
+}
+
+al_status al_adafactor_workspace_bytes(const al_tensor*, int32_t, const al_adafactor_cfg*, size_t* bytes) {
+    if (bytes) *bytes = 0;
+    return fail(AL_EUNSUPPORTED, "al_adafactor_workspace_bytes: not built yet");
+}
+al_status al_came_workspace_bytes(const al_tensor*, int32_t, const al_came_cfg*, size_t* bytes) {
+    if (bytes) *bytes = 0;
+    return fail(AL_EUNSUPPORTED, "al_came_workspace_bytes: not built yet");
+}
+al_status al_adafactor_step(const al_tensor*, int32_t, const al_adafactor_cfg*, int64_t, void*, size_t, void*) {
+    return fail(AL_EUNSUPPORTED, "al_adafactor_step: not built yet");
+}
+al_status al_came_step(const al_tensor*, int32_t, const al_came_cfg*, int64_t, void*, size_t, void*) {
+    return fail(AL_EUNSUPPORTED, "al_came_step: not built yet");
+}
+
+}  // extern "C"

@@ -1,0 +1,226 @@
+// Device helpers shared by the gfx950 kernels: cross-lane reductions on a
+// 64-wide wavefront, bfloat16 unpacking, and the per-element / per-block
+// pieces of the AL and UF8 codes.
+//
+// Every kernel maps 4 consecutive elements to a lane, so a wavefront covers
+// 256 consecutive elements (a "sub-tile"). A block of B <= 256 elements then
+// spans B/4 lanes (16, 32 or 64); a larger block spans B/256 sub-tiles held
+// in registers by one wavefront.
+//
+// The sources are built with -ffp-contract=off: every binary64 expression
+// below rounds after each operation, in the order written, which is what
+// makes the fp32-rounded states reproducible bit for bit.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace al {
+
+constexpr int kWave = 64;
+constexpr int kSub = 256;  // elements per wavefront sub-tile (4 per lane)
+
+enum Codec : int { FP32 = 0, AL8 = 1, AL16 = 2, UF8 = 3 };
+enum GradT : int { G_F32 = 0, G_BF16 = 1 };
+
+// ---------------------------------------------------------------- bit casts
+__device__ __forceinline__ uint32_t f2u(float x) { return __builtin_bit_cast(uint32_t, x); }
+__device__ __forceinline__ float u2f(uint32_t x) { return __builtin_bit_cast(float, x); }
+__device__ __forceinline__ float bf16_to_f32(uint32_t b16) { return u2f(b16 << 16); }
+
+// ------------------------------------------------------- cross-lane helpers
+// DPP control words (GCN/CDNA "dpp_ctrl"): quad permutations, row mirrors.
+constexpr int kDppQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
+constexpr int kDppRowHalfMirror = 0x141;  // lane i -> 7-i within 8
+constexpr int kDppRowMirror = 0x140;      // lane i -> 15-i within 16
+// ds_swizzle bit mode: and_mask 0x1F, xor_mask 0x10 -> lane ^ 16 within 32
+constexpr int kSwzXor16 = 0x401F;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, false);
+}
+
+struct OpMax {
+    __device__ static uint32_t f(uint32_t a, uint32_t b) { return a > b ? a : b; }
+};
+struct OpMin {
+    __device__ static uint32_t f(uint32_t a, uint32_t b) { return a < b ? a : b; }
+};
+
+// Reduce over aligned groups of LANES lanes (16, 32 or 64). Every lane gets
+// its group's result; for 64 the result is wave-uniform.
+template <class Op, int LANES>
+__device__ __forceinline__ uint32_t group_reduce(uint32_t x) {
+    static_assert(LANES == 16 || LANES == 32 || LANES == 64, "group size");
+    x = Op::f(x, dpp<kDppQuadXor1>(x));
+    x = Op::f(x, dpp<kDppQuadXor2>(x));
+    x = Op::f(x, dpp<kDppRowHalfMirror>(x));
+    x = Op::f(x, dpp<kDppRowMirror>(x));
+    if constexpr (LANES >= 32) x = Op::f(x, (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, kSwzXor16));
+    if constexpr (LANES == 64) {
+        uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+        uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+        x = Op::f(a, b);
+    }
+    return x;
+}
+
+// ------------------------------------------------------------------ AL code
+// Fitted interval of one block from its exact positive min / max bit
+// patterns (0 max means "no positive value").
+struct ALFit {
+    double lmin;   // unrounded binary64 l_min
+    double delta;  // unrounded binary64 width
+    bool any;
+};
+
+__device__ __forceinline__ ALFit al_fit(uint32_t min_bits, uint32_t max_bits, float log_floor) {
+    ALFit f;
+    f.any = max_bits != 0u;
+    if (!f.any) {
+        f.lmin = 0.0;
+        f.delta = 0.0;
+        return f;
+    }
+    double lo = log2((double)u2f(min_bits));
+    double hi = log2((double)u2f(max_bits));
+    double l0 = lo > (double)log_floor ? lo : (double)log_floor;
+    double l1 = hi < 126.0 ? hi : 126.0;
+    if (min_bits == max_bits) l1 = l0 + 1.0;
+    double d = l1 - l0;
+    if (d < 1e-12) d = 1e-12;
+    f.lmin = l0;
+    f.delta = d;
+    return f;
+}
+
+// Code of one element under a fitted interval; LEVELS = L - 2.
+template <int LEVELS>
+__device__ __forceinline__ uint32_t al_encode(float x, const ALFit& f) {
+    if (!(x > 0.0f)) return 0u;
+    double z = (log2((double)x) - f.lmin) / f.delta;
+    z = z < 0.0 ? 0.0 : z;
+    z = z > 1.0 ? 1.0 : z;
+    double y = (double)LEVELS * z;
+    return 1u + (uint32_t)__builtin_rint(y);
+}
+
+// Decode of one code from the stored fp32 metadata: step = delta32 / (L-2),
+// value = fl32(2^(lmin32 + (q-1) * step)).
+__device__ __forceinline__ float al_decode(uint32_t q, double lmin32, double step) {
+    if (q == 0u) return 0.0f;
+    double e = lmin32 + (double)(q - 1u) * step;
+    return (float)exp2(e);
+}
+
+// ----------------------------------------------------------------- UF8 code
+// Encode with r = 127 / absmax (binary64), y = x * r, round to nearest even,
+// clamp to [-127, 127].
+__device__ __forceinline__ int32_t uf8_encode(float x, double r) {
+    double y = (double)x * r;
+    double q = __builtin_rint(y);
+    q = q > 127.0 ? 127.0 : q;
+    q = q < -127.0 ? -127.0 : q;
+    return (int32_t)q;
+}
+
+// Decode with step = absmax / 127 (binary64): fl32(q * step).
+__device__ __forceinline__ float uf8_decode(int32_t q, double step) { return (float)((double)q * step); }
+
+__device__ __forceinline__ uint32_t abs_bits(float x) { return f2u(x) & 0x7FFFFFFFu; }
+// For the positive minimum: zero (and -0) map to the largest key.
+__device__ __forceinline__ uint32_t pos_min_key(float x) {
+    uint32_t b = f2u(x);
+    return (b == 0u || (b & 0x80000000u)) ? 0xFFFFFFFFu : b;
+}
+__device__ __forceinline__ uint32_t pos_max_key(float x) {
+    uint32_t b = f2u(x);
+    return (b & 0x80000000u) ? 0u : b;
+}
+
+// ------------------------------------------------------- packed 4-wide I/O
+struct F4 {
+    float v[4];
+};
+
+__device__ __forceinline__ F4 load_f4(const float* p) {
+    float4 t = *reinterpret_cast<const float4*>(p);
+    return F4{{t.x, t.y, t.z, t.w}};
+}
+__device__ __forceinline__ void store_f4(float* p, const F4& x) {
+    *reinterpret_cast<float4*>(p) = make_float4(x.v[0], x.v[1], x.v[2], x.v[3]);
+}
+
+// Gradients: 4 consecutive elements as fp32.
+template <int G>
+__device__ __forceinline__ F4 load_grad4(const void* g, int64_t e) {
+    if constexpr (G == G_BF16) {
+        uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(g) + e);
+        return F4{{bf16_to_f32(w.x & 0xFFFFu), bf16_to_f32(w.x >> 16), bf16_to_f32(w.y & 0xFFFFu),
+                   bf16_to_f32(w.y >> 16)}};
+    } else {
+        return load_f4(reinterpret_cast<const float*>(g) + e);
+    }
+}
+
+template <int G>
+__device__ __forceinline__ float load_grad1(const void* g, int64_t e) {
+    if constexpr (G == G_BF16)
+        return bf16_to_f32(reinterpret_cast<const uint16_t*>(g)[e]);
+    else
+        return reinterpret_cast<const float*>(g)[e];
+}
+
+// Codes: 4 consecutive codes as unsigned (AL) or signed (UF8) integers.
+template <int C>
+__device__ __forceinline__ void load_codes4(const void* c, int64_t e, uint32_t q[4]) {
+    if constexpr (C == AL8 || C == UF8) {
+        uint32_t w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(c) + e);
+        q[0] = w & 0xFFu;
+        q[1] = (w >> 8) & 0xFFu;
+        q[2] = (w >> 16) & 0xFFu;
+        q[3] = w >> 24;
+    } else {
+        uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(c) + e);
+        q[0] = w.x & 0xFFFFu;
+        q[1] = w.x >> 16;
+        q[2] = w.y & 0xFFFFu;
+        q[3] = w.y >> 16;
+    }
+}
+
+template <int C>
+__device__ __forceinline__ uint32_t load_code1(const void* c, int64_t e) {
+    if constexpr (C == AL8 || C == UF8)
+        return reinterpret_cast<const uint8_t*>(c)[e];
+    else
+        return reinterpret_cast<const uint16_t*>(c)[e];
+}
+
+template <int C>
+__device__ __forceinline__ void store_codes4(void* c, int64_t e, const uint32_t q[4]) {
+    if constexpr (C == AL8 || C == UF8) {
+        uint32_t w = (q[0] & 0xFFu) | ((q[1] & 0xFFu) << 8) | ((q[2] & 0xFFu) << 16) | (q[3] << 24);
+        *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(c) + e) = w;
+    } else {
+        uint2 w = make_uint2((q[0] & 0xFFFFu) | (q[1] << 16), (q[2] & 0xFFFFu) | (q[3] << 16));
+        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(c) + e) = w;
+    }
+}
+
+template <int C>
+__device__ __forceinline__ void store_code1(void* c, int64_t e, uint32_t q) {
+    if constexpr (C == AL8 || C == UF8)
+        reinterpret_cast<uint8_t*>(c)[e] = (uint8_t)q;
+    else
+        reinterpret_cast<uint16_t*>(c)[e] = (uint16_t)q;
+}
+
+template <int C>
+constexpr int levels_of() {
+    return C == AL16 ? 65534 : 254;
+}
+
+}  // namespace al

@@ -1,0 +1,164 @@
+"""CPU tests of the C ABI (no GPU needed): the library loads, exports every
+declared symbol, rejects bad arguments with the documented status before any
+HIP call, and its storage accounting reproduces the paper's numbers.
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2608_22322_amd as al
+from paper_2608_22322_amd.workloads import tinyllama_shapes
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+MiB = 2.0**20
+A = 1 << 20  # a 16-byte aligned fake device address (never dereferenced: validation fails first)
+
+
+def _declared_symbols():
+    names = set()
+    for h in ("al.h", "al_synth.h"):
+        txt = open(os.path.join(ROOT, "include", h)).read()
+        txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+        names |= set(re.findall(r"\b(al_[a-z0-9_]+)\s*\(", txt))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = al.lib()
+    declared = _declared_symbols()
+    assert declared == set(al.EXPORTS), declared ^ set(al.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+    assert al.version().endswith("gfx950")
+
+
+# ----------------------------------------------------------------- storage (section 4.4)
+def test_al8_bits_per_element():
+    """Eq. al_memory: c_AL8 = 1 + 8/B bytes; 8.25 bits at B=256 and 8.031 at B=2048 (section 5)."""
+    n = 2048 * 1000
+    assert al.state_bytes(al.AL8, n, 256) * 8 / n == pytest.approx(8.25, abs=0)
+    assert al.state_bytes(al.AL8, n, 2048) * 8 / n == pytest.approx(8.03125, abs=0)
+    assert al.state_bytes(al.AL16, n, 2048) == 2 * n + 8 * (n // 2048)
+
+
+def test_block_size_memory_estimates():
+    """Section 5 (topology and block scale): a 1.1B-element AL8 state takes 1081.8 MiB at B=256 and
+    1053.1 MiB at B=2048."""
+    assert round(al.state_bytes(al.AL8, 1_100_000_000, 256) / MiB, 1) == 1081.8
+    assert round(al.state_bytes(al.AL8, 1_100_000_000, 2048) / MiB, 1) == 1053.1
+
+
+def test_table4_state_memory_reproduced():
+    """Table 4 optimizer-state MiB on TinyLlama-1.1B, reproduced from per-tensor padded storage: 2-D tensors
+    quantized, 1-D tensors' states kept FP32 (the paper's default grouping), factored vectors padded per
+    vector."""
+    sh = tinyllama_shapes()
+    n_all = sum(s.n for s in sh)
+    assert n_all == 1_100_048_384 and len(sh) == 201
+    assert round(8 * n_all / MiB, 1) == 8392.7  # AdamW FP32
+    ours = sum(al.state_bytes(al.UF8, s.n, 256) + al.state_bytes(al.AL8, s.n, 2048) if s.is_2d else 8 * s.n
+               for s in sh)
+    assert round(ours / MiB, 1) == 2119.2  # AdamW UF8 + AL8, B_V 2048
+    for B, want in ((256, 1.2), (2048, 1.3)):
+        af = sum(al.state_bytes(al.AL8, s.rows, B) + al.state_bytes(al.AL8, s.cols, B) if s.is_2d else 4 * s.n
+                 for s in sh)
+        assert round(af / MiB, 1) == want  # Adafactor AL8 factored
+    assert round(sum(4 * (s.rows + s.cols) if s.is_2d else 4 * s.n for s in sh) / MiB, 1) == 3.6  # HF
+
+    def came(vc, cc):
+        tot = 0
+        for s in sh:
+            if s.is_2d:
+                tot += al.state_bytes(al.UF8, s.n, 256)
+                for L in (s.rows, s.cols):
+                    tot += al.state_bytes(vc, L, 2048) + al.state_bytes(cc, L, 2048)
+            else:
+                tot += 8 * s.n
+        return round(tot / MiB, 1)
+
+    assert came(al.AL8, al.AL8) == 1068.0
+    assert came(al.AL8, al.FP32) == 1070.3
+    assert came(al.AL16, al.AL16) == 1069.8
+    cf = sum(4 * s.n + 8 * (s.rows + s.cols) if s.is_2d else 8 * s.n for s in sh)
+    assert round(cf / MiB, 1) == 4203.2  # CAME FP32
+
+
+def test_storage_queries_reject_bad_arguments():
+    assert al.code_bytes(al.AL8, -1, 256) == -1
+    assert al.code_bytes(al.AL8, 10, 100) == -1
+    assert al.code_bytes(9, 10, 256) == -1
+    assert al.code_bytes(al.FP32, 10, 0) == 40
+    assert al.meta_floats(al.UF8, 257, 256) == 2
+    assert al.code_bytes(al.AL16, 257, 256) == 1024
+
+
+# ----------------------------------------------------------------- validation before any HIP call
+def _status(fn):
+    with pytest.raises(al.ALError) as ei:
+        fn()
+    return ei.value.status
+
+
+def _q(codec=al.AL8, x=A, n=1000, block=256, lf=-53.0, codes=A, meta=A):
+    al.check(al.lib().al_quantize(codec, x, n, block, lf, codes, meta, None))
+
+
+def test_quantize_validation():
+    assert _status(lambda: _q(codec=al.FP32)) == 1
+    assert _status(lambda: _q(codec=7)) == 1
+    assert _status(lambda: _q(n=-1)) == 1
+    assert _status(lambda: _q(block=100)) == 1
+    assert _status(lambda: _q(block=32)) == 1
+    assert _status(lambda: _q(lf=math.inf)) == 1
+    assert _status(lambda: _q(x=None)) == 1
+    assert _status(lambda: _q(x=A + 4)) == 2
+    assert _status(lambda: _q(meta=A + 8)) == 2
+    _q(n=0)  # empty input is a no-op, no HIP call
+    assert "block" in al.lib().al_last_error().decode() or al.lib().al_last_error().decode() == ""
+
+
+def test_dequantize_validation():
+    L = al.lib()
+    assert _status(lambda: al.check(L.al_dequantize(al.FP32, A, A, 10, 256, A, None))) == 1
+    assert _status(lambda: al.check(L.al_dequantize(al.AL8, A, A, 10, 48, A, None))) == 1
+    assert _status(lambda: al.check(L.al_dequantize(al.AL8, None, A, 10, 256, A, None))) == 1
+    assert _status(lambda: al.check(L.al_dequantize(al.AL8, A, A, 10, 256, A + 2, None))) == 2
+    al.check(L.al_dequantize(al.AL8, None, None, 0, 256, None, None))
+
+
+def _adamw(ts, cfg=None, step=1, nt=None):
+    arr = (al.Tensor * max(len(ts), 1))(*ts)
+    cfg = cfg or al.adamw_cfg()
+    al.check(al.lib().al_adamw_step(arr, len(ts) if nt is None else nt, ctypes.byref(cfg), step, None))
+
+
+def _t(**kw):
+    base = dict(param=A, grad=A, rows=4, cols=256, m=A, m_meta=A, v=A, v_meta=A)
+    base.update(kw)
+    return al.Tensor(**base)
+
+
+def test_adamw_validation():
+    assert _status(lambda: _adamw([_t()], step=0)) == 1
+    assert _status(lambda: _adamw([_t()], nt=-1)) == 1
+    assert _status(lambda: _adamw([_t(rows=-1)])) == 1
+    assert _status(lambda: _adamw([_t(param=None)])) == 1
+    assert _status(lambda: _adamw([_t(v_meta=None)])) == 1
+    assert _status(lambda: _adamw([_t(m=A + 1)])) == 2
+    assert _status(lambda: _adamw([_t(vr=A)])) == 1  # factored slot on the dense path
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(beta1=1.0))) == 1
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(lr=math.nan))) == 1
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(m=al.Spec(al.AL8, 256)))) == 1
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(v=al.Spec(al.UF8, 256)))) == 1
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(v=al.Spec(al.AL8, 96)))) == 1
+    assert _status(lambda: _adamw([_t()], cfg=al.adamw_cfg(m=al.Spec(al.UF8, 128)))) == 4
+    cfg = al.adamw_cfg()
+    cfg.grad_dtype = 5
+    assert _status(lambda: _adamw([_t()], cfg=cfg)) == 1
+    # FP32 states need no metadata; empty tensors and empty lists enqueue nothing
+    _adamw([_t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None)])
+    _adamw([])
+    assert "NULL" not in al.lib().al_last_error().decode()
