@@ -212,6 +212,23 @@ al_status al_adafactor_step(const al_tensor* tensors, int32_t nt, const al_adafa
 al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg,
                        int64_t step, void* ws, size_t ws_bytes, void* stream);
 
+/* Diagnostic: evaluate, elementwise on the device, a math primitive the
+ * codes rely on, so tests can bound it against the host: fn 0 = hardware
+ * fp32 log2 of (float)x (the fast code position uses it on mantissas in
+ * [1/2, 1)), 1 = the binary64 exp2 used by decoding, 2 = binary64 log2 (block
+ * endpoints and near-boundary positions), 3 = binary64 sqrt, 4 = 1/sqrt(x)
+ * (factored second-moment reconstruction). x, out: n doubles (device). */
+al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
+
+/* Diagnostic: the streaming ceiling of the fused AdamW access pattern. Reads
+ * p (n fp32), g (n bf16), m and v (n bytes each) and writes p, m, v with no
+ * optimizer arithmetic (the values written are meaningless), using the same
+ * lane mapping as al_adamw_step (2048-element chunks); nontemporal != 0
+ * uses non-temporal loads and stores. n must be a multiple of 2048. Timing it gives the achievable HBM
+ * bandwidth for the step's exact byte mix. */
+al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n,
+                         void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -67,7 +67,8 @@ _lib = None
 # every symbol include/al.h and include/al_synth.h declare
 EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al_state_bytes", "al_quantize",
            "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
-           "al_adafactor_step", "al_came_step", "al_synth_normal")
+           "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream",
+           "al_synth_normal")
 
 
 def lib():
@@ -95,8 +96,11 @@ def lib():
         L.al_adafactor_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdafactorCfg), i64, vp, sz, vp]
         L.al_came_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(CAMECfg), i64, vp, sz, vp]
         L.al_synth_normal.argtypes = [vp, i32, i64, u64, f, u64, u64, vp]
+        L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
+        L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
         for name in ("al_quantize", "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes",
-                     "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_synth_normal"):
+                     "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream",
+           "al_synth_normal"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -171,6 +175,14 @@ def quantize(codec: int, x, block: int, log_floor: float, codes, meta, stream=No
 
 def dequantize(codec: int, codes, meta, n: int, block: int, out, stream=None) -> None:
     check(lib().al_dequantize(codec, _ptr(codes), _ptr(meta), n, block, _ptr(out), _stream(stream)))
+
+
+def diag_math(fn: int, x, out, stream=None) -> None:
+    check(lib().al_diag_math(fn, _ptr(x), x.numel(), _ptr(out), _stream(stream)))
+
+
+def diag_stream(nontemporal: bool, p, g, m, v, stream=None) -> None:
+    check(lib().al_diag_stream(int(nontemporal), _ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), _stream(stream)))
 
 
 def synth_normal(out, key: int, sigma: float, mask_key: int = 0, mask_frac: float = 0.0, stream=None) -> None:

@@ -7,229 +7,448 @@
 // corrections; codes per section 4 (Eq. al_bounds, al_quant, al_dequant,
 // exact_zero) and the uniform signed momentum code of section 4.3.
 //
-// Work decomposition: a tile is max(B_V, 256) consecutive elements of one
-// tensor; a wavefront owns a tile at a time (4 elements per lane per
-// 256-element sub-tile), so every block reduction stays inside the
-// wavefront (DPP / swizzle / readlane) and each element is read once and
-// written once. Waves stride over the launch's tiles; the tile -> tensor
-// map is a binary search over the descriptor table in the kernel arguments.
+// Work decomposition. A chunk is max(1024, B_V) consecutive elements of one
+// tensor, owned by one wavefront: 4 consecutive elements per lane in each of
+// K = chunk/256 sub-tiles, so every load and store is a coalesced 16/8/4-byte
+// access and every block reduction stays inside the wavefront (DPP, swizzle,
+// readlane). The momentum block (256) is one sub-tile and is encoded as soon
+// as that sub-tile's moments are computed; the second moment is held in
+// registers until its block is complete. Per-block scalar work of the second
+// moment (the binary64 divisions and endpoint logarithms of up to 16 blocks)
+// runs once per chunk with one block per lane, and the results are broadcast
+// back (readlane for blocks that span whole sub-tiles, ds_bpermute for
+// smaller ones). Waves stride over the launch's chunks; the
+// chunk -> tensor map is a binary search over the descriptor table held in
+// the kernel arguments.
 #include "al_device.hpp"
 #include "al_internal.hpp"
 
 namespace al {
 
+template <int MC, int VC, int BV>
+struct Geo {
+    static constexpr bool VQ = (VC == AL8 || VC == AL16);
+    static constexpr int C = (VQ && BV > 1024) ? BV : 1024;  // elements per chunk
+    static constexpr int K = C / kSub;                       // sub-tiles per chunk
+    static constexpr int NB = VQ ? C / BV : 1;               // v blocks per chunk
+    static constexpr int GL = BV < kSub ? BV / 4 : 64;       // lanes per v block within a sub-tile
+    static constexpr int PER = kSub / BV > 0 ? kSub / BV : 1;  // v blocks per sub-tile (BV < 256)
+    static constexpr int LEVELS = VQ ? levels_of<VC>() : 1;
+    static constexpr int NSLOT = BV < kSub ? K : NB;         // in-lane min/max slots
+    static constexpr bool LUT = (VC == AL8) && BV >= 512;     // decode through an LDS level table
+};
+
+template <bool C_, class A, class B>
+struct Pick {
+    using T = A;
+};
+template <class A, class B>
+struct Pick<false, A, B> {
+    using T = B;
+};
+
+__device__ __forceinline__ float f4_at(const float4& v, int j) {
+    return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
+// Raw inputs of up to 4 sub-tiles as loaded from HBM (packed: a bf16 pair or
+// four 8-bit codes per register).
+template <int G, int MC, int VC, int BV>
+struct Raw {
+    using Q = Geo<MC, VC, BV>;
+    using GT = typename Pick<G == G_BF16, uint2, float4>::T;
+    using MT = typename Pick<MC == UF8, uint32_t, float4>::T;
+    using VT = typename Pick<VC == AL16, uint2, typename Pick<VC == AL8, uint32_t, float4>::T>::T;
+    static constexpr int P = Q::K < 4 ? Q::K : 4;  // sub-tiles per load phase
+    float4 p[P];
+    GT g[P];
+    MT m[P];
+    VT v[P];
+};
+
+// Old block metadata, one block per lane: lanes [0, K) hold the momentum
+// scales of the K sub-tiles, lanes [32, 32 + NB) the {l_min, delta} of the NB
+// second-moment blocks.
+struct OldMeta {
+    float a;  // momentum absmax (lanes < K) or v delta (lanes 32..)
+    float l;  // v l_min (lanes 32..)
+};
+
 template <int G, int MC, int VC, int BV, bool FULL>
-__device__ __forceinline__ void adamw_tile(const AdamWLaunch& a, const AdamWDesc& d, int64_t e0,
-                                           int64_t valid, int lane) {
-    constexpr int T = BV > kSub ? BV : kSub;
-    constexpr int K = T / kSub;
-    constexpr bool VQ = (VC == AL8 || VC == AL16);
-    constexpr int LEVELS = levels_of<VC>();
-
-    float vkeep[K][4];
-    uint32_t vmin = 0xFFFFFFFFu, vmax = 0u;
-
-    // second-moment metadata of the block(s) this lane decodes
-    double v_lmin32 = 0.0, v_step = 0.0;
-    if constexpr (VQ) {
-        const int64_t vb = (e0 + (BV < kSub ? 4 * lane : 0)) / BV;
-        const bool vb_live = FULL || (BV < kSub ? (4 * lane < valid) : true);
-        if (vb_live) {
-            float2 mm = *reinterpret_cast<const float2*>(d.vm + 2 * vb);
-            v_lmin32 = (double)mm.x;
-            v_step = (double)mm.y / (double)LEVELS;
-        }
-    }
-
+__device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc& d, int64_t e0, int64_t valid,
+                                         int lane, int ph) {
+    using R = Raw<G, MC, VC, BV>;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {
-        const int rel = k * kSub + 4 * lane;  // offset of this lane's first element in the tile
+    for (int k = 0; k < R::P; ++k) {
+        const int rel = (ph * R::P + k) * kSub + 4 * lane;
         const int64_t e = e0 + rel;
-        const bool sub_live = FULL || (k * kSub < valid);
-
-        // ---------------- loads
-        F4 p, g, mh, vh;
         if constexpr (FULL) {
-            p = load_f4(d.p + e);
-            g = load_grad4<G>(d.g, e);
+            r.p[k] = *reinterpret_cast<const float4*>(d.p + e);
+            if constexpr (G == G_BF16)
+                r.g[k] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.g) + e);
+            else
+                r.g[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.g) + e);
+            if constexpr (MC == UF8)
+                r.m[k] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+            else
+                r.m[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
+            if constexpr (VC == AL16)
+                r.v[k] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.v) + e);
+            else if constexpr (VC == AL8)
+                r.v[k] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.v) + e);
+            else
+                r.v[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.v) + e);
         } else {
+            float pp[4];
+            uint32_t gb[4], mb[4], vb[4];
+            float gf[4], mf[4], vf[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const bool ok = rel + j < valid;
-                p.v[j] = ok ? d.p[e + j] : 0.0f;
-                g.v[j] = ok ? load_grad1<G>(d.g, e + j) : 0.0f;
+                pp[j] = ok ? d.p[e + j] : 0.0f;
+                if constexpr (G == G_BF16) gb[j] = ok ? reinterpret_cast<const uint16_t*>(d.g)[e + j] : 0u;
+                else gf[j] = ok ? reinterpret_cast<const float*>(d.g)[e + j] : 0.0f;
+                if constexpr (MC == UF8) mb[j] = ok ? reinterpret_cast<const uint8_t*>(d.m)[e + j] : 0u;
+                else mf[j] = ok ? reinterpret_cast<const float*>(d.m)[e + j] : 0.0f;
+                if constexpr (VC == AL16) vb[j] = ok ? reinterpret_cast<const uint16_t*>(d.v)[e + j] : 0u;
+                else if constexpr (VC == AL8) vb[j] = ok ? reinterpret_cast<const uint8_t*>(d.v)[e + j] : 0u;
+                else vf[j] = ok ? reinterpret_cast<const float*>(d.v)[e + j] : 0.0f;
             }
-        }
-        // momentum decode
-        if constexpr (MC == UF8) {
-            const double m_step = sub_live ? (double)d.ms[(e0 + k * kSub) / kSub] / 127.0 : 0.0;
-            uint32_t q[4];
-            if constexpr (FULL) {
-                load_codes4<UF8>(d.m, e, q);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) q[j] = (rel + j < valid) ? load_code1<UF8>(d.m, e + j) : 0u;
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) mh.v[j] = uf8_decode((int32_t)(int8_t)(uint8_t)q[j], m_step);
-        } else {
-            if constexpr (FULL) {
-                mh = load_f4(reinterpret_cast<const float*>(d.m) + e);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    mh.v[j] = (rel + j < valid) ? reinterpret_cast<const float*>(d.m)[e + j] : 0.0f;
-            }
-        }
-        // second-moment decode
-        if constexpr (VQ) {
-            uint32_t q[4];
-            if constexpr (FULL) {
-                load_codes4<VC>(d.v, e, q);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) q[j] = (rel + j < valid) ? load_code1<VC>(d.v, e + j) : 0u;
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) vh.v[j] = al_decode(q[j], v_lmin32, v_step);
-        } else {
-            if constexpr (FULL) {
-                vh = load_f4(reinterpret_cast<const float*>(d.v) + e);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    vh.v[j] = (rel + j < valid) ? reinterpret_cast<const float*>(d.v)[e + j] : 0.0f;
-            }
-        }
-
-        // ---------------- moments (binary64, rounded once to fp32) and parameter (fp32)
-        F4 mn, vn;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const double gd = (double)g.v[j];
-            mn.v[j] = (float)(a.beta1 * (double)mh.v[j] + a.omb1 * gd);
-            vn.v[j] = (float)(a.beta2 * (double)vh.v[j] + a.omb2 * (gd * gd));
-            float pn = p.v[j] * a.decay;
-            const float den = __builtin_amdgcn_sqrtf(vn.v[j]) * a.inv_sqrt_bc2 + a.eps;
-            pn = pn - a.step_size * mn.v[j] * __builtin_amdgcn_rcpf(den);
-            p.v[j] = pn;
-        }
-        if constexpr (!FULL) {
-            // elements past the end are absent: no state, no contribution to reductions
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (rel + j >= valid) mn.v[j] = vn.v[j] = 0.0f;
-        }
-        if constexpr (FULL) {
-            store_f4(d.p + e, p);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (rel + j < valid) d.p[e + j] = p.v[j];
-        }
-
-        // ---------------- momentum encode (block = this 256-element sub-tile)
-        if constexpr (MC == UF8) {
-            uint32_t am = abs_bits(mn.v[0]);
-#pragma unroll
-            for (int j = 1; j < 4; ++j) am = OpMax::f(am, abs_bits(mn.v[j]));
-            am = group_reduce<OpMax, 64>(am);
-            const float s = u2f(am);
-            const double r = am != 0u ? 127.0 / (double)s : 0.0;
-            uint32_t q[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = (uint32_t)uf8_encode(mn.v[j], r) & 0xFFu;
-            if (sub_live) {
-                store_codes4<UF8>(d.m, e, q);
-                if (lane == 0) d.ms[(e0 + k * kSub) / kSub] = s;
-            }
-        } else {
-            if constexpr (FULL) {
-                store_f4(reinterpret_cast<float*>(d.m) + e, mn);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (rel + j < valid) reinterpret_cast<float*>(d.m)[e + j] = mn.v[j];
-            }
-        }
-
-        // ---------------- second moment: keep for the block encode
-        if constexpr (VQ) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                vkeep[k][j] = vn.v[j];
-                vmin = OpMin::f(vmin, pos_min_key(vn.v[j]));
-                vmax = OpMax::f(vmax, pos_max_key(vn.v[j]));
-            }
-        } else {
-            if constexpr (FULL) {
-                store_f4(reinterpret_cast<float*>(d.v) + e, vn);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (rel + j < valid) reinterpret_cast<float*>(d.v)[e + j] = vn.v[j];
-            }
-        }
-    }
-
-    // ---------------- second-moment block fit and encode
-    if constexpr (VQ) {
-        constexpr int GL = BV < kSub ? BV / 4 : 64;  // lanes per block
-        vmin = group_reduce<OpMin, GL>(vmin);
-        vmax = group_reduce<OpMax, GL>(vmax);
-        const ALFit f = al_fit(vmin, vmax, a.v_floor);
-        const int64_t vb = (e0 + (BV < kSub ? 4 * lane : 0)) / BV;
-        const bool leader = (BV < kSub) ? ((lane % GL) == 0) : (lane == 0);
-        const bool blk_live = FULL || (BV < kSub ? (4 * (lane - lane % GL) < valid) : true);
-        if (leader && blk_live) {
-            float2 mm = make_float2(f.any ? (float)f.lmin : 0.0f, f.any ? (float)f.delta : 0.0f);
-            *reinterpret_cast<float2*>(d.vm + 2 * vb) = mm;
-        }
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            uint32_t q[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = al_encode<LEVELS>(vkeep[k][j], f);
-            if (blk_live) store_codes4<VC>(d.v, e0 + k * kSub + 4 * lane, q);
+            r.p[k] = make_float4(pp[0], pp[1], pp[2], pp[3]);
+            if constexpr (G == G_BF16) r.g[k] = make_uint2(gb[0] | (gb[1] << 16), gb[2] | (gb[3] << 16));
+            else r.g[k] = make_float4(gf[0], gf[1], gf[2], gf[3]);
+            if constexpr (MC == UF8) r.m[k] = mb[0] | (mb[1] << 8) | (mb[2] << 16) | (mb[3] << 24);
+            else r.m[k] = make_float4(mf[0], mf[1], mf[2], mf[3]);
+            if constexpr (VC == AL16) r.v[k] = make_uint2(vb[0] | (vb[1] << 16), vb[2] | (vb[3] << 16));
+            else if constexpr (VC == AL8) r.v[k] = vb[0] | (vb[1] << 8) | (vb[2] << 16) | (vb[3] << 24);
+            else r.v[k] = make_float4(vf[0], vf[1], vf[2], vf[3]);
         }
     }
 }
 
+template <int MC, int VC, int BV, bool FULL>
+__device__ __forceinline__ OldMeta load_meta(const AdamWDesc& d, int64_t e0, int64_t valid, int lane) {
+    using Q = Geo<MC, VC, BV>;
+    OldMeta r;
+    r.a = 0.0f;
+    r.l = 0.0f;
+    if constexpr (MC == UF8) {
+        if (lane < Q::K && (FULL || lane * kSub < valid)) r.a = d.ms[e0 / kSub + lane];
+    }
+    if constexpr (Q::VQ) {
+        const int b = lane - 32;
+        if (b >= 0 && b < Q::NB && (FULL || (int64_t)b * BV < valid)) {
+            const float2 mm = *reinterpret_cast<const float2*>(d.vm + 2 * (e0 / BV + b));
+            r.l = mm.x;
+            r.a = mm.y;
+        }
+    }
+    return r;
+}
+
+template <int G>
+__device__ __forceinline__ float grad_at(const typename Pick<G == G_BF16, uint2, float4>::T& w, int j) {
+    if constexpr (G == G_BF16)
+        return bf16_to_f32(((j < 2 ? w.x : w.y) >> (16 * (j & 1))) & 0xFFFFu);
+    else
+        return f4_at(w, j);
+}
+
+template <int G, int MC, int VC, int BV, bool FULL>
+__device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWDesc& d, int64_t e0, int64_t valid,
+                                              int lane, float* lut) {
+    using Q = Geo<MC, VC, BV>;
+    constexpr int K = Q::K;
+    constexpr int NB = Q::NB;
+    constexpr bool VQ = Q::VQ;
+    constexpr int LEVELS = Q::LEVELS;
+
+    using R = Raw<G, MC, VC, BV>;
+    // first load phase and the old metadata are issued before any arithmetic
+    R r;
+    load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, 0);
+    const OldMeta om = load_meta<MC, VC, BV, FULL>(d, e0, valid, lane);
+
+    // ------------------------------------------------ 1. decode steps of the old metadata, one block per lane
+    double num = 1.0, den = 1.0;
+    if constexpr (MC == UF8) {
+        if (lane < K) {
+            num = (double)om.a;
+            den = 127.0;
+        }
+    }
+    if constexpr (VQ) {
+        if (lane >= 32 && lane < 32 + NB) {
+            num = (double)om.a;
+            den = (double)LEVELS;
+        }
+    }
+    const double q1 = num / den;  // UF8: absmax / 127; AL: delta / (L - 2)
+
+    // Blocks of 512+ elements: decode through a per-block table of the 255
+    // positive levels fl32(2^(l_min + k step)), k = 0..254, built in this
+    // wavefront's LDS slice (4 levels per lane) -- 255 evaluations per block
+    // instead of one per element. LDS traffic of one wavefront is ordered, so
+    // no barrier is needed between building and reading its own table.
+    if constexpr (Q::LUT) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const double st = readlane_d(q1, 32 + b);
+            const double l32 = (double)u2f(readlane_u(f2u(om.l), 32 + b));
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int k = lane + 64 * i;
+                if (k < LEVELS + 1) lut[b * 256 + k] = (float)exp2_d(l32 + (double)k * st, a.cf);
+            }
+        }
+    }
+
+    // ------------------------------------------------ 2. per sub-tile: decode, moments, parameter, momentum code
+    float vk[K][4];
+    uint32_t vmn[Q::NSLOT], vmx[Q::NSLOT];
+#pragma unroll
+    for (int s = 0; s < Q::NSLOT; ++s) {
+        vmn[s] = 0xFFFFFFFFu;
+        vmx[s] = 0u;
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int rel = k * kSub + 4 * lane;
+        const int64_t e = e0 + rel;
+        const int kk = k % R::P;  // slot of this sub-tile in the current load phase
+        if (k > 0 && kk == 0) load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, k / R::P);
+        float mh[4], vh[4], mn[4], vn[4], pn[4];
+        if constexpr (MC == UF8) {
+            const double mstep = readlane_d(q1, k);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(r.m[kk] >> (8 * j)), mstep);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) mh[j] = f4_at(r.m[kk], j);
+        }
+        if constexpr (Q::LUT) {
+            const float* t = lut + (k * kSub / BV) * 256;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
+                const float lv = t[q == 0u ? 0u : q - 1u];
+                vh[j] = q == 0u ? 0.0f : lv;
+            }
+        } else if constexpr (VQ) {
+            double vstep, vl32;
+            if constexpr (BV >= kSub) {
+                const int b = k * kSub / BV;
+                vstep = readlane_d(q1, 32 + b);
+                vl32 = (double)u2f(readlane_u(f2u(om.l), 32 + b));
+            } else {
+                const int src = 32 + (k * kSub + 4 * lane) / BV;
+                vstep = shfl_d(q1, src);
+                vl32 = (double)__shfl(om.l, src);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                uint32_t q;
+                if constexpr (VC == AL16)
+                    q = ((j < 2 ? r.v[kk].x : r.v[kk].y) >> (16 * (j & 1))) & 0xFFFFu;
+                else
+                    q = (r.v[kk] >> (8 * j)) & 0xFFu;
+                vh[j] = al_decode_fast(q, vl32, vstep, a.cf);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) vh[j] = f4_at(r.v[kk], j);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const double gd = (double)grad_at<G>(r.g[kk], j);
+            mn[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * gd);
+            vn[j] = (float)(a.beta2 * (double)vh[j] + a.omb2 * (gd * gd));
+            const float den_p = __builtin_fmaf(__builtin_amdgcn_sqrtf(vn[j]), a.inv_sqrt_bc2, a.eps);
+            const float upd = mn[j] * __builtin_amdgcn_rcpf(den_p);
+            pn[j] = __builtin_fmaf(-a.step_size, upd, f4_at(r.p[kk], j) * a.decay);
+        }
+        if constexpr (!FULL) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (rel + j >= valid) mn[j] = vn[j] = 0.0f;  // absent: no state, no reduction input
+        }
+        if constexpr (FULL) {
+            *reinterpret_cast<float4*>(d.p + e) = make_float4(pn[0], pn[1], pn[2], pn[3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (rel + j < valid) d.p[e + j] = pn[j];
+        }
+        // momentum: the UF8 block is this sub-tile
+        if constexpr (MC == UF8) {
+            uint32_t am = abs_bits(mn[0]);
+#pragma unroll
+            for (int j = 1; j < 4; ++j) am = OpMax::f(am, abs_bits(mn[j]));
+            am = group_reduce<OpMax, 64>(am);
+            const double rr = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+            uint32_t q[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mn[j] * rr) & 0xFFu;
+            if (FULL || k * kSub < valid) {
+                store_codes4<UF8>(d.m, e, q);
+                if (lane == 0) d.ms[e0 / kSub + k] = u2f(am);
+            }
+        } else if constexpr (FULL) {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.m) + e) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (rel + j < valid) reinterpret_cast<float*>(d.m)[e + j] = mn[j];
+        }
+        if constexpr (VQ) {
+            const int s = BV < kSub ? k : k * kSub / BV;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                vk[k][j] = vn[j];
+                vmn[s] = OpMin::f(vmn[s], pos_min_key(vn[j]));
+                vmx[s] = OpMax::f(vmx[s], pos_max_key(vn[j]));
+            }
+        } else if constexpr (FULL) {
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.v) + e) = make_float4(vn[0], vn[1], vn[2], vn[3]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (rel + j < valid) reinterpret_cast<float*>(d.v)[e + j] = vn[j];
+        }
+    }
+    if constexpr (VQ) {
+        // -------------------------------------------- 3. second-moment block reductions
+#pragma unroll
+        for (int s = 0; s < Q::NSLOT; ++s) {
+            vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]);
+            vmx[s] = group_reduce<OpMax, Q::GL>(vmx[s]);
+        }
+
+        // -------------------------------------------- 4. block fits, one block per lane pair
+        // lanes 2b, 2b+1 hold block b's min / max key; both compute its interval.
+        uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+        const int b = lane >> 1;
+        if constexpr (BV >= kSub) {
+#pragma unroll
+            for (int s = 0; s < NB; ++s) {
+                kmin = (b == s) ? vmn[s] : kmin;
+                kmax = (b == s) ? vmx[s] : kmax;
+            }
+        } else {
+            // block b of the chunk = sub-tile b / PER, lane group b % PER (leader lane (b % PER) * GL)
+            const int src = (b % Q::PER) * Q::GL;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                const uint32_t tmn = (uint32_t)__shfl((int)vmn[k], src);
+                const uint32_t tmx = (uint32_t)__shfl((int)vmx[k], src);
+                kmin = (b / Q::PER == k) ? tmn : kmin;
+                kmax = (b / Q::PER == k) ? tmx : kmax;
+            }
+        }
+        const bool any = kmax != 0u && b < NB;
+        const uint32_t key = (lane & 1) ? kmax : kmin;
+        const double lg = log2((double)(any ? u2f(key) : 1.0f));
+        const double lg_other = __shfl_xor(lg, 1);
+        const double lo = (lane & 1) ? lg_other : lg;
+        const double hi = (lane & 1) ? lg : lg_other;
+        const double l0 = lo > (double)a.v_floor ? lo : (double)a.v_floor;
+        double l1 = hi < 126.0 ? hi : 126.0;
+        if (kmin == kmax) l1 = l0 + 1.0;
+        double dl = l1 - l0;
+        dl = dl < 1e-12 ? 1e-12 : dl;
+        if ((lane & 1) == 0 && b < NB && (FULL || (int64_t)b * BV < valid)) {
+            const float2 mm = any ? make_float2((float)l0, (float)dl) : make_float2(0.0f, 0.0f);
+            *reinterpret_cast<float2*>(d.vm + 2 * (e0 / BV + b)) = mm;
+        }
+        const double q2 = any ? (double)LEVELS / dl : 1.0;  // (L - 2) / delta
+
+        // -------------------------------------------- 5. second-moment codes
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int64_t e = e0 + k * kSub + 4 * lane;
+            ALEnc enc;
+            bool live;
+            if constexpr (BV >= kSub) {
+                const int bb = k * kSub / BV;
+                enc = al_enc_params(readlane_d(l0, 2 * bb), readlane_d(q2, 2 * bb));
+                live = FULL || (int64_t)bb * BV < valid;
+            } else {
+                const int bb = (k * kSub + 4 * lane) / BV;
+                enc = al_enc_params(shfl_d(l0, 2 * bb), shfl_d(q2, 2 * bb));
+                live = FULL || (int64_t)bb * BV < valid;
+            }
+            uint32_t q[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) q[j] = al_encode_fast<LEVELS>(vk[k][j], enc);
+            if (live) store_codes4<VC>(d.v, e, q);
+        }
+    }
+}
+
+#ifndef AL_ADAMW_WAVES_PER_EU
+#define AL_ADAMW_WAVES_PER_EU 2
+#endif
+
+// largest ti with t[ti].tile_begin <= chunk
+__device__ __forceinline__ int locate(const AdamWLaunch& a, int64_t chunk) {
+    int lo = 0, hi = a.nt - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.t[mid].tile_begin <= chunk)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// Waves stride over the launch's chunks; each wave issues the loads of up to 4
+// sub-tiles (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it
+// computes on them. A chunk that ends a tensor takes the guarded path.
 template <int G, int MC, int VC, int BV>
-__global__ __launch_bounds__(256) void adamw_kernel(const AdamWLaunch a) {
-    constexpr int T = BV > kSub ? BV : kSub;
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(AL_ADAMW_WAVES_PER_EU)))
+void adamw_kernel(const AdamWLaunch a) {
+    constexpr int C = Geo<MC, VC, BV>::C;
     const int lane = threadIdx.x & 63;
     const int64_t wpb = blockDim.x >> 6;
     const int64_t wave = (int64_t)blockIdx.x * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t nwaves = (int64_t)gridDim.x * wpb;
-    for (int64_t tile = wave; tile < a.total_tiles; tile += nwaves) {
-        // largest ti with t[ti].tile_begin <= tile
-        int lo = 0, hi = a.nt - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (a.t[mid].tile_begin <= tile)
-                lo = mid;
-            else
-                hi = mid - 1;
-        }
-        const AdamWDesc& d = a.t[lo];
-        const int64_t e0 = (tile - d.tile_begin) * T;
+    constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
+    __shared__ float lut_all[4][NT];
+    float* lut = lut_all[threadIdx.x >> 6];
+    for (int64_t chunk = wave; chunk < a.total_tiles; chunk += nwaves) {
+        const AdamWDesc& d = a.t[locate(a, chunk)];
+        const int64_t e0 = (chunk - d.tile_begin) * C;
         const int64_t valid = d.n - e0;
-        if (valid >= T)
-            adamw_tile<G, MC, VC, BV, true>(a, d, e0, T, lane);
+        if (valid >= C)
+            adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut);
         else
-            adamw_tile<G, MC, VC, BV, false>(a, d, e0, valid, lane);
+            adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut);
     }
 }
 
 int adamw_tile_elems(int v_codec, int v_block) {
-    if (v_codec == FP32) return kSub;
-    return v_block > kSub ? v_block : kSub;
+    if (v_codec == FP32) return Geo<UF8, FP32, 256>::C;
+    return v_block > 1024 ? v_block : 1024;
 }
 
+// Persistent grid: exactly as many workgroups as can be resident at once
+// (occupancy of this instantiation x compute units), capped by the work.
 template <int G, int MC, int VC, int BV>
-static hipError_t launch_t(const AdamWLaunch& a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3(grid), dim3(256), 0, s, a);
+static hipError_t launch_t(const AdamWLaunch& a, int grid_cap, hipStream_t s) {
+    static int per_cu = 0;
+    if (per_cu == 0) {
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, adamw_kernel<G, MC, VC, BV>, 256, 0) != hipSuccess ||
+            n <= 0)
+            n = 2;
+        per_cu = n;
+    }
+    const int64_t want = (a.total_tiles + 3) / 4;
+    int64_t grid = (int64_t)per_cu * device_cu_count();
+    if (grid > want) grid = want;
+    if (grid > grid_cap) grid = grid_cap;
+    hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3((unsigned)grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

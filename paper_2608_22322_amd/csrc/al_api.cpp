@@ -208,15 +208,14 @@ al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg
     a.eps = (float)cfg->eps;
     a.decay = (float)(1.0 - cfg->lr * cfg->weight_decay);
     a.v_floor = cfg->v.log_floor;
+    a.cf = al::exp2_coef();
     const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
-    const int grid_cap = al::device_cu_count() * 8;
+    const int grid_cap = al::device_cu_count() * 16;
     hipStream_t s = as_stream(stream);
 
     auto flush = [&]() -> al_status {
         if (a.nt == 0) return AL_OK;
-        const int64_t want = (a.total_tiles + 3) / 4;
-        const int grid = (int)(want < grid_cap ? want : grid_cap);
-        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, grid, s);
+        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, grid_cap, s);
         a.nt = 0;
         a.total_tiles = 0;
         return e == hipSuccess ? AL_OK : hip_fail(e, "al_adamw_step launch");
@@ -238,6 +237,29 @@ al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg
             if ((st = flush()) != AL_OK) return st;
     }
     return flush();
+}
+
+al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream) {
+    g_err[0] = 0;
+    if (fn < 0 || fn > 4) return fail(AL_EINVAL, "al_diag_math: fn %d", fn);
+    if (n < 0) return fail(AL_EINVAL, "al_diag_math: n < 0");
+    if (n == 0) return AL_OK;
+    if (!x || !out) return fail(AL_EINVAL, "al_diag_math: NULL buffer");
+    if (!aligned16(x) || !aligned16(out)) return fail(AL_EALIGN, "al_diag_math: alignment");
+    hipError_t e = al::launch_diag_math(fn, x, n, out, al::device_cu_count() * 8, as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_math launch");
+}
+
+al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n, void* stream) {
+    g_err[0] = 0;
+    if (n < 0 || n % 2048 != 0) return fail(AL_EINVAL, "al_diag_stream: n must be a non-negative multiple of 2048");
+    if (n == 0) return AL_OK;
+    if (!p || !g || !m || !v) return fail(AL_EINVAL, "al_diag_stream: NULL buffer");
+    if (!aligned16(p) || !aligned16(g) || !aligned16(m) || !aligned16(v))
+        return fail(AL_EALIGN, "al_diag_stream: alignment");
+    hipError_t e = al::launch_diag_stream(nontemporal != 0, p, static_cast<const uint16_t*>(g),
+                                          static_cast<uint8_t*>(m), static_cast<uint8_t*>(v), n, as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_stream launch");
 }
 
 al_status al_synth_normal(void* out, int32_t out_dtype, int64_t n, uint64_t key, float scale, uint64_t mask_key,

@@ -115,6 +115,95 @@ __device__ __forceinline__ float al_decode(uint32_t q, double lmin32, double ste
     return (float)exp2(e);
 }
 
+// ------------------------------------------------- fast binary64 exp2 / encode
+// 2^E in binary64 for |E| < 1000: E = n + f with n = rint(E), |f| <= 1/2, and
+// 2^f = e^(f ln 2) by its Taylor series to degree 13 (coefficients
+// (ln 2)^k / k!, rounded to binary64); relative error <= 1.4e-16 over the
+// range, i.e. about one ulp, so fl32 of it equals fl32 of a faithfully
+// rounded exp2 except within ~1e-16 of an fp32 rounding midpoint.
+// The coefficients travel in the kernel arguments, so they are read with
+// scalar loads and each Horner step is one v_fma_f64 with a scalar-register
+// addend (there are no 64-bit literal operands on this ISA; as immediates the
+// compiler keeps them in vector registers and copies one per step).
+struct Exp2Coef {
+    double c[14];  // (ln 2)^k / k!, k = 0..13, rounded to binary64
+};
+
+__device__ __forceinline__ double exp2_d(double E, const Exp2Coef& cf) {
+    const double n = __builtin_rint(E);
+    const double f = E - n;
+    double p = cf.c[13];
+#pragma unroll
+    for (int k = 12; k >= 0; --k) p = __builtin_fma(p, f, cf.c[k]);
+    return __builtin_amdgcn_ldexp(p, (int)n);
+}
+
+// Branch-free: code 0 evaluates level 0 and is then replaced by exact zero.
+__device__ __forceinline__ float al_decode_fast(uint32_t q, double lmin32, double step, const Exp2Coef& cf) {
+    const uint32_t k = q == 0u ? 0u : q - 1u;
+    const float v = (float)exp2_d(lmin32 + (double)k * step, cf);
+    return q == 0u ? 0.0f : v;
+}
+
+// Bound on |log2f_hw(m) - log2(m)| for m in [1/2, 1), the hardware fp32 log2
+// on a mantissa (measured exhaustively on the device by the diagnostic test,
+// which requires the measured maximum to stay below a quarter of this).
+constexpr double kLog2MantErr = 0x1p-21;
+
+// Per-block encode parameters: the binary64 interval start, LEVELS/delta,
+// and a guard band on the code position.
+struct ALEnc {
+    double lmin;
+    double inv;    // (L - 2) / delta
+    double fr;     // lmin - floor(lmin), exact
+    double guard;  // bound on |fast position - binary64 position|
+    int I;         // floor(lmin)
+};
+
+__device__ __forceinline__ ALEnc al_enc_params(double lmin, double inv) {
+    ALEnc p;
+    p.lmin = lmin;
+    p.inv = inv;
+    const double I = __builtin_floor(lmin);
+    p.I = (int)I;
+    p.fr = lmin - I;
+    p.guard = inv * kLog2MantErr + 1e-9;
+    return p;
+}
+
+// Code of x > 0 (0 for x <= 0). The position y = LEVELS * (log2 x - lmin) /
+// delta comes from x = mant * 2^ex: y = ((ex - I) + (log2f_hw(mant) - fr)) *
+// inv, whose only sizeable error is the fp32 mantissa log (kLog2MantErr); a
+// position within that guard of a rounding boundary is recomputed with the
+// binary64 log2, so the rounding decision is the binary64 one.
+template <int LEVELS>
+__device__ __forceinline__ uint32_t al_encode_fast(float x, const ALEnc& p) {
+    const float mant = __builtin_amdgcn_frexp_mantf(x);
+    const int ex = __builtin_amdgcn_frexp_expf(x);
+    const float l = __builtin_amdgcn_logf(mant);
+    const double d = (double)(ex - p.I) + ((double)l - p.fr);
+    double yc = __builtin_fmin(__builtin_fmax(d * p.inv, 0.0), (double)LEVELS);
+    double r = __builtin_rint(yc);
+    if (__builtin_fabs(yc - r) > 0.5 - p.guard) {
+        const double ys = (log2((double)x) - p.lmin) * p.inv;
+        yc = __builtin_fmin(__builtin_fmax(ys, 0.0), (double)LEVELS);
+        r = __builtin_rint(yc);
+    }
+    return x > 0.0f ? 1u + (uint32_t)r : 0u;
+}
+
+// Cross-lane moves of 64-bit values.
+__device__ __forceinline__ double shfl_d(double v, int src) { return __shfl(v, src); }
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+    const uint64_t b = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ uint32_t readlane_u(uint32_t v, int lane) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+
 // ----------------------------------------------------------------- UF8 code
 // Encode with r = 127 / absmax (binary64), y = x * r, round to nearest even,
 // clamp to [-127, 127].

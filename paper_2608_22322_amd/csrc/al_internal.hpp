@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "al_device.hpp"
+
 namespace al {
 
 // ------------------------------------------------------------------ AdamW
@@ -30,6 +32,7 @@ struct AdamWLaunch {
     float eps;
     float decay;                      // 1 - lr * weight_decay
     float v_floor;                    // l_floor of the second-moment code
+    Exp2Coef cf;                      // decode polynomial
     int32_t nt;
     int64_t total_tiles;
     AdamWDesc t[kAdamWMaxTensors];
@@ -46,9 +49,16 @@ hipError_t launch_quantize(int codec, const float* x, int64_t n, int block, floa
 hipError_t launch_dequantize(int codec, const void* codes, const float* meta, int64_t n, int block,
                              float* out, int grid_cap, hipStream_t s);
 
+hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
+                              hipStream_t s);
+hipError_t launch_diag_math(int fn, const double* x, int64_t n, double* out, int grid_cap, hipStream_t s);
+
 // ---------------------------------------------------- synthetic input fill
 hipError_t launch_synth_normal(void* out, int out_bf16, int64_t n, uint64_t key, float scale,
                                uint64_t mask_key, uint64_t mask_threshold, int grid_cap, hipStream_t s);
+
+// Taylor coefficients of the binary64 exp2 used by every decode.
+const Exp2Coef& exp2_coef();
 
 // Compute units of the current device (cached per device).
 int device_cu_count();

@@ -11,6 +11,17 @@
 
 namespace al {
 
+const Exp2Coef& exp2_coef() {
+    // (ln 2)^k / k!, the Taylor coefficients of 2^f = e^(f ln 2), in binary64
+    static const Exp2Coef c = {{1.0, 0x1.62e42fefa39efp-1, 0x1.ebfbdff82c58fp-3, 0x1.c6b08d704a0c0p-5,
+                                0x1.3b2ab6fba4e77p-7, 0x1.5d87fe78a6731p-10, 0x1.430912f86c787p-13,
+                                0x1.ffcbfc588b0c7p-17, 0x1.62c0223a5c824p-20, 0x1.b5253d395e7c4p-24,
+                                0x1.e4cf5158b8ecap-28, 0x1.e8cac7351bb25p-32, 0x1.c3bd650fc2986p-36,
+                                0x1.816193166d0f9p-40}};
+    return c;
+}
+
+
 template <int C, int B, bool FULL>
 __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, int64_t e0, int64_t valid, int lane,
                                               float log_floor, void* codes, float* meta) {
@@ -67,11 +78,12 @@ __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, int64
         if (leader && blk_live)
             *reinterpret_cast<float2*>(meta + 2 * blk) =
                 make_float2(f.any ? (float)f.lmin : 0.0f, f.any ? (float)f.delta : 0.0f);
+        const ALEnc enc = al_enc_params(f.lmin, f.any ? (double)LEVELS / f.delta : 1.0);
 #pragma unroll
         for (int k = 0; k < K; ++k) {
             uint32_t q[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = al_encode<LEVELS>(xv[k][j], f);
+            for (int j = 0; j < 4; ++j) q[j] = al_encode_fast<LEVELS>(xv[k][j], enc);
             if (blk_live) store_codes4<C>(codes, e0 + k * kSub + 4 * lane, q);
         }
     }
@@ -99,7 +111,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 template <int C, int B>
 __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict__ codes,
                                                           const float* __restrict__ meta, int64_t n,
-                                                          float* __restrict__ out) {
+                                                          float* __restrict__ out, const Exp2Coef cf) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; 4 * i < n; i += stride) {
         const int64_t e = 4 * i;
@@ -122,7 +134,7 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
             const double l32 = (double)mm.x;
             const double step = (double)mm.y / (double)levels_of<C>();
 #pragma unroll
-            for (int j = 0; j < 4; ++j) o.v[j] = al_decode(q[j], l32, step);
+            for (int j = 0; j < 4; ++j) o.v[j] = al_decode_fast(q[j], l32, step, cf);
         }
         if (full) {
             store_f4(out + e, o);
@@ -132,6 +144,107 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
                 if (e + j < n) out[e + j] = o.v[j];
         }
     }
+}
+
+// Device math primitives the codes rely on, evaluated elementwise so a test
+// can compare them with the host: 0 = hardware fp32 log2, 1 = the binary64
+// exp2 polynomial, 2 = binary64 log2, 3 = binary64 sqrt, 4 = 1 / sqrt(x).
+__global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __restrict__ x, int64_t n,
+                                                         double* __restrict__ out, const Exp2Coef cf) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const double v = x[i];
+        double r = 0.0;
+        switch (fn) {
+            case 0: r = (double)__builtin_amdgcn_logf((float)v); break;
+            case 1: r = exp2_d(v, cf); break;
+            case 2: r = log2(v); break;
+            case 3: r = sqrt(v); break;
+            case 4: r = 1.0 / sqrt(v); break;
+        }
+        out[i] = r;
+    }
+}
+
+hipError_t launch_diag_math(int fn, const double* x, int64_t n, double* out, int grid_cap, hipStream_t s) {
+    const int64_t want = (n + 255) / 256;
+    const int grid = (int)(want < grid_cap ? want : grid_cap);
+    if (grid <= 0) return hipSuccess;
+    hipLaunchKernelGGL(diag_math_kernel, dim3(grid), dim3(256), 0, s, fn, x, n, out, exp2_coef());
+    return hipGetLastError();
+}
+
+// Streaming ceiling of the fused AdamW access pattern: per element read p
+// (fp32), g (bf16), m and v (1 byte each), write p, m, v -- the same bytes,
+// chunking and lane mapping as the AdamW kernel, with no optimizer
+// arithmetic, 2048 elements per wavefront chunk. NT selects non-temporal
+// loads and stores.
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+
+template <bool NT>
+__global__ __launch_bounds__(256) void stream_kernel(float* __restrict__ p, const uint16_t* __restrict__ g,
+                                                      uint8_t* __restrict__ m, uint8_t* __restrict__ v,
+                                                      int64_t chunks) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wpb = blockDim.x >> 6;
+    const int64_t wave = (int64_t)blockIdx.x * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t nwaves = (int64_t)gridDim.x * wpb;
+    for (int64_t c = wave; c < chunks; c += nwaves) {
+        f4v pv[8];
+        u2v gv[8];
+        uint32_t mv[8], vv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int64_t e = c * 2048 + k * 256 + 4 * lane;
+            if constexpr (NT) {
+                pv[k] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p + e));
+                gv[k] = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(g + e));
+                mv[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(m + e));
+                vv[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v + e));
+            } else {
+                pv[k] = *reinterpret_cast<const f4v*>(p + e);
+                gv[k] = *reinterpret_cast<const u2v*>(g + e);
+                mv[k] = *reinterpret_cast<const uint32_t*>(m + e);
+                vv[k] = *reinterpret_cast<const uint32_t*>(v + e);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int64_t e = c * 2048 + k * 256 + 4 * lane;
+            f4v o = pv[k];
+            o.x += bf16_to_f32(gv[k].x & 0xFFFFu);
+            o.w += bf16_to_f32(gv[k].y >> 16);
+            const uint32_t mo = mv[k] ^ vv[k], vo = vv[k] + 0x01010101u;
+            if constexpr (NT) {
+                __builtin_nontemporal_store(o, reinterpret_cast<f4v*>(p + e));
+                __builtin_nontemporal_store(mo, reinterpret_cast<uint32_t*>(m + e));
+                __builtin_nontemporal_store(vo, reinterpret_cast<uint32_t*>(v + e));
+            } else {
+                *reinterpret_cast<f4v*>(p + e) = o;
+                *reinterpret_cast<uint32_t*>(m + e) = mo;
+                *reinterpret_cast<uint32_t*>(v + e) = vo;
+            }
+        }
+    }
+}
+
+hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
+                              hipStream_t s) {
+    const int64_t chunks = n / 2048;
+    int per_cu = 0;
+    hipError_t e = nt ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<true>, 256, 0)
+                      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<false>, 256, 0);
+    if (e != hipSuccess || per_cu <= 0) per_cu = 2;
+    int64_t grid = (int64_t)per_cu * device_cu_count();
+    const int64_t want = (chunks + 3) / 4;
+    if (grid > want) grid = want;
+    if (grid <= 0) return hipSuccess;
+    if (nt)
+        hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, chunks);
+    else
+        hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, chunks);
+    return hipGetLastError();
 }
 
 template <int C>
@@ -159,7 +272,7 @@ static hipError_t dequant_b(const void* codes, const float* meta, int64_t n, int
     switch (block) {
 #define AL_D(BB)                                                                                           \
     case BB:                                                                                               \
-        hipLaunchKernelGGL((dequantize_kernel<C, BB>), dim3(grid), dim3(256), 0, s, codes, meta, n, out); \
+        hipLaunchKernelGGL((dequantize_kernel<C, BB>), dim3(grid), dim3(256), 0, s, codes, meta, n, out, exp2_coef()); \
         return hipGetLastError();
         AL_D(64)
         AL_D(128)

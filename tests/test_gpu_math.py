@@ -1,0 +1,66 @@
+"""Device math primitives the codes rely on, bounded against the host.
+
+* The hardware fp32 log2 on mantissas in [1/2, 1) (the fast code position):
+  its error over all 2^23 mantissas must stay below a quarter of the guard
+  band the encoder assumes (kLog2MantErr = 2^-21), so every code decision
+  outside the band equals the binary64 one.
+* The binary64 exp2 polynomial (decoding): relative error about one ulp.
+* binary64 log2, sqrt and 1/sqrt (block endpoints, factored reconstruction):
+  sqrt and the division are IEEE correctly rounded, so they must match the
+  host bit for bit; log2 within one ulp.
+"""
+import numpy as np
+import pytest
+
+from .gpu_util import log, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 2.0**-21
+
+
+def _run(fn, x):
+    import torch
+
+    import paper_2608_22322_amd as al
+
+    xd = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64)).cuda()
+    out = torch.empty_like(xd)
+    al.diag_math(fn, xd, out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def test_hw_log2_on_mantissas_is_within_guard():
+    require_gpu()
+    m = (np.arange(1 << 23, dtype=np.uint32) | np.uint32(0x3F000000)).view(np.float32)  # all of [1/2, 1)
+    got = _run(0, m.astype(np.float64))
+    ref = np.log2(m.astype(np.float64))
+    err = np.abs(got - ref).max()
+    log(f"hardware fp32 log2 on [1/2,1): max abs error {err:.3e} = 2^{np.log2(err):.2f}")
+    assert err <= GUARD / 4
+
+
+def test_exp2_polynomial_relative_error():
+    require_gpu()
+    rng = np.random.default_rng(1)
+    x = np.concatenate([rng.uniform(-150, 128, 1 << 20), np.arange(-150, 128, 0.25)])
+    got = _run(1, x)
+    ld = np.exp2(x.astype(np.longdouble))
+    rel = float(np.abs((got.astype(np.longdouble) - ld) / ld).max())
+    log(f"exp2 polynomial: max rel error {rel:.3e}")
+    assert rel < 2.5e-16
+    # rounded to fp32 it agrees with the host's exp2 except within ~1e-16 of a midpoint
+    mism = np.count_nonzero(got.astype(np.float32) != np.exp2(x).astype(np.float32))
+    assert mism <= 2, mism
+
+
+def test_log2_sqrt_rsqrt():
+    require_gpu()
+    rng = np.random.default_rng(2)
+    x = np.exp2(rng.uniform(-140, 120, 1 << 20))
+    lg = _run(2, x)
+    ulp = np.spacing(np.abs(np.log2(x)))
+    assert np.all(np.abs(lg - np.log2(x)) <= ulp)
+    assert np.array_equal(_run(3, x), np.sqrt(x))
+    assert np.array_equal(_run(4, x), 1.0 / np.sqrt(x))
