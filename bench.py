@@ -49,14 +49,15 @@ def kernel_hash() -> str:
 
 
 def measured_traffic(block_v: int):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernel source."""
+    """Measured HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated on al_diag_stream), if the
+    counters were taken on the current kernel source."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
     if t.get("kernel_hash") != kernel_hash():
         return None
-    return t.get("bytes_per_step", {}).get(str(block_v))
+    return t.get("bytes_per_launch", {}).get(str(block_v))
 
 
 def build_states(shapes, dev, block_v):
@@ -149,7 +150,7 @@ def copy_ceiling(n, steps=10):
 
 
 def cpu_baseline(shapes, block_v):
-    """The oracle, untuned, on a bounded sample: layer 0's four attention projections, two steps."""
+    """The oracle, untuned, on a bounded sample: layer 0's seven weight matrices, two steps."""
     import numpy as np
 
     import oracle
@@ -157,7 +158,7 @@ def cpu_baseline(shapes, block_v):
     from paper_2608_22322_amd.workloads import workload_llama7b
 
     w = workload_llama7b()
-    idx = [i for i, s in enumerate(shapes) if s.name in ("layer0.q", "layer0.k", "layer0.v", "layer0.o")]
+    idx = [i for i, s in enumerate(shapes) if s.name.startswith("layer0.") and s.is_2d]
     floor = float(np.float32(2 * math.log2(1e-8)))
     n_total, secs = 0, 0.0
     for i in idx:
@@ -172,7 +173,7 @@ def cpu_baseline(shapes, block_v):
             secs += time.perf_counter() - t0
             n_total += s.n
     return {"value": n_total / secs / 1e9, "unit": "Gparams/s", "cores": 1, "kind": "oracle",
-            "sample": f"Llama-7B layer-0 q/k/v/o projections ({n_total // 2:,} params), 2 AdamW steps, "
+            "sample": f"Llama-7B layer-0 weight matrices ({n_total // 2:,} params), 2 AdamW steps, "
                       f"AL8 B_V {block_v} + UF8, single-threaded binary64 C oracle; {secs:.1f} s of CPU time"}
 
 
@@ -244,9 +245,12 @@ def main():
                                "1%% zeros, fp32 params" % args.block,
                    "params": n, "tensors": len(shapes), "block_v": args.block, "block_m": 256,
                    "grad_dtype": "bf16", "parallelism": "none (1 GPU)"},
+        # achieved = algorithmic bytes per launch / average launch duration (= per step / per step)
         "roofline": {"bound": "hbm", "achieved": round(bpp * n / (mean * 1e-3) / 1e9, 1), "peak": PEAK_GBS,
                      "unit": "GB/s", "frac": round(bpp * n / (mean * 1e-3) / 1e9 / PEAK_GBS, 4),
                      "traffic": traffic, "bytes_per_param": bpp, "launches_per_step": launches,
+                     "avg_launch_ms": round(mean / launches, 4),
+                     "algorithmic_bytes_per_launch": round(bpp * n / launches),
                      "kernel": "adamw_kernel<bf16, UF8, AL8, %d>" % args.block,
                      "copy_ceiling_gbs": max(ceil["temporal"], ceil["nontemporal"]),
                      "frac_of_copy_ceiling": round(bpp * n / (mean * 1e-3) / 1e9 / max(ceil["temporal"],
