@@ -82,6 +82,178 @@ al_status check_shape(const al_tensor& t, int i, int64_t* n_out) {
     return AL_OK;
 }
 
+// ------------------------------------------------------ factored-path plan
+const al_state_spec kNoSpec = {AL_CODEC_FP32, 256, 0.0f};
+
+al_status check_adafactor_cfg(const al_adafactor_cfg* cfg) {
+    if (!cfg) return fail(AL_EINVAL, "adafactor: cfg is NULL");
+    if (cfg->grad_dtype != AL_DTYPE_F32 && cfg->grad_dtype != AL_DTYPE_BF16)
+        return fail(AL_EINVAL, "adafactor: grad_dtype %d", cfg->grad_dtype);
+    if (!is_fin(cfg->lr) || cfg->lr < 0 || !is_fin(cfg->eps1) || cfg->eps1 < 0 || !is_fin(cfg->clip_threshold) ||
+        !(cfg->clip_threshold > 0) || !is_fin(cfg->decay_rate) || cfg->decay_rate > 0 ||
+        !is_fin(cfg->weight_decay) || cfg->weight_decay < 0)
+        return fail(AL_EINVAL, "adafactor: hyperparameters out of range");
+    return check_spec(cfg->v, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16), "v");
+}
+
+al_status check_came_cfg(const al_came_cfg* cfg) {
+    if (!cfg) return fail(AL_EINVAL, "came: cfg is NULL");
+    if (cfg->grad_dtype != AL_DTYPE_F32 && cfg->grad_dtype != AL_DTYPE_BF16)
+        return fail(AL_EINVAL, "came: grad_dtype %d", cfg->grad_dtype);
+    if (!is_fin(cfg->lr) || cfg->lr < 0 || !is_fin(cfg->eps1) || cfg->eps1 < 0 || !is_fin(cfg->eps2) ||
+        cfg->eps2 < 0 || !is_fin(cfg->clip_threshold) || !(cfg->clip_threshold > 0) || !is_fin(cfg->weight_decay) ||
+        cfg->weight_decay < 0 || !(cfg->beta1 >= 0 && cfg->beta1 < 1) || !(cfg->beta2 >= 0 && cfg->beta2 < 1) ||
+        !(cfg->beta3 >= 0 && cfg->beta3 < 1))
+        return fail(AL_EINVAL, "came: hyperparameters out of range");
+    al_status st;
+    const unsigned nonneg = (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16);
+    if ((st = check_spec(cfg->m, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_UF8), "m")) != AL_OK) return st;
+    if ((st = check_spec(cfg->v, nonneg, "v")) != AL_OK) return st;
+    if ((st = check_spec(cfg->conf, nonneg, "conf")) != AL_OK) return st;
+    if (cfg->m.codec == AL_CODEC_UF8 && cfg->m.block != 256)
+        return fail(AL_EUNSUPPORTED, "came: UF8 momentum block must be 256 (got %d)", cfg->m.block);
+    return AL_OK;
+}
+
+al_status check_ws(void* ws, size_t ws_bytes, size_t need, const char* who) {
+    if (need == 0) return AL_OK;
+    if (!ws) return fail(AL_EWORKSPACE, "%s: workspace is NULL (need %zu bytes)", who, need);
+    if (ws_bytes < need) return fail(AL_EWORKSPACE, "%s: workspace %zu bytes < %zu needed", who, ws_bytes, need);
+    if (reinterpret_cast<uintptr_t>(ws) & 255u) return fail(AL_EALIGN, "%s: workspace not 256-byte aligned", who);
+    return AL_OK;
+}
+
+struct FacPlan {
+    std::vector<al::FacDesc> desc;  // 2-D tensors first, then 1-D
+    int n2 = 0, n1 = 0;
+    int64_t total_units = 0, total_chunks = 0;
+    size_t bytes = 0;
+    size_t rms_off = 0;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Validate the tensor list and lay out the workspace: descriptor table, RMS
+// partials, then per-tensor regions. With ws == NULL only sizes are computed.
+al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& ms, const al_state_spec& vs,
+                   const al_state_spec& cs, char* ws, FacPlan& P) {
+    const char* who = came ? "al_came_step" : "al_adafactor_step";
+    if (nt < 0) return fail(AL_EINVAL, "%s: nt < 0", who);
+    if (nt > 0 && !ts) return fail(AL_EINVAL, "%s: tensors is NULL", who);
+    P = FacPlan();
+    std::vector<int> twod, oned;
+    al_status st;
+    for (int i = 0; i < nt; ++i) {
+        const al_tensor& t = ts[i];
+        int64_t n = 0;
+        if ((st = check_shape(t, i, &n)) != AL_OK) return st;
+        if (n == 0) continue;
+        const bool fac = t.rows > 1;
+        if (fac) {
+            if ((st = check_state(t.vr, t.vr_meta, vs, t.rows, "vr", i)) != AL_OK) return st;
+            if ((st = check_state(t.vc, t.vc_meta, vs, t.cols, "vc", i)) != AL_OK) return st;
+            if ((st = check_unused(t.v, t.v_meta, "v (2-D tensor)", i)) != AL_OK) return st;
+            if (came) {
+                if ((st = check_state(t.cr, t.cr_meta, cs, t.rows, "cr", i)) != AL_OK) return st;
+                if ((st = check_state(t.cc, t.cc_meta, cs, t.cols, "cc", i)) != AL_OK) return st;
+            } else {
+                if ((st = check_unused(t.cr, t.cr_meta, "cr", i)) != AL_OK) return st;
+                if ((st = check_unused(t.cc, t.cc_meta, "cc", i)) != AL_OK) return st;
+            }
+            twod.push_back(i);
+        } else {
+            if ((st = check_state(t.v, t.v_meta, vs, n, "v", i)) != AL_OK) return st;
+            if ((st = check_unused(t.vr, t.vr_meta, "vr (1-D tensor)", i)) != AL_OK) return st;
+            if ((st = check_unused(t.vc, t.vc_meta, "vc (1-D tensor)", i)) != AL_OK) return st;
+            if ((st = check_unused(t.cr, t.cr_meta, "cr (1-D tensor)", i)) != AL_OK) return st;
+            if ((st = check_unused(t.cc, t.cc_meta, "cc (1-D tensor)", i)) != AL_OK) return st;
+            oned.push_back(i);
+        }
+        if (came) {
+            if ((st = check_state(t.m, t.m_meta, ms, n, "m", i)) != AL_OK) return st;
+        } else {
+            if ((st = check_unused(t.m, t.m_meta, "m", i)) != AL_OK) return st;
+        }
+    }
+    P.n2 = (int)twod.size();
+    P.n1 = (int)oned.size();
+    const int ntot = P.n2 + P.n1;
+    P.desc.resize(ntot);
+    for (int k = 0; k < P.n2; ++k) {
+        const al_tensor& t = ts[twod[k]];
+        al::FacDesc& d = P.desc[k];
+        d.nru = (int32_t)((t.rows + 255) / 256);
+        d.ncu = (int32_t)((t.cols + 255) / 256);
+        d.unit_begin = P.total_units;
+        P.total_units += (int64_t)d.nru * d.ncu;
+        d.chunk_begin = P.total_chunks;
+        P.total_chunks += (t.rows * t.cols + 1023) / 1024;
+    }
+    size_t off = align256((size_t)ntot * sizeof(al::FacDesc));
+    P.rms_off = off;
+    off += align256((size_t)P.total_units * 16);
+    auto take = [&](size_t nbytes) -> char* {
+        char* ptr = ws ? ws + off : nullptr;
+        off += align256(nbytes);
+        return ptr;
+    };
+    for (int k = 0; k < ntot; ++k) {
+        const bool fac = k < P.n2;
+        const al_tensor& t = ts[fac ? twod[k] : oned[k - P.n2]];
+        al::FacDesc& d = P.desc[k];
+        d.p = t.param;
+        d.g = t.grad;
+        d.rows = t.rows;
+        d.cols = t.cols;
+        d.v = t.v;
+        d.vm = t.v_meta;
+        d.vr = t.vr;
+        d.vrm = t.vr_meta;
+        d.vc = t.vc;
+        d.vcm = t.vc_meta;
+        d.m = t.m;
+        d.mm = t.m_meta;
+        d.cr = t.cr;
+        d.crm = t.cr_meta;
+        d.cc = t.cc;
+        d.ccm = t.cc_meta;
+        if (fac) {
+            d.colpart = reinterpret_cast<double*>(take((size_t)d.nru * t.cols * 16));
+            d.rowpart = reinterpret_cast<double*>(take((size_t)d.ncu * t.rows * 16));
+            d.rfac = reinterpret_cast<double*>(take((size_t)t.rows * 8));
+            d.cfac = reinterpret_cast<double*>(take((size_t)t.cols * 8));
+            if (came) {
+                d.sr = reinterpret_cast<double*>(take((size_t)t.rows * 8));
+                d.sc = reinterpret_cast<double*>(take((size_t)t.cols * 8));
+            }
+            d.rtmp = reinterpret_cast<float*>(take((size_t)t.rows * 4));
+            d.ctmp = reinterpret_cast<float*>(take((size_t)t.cols * 4));
+        } else {
+            d.nru = d.ncu = 0;
+            const size_t n = (size_t)(t.rows * t.cols);
+            d.rtmp = reinterpret_cast<float*>(take(n * 4));
+            if (came) d.ctmp = reinterpret_cast<float*>(take(n * 4));
+        }
+        d.scal = reinterpret_cast<double*>(take(16));
+    }
+    P.bytes = off;
+    return AL_OK;
+}
+
+al::FacArgs fac_args(const FacPlan& P, char* ws) {
+    al::FacArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.D = reinterpret_cast<const al::FacDesc*>(ws);
+    a.rmspart = reinterpret_cast<double*>(ws + P.rms_off);
+    a.n2 = P.n2;
+    a.n1 = P.n1;
+    a.total_units = P.total_units;
+    a.total_chunks = P.total_chunks;
+    a.cf = al::exp2_coef();
+    a.m_block = 256;
+    return a;
+}
+
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 }  // namespace
@@ -275,19 +447,106 @@ al_status al_synth_normal(void* out, int32_t out_dtype, int64_t n, uint64_t key,
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_synth_normal launch");
 }
 
-al_status al_adafactor_workspace_bytes(const al_tensor*, int32_t, const al_adafactor_cfg*, size_t* bytes) {
-    if (bytes) *bytes = 0;
-    return fail(AL_EUNSUPPORTED, "al_adafactor_workspace_bytes: not built yet");
+al_status al_adafactor_workspace_bytes(const al_tensor* tensors, int32_t nt, const al_adafactor_cfg* cfg,
+                                       size_t* bytes) {
+    g_err[0] = 0;
+    if (!bytes) return fail(AL_EINVAL, "al_adafactor_workspace_bytes: bytes is NULL");
+    *bytes = 0;
+    al_status st = check_adafactor_cfg(cfg);
+    if (st != AL_OK) return st;
+    FacPlan P;
+    if ((st = fac_plan(tensors, nt, false, kNoSpec, cfg->v, kNoSpec, nullptr, P)) != AL_OK) return st;
+    *bytes = P.bytes;
+    return AL_OK;
 }
-al_status al_came_workspace_bytes(const al_tensor*, int32_t, const al_came_cfg*, size_t* bytes) {
-    if (bytes) *bytes = 0;
-    return fail(AL_EUNSUPPORTED, "al_came_workspace_bytes: not built yet");
+
+al_status al_came_workspace_bytes(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg, size_t* bytes) {
+    g_err[0] = 0;
+    if (!bytes) return fail(AL_EINVAL, "al_came_workspace_bytes: bytes is NULL");
+    *bytes = 0;
+    al_status st = check_came_cfg(cfg);
+    if (st != AL_OK) return st;
+    FacPlan P;
+    if ((st = fac_plan(tensors, nt, true, cfg->m, cfg->v, cfg->conf, nullptr, P)) != AL_OK) return st;
+    *bytes = P.bytes;
+    return AL_OK;
 }
-al_status al_adafactor_step(const al_tensor*, int32_t, const al_adafactor_cfg*, int64_t, void*, size_t, void*) {
-    return fail(AL_EUNSUPPORTED, "al_adafactor_step: not built yet");
+
+al_status al_adafactor_step(const al_tensor* tensors, int32_t nt, const al_adafactor_cfg* cfg, int64_t step,
+                            void* ws, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    al_status st = check_adafactor_cfg(cfg);
+    if (st != AL_OK) return st;
+    if (step < 1) return fail(AL_EINVAL, "al_adafactor_step: step must be >= 1");
+    FacPlan P;
+    if ((st = fac_plan(tensors, nt, false, kNoSpec, cfg->v, kNoSpec, nullptr, P)) != AL_OK) return st;
+    if (P.desc.empty()) return AL_OK;
+    if ((st = check_ws(ws, ws_bytes, P.bytes, "al_adafactor_step")) != AL_OK) return st;
+    if ((st = fac_plan(tensors, nt, false, kNoSpec, cfg->v, kNoSpec, static_cast<char*>(ws), P)) != AL_OK) return st;
+
+    al::FacArgs a = fac_args(P, static_cast<char*>(ws));
+    a.beta = 1.0 - std::pow((double)step, cfg->decay_rate);
+    a.omb = 1.0 - a.beta;
+    a.eps1 = cfg->eps1;
+    a.lr = cfg->lr;
+    a.decay = 1.0 - cfg->lr * cfg->weight_decay;
+    a.clip_d = cfg->clip_threshold;
+    a.v_codec = cfg->v.codec;
+    a.v_block = cfg->v.block;
+    a.v_floor = cfg->v.log_floor;
+    hipStream_t s = as_stream(stream);
+    const int G = cfg->grad_dtype;
+    hipError_t e;
+    if ((e = al::fac_copy_desc(P.desc.data(), (int)P.desc.size(), const_cast<al::FacDesc*>(a.D), s)) != hipSuccess ||
+        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, s)) != hipSuccess ||
+        (e = al::launch_fac_rms(a, G, s)) != hipSuccess || (e = al::launch_fac_clip(a, s)) != hipSuccess ||
+        (e = al::launch_ada_apply(a, G, s)) != hipSuccess || (e = al::launch_ada_vec1d(a, G, s)) != hipSuccess)
+        return hip_fail(e, "al_adafactor_step launch");
+    return AL_OK;
 }
-al_status al_came_step(const al_tensor*, int32_t, const al_came_cfg*, int64_t, void*, size_t, void*) {
-    return fail(AL_EUNSUPPORTED, "al_came_step: not built yet");
+
+al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg, int64_t step, void* ws,
+                       size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    al_status st = check_came_cfg(cfg);
+    if (st != AL_OK) return st;
+    if (step < 1) return fail(AL_EINVAL, "al_came_step: step must be >= 1");
+    FacPlan P;
+    if ((st = fac_plan(tensors, nt, true, cfg->m, cfg->v, cfg->conf, nullptr, P)) != AL_OK) return st;
+    if (P.desc.empty()) return AL_OK;
+    if ((st = check_ws(ws, ws_bytes, P.bytes, "al_came_step")) != AL_OK) return st;
+    if ((st = fac_plan(tensors, nt, true, cfg->m, cfg->v, cfg->conf, static_cast<char*>(ws), P)) != AL_OK) return st;
+
+    al::FacArgs a = fac_args(P, static_cast<char*>(ws));
+    a.beta = cfg->beta2;
+    a.omb = 1.0 - cfg->beta2;
+    a.beta1 = cfg->beta1;
+    a.omb1 = 1.0 - cfg->beta1;
+    a.beta3 = cfg->beta3;
+    a.omb3 = 1.0 - cfg->beta3;
+    a.eps1 = cfg->eps1;
+    a.eps2 = cfg->eps2;
+    a.lr = cfg->lr;
+    a.decay = 1.0 - cfg->lr * cfg->weight_decay;
+    a.clip_d = cfg->clip_threshold;
+    a.v_codec = cfg->v.codec;
+    a.v_block = cfg->v.block;
+    a.v_floor = cfg->v.log_floor;
+    a.c_codec = cfg->conf.codec;
+    a.c_block = cfg->conf.block;
+    a.c_floor = cfg->conf.log_floor;
+    a.m_codec = cfg->m.codec;
+    a.m_block = cfg->m.codec == AL_CODEC_UF8 ? cfg->m.block : 256;
+    hipStream_t s = as_stream(stream);
+    const int G = cfg->grad_dtype;
+    hipError_t e;
+    if ((e = al::fac_copy_desc(P.desc.data(), (int)P.desc.size(), const_cast<al::FacDesc*>(a.D), s)) != hipSuccess ||
+        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, s)) != hipSuccess ||
+        (e = al::launch_fac_rms(a, G, s)) != hipSuccess || (e = al::launch_fac_clip(a, s)) != hipSuccess ||
+        (e = al::launch_came_res(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 1, s)) != hipSuccess ||
+        (e = al::launch_came_apply(a, G, s)) != hipSuccess || (e = al::launch_came_vec1d(a, G, s)) != hipSuccess)
+        return hip_fail(e, "al_came_step launch");
+    return AL_OK;
 }
 
 }  // extern "C"

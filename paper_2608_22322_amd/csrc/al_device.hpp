@@ -204,6 +204,43 @@ __device__ __forceinline__ uint32_t readlane_u(uint32_t v, int lane) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
 }
 
+// ---------------------------------------------------- double-double sums
+// Sums of non-negative binary64 terms carried as (hi, lo) with TwoSum
+// (Knuth): hi + lo equals the exact sum up to ~n 2^-106 relative, so
+// fl64(hi + lo) is the correctly rounded exact sum except within that of a
+// rounding boundary, whatever the order of accumulation.
+struct DD {
+    double hi, lo;
+};
+
+__device__ __forceinline__ void dd_add(DD& a, double x) {
+    const double s = a.hi + x;
+    const double bp = s - a.hi;
+    const double e = (a.hi - (s - bp)) + (x - bp);
+    a.hi = s;
+    a.lo += e;
+}
+
+__device__ __forceinline__ DD dd_merge(DD a, DD b) {
+    const double s = a.hi + b.hi;
+    const double bp = s - a.hi;
+    double e = (a.hi - (s - bp)) + (b.hi - bp);
+    e += a.lo + b.lo;
+    const double hi = s + e;
+    return DD{hi, e - (hi - s)};
+}
+
+__device__ __forceinline__ double dd_value(DD a) { return a.hi + a.lo; }
+
+__device__ __forceinline__ DD dd_shfl_xor(DD a, int m) { return DD{__shfl_xor(a.hi, m), __shfl_xor(a.lo, m)}; }
+
+// Wave-wide merge; every lane gets the total (fixed butterfly order).
+__device__ __forceinline__ DD dd_wave_sum(DD a) {
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) a = dd_merge(a, dd_shfl_xor(a, m));
+    return a;
+}
+
 // ----------------------------------------------------------------- UF8 code
 // Encode with r = 127 / absmax (binary64), y = x * r, round to nearest even,
 // clamp to [-127, 127].

@@ -57,6 +57,75 @@ hipError_t launch_diag_math(int fn, const double* x, int64_t n, double* out, int
 hipError_t launch_synth_normal(void* out, int out_bf16, int64_t n, uint64_t key, float scale,
                                uint64_t mask_key, uint64_t mask_threshold, int grid_cap, hipStream_t s);
 
+
+// ------------------------------------------------------ factored optimizers
+// One descriptor per tensor, held in the caller's workspace (written there by
+// a device-side copy from the kernel arguments). 2-D tensors (rows > 1) come
+// first, then 1-D tensors. Per-tensor workspace regions: column partial sums
+// [nru][cols] and row partial sums [ncu][rows] as double-double pairs, the
+// reconstruction factors (binary64), fp32 staging for the vector encodes and
+// a scalar slot (the clip divisor).
+struct FacDesc {
+    float* p;
+    const void* g;
+    int64_t rows, cols;
+    void* v;
+    float* vm;
+    void* vr;
+    float* vrm;
+    void* vc;
+    float* vcm;
+    void* m;
+    float* mm;
+    void* cr;
+    float* crm;
+    void* cc;
+    float* ccm;
+    double* colpart;  // [nru][cols] (hi, lo)
+    double* rowpart;  // [ncu][rows] (hi, lo)
+    double* rfac;     // (R_i / mean R)^-1/2
+    double* cfac;     // C_j^-1/2
+    double* sr;       // CAME confidence factors
+    double* sc;
+    float* rtmp;      // staging: R (2-D) or V (1-D)
+    float* ctmp;      // staging: C (2-D) or momentum (1-D)
+    double* scal;     // [0] = clip divisor max(1, RMS / d)
+    int64_t unit_begin;   // first 256x256 unit of this tensor (2-D)
+    int64_t chunk_begin;  // first 1024-element chunk of this tensor (2-D)
+    int32_t nru, ncu;     // units along rows / columns
+};
+
+constexpr int kFacCopyBatch = 16;
+struct FacDescBatch {
+    int32_t count, offset;
+    FacDesc d[kFacCopyBatch];
+};
+
+struct FacArgs {
+    const FacDesc* D;
+    double* rmspart;      // [total_units] (hi, lo): partial sums of u^2
+    int32_t n2, n1;       // 2-D tensors, 1-D tensors (D[n2 .. n2 + n1))
+    int64_t total_units, total_chunks;
+    double beta, omb;     // second-moment EMA: Adafactor beta2_t / CAME beta2, and 1 - beta
+    double beta1, omb1;   // CAME momentum
+    double beta3, omb3;   // CAME confidence
+    double eps1, eps2, lr, decay, clip_d;
+    int32_t v_codec, v_block, c_codec, c_block, m_codec, m_block;
+    float v_floor, c_floor;
+    Exp2Coef cf;
+};
+
+hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream_t s);
+hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s);
+hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s);
+hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_ada_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_came_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s);
+
 // Taylor coefficients of the binary64 exp2 used by every decode.
 const Exp2Coef& exp2_coef();
 

@@ -1,0 +1,776 @@
+// Factored-state optimizer steps on gfx950: Adafactor (factored second
+// moment) and CAME (factored second moment + factored confidence + dense
+// momentum), section 3.1, with AL/UF8/FP32 codes per state role (section 4).
+//
+// Kernel sequence of one Adafactor step (2-D tensors):
+//   marg   row and column sums of G2 = g^2 + eps1, exact (double-double)
+//   fin    one workgroup per tensor: R, C = EMA of the means, rounded to fp32,
+//          re-encoded; mean(R); factors r_i = (R_i / mean R)^-1/2, c_j = C_j^-1/2
+//   rms    partial sums of u^2, u_ij = (r_i c_j) g_ij, per 256x256 unit
+//   clip   per tensor: max(1, RMS(u) / d)
+//   apply  p <- p (1 - lr wd) - lr u / clip
+// 1-D tensors run their whole step in one workgroup (vec1d).
+// CAME adds: res (sums of (uhat - m)^2 + eps2 with the in-step momentum),
+// fin over the confidence, and apply (recompute uhat and m, encode m, update p).
+//
+// Marginal sums. A wavefront owns a 256x256 unit as 4x4 tiles of 64x64. It
+// loads a tile in the natural layout (16 lanes x 4 columns x 4 rows per
+// instruction, coalesced 128-byte row segments), adds each term to in-lane
+// column accumulators, and writes the tile to LDS; each lane then sums one
+// tile row out of LDS. All sums are double-double and every partial is
+// merged in a fixed order, so the means are the exactly rounded ones.
+#include "al_codec_dev.hpp"
+#include "al_device.hpp"
+#include "al_internal.hpp"
+
+namespace al {
+
+// ------------------------------------------------------------------ helpers
+__device__ __forceinline__ int locate_unit(const FacDesc* D, int n, int64_t unit) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (D[mid].unit_begin <= unit)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int locate_chunk(const FacDesc* D, int n, int64_t chunk) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (D[mid].chunk_begin <= chunk)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+template <int G>
+__device__ __forceinline__ float grad1(const void* g, int64_t e) {
+    if constexpr (G == G_BF16)
+        return bf16_to_f32(reinterpret_cast<const uint16_t*>(g)[e]);
+    else
+        return reinterpret_cast<const float*>(g)[e];
+}
+
+// 4 consecutive gradients at element e (the caller guarantees alignment).
+template <int G>
+__device__ __forceinline__ void grad4(const void* g, int64_t e, float out[4]) {
+    if constexpr (G == G_BF16) {
+        const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(g) + e);
+        out[0] = bf16_to_f32(w.x & 0xFFFFu);
+        out[1] = bf16_to_f32(w.x >> 16);
+        out[2] = bf16_to_f32(w.y & 0xFFFFu);
+        out[3] = bf16_to_f32(w.y >> 16);
+    } else {
+        const float4 w = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + e);
+        out[0] = w.x;
+        out[1] = w.y;
+        out[2] = w.z;
+        out[3] = w.w;
+    }
+}
+
+// Decode element i of a vector state (runtime codec / block).
+__device__ __forceinline__ float vec_decode(int codec, int B, const void* codes, const float* meta, int64_t i,
+                                            const Exp2Coef& cf) {
+    if (codec == FP32) return reinterpret_cast<const float*>(codes)[i];
+    if (codec == UF8) {
+        const int32_t q = reinterpret_cast<const int8_t*>(codes)[i];
+        return uf8_decode(q, (double)meta[i / B] / 127.0);
+    }
+    const uint32_t q = codec == AL16 ? reinterpret_cast<const uint16_t*>(codes)[i]
+                                     : reinterpret_cast<const uint8_t*>(codes)[i];
+    if (q == 0u) return 0.0f;
+    const int64_t b = i / B;
+    const double step = (double)meta[2 * b + 1] / (codec == AL16 ? 65534.0 : 254.0);
+    return al_decode_fast(q, (double)meta[2 * b], step, cf);
+}
+
+// Encode x[0, n) into a vector state, one block per wavefront at a time
+// (runtime codec / block; the vectors are small). Padding codes are 0.
+__device__ void vec_encode(int codec, int B, const float* x, int64_t n, float log_floor, void* codes, float* meta,
+                           int wave, int nwaves, int lane) {
+    if (codec == FP32) {
+        for (int64_t i = (int64_t)wave * 64 + lane; i < n; i += (int64_t)nwaves * 64)
+            reinterpret_cast<float*>(codes)[i] = x[i];
+        return;
+    }
+    const int64_t nb = (n + B - 1) / B;
+    for (int64_t b = wave; b < nb; b += nwaves) {
+        const int64_t s = b * B;
+        const int64_t e = s + B < n ? s + B : n;
+        if (codec == UF8) {
+            uint32_t am = 0u;
+            for (int64_t i = s + lane; i < e; i += 64) am = OpMax::f(am, abs_bits(x[i]));
+            am = group_reduce<OpMax, 64>(am);
+            const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+            if (lane == 0) meta[b] = u2f(am);
+            for (int64_t i = s + lane; i < s + B; i += 64) {
+                const int32_t q = i < e ? (int32_t)__builtin_rint((double)x[i] * r) : 0;
+                reinterpret_cast<int8_t*>(codes)[i] = (int8_t)q;
+            }
+        } else {
+            uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+            for (int64_t i = s + lane; i < e; i += 64) {
+                mn = OpMin::f(mn, pos_min_key(x[i]));
+                mx = OpMax::f(mx, pos_max_key(x[i]));
+            }
+            mn = group_reduce<OpMin, 64>(mn);
+            mx = group_reduce<OpMax, 64>(mx);
+            const ALFit f = al_fit(mn, mx, log_floor);
+            if (lane == 0) {
+                meta[2 * b] = f.any ? (float)f.lmin : 0.0f;
+                meta[2 * b + 1] = f.any ? (float)f.delta : 0.0f;
+            }
+            const int levels = codec == AL16 ? 65534 : 254;
+            const ALEnc enc = al_enc_params(f.lmin, f.any ? (double)levels / f.delta : 1.0);
+            for (int64_t i = s + lane; i < s + B; i += 64) {
+                const float v = i < e ? x[i] : 0.0f;
+                const uint32_t q = codec == AL16 ? al_encode_fast<65534>(v, enc) : al_encode_fast<254>(v, enc);
+                if (codec == AL16)
+                    reinterpret_cast<uint16_t*>(codes)[i] = (uint16_t)q;
+                else
+                    reinterpret_cast<uint8_t*>(codes)[i] = (uint8_t)q;
+            }
+        }
+    }
+}
+
+// Block-wide (256 threads) double-double total in a fixed order.
+__device__ DD block_dd_sum(DD v, DD* sh) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    v = dd_wave_sum(v);
+    if (lane == 0) sh[w] = v;
+    __syncthreads();
+    DD t = sh[0];
+    for (int k = 1; k < (int)(blockDim.x >> 6); ++k) t = dd_merge(t, sh[k]);
+    __syncthreads();
+    return t;
+}
+
+// --------------------------------------------------------------- descriptors
+__global__ void fac_desc_copy_kernel(const FacDescBatch b, FacDesc* dst) {
+    constexpr int W = sizeof(FacDesc) / 8;
+    const int total = b.count * W;
+    const uint64_t* src = reinterpret_cast<const uint64_t*>(b.d);
+    uint64_t* out = reinterpret_cast<uint64_t*>(dst + b.offset);
+    for (int i = threadIdx.x; i < total; i += blockDim.x) out[i] = src[i];
+}
+
+hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream_t s) {
+    static_assert(sizeof(FacDesc) % 8 == 0, "descriptor size");
+    for (int off = 0; off < count; off += kFacCopyBatch) {
+        FacDescBatch b;
+        b.count = count - off < kFacCopyBatch ? count - off : kFacCopyBatch;
+        b.offset = off;
+        for (int i = 0; i < b.count; ++i) b.d[i] = host[off + i];
+        hipLaunchKernelGGL(fac_desc_copy_kernel, dim3(1), dim3(256), 0, s, b, dev);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// ------------------------------------------------------- marginal sums of G2
+template <int G>
+__global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
+    __shared__ float tile[64][68];
+    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4;
+    for (int64_t unit = blockIdx.x; unit < a.total_units; unit += gridDim.x) {
+        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+        const int64_t u = unit - d.unit_begin;
+        const int64_t ru = u / d.ncu, cu = u % d.ncu;
+        const int64_t r0 = ru * 256, c0 = cu * 256;
+        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+        const bool vec = (d.cols & 3) == 0;
+        DD cacc[4][4];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
+        for (int rt = 0; rt < 4 && rt * 64 < nr; ++rt) {
+            DD racc{0.0, 0.0};
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                if (ct * 64 >= nc) break;
+                const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
+                for (int i = 0; i < 16; ++i) {
+                    const int rr = rt * 64 + lr + 4 * i;
+                    const int cc = ct * 64 + 4 * lc;
+                    const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+                    float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (rr < nr) {
+                        if (vec && cc + 4 <= nc) {
+                            grad4<G>(d.g, e, gv);
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
+                        }
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (cc + j < nc) {
+                                const double x = (double)gv[j];
+                                dd_add(cacc[ct][j], x * x + a.eps1);
+                            }
+                        }
+                    }
+                    *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
+                }
+                __syncthreads();
+                if (rt * 64 + lane < nr) {
+                    if (ncol == 64) {
+#pragma unroll 4
+                        for (int c = 0; c < 64; c += 4) {
+                            const float4 t = *reinterpret_cast<const float4*>(&tile[lane][c]);
+                            const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
+                            dd_add(racc, x0 * x0 + a.eps1);
+                            dd_add(racc, x1 * x1 + a.eps1);
+                            dd_add(racc, x2 * x2 + a.eps1);
+                            dd_add(racc, x3 * x3 + a.eps1);
+                        }
+                    } else {
+                        for (int c = 0; c < ncol; ++c) {
+                            const double x = tile[lane][c];
+                            dd_add(racc, x * x + a.eps1);
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+            const int row = rt * 64 + lane;
+            if (row < nr) {
+                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+                rp[0] = racc.hi;
+                rp[1] = racc.lo;
+            }
+        }
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                DD v = cacc[ct][j];
+                v = dd_merge(v, dd_shfl_xor(v, 16));
+                v = dd_merge(v, dd_shfl_xor(v, 32));
+                const int col = ct * 64 + 4 * lc + j;
+                if (lr == 0 && col < nc) {
+                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    cp[0] = v.hi;
+                    cp[1] = v.lo;
+                }
+            }
+        }
+    }
+}
+
+hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_units == 0) return hipSuccess;
+    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int grid = (int)(a.total_units < cap ? a.total_units : cap);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(fac_marg_g2_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
+    else
+        hipLaunchKernelGGL(fac_marg_g2_kernel<G_F32>, dim3(grid), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------- finalize (one WG / tensor)
+// role 0: second moment (EMA beta, codes vr/vc, factors rfac/cfac);
+// role 1: CAME confidence (EMA beta3, codes cr/cc, factors sr/sc).
+__global__ __launch_bounds__(256) void fac_fin_kernel(const FacArgs a, int role) {
+    __shared__ DD sh[4];
+    __shared__ double mean_r;
+    const FacDesc& d = a.D[blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int codec = role ? a.c_codec : a.v_codec;
+    const int B = role ? a.c_block : a.v_block;
+    void* rc = role ? d.cr : d.vr;
+    float* rm = role ? d.crm : d.vrm;
+    void* ccd = role ? d.cc : d.vc;
+    float* cm = role ? d.ccm : d.vcm;
+    double* fr = role ? d.sr : d.rfac;
+    double* fc = role ? d.sc : d.cfac;
+    const double beta = role ? a.beta3 : a.beta, omb = role ? a.omb3 : a.omb;
+    const float lf = role ? a.c_floor : a.v_floor;
+    const int64_t rows = d.rows, cols = d.cols;
+
+    for (int64_t i = tid; i < rows; i += blockDim.x) {
+        DD s{0.0, 0.0};
+        for (int cu = 0; cu < d.ncu; ++cu) {
+            const double* rp = d.rowpart + 2 * ((int64_t)cu * rows + i);
+            s = dd_merge(s, DD{rp[0], rp[1]});
+        }
+        const double mean = dd_value(s) / (double)cols;
+        const float old = vec_decode(codec, B, rc, rm, i, a.cf);
+        d.rtmp[i] = (float)(beta * (double)old + omb * mean);
+    }
+    for (int64_t j = tid; j < cols; j += blockDim.x) {
+        DD s{0.0, 0.0};
+        for (int ru = 0; ru < d.nru; ++ru) {
+            const double* cp = d.colpart + 2 * ((int64_t)ru * cols + j);
+            s = dd_merge(s, DD{cp[0], cp[1]});
+        }
+        const double mean = dd_value(s) / (double)rows;
+        const float old = vec_decode(codec, B, ccd, cm, j, a.cf);
+        d.ctmp[j] = (float)(beta * (double)old + omb * mean);
+    }
+    __syncthreads();
+    vec_encode(codec, B, d.rtmp, rows, lf, rc, rm, wave, 4, lane);
+    vec_encode(codec, B, d.ctmp, cols, lf, ccd, cm, wave, 4, lane);
+    DD s{0.0, 0.0};
+    for (int64_t i = tid; i < rows; i += blockDim.x) dd_add(s, (double)d.rtmp[i]);
+    s = block_dd_sum(s, sh);
+    if (tid == 0) mean_r = dd_value(s) / (double)rows;
+    __syncthreads();
+    const double mr = mean_r;
+    for (int64_t i = tid; i < rows; i += blockDim.x) fr[i] = 1.0 / sqrt((double)d.rtmp[i] / mr);
+    for (int64_t j = tid; j < cols; j += blockDim.x) fc[j] = 1.0 / sqrt((double)d.ctmp[j]);
+}
+
+hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
+    if (a.n2 == 0) return hipSuccess;
+    hipLaunchKernelGGL(fac_fin_kernel, dim3(a.n2), dim3(256), 0, s, a, role);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------ RMS partials (per unit)
+// Natural layout: lane = 4 consecutive columns of a 256-column segment; the
+// wave walks the unit's rows. u_ij = (r_i c_j) g_ij, exactly the reference
+// operation order; u^2 summed double-double.
+template <int G>
+__global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t unit = wave; unit < a.total_units; unit += nw) {
+        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+        const int64_t u = unit - d.unit_begin;
+        const int64_t ru = u / d.ncu, cu = u % d.ncu;
+        const int64_t r0 = ru * 256, c0 = cu * 256;
+        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+        const bool vec = (d.cols & 3) == 0 && 4 * lane + 4 <= nc;
+        double cf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cf[j] = 4 * lane + j < nc ? d.cfac[c0 + 4 * lane + j] : 0.0;
+        DD acc{0.0, 0.0};
+        for (int r = 0; r < nr; ++r) {
+            const double ri = d.rfac[r0 + r];
+            const int64_t e = (r0 + r) * d.cols + c0 + 4 * lane;
+            float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (vec) {
+                grad4<G>(d.g, e, gv);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (4 * lane + j < nc) gv[j] = grad1<G>(d.g, e + j);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (4 * lane + j < nc) {
+                    const double uu = (ri * cf[j]) * (double)gv[j];
+                    dd_add(acc, uu * uu);
+                }
+            }
+        }
+        acc = dd_wave_sum(acc);
+        if (lane == 0) {
+            a.rmspart[2 * unit] = acc.hi;
+            a.rmspart[2 * unit + 1] = acc.lo;
+        }
+    }
+}
+
+hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_units == 0) return hipSuccess;
+    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t want = (a.total_units + 3) / 4;
+    const int grid = (int)(want < cap ? want : cap);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(fac_rms_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(fac_rms_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------ clip divisor (wave / tensor)
+__global__ __launch_bounds__(64) void fac_clip_kernel(const FacArgs a) {
+    const FacDesc& d = a.D[blockIdx.x];
+    const int lane = threadIdx.x;
+    const int64_t nu = (int64_t)d.nru * d.ncu;
+    DD s{0.0, 0.0};
+    for (int64_t k = lane; k < nu; k += 64) {
+        const int64_t unit = d.unit_begin + k;
+        s = dd_merge(s, DD{a.rmspart[2 * unit], a.rmspart[2 * unit + 1]});
+    }
+    s = dd_wave_sum(s);
+    if (lane == 0) {
+        const double rms = sqrt(dd_value(s) / (double)(d.rows * d.cols));
+        d.scal[0] = rms / a.clip_d > 1.0 ? rms / a.clip_d : 1.0;
+    }
+}
+
+hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s) {
+    if (a.n2 == 0) return hipSuccess;
+    hipLaunchKernelGGL(fac_clip_kernel, dim3(a.n2), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+// --------------------------------------------------- Adafactor apply (2-D)
+template <int G>
+__global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t unit = wave; unit < a.total_units; unit += nw) {
+        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+        const int64_t u = unit - d.unit_begin;
+        const int64_t ru = u / d.ncu, cu = u % d.ncu;
+        const int64_t r0 = ru * 256, c0 = cu * 256;
+        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+        const bool vec = (d.cols & 3) == 0 && 4 * lane + 4 <= nc;
+        const double clip = d.scal[0];
+        double cf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cf[j] = 4 * lane + j < nc ? d.cfac[c0 + 4 * lane + j] : 0.0;
+        for (int r = 0; r < nr; ++r) {
+            const double ri = d.rfac[r0 + r];
+            const int64_t e = (r0 + r) * d.cols + c0 + 4 * lane;
+            float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            float pv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (vec) {
+                grad4<G>(d.g, e, gv);
+                const float4 t = *reinterpret_cast<const float4*>(d.p + e);
+                pv[0] = t.x;
+                pv[1] = t.y;
+                pv[2] = t.z;
+                pv[3] = t.w;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (4 * lane + j < nc) {
+                        gv[j] = grad1<G>(d.g, e + j);
+                        pv[j] = d.p[e + j];
+                    }
+            }
+            float out[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const double uu = (ri * cf[j]) * (double)gv[j];
+                const double pd = (double)pv[j] * a.decay;
+                out[j] = (float)(pd - a.lr * (uu / clip));
+            }
+            if (vec) {
+                *reinterpret_cast<float4*>(d.p + e) = make_float4(out[0], out[1], out[2], out[3]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (4 * lane + j < nc) d.p[e + j] = out[j];
+            }
+        }
+    }
+}
+
+hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_units == 0) return hipSuccess;
+    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t want = (a.total_units + 3) / 4;
+    const int grid = (int)(want < cap ? want : cap);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(ada_apply_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(ada_apply_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------- Adafactor 1-D tensors (WG each)
+template <int G>
+__global__ __launch_bounds__(256) void ada_vec1d_kernel(const FacArgs a) {
+    __shared__ DD sh[4];
+    __shared__ double clip_s;
+    const FacDesc& d = a.D[a.n2 + blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t n = d.rows * d.cols;
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double gi = (double)grad1<G>(d.g, i);
+        const float old = vec_decode(a.v_codec, a.v_block, d.v, d.vm, i, a.cf);
+        d.rtmp[i] = (float)(a.beta * (double)old + a.omb * (gi * gi + a.eps1));
+    }
+    __syncthreads();
+    vec_encode(a.v_codec, a.v_block, d.rtmp, n, a.v_floor, d.v, d.vm, wave, 4, lane);
+    DD s{0.0, 0.0};
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double uu = (1.0 / sqrt((double)d.rtmp[i])) * (double)grad1<G>(d.g, i);
+        dd_add(s, uu * uu);
+    }
+    s = block_dd_sum(s, sh);
+    if (tid == 0) {
+        const double rms = sqrt(dd_value(s) / (double)n);
+        clip_s = rms / a.clip_d > 1.0 ? rms / a.clip_d : 1.0;
+    }
+    __syncthreads();
+    const double clip = clip_s;
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double uu = (1.0 / sqrt((double)d.rtmp[i])) * (double)grad1<G>(d.g, i);
+        const double pd = (double)d.p[i] * a.decay;
+        d.p[i] = (float)(pd - a.lr * (uu / clip));
+    }
+}
+
+hipError_t launch_ada_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.n1 == 0) return hipSuccess;
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(ada_vec1d_kernel<G_BF16>, dim3(a.n1), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(ada_vec1d_kernel<G_F32>, dim3(a.n1), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------- CAME momentum
+// In-step momentum of element e of tensor d from its uhat (binary64 EMA,
+// rounded to fp32): m = fl32(beta1 * mhat + (1 - beta1) * uhat).
+__device__ __forceinline__ float came_momentum(const FacArgs& a, const FacDesc& d, int64_t e, float uh) {
+    float mh;
+    if (a.m_codec == UF8) {
+        const int32_t q = reinterpret_cast<const int8_t*>(d.m)[e];
+        mh = uf8_decode(q, (double)d.mm[e / a.m_block] / 127.0);
+    } else {
+        mh = reinterpret_cast<const float*>(d.m)[e];
+    }
+    return (float)(a.beta1 * (double)mh + a.omb1 * (double)uh);
+}
+
+// --------------------------- CAME residual marginal sums (tile layout, fp64)
+// Term (uhat - m)^2 + eps2 with uhat = fl32(u / clip), m the in-step
+// momentum; row sums through an fp64 LDS tile.
+template <int G>
+__global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
+    __shared__ double tile[64][66];
+    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4;
+    for (int64_t unit = blockIdx.x; unit < a.total_units; unit += gridDim.x) {
+        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+        const int64_t u = unit - d.unit_begin;
+        const int64_t ru = u / d.ncu, cu = u % d.ncu;
+        const int64_t r0 = ru * 256, c0 = cu * 256;
+        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+        const double clip = d.scal[0];
+        DD cacc[4][4];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
+        for (int rt = 0; rt < 4 && rt * 64 < nr; ++rt) {
+            DD racc{0.0, 0.0};
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct) {
+                if (ct * 64 >= nc) break;
+                const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
+                double cf[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int cc = ct * 64 + 4 * lc + j;
+                    cf[j] = cc < nc ? d.cfac[c0 + cc] : 0.0;
+                }
+                for (int i = 0; i < 16; ++i) {
+                    const int rr = rt * 64 + lr + 4 * i;
+                    double term[4] = {0.0, 0.0, 0.0, 0.0};
+                    if (rr < nr) {
+                        const double ri = d.rfac[r0 + rr];
+                        const int64_t e = (r0 + rr) * d.cols + c0 + ct * 64 + 4 * lc;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            if (ct * 64 + 4 * lc + j < nc) {
+                                const double uu = (ri * cf[j]) * (double)grad1<G>(d.g, e + j);
+                                const float uh = (float)(uu / clip);
+                                const float m = came_momentum(a, d, e + j, uh);
+                                const double df = (double)uh - (double)m;
+                                term[j] = df * df + a.eps2;
+                                dd_add(cacc[ct][j], term[j]);
+                            }
+                        }
+                    }
+                    double* tp = &tile[lr + 4 * i][4 * lc];
+                    tp[0] = term[0];
+                    tp[1] = term[1];
+                    tp[2] = term[2];
+                    tp[3] = term[3];
+                }
+                __syncthreads();
+                if (rt * 64 + lane < nr)
+                    for (int c = 0; c < ncol; ++c) dd_add(racc, tile[lane][c]);
+                __syncthreads();
+            }
+            const int row = rt * 64 + lane;
+            if (row < nr) {
+                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+                rp[0] = racc.hi;
+                rp[1] = racc.lo;
+            }
+        }
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                DD v = cacc[ct][j];
+                v = dd_merge(v, dd_shfl_xor(v, 16));
+                v = dd_merge(v, dd_shfl_xor(v, 32));
+                const int col = ct * 64 + 4 * lc + j;
+                if (lr == 0 && col < nc) {
+                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    cp[0] = v.hi;
+                    cp[1] = v.lo;
+                }
+            }
+        }
+    }
+}
+
+hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_units == 0) return hipSuccess;
+    const int64_t cap = (int64_t)device_cu_count() * 4;
+    const int grid = (int)(a.total_units < cap ? a.total_units : cap);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(came_res_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
+    else
+        hipLaunchKernelGGL(came_res_kernel<G_F32>, dim3(grid), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------ CAME apply (2-D)
+// Flattened 1024-element chunks, 4 sub-tiles of 256 per wave, so each
+// momentum block (256) is one sub-tile: recompute uhat and m, encode m, and
+// p <- p (1 - lr wd) - lr (s_i s_j) m.
+template <int G>
+__global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    for (int64_t chunk = wave; chunk < a.total_chunks; chunk += nw) {
+        const FacDesc& d = a.D[locate_chunk(a.D, a.n2, chunk)];
+        const int64_t n = d.rows * d.cols;
+        const int64_t e0 = (chunk - d.chunk_begin) * 1024;
+        const double clip = d.scal[0];
+        for (int k = 0; k < 4; ++k) {
+            const int64_t sb = e0 + 256 * k;
+            if (sb >= n) break;
+            const int64_t eb = sb + 4 * lane;
+            // row / column of the lane's first element (binary64 estimate, then exact correction)
+            int64_t i = (int64_t)((double)eb / (double)d.cols);
+            int64_t jc = eb - i * d.cols;
+            while (jc < 0) {
+                --i;
+                jc += d.cols;
+            }
+            while (jc >= d.cols) {
+                ++i;
+                jc -= d.cols;
+            }
+            float mnew[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t e = eb + j;
+                if (e < n) {
+                    const double uu = (d.rfac[i] * d.cfac[jc]) * (double)grad1<G>(d.g, e);
+                    const float uh = (float)(uu / clip);
+                    const float m = came_momentum(a, d, e, uh);
+                    mnew[j] = m;
+                    const double upd = (d.sr[i] * d.sc[jc]) * (double)m;
+                    const double pd = (double)d.p[e] * a.decay;
+                    d.p[e] = (float)(pd - a.lr * upd);
+                }
+                if (++jc == d.cols) {
+                    jc = 0;
+                    ++i;
+                }
+            }
+            if (a.m_codec == UF8) {
+                uint32_t am = 0u;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
+                am = group_reduce<OpMax, 64>(am);
+                const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int32_t q = (int32_t)__builtin_rint((double)mnew[j] * r);
+                    reinterpret_cast<int8_t*>(d.m)[eb + j] = (int8_t)q;  // padded to whole blocks
+                }
+                if (lane == 0) d.mm[sb / 256] = u2f(am);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (eb + j < n) reinterpret_cast<float*>(d.m)[eb + j] = mnew[j];
+            }
+        }
+    }
+}
+
+hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_chunks == 0) return hipSuccess;
+    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t want = (a.total_chunks + 3) / 4;
+    const int grid = (int)(want < cap ? want : cap);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(came_apply_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(came_apply_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------ CAME 1-D tensors (WG each)
+template <int G>
+__global__ __launch_bounds__(256) void came_vec1d_kernel(const FacArgs a) {
+    __shared__ DD sh[4];
+    __shared__ double clip_s;
+    const FacDesc& d = a.D[a.n2 + blockIdx.x];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t n = d.rows * d.cols;
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double gi = (double)grad1<G>(d.g, i);
+        const float old = vec_decode(a.v_codec, a.v_block, d.v, d.vm, i, a.cf);
+        d.rtmp[i] = (float)(a.beta * (double)old + a.omb * (gi * gi + a.eps1));
+    }
+    __syncthreads();
+    vec_encode(a.v_codec, a.v_block, d.rtmp, n, a.v_floor, d.v, d.vm, wave, 4, lane);
+    DD s{0.0, 0.0};
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double uu = (1.0 / sqrt((double)d.rtmp[i])) * (double)grad1<G>(d.g, i);
+        dd_add(s, uu * uu);
+    }
+    s = block_dd_sum(s, sh);
+    if (tid == 0) {
+        const double rms = sqrt(dd_value(s) / (double)n);
+        clip_s = rms / a.clip_d > 1.0 ? rms / a.clip_d : 1.0;
+    }
+    __syncthreads();
+    const double clip = clip_s;
+    for (int64_t i = tid; i < n; i += blockDim.x) {
+        const double uu = (1.0 / sqrt((double)d.rtmp[i])) * (double)grad1<G>(d.g, i);
+        const float uh = (float)(uu / clip);
+        const float m = came_momentum(a, d, i, uh);
+        d.ctmp[i] = m;
+        const double pd = (double)d.p[i] * a.decay;
+        d.p[i] = (float)(pd - a.lr * (double)m);
+    }
+    __syncthreads();
+    vec_encode(a.m_codec, a.m_block, d.ctmp, n, 0.0f, d.m, d.mm, wave, 4, lane);
+}
+
+hipError_t launch_came_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.n1 == 0) return hipSuccess;
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(came_vec1d_kernel<G_BF16>, dim3(a.n1), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(came_vec1d_kernel<G_F32>, dim3(a.n1), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace al
