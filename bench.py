@@ -149,6 +149,95 @@ def copy_ceiling(n, steps=10):
     return out
 
 
+def factored_bytes_per_param(shapes, came: bool):
+    """(algorithmic, multi-pass schedule) HBM bytes per parameter of one Adafactor / CAME step on a tensor
+    list: p read+write 8, g 2, (CAME) m codes read+write 2 plus its absmax per 256; the factored vectors add
+    2 (rows + cols) x (code + meta) per 2-D tensor. The schedule re-reads g (Adafactor: marginals, RMS,
+    update = 3x; CAME: 4x) and (CAME) m once more."""
+    n = sum(s.n for s in shapes)
+    vec = 0.0
+    for s in shapes:
+        if s.is_2d:
+            k = 2 if came else 1  # CAME: V and confidence factors
+            vec += k * 2 * (s.rows + s.cols) * (2 if came else 1)  # codes read + write (AL16 2 B, AL8 1 B)
+        else:
+            vec += 2 * s.n * (2 if came else 1)
+    m = (2 + 8 / 256) if came else 0.0
+    alg = 8 + 2 + m + vec / n
+    sched = alg + (3 if came else 2) * 2 + (1 if came else 0)
+    return alg, sched
+
+
+def time_factored(came: bool, steps: int, warmup: int):
+    """One Adafactor (AL8 B256 factored + 1-D, no zero mask) or CAME (AL16 B128 V and confidence, UF8 m,
+    2% zeros) step over the TinyLlama-1.1B list, grads generated once."""
+    import torch
+
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import data
+    from paper_2608_22322_amd.workloads import tinyllama_shapes, workload_tinyllama
+
+    shapes = tinyllama_shapes()
+    w = workload_tinyllama(zero_frac=0.02 if came else 0.0)
+    dev = torch.device("cuda:0")
+    if came:
+        cfg = al.came_cfg()
+        vs, ms, cs = al.Spec(al.AL16, 128, al.log2_floor_of(1e-30)), al.Spec(al.UF8, 256), \
+            al.Spec(al.AL16, 128, al.log2_floor_of(1e-16))
+    else:
+        cfg = al.adafactor_cfg()
+        vs = al.Spec(al.AL8, 256, al.log2_floor_of(1e-30))
+    states = []
+    for i, s in enumerate(shapes):
+        st = al.ParamState(data.device_param(i, s, dev), data.device_grad_buffer(s, w, dev), s.rows, s.cols)
+        data.fill_grad(st.grad, i, s, w, 1)
+        if s.is_2d:
+            st.vr, st.vr_meta = al.alloc_state(s.rows, vs, dev)
+            st.vc, st.vc_meta = al.alloc_state(s.cols, vs, dev)
+            if came:
+                st.cr, st.cr_meta = al.alloc_state(s.rows, cs, dev)
+                st.cc, st.cc_meta = al.alloc_state(s.cols, cs, dev)
+        else:
+            st.v, st.v_meta = al.alloc_state(s.n, vs, dev)
+        if came:
+            st.m, st.m_meta = al.alloc_state(s.n, ms, dev)
+        states.append(st)
+    arr = al.tensor_array(states)
+    nbytes = al.came_workspace_bytes(states, cfg, arr=arr) if came else al.adafactor_workspace_bytes(states, cfg,
+                                                                                                        arr=arr)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    stepf = al.came_step if came else al.adafactor_step
+    stream = torch.cuda.current_stream()
+    t = 0
+    for _ in range(warmup):
+        t += 1
+        stepf(states, cfg, t, ws, stream=stream, arr=arr)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        t += 1
+        evs[k][0].record(stream)
+        stepf(states, cfg, t, ws, stream=stream, arr=arr)
+        evs[k][1].record(stream)
+    torch.cuda.synchronize()
+    ms_ = [a.elapsed_time(b) for a, b in evs]
+    mean = sum(ms_) / len(ms_)
+    n = sum(s.n for s in shapes)
+    alg, sched = factored_bytes_per_param(shapes, came)
+    rec = {"workload": "tinyllama-1.1b list (201 tensors), " + ("CAME: AL16 B128 V and confidence, UF8 m B256, "
+                                                               "2% zero grads" if came else
+                                                               "Adafactor: AL8 B256 factored V and 1-D v"),
+           "params": n, "ms_mean": round(mean, 4), "ms_min": round(min(ms_), 4),
+           "gparams_s": round(n / (mean * 1e-3) / 1e9, 2),
+           "algorithmic_bytes_per_param": round(alg, 4), "schedule_bytes_per_param": round(sched, 4),
+           "algorithmic_gbs": round(alg * n / (mean * 1e-3) / 1e9, 1),
+           "frac_of_peak": round(alg * n / (mean * 1e-3) / 1e9 / PEAK_GBS, 4),
+           "workspace_bytes": nbytes}
+    del states, ws
+    torch.cuda.empty_cache()
+    return rec
+
+
 def cpu_baseline(shapes, block_v):
     """The oracle, untuned, on a bounded sample: layer 0's seven weight matrices, two steps. Inputs for this
     timing-only leg are drawn with numpy's generator (same shapes and distributions as the workload: params
@@ -188,6 +277,7 @@ def main():
     ap.add_argument("--block", type=int, default=2048, help="headline B_V (2048: the paper's AdamW configuration)")
     ap.add_argument("--sweep", default="64,128,256,2048", help="B_V values to time ('' for headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-paths", action="store_true", help="skip the Adafactor / CAME timings")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the step needs no collective and every box here has one GPU "
@@ -227,6 +317,8 @@ def main():
         if b == args.block:
             head = (rec, ms, wall, bpp)
     rec, ms, wall, bpp = head
+    del states
+    torch.cuda.empty_cache()
     ceil = copy_ceiling(n // 4)
     log("copy ceiling: " + json.dumps(ceil))
     mean = rec["ms_mean"]
@@ -260,6 +352,12 @@ def main():
                                                                                          ceil["nontemporal"]), 4)},
         "sweep": sweep,
     }
+    if not args.no_paths:
+        paths = {}
+        for name, came in (("adafactor", False), ("came", True)):
+            paths[name] = time_factored(came, args.steps, args.warmup)
+            log(name + ": " + json.dumps(paths[name]))
+        out["paths"] = paths
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(shapes, args.block)

@@ -190,17 +190,18 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
         const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
         const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
         const bool vec = (d.cols & 3) == 0;
-        DD cacc[4][4];
+        DD racc[4];
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
+        for (int rt = 0; rt < 4; ++rt) racc[rt] = DD{0.0, 0.0};
+        for (int ct = 0; ct < 4 && ct * 64 < nc; ++ct) {
+            const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
+            DD cacc[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
-        for (int rt = 0; rt < 4 && rt * 64 < nr; ++rt) {
-            DD racc{0.0, 0.0};
+            for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
 #pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
-                if (ct * 64 >= nc) break;
-                const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
+            for (int rt = 0; rt < 4; ++rt) {
+                if (rt * 64 >= nr) break;
+#pragma unroll 4
                 for (int i = 0; i < 16; ++i) {
                     const int rr = rt * 64 + lr + 4 * i;
                     const int cc = ct * 64 + 4 * lc;
@@ -218,7 +219,7 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
                         for (int j = 0; j < 4; ++j) {
                             if (cc + j < nc) {
                                 const double x = (double)gv[j];
-                                dd_add(cacc[ct][j], x * x + a.eps1);
+                                dd_add(cacc[j], x * x + a.eps1);
                             }
                         }
                     }
@@ -231,32 +232,23 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
                         for (int c = 0; c < 64; c += 4) {
                             const float4 t = *reinterpret_cast<const float4*>(&tile[lane][c]);
                             const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
-                            dd_add(racc, x0 * x0 + a.eps1);
-                            dd_add(racc, x1 * x1 + a.eps1);
-                            dd_add(racc, x2 * x2 + a.eps1);
-                            dd_add(racc, x3 * x3 + a.eps1);
+                            dd_add(racc[rt], x0 * x0 + a.eps1);
+                            dd_add(racc[rt], x1 * x1 + a.eps1);
+                            dd_add(racc[rt], x2 * x2 + a.eps1);
+                            dd_add(racc[rt], x3 * x3 + a.eps1);
                         }
                     } else {
                         for (int c = 0; c < ncol; ++c) {
                             const double x = tile[lane][c];
-                            dd_add(racc, x * x + a.eps1);
+                            dd_add(racc[rt], x * x + a.eps1);
                         }
                     }
                 }
                 __syncthreads();
             }
-            const int row = rt * 64 + lane;
-            if (row < nr) {
-                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
-                rp[0] = racc.hi;
-                rp[1] = racc.lo;
-            }
-        }
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                DD v = cacc[ct][j];
+                DD v = cacc[j];
                 v = dd_merge(v, dd_shfl_xor(v, 16));
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = ct * 64 + 4 * lc + j;
@@ -265,6 +257,15 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
                     cp[0] = v.hi;
                     cp[1] = v.lo;
                 }
+            }
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            const int row = rt * 64 + lane;
+            if (row < nr) {
+                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+                rp[0] = racc[rt].hi;
+                rp[1] = racc[rt].lo;
             }
         }
     }
@@ -562,39 +563,73 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
         const int64_t r0 = ru * 256, c0 = cu * 256;
         const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
         const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+        const bool vec = (d.cols & 3) == 0;
         const double clip = d.scal[0];
-        DD cacc[4][4];
+        DD racc[4];
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct)
+        for (int rt = 0; rt < 4; ++rt) racc[rt] = DD{0.0, 0.0};
+        for (int ct = 0; ct < 4 && ct * 64 < nc; ++ct) {
+            const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
+            const int cc = ct * 64 + 4 * lc;  // column of this lane's first element within the unit
+            double cf[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
-        for (int rt = 0; rt < 4 && rt * 64 < nr; ++rt) {
-            DD racc{0.0, 0.0};
+            for (int j = 0; j < 4; ++j) cf[j] = cc + j < nc ? d.cfac[c0 + cc + j] : 0.0;
+            DD cacc[4];
 #pragma unroll
-            for (int ct = 0; ct < 4; ++ct) {
-                if (ct * 64 >= nc) break;
-                const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
-                double cf[4];
+            for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int cc = ct * 64 + 4 * lc + j;
-                    cf[j] = cc < nc ? d.cfac[c0 + cc] : 0.0;
-                }
+            for (int rt = 0; rt < 4; ++rt) {
+                if (rt * 64 >= nr) break;
+#pragma unroll 2
                 for (int i = 0; i < 16; ++i) {
                     const int rr = rt * 64 + lr + 4 * i;
                     double term[4] = {0.0, 0.0, 0.0, 0.0};
                     if (rr < nr) {
                         const double ri = d.rfac[r0 + rr];
-                        const int64_t e = (r0 + rr) * d.cols + c0 + ct * 64 + 4 * lc;
+                        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+                        float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                        float mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                        const bool full = vec && cc + 4 <= nc;
+                        if (full) {
+                            grad4<G>(d.g, e, gv);
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
+                        }
+                        if (a.m_codec == UF8) {
+                            // the lane's 4 elements share a momentum block unless they straddle one
+                            const int64_t b0 = e / 256, b3 = (e + 3) / 256;
+                            const double st0 = (double)d.mm[b0] / 127.0;
+                            const double st3 = b3 == b0 ? st0 : (double)d.mm[b3] / 127.0;
+                            uint32_t w;
+                            if (full && (e & 3) == 0) {
+                                w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                            } else {
+                                w = 0u;
+#pragma unroll
+                                for (int j = 0; j < 4; ++j)
+                                    if (cc + j < nc) w |= (uint32_t)reinterpret_cast<const uint8_t*>(d.m)[e + j] << (8 * j);
+                            }
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                const double st = (e + j) / 256 == b0 ? st0 : st3;
+                                mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
+                            }
+                        } else {
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                if (cc + j < nc) mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
+                        }
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
-                            if (ct * 64 + 4 * lc + j < nc) {
-                                const double uu = (ri * cf[j]) * (double)grad1<G>(d.g, e + j);
+                            if (cc + j < nc) {
+                                const double uu = (ri * cf[j]) * (double)gv[j];
                                 const float uh = (float)(uu / clip);
-                                const float m = came_momentum(a, d, e + j, uh);
+                                const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
                                 const double df = (double)uh - (double)m;
                                 term[j] = df * df + a.eps2;
-                                dd_add(cacc[ct][j], term[j]);
+                                dd_add(cacc[j], term[j]);
                             }
                         }
                     }
@@ -606,29 +641,29 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
                 }
                 __syncthreads();
                 if (rt * 64 + lane < nr)
-                    for (int c = 0; c < ncol; ++c) dd_add(racc, tile[lane][c]);
+                    for (int c = 0; c < ncol; ++c) dd_add(racc[rt], tile[lane][c]);
                 __syncthreads();
             }
-            const int row = rt * 64 + lane;
-            if (row < nr) {
-                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
-                rp[0] = racc.hi;
-                rp[1] = racc.lo;
-            }
-        }
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                DD v = cacc[ct][j];
+                DD v = cacc[j];
                 v = dd_merge(v, dd_shfl_xor(v, 16));
                 v = dd_merge(v, dd_shfl_xor(v, 32));
-                const int col = ct * 64 + 4 * lc + j;
+                const int col = cc + j;
                 if (lr == 0 && col < nc) {
                     double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
                     cp[0] = v.hi;
                     cp[1] = v.lo;
                 }
+            }
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            const int row = rt * 64 + lane;
+            if (row < nr) {
+                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+                rp[0] = racc[rt].hi;
+                rp[1] = racc[rt].lo;
             }
         }
     }
@@ -659,6 +694,65 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
         const int64_t n = d.rows * d.cols;
         const int64_t e0 = (chunk - d.chunk_begin) * 1024;
         const double clip = d.scal[0];
+        if ((d.cols & 255) == 0 && e0 + 1024 <= n) {
+            // every 256-element sub-tile lies in one row: row factors are uniform,
+            // column factors are 4 consecutive values per lane, loads are vectors
+            for (int k = 0; k < 4; ++k) {
+                const int64_t sb = e0 + 256 * k;
+                const int64_t i = sb / d.cols;
+                const int64_t jc = sb - i * d.cols + 4 * lane;
+                const int64_t eb = sb + 4 * lane;
+                const double ri = d.rfac[i], si = d.sr[i];
+                const double2 c01 = *reinterpret_cast<const double2*>(d.cfac + jc);
+                const double2 c23 = *reinterpret_cast<const double2*>(d.cfac + jc + 2);
+                const double2 s01 = *reinterpret_cast<const double2*>(d.sc + jc);
+                const double2 s23 = *reinterpret_cast<const double2*>(d.sc + jc + 2);
+                const double cfj[4] = {c01.x, c01.y, c23.x, c23.y};
+                const double sfj[4] = {s01.x, s01.y, s23.x, s23.y};
+                float gv[4], mh[4];
+                grad4<G>(d.g, eb, gv);
+                const float4 pv = *reinterpret_cast<const float4*>(d.p + eb);
+                const float pin[4] = {pv.x, pv.y, pv.z, pv.w};
+                if (a.m_codec == UF8) {
+                    const double st = (double)d.mm[sb / 256] / 127.0;
+                    const uint32_t w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + eb);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
+                } else {
+                    const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + eb);
+                    mh[0] = t.x;
+                    mh[1] = t.y;
+                    mh[2] = t.z;
+                    mh[3] = t.w;
+                }
+                float mnew[4], pout[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const double uu = (ri * cfj[j]) * (double)gv[j];
+                    const float uh = (float)(uu / clip);
+                    mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
+                    const double upd = (si * sfj[j]) * (double)mnew[j];
+                    pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+                }
+                *reinterpret_cast<float4*>(d.p + eb) = make_float4(pout[0], pout[1], pout[2], pout[3]);
+                if (a.m_codec == UF8) {
+                    uint32_t am = 0u;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
+                    am = group_reduce<OpMax, 64>(am);
+                    const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+                    uint32_t q[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * r) & 0xFFu;
+                    store_codes4<UF8>(d.m, eb, q);
+                    if (lane == 0) d.mm[sb / 256] = u2f(am);
+                } else {
+                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.m) + eb) =
+                        make_float4(mnew[0], mnew[1], mnew[2], mnew[3]);
+                }
+            }
+            continue;
+        }
         for (int k = 0; k < 4; ++k) {
             const int64_t sb = e0 + 256 * k;
             if (sb >= n) break;
