@@ -162,3 +162,126 @@ def test_adamw_validation():
     _adamw([_t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None)])
     _adamw([])
     assert "NULL" not in al.lib().al_last_error().decode()
+
+
+# ----------------------------------------------------------------- factored paths (Adafactor, CAME)
+def _ft(rows=8, cols=256, came=False, **kw):
+    """A fake 2-D (rows > 1) or 1-D tensor with the slots the factored paths expect."""
+    base = dict(param=A, grad=A, rows=rows, cols=cols)
+    if rows > 1:
+        base.update(vr=A, vr_meta=A, vc=A, vc_meta=A)
+        if came:
+            base.update(cr=A, cr_meta=A, cc=A, cc_meta=A)
+    else:
+        base.update(v=A, v_meta=A)
+    if came:
+        base.update(m=A, m_meta=A)
+    base.update(kw)
+    return al.Tensor(**base)
+
+
+def _fac_ws(ts, came, cfg=None):
+    arr = (al.Tensor * max(len(ts), 1))(*ts)
+    out = ctypes.c_size_t(0)
+    if came:
+        cfg = cfg or al.came_cfg()
+        al.check(al.lib().al_came_workspace_bytes(arr, len(ts), ctypes.byref(cfg), ctypes.byref(out)))
+    else:
+        cfg = cfg or al.adafactor_cfg()
+        al.check(al.lib().al_adafactor_workspace_bytes(arr, len(ts), ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def _fac_step(ts, came, cfg=None, step=1, ws=A, ws_bytes=None, nt=None):
+    arr = (al.Tensor * max(len(ts), 1))(*ts)
+    if ws_bytes is None:
+        ws_bytes = _fac_ws(ts, came, cfg) if ts else 0
+    n = len(ts) if nt is None else nt
+    if came:
+        cfg = cfg or al.came_cfg()
+        al.check(al.lib().al_came_step(arr, n, ctypes.byref(cfg), step, ws, ws_bytes, None))
+    else:
+        cfg = cfg or al.adafactor_cfg()
+        al.check(al.lib().al_adafactor_step(arr, n, ctypes.byref(cfg), step, ws, ws_bytes, None))
+
+
+@pytest.mark.parametrize("came", [False, True])
+def test_factored_validation_shapes_and_slots(came):
+    good = [_ft(came=came), _ft(rows=1, cols=512, came=came)]
+    assert _status(lambda: _fac_step(good, came, step=0)) == 1
+    assert _status(lambda: _fac_step(good, came, nt=-1)) == 1
+    assert _status(lambda: _fac_step([_ft(rows=-2, came=came)], came, ws_bytes=1 << 20)) == 1
+    assert _status(lambda: _fac_step([_ft(came=came, param=None)], came, ws_bytes=1 << 20)) == 1
+    assert _status(lambda: _fac_step([_ft(came=came, grad=A + 2)], came, ws_bytes=1 << 20)) == 2
+    # a 2-D tensor needs its row and column factors and must not carry an unfactored v
+    assert _status(lambda: _fac_step([_ft(came=came, vr=None)], came, ws_bytes=1 << 20)) == 1
+    assert _status(lambda: _fac_step([_ft(came=came, vc_meta=None)], came, ws_bytes=1 << 20)) == 1
+    assert _status(lambda: _fac_step([_ft(came=came, vc=A + 8)], came, ws_bytes=1 << 20)) == 2
+    assert _status(lambda: _fac_step([_ft(came=came, v=A, v_meta=A)], came, ws_bytes=1 << 20)) == 1
+    # a 1-D tensor keeps an unfactored v and no factors
+    assert _status(lambda: _fac_step([_ft(rows=1, came=came, v=None)], came, ws_bytes=1 << 20)) == 1
+    assert _status(lambda: _fac_step([_ft(rows=1, came=came, vr=A, vr_meta=A)], came, ws_bytes=1 << 20)) == 1
+    if came:
+        assert _status(lambda: _fac_step([_ft(came=True, cr=None)], True, ws_bytes=1 << 20)) == 1
+        assert _status(lambda: _fac_step([_ft(came=True, m=None)], True, ws_bytes=1 << 20)) == 1
+        assert _status(lambda: _fac_step([_ft(rows=1, came=True, cc=A, cc_meta=A)], True, ws_bytes=1 << 20)) == 1
+    else:
+        # Adafactor keeps no momentum and no confidence factors
+        assert _status(lambda: _fac_step([_ft(m=A, m_meta=A)], False, ws_bytes=1 << 20)) == 1
+        assert _status(lambda: _fac_step([_ft(cr=A, cr_meta=A)], False, ws_bytes=1 << 20)) == 1
+    # empty tensors and empty lists enqueue nothing and need no workspace
+    _fac_step([_ft(rows=0, cols=0, came=came, param=None, grad=None)], came, ws=None, ws_bytes=0)
+    _fac_step([], came, ws=None, ws_bytes=0)
+
+
+@pytest.mark.parametrize("came", [False, True])
+def test_factored_validation_workspace(came):
+    ts = [_ft(rows=300, cols=66, came=came), _ft(rows=1, cols=777, came=came), _ft(rows=5, cols=7, came=came)]
+    need = _fac_ws(ts, came)
+    assert need > 0 and need % 256 == 0
+    assert _status(lambda: _fac_step(ts, came, ws=None, ws_bytes=need)) == 3
+    assert _status(lambda: _fac_step(ts, came, ws_bytes=need - 1)) == 3
+    assert _status(lambda: _fac_step(ts, came, ws=A + 16, ws_bytes=need)) == 2
+    assert "workspace" in al.lib().al_last_error().decode()
+    # the column and row partials are double-double pairs: at least n/8 bytes per factored tensor
+    assert need >= (300 * 66 + 5 * 7) // 8
+    assert _fac_ws(ts + [_ft(rows=64, cols=4096, came=came)], came) > need
+    arr = (al.Tensor * 1)()
+    cfg = al.came_cfg() if came else al.adafactor_cfg()
+    fn = al.lib().al_came_workspace_bytes if came else al.lib().al_adafactor_workspace_bytes
+    assert _status(lambda: al.check(fn(arr, 0, ctypes.byref(cfg), None))) == 1
+
+
+def test_adafactor_cfg_validation():
+    t = [_ft()]
+    bad = [dict(lr=-1.0), dict(eps1=math.nan), dict(clip_threshold=0.0), dict(decay_rate=0.5),
+           dict(weight_decay=-0.1)]
+    for kw in bad:
+        assert _status(lambda: _fac_step(t, False, cfg=al.adafactor_cfg(**kw), ws_bytes=1 << 20)) == 1, kw
+    for spec in (al.Spec(al.UF8, 256), al.Spec(al.AL8, 96), al.Spec(al.AL8, 256, math.inf)):
+        assert _status(lambda: _fac_step(t, False, cfg=al.adafactor_cfg(v=spec), ws_bytes=1 << 20)) == 1, spec
+    cfg = al.adafactor_cfg()
+    cfg.grad_dtype = 9
+    assert _status(lambda: _fac_step(t, False, cfg=cfg, ws_bytes=1 << 20)) == 1
+
+
+def test_came_cfg_validation():
+    t = [_ft(came=True)]
+    bad = [dict(beta1=1.0), dict(beta2=-0.1), dict(beta3=1.5), dict(eps2=-1.0, conf=al.Spec(al.AL16, 128, -53.0)), dict(clip_threshold=-1.0),
+           dict(lr=math.inf)]
+    for kw in bad:
+        assert _status(lambda: _fac_step(t, True, cfg=al.came_cfg(**kw), ws_bytes=1 << 20)) == 1, kw
+    for kw in (dict(m=al.Spec(al.AL8, 256)), dict(v=al.Spec(al.UF8, 256)), dict(conf=al.Spec(al.UF8, 256)),
+               dict(conf=al.Spec(al.AL16, 4096))):
+        assert _status(lambda: _fac_step(t, True, cfg=al.came_cfg(**kw), ws_bytes=1 << 20)) == 1, kw
+    assert _status(lambda: _fac_step(t, True, cfg=al.came_cfg(m=al.Spec(al.UF8, 128)), ws_bytes=1 << 20)) == 4
+
+
+def test_tinyllama_workspace_sizes():
+    """Workspace for the full TinyLlama list: descriptor table, RMS partials and per-tensor partials."""
+    shapes = tinyllama_shapes()
+    for came in (False, True):
+        ts = [_ft(rows=s.rows, cols=s.cols, came=came) for s in shapes]
+        need = _fac_ws(ts, came)
+        two_d = sum(s.n for s in shapes if s.rows > 1)
+        assert two_d / 8 <= need <= two_d / 8 * 1.2, (came, need)

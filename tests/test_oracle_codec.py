@@ -155,6 +155,26 @@ def test_al8_uses_every_level():
     assert set(np.unique(codes).tolist()) == set(range(1, 256))
 
 
+def test_al16_uses_every_level():
+    """AL16 has 65,535 positive levels (section 4.1). Blocks with endpoints 1 and 2 (l_min 0, width 1)
+    and interior values placed on the level grid reach every code exactly once per level."""
+    L2 = 65534
+    B = 2048
+    levels = np.arange(L2 + 1, dtype=np.float64)  # code - 1
+    per = B - 2
+    nblk = -(-levels.shape[0] // per)
+    x = np.empty(nblk * B, np.float32)
+    for b in range(nblk):
+        k = levels[b * per:(b + 1) * per]
+        k = np.concatenate([k, np.full(per - k.shape[0], k[-1])])
+        x[b * B:(b + 1) * B] = _f32(np.concatenate([[1.0, 2.0], np.exp2(k / L2)]))
+    codes, meta, _ = oracle.al_quantize(16, x, B, -126.0)
+    assert np.all(meta[0::2] == 0.0) and np.all(meta[1::2] == 1.0)
+    assert set(np.unique(codes).tolist()) == set(range(1, 65536))
+    interior = codes.reshape(nblk, B)[:, 2:].reshape(-1)[: levels.shape[0]]
+    assert np.array_equal(interior.astype(np.int64), levels.astype(np.int64) + 1)
+
+
 def test_block_below_floor_decodes_to_floor():
     """Every value below the floor: interval width clamps, all codes 1, decode 2^floor."""
     x = _f32([2.0**-80, 2.0**-70, 2.0**-60])

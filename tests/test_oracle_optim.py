@@ -89,6 +89,24 @@ def test_adamw_dormant_entries():
             assert np.all(v.codes > 0)
 
 
+def test_adamw_first_live_step_from_zero_state():
+    """An entry whose gradient was exactly zero so far has decoded state exactly 0, so on its first
+    nonzero gradient the moments reduce to m = fl32((1 - beta1) g), v = fl32((1 - beta2) g^2)."""
+    n = 4096
+    p = _param(n, 31)
+    m, v = State(FP32, n), State(FP32, n)
+    b1, b2 = 0.9, 0.999
+    zero = np.zeros(n, np.float32)
+    for t in (1, 2, 3):
+        oracle.adamw_step(p, zero, m, v, t, beta1=b1, beta2=b2)
+        assert not m.codes.any() and not v.codes.any()
+    g = synth.normal_f32(synth.grad_key(31, 4), n, 1e-3)
+    oracle.adamw_step(p, g, m, v, 4, beta1=b1, beta2=b2)
+    g64 = g.astype(np.float64)
+    assert np.array_equal(m.codes, ((1.0 - b1) * g64).astype(np.float32))
+    assert np.array_equal(v.codes, ((1.0 - b2) * (g64 * g64)).astype(np.float32))
+
+
 def test_adamw_quantized_close_to_fp32():
     """AL8 second moment + UF8 momentum stays close to the FP32 trajectory (qualitative)."""
     n = 256 * 64
@@ -140,6 +158,21 @@ def test_adafactor_fp32_matches_hf(shape):
         np.testing.assert_allclose(vc.codes, st["exp_avg_sq_col"].numpy(), rtol=2e-6)
     else:
         np.testing.assert_allclose(v.codes, st["exp_avg_sq"].numpy(), rtol=2e-6)
+
+
+def test_adafactor_first_step_factors_are_exact_means():
+    """At t = 1 the decay 1 - t^-0.8 is 0, so R and C are the exactly rounded row and column means of
+    g^2 + eps1 (reference sums by math.fsum; a transposed reduction fails on a non-square matrix)."""
+    rows, cols = 12, 37
+    g = _grads(rows, cols, 1, 33, zero_frac=0.05)[0]
+    p = _param(rows * cols, 34)
+    vr, vc = State(FP32, rows), State(FP32, cols)
+    oracle.adafactor_step(p, g, rows, cols, vr, vc, None, 1, lr=1e-3, eps1=1e-30)
+    g2 = g.astype(np.float64).reshape(rows, cols) ** 2 + 1e-30
+    want_r = np.array([math.fsum(g2[i]) / cols for i in range(rows)]).astype(np.float32)
+    want_c = np.array([math.fsum(g2[:, j]) / rows for j in range(cols)]).astype(np.float32)
+    assert np.array_equal(vr.codes, want_r)
+    assert np.array_equal(vc.codes, want_c)
 
 
 def test_adafactor_rank1_closed_form():
