@@ -17,13 +17,26 @@
 // moment (the binary64 divisions and endpoint logarithms of up to 16 blocks)
 // runs once per chunk with one block per lane, and the results are broadcast
 // back (readlane for blocks that span whole sub-tiles, ds_bpermute for
-// smaller ones). Waves stride over the launch's chunks; the
-// chunk -> tensor map is a binary search over the descriptor table held in
-// the kernel arguments.
+// smaller ones). The grid holds one wave per chunk, and the chunk -> tensor
+// map is a binary search over the descriptor table held in the kernel
+// arguments. Full chunks use non-temporal loads and stores: every byte of
+// the step is touched exactly once.
 #include "al_device.hpp"
 #include "al_internal.hpp"
 
+#ifndef AL_ADAMW_NT_LOAD
+#define AL_ADAMW_NT_LOAD 1
+#endif
+#ifndef AL_ADAMW_NT_STORE
+#define AL_ADAMW_NT_STORE 1
+#endif
+
 namespace al {
+
+// Every byte the step touches is read once and written once, so the full-chunk
+// path may mark its loads and stores non-temporal (streaming).
+constexpr bool kNtLoad = AL_ADAMW_NT_LOAD != 0;
+constexpr bool kNtStore = AL_ADAMW_NT_STORE != 0;
 
 template <int MC, int VC, int BV>
 struct Geo {
@@ -83,21 +96,21 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc&
         const int rel = (ph * R::P + k) * kSub + 4 * lane;
         const int64_t e = e0 + rel;
         if constexpr (FULL) {
-            r.p[k] = *reinterpret_cast<const float4*>(d.p + e);
+            r.p[k] = ld_f4<kNtLoad>(d.p + e);
             if constexpr (G == G_BF16)
-                r.g[k] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.g) + e);
+                r.g[k] = ld_u2<kNtLoad>(reinterpret_cast<const uint16_t*>(d.g) + e);
             else
-                r.g[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.g) + e);
+                r.g[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.g) + e);
             if constexpr (MC == UF8)
-                r.m[k] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                r.m[k] = ld_u1<kNtLoad>(reinterpret_cast<const uint8_t*>(d.m) + e);
             else
-                r.m[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
+                r.m[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.m) + e);
             if constexpr (VC == AL16)
-                r.v[k] = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.v) + e);
+                r.v[k] = ld_u2<kNtLoad>(reinterpret_cast<const uint16_t*>(d.v) + e);
             else if constexpr (VC == AL8)
-                r.v[k] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.v) + e);
+                r.v[k] = ld_u1<kNtLoad>(reinterpret_cast<const uint8_t*>(d.v) + e);
             else
-                r.v[k] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.v) + e);
+                r.v[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.v) + e);
         } else {
             float pp[4];
             uint32_t gb[4], mb[4], vb[4];
@@ -190,6 +203,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
     // wavefront's LDS slice (4 levels per lane) -- 255 evaluations per block
     // instead of one per element. LDS traffic of one wavefront is ordered, so
     // no barrier is needed between building and reading its own table.
+    // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q.
     if constexpr (Q::LUT) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
@@ -198,7 +212,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int k = lane + 64 * i;
-                if (k < LEVELS + 1) lut[b * 256 + k] = (float)exp2_d(l32 + (double)k * st, a.cf);
+                const float lv = (float)exp2_d(l32 + (double)(k - 1) * st, a.cf);
+                lut[b * 256 + k] = k == 0 ? 0.0f : lv;
             }
         }
     }
@@ -229,11 +244,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         if constexpr (Q::LUT) {
             const float* t = lut + (k * kSub / BV) * 256;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const float lv = t[q == 0u ? 0u : q - 1u];
-                vh[j] = q == 0u ? 0.0f : lv;
-            }
+            for (int j = 0; j < 4; ++j) vh[j] = t[(r.v[kk] >> (8 * j)) & 0xFFu];
         } else if constexpr (VQ) {
             double vstep, vl32;
             if constexpr (BV >= kSub) {
@@ -273,7 +284,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 if (rel + j >= valid) mn[j] = vn[j] = 0.0f;  // absent: no state, no reduction input
         }
         if constexpr (FULL) {
-            *reinterpret_cast<float4*>(d.p + e) = make_float4(pn[0], pn[1], pn[2], pn[3]);
+            st_f4<kNtStore>(d.p + e, make_float4(pn[0], pn[1], pn[2], pn[3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
@@ -290,11 +301,11 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 #pragma unroll
             for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mn[j] * rr) & 0xFFu;
             if (FULL || k * kSub < valid) {
-                store_codes4<UF8>(d.m, e, q);
+                store_codes4<UF8, FULL && kNtStore>(d.m, e, q);
                 if (lane == 0) d.ms[e0 / kSub + k] = u2f(am);
             }
         } else if constexpr (FULL) {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.m) + e) = make_float4(mn[0], mn[1], mn[2], mn[3]);
+            st_f4<kNtStore>(reinterpret_cast<float*>(d.m) + e, make_float4(mn[0], mn[1], mn[2], mn[3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
@@ -304,12 +315,14 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             const int s = BV < kSub ? k : k * kSub / BV;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
+                // vn >= 0 here, so its bit pattern orders it; bits - 1 sends
+                // +0 to the largest key, out of the positive minimum
                 vk[k][j] = vn[j];
-                vmn[s] = OpMin::f(vmn[s], pos_min_key(vn[j]));
-                vmx[s] = OpMax::f(vmx[s], pos_max_key(vn[j]));
+                vmn[s] = OpMin::f(vmn[s], f2u(vn[j]) - 1u);
+                vmx[s] = OpMax::f(vmx[s], f2u(vn[j]));
             }
         } else if constexpr (FULL) {
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.v) + e) = make_float4(vn[0], vn[1], vn[2], vn[3]);
+            st_f4<kNtStore>(reinterpret_cast<float*>(d.v) + e, make_float4(vn[0], vn[1], vn[2], vn[3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
@@ -320,7 +333,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         // -------------------------------------------- 3. second-moment block reductions
 #pragma unroll
         for (int s = 0; s < Q::NSLOT; ++s) {
-            vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]);
+            vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]) + 1u;  // back to bits; 0 when no positive
             vmx[s] = group_reduce<OpMax, Q::GL>(vmx[s]);
         }
 
@@ -380,14 +393,19 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             uint32_t q[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) q[j] = al_encode_fast<LEVELS>(vk[k][j], enc);
-            if (live) store_codes4<VC>(d.v, e, q);
+            if (live) store_codes4<VC, FULL && kNtStore>(d.v, e, q);
         }
     }
 }
 
-#ifndef AL_ADAMW_WAVES_PER_EU
-#define AL_ADAMW_WAVES_PER_EU 2
-#endif
+// Waves per SIMD the register allocator targets: 3 (at most 168 VGPRs) where
+// the chunk is 1024 elements, which hides more memory latency behind the
+// per-element decode/encode; 2 for 2048-element chunks, whose registers do not
+// fit 168 without spilling.
+template <int BV>
+constexpr int adamw_waves_per_eu() {
+    return BV >= 2048 ? 2 : 3;
+}
 
 // largest ti with t[ti].tile_begin <= chunk
 __device__ __forceinline__ int locate(const AdamWLaunch& a, int64_t chunk) {
@@ -402,11 +420,11 @@ __device__ __forceinline__ int locate(const AdamWLaunch& a, int64_t chunk) {
     return lo;
 }
 
-// Waves stride over the launch's chunks; each wave issues the loads of up to 4
-// sub-tiles (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it
+// One chunk per wave (waves stride only if a launch exceeds 2^30 workgroups);
+// each wave issues the loads of up to 4 sub-tiles (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it
 // computes on them. A chunk that ends a tensor takes the guarded path.
 template <int G, int MC, int VC, int BV>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(AL_ADAMW_WAVES_PER_EU)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(adamw_waves_per_eu<BV>())))
 void adamw_kernel(const AdamWLaunch a) {
     constexpr int C = Geo<MC, VC, BV>::C;
     const int lane = threadIdx.x & 63;
@@ -432,10 +450,18 @@ int adamw_tile_elems(int v_codec, int v_block) {
     return v_block > 1024 ? v_block : 1024;
 }
 
-// Persistent grid: exactly as many workgroups as can be resident at once
-// (occupancy of this instantiation x compute units), capped by the work.
+#ifndef AL_ADAMW_PERSISTENT
+#define AL_ADAMW_PERSISTENT 0
+#endif
+
+// One chunk per wave: the grid covers every chunk of the launch, and the
+// hardware dispatcher refills each CU as its waves retire. (A persistent grid
+// sized by occupancy moves the same byte mix about 6% slower on gfx950.)
 template <int G, int MC, int VC, int BV>
 static hipError_t launch_t(const AdamWLaunch& a, int grid_cap, hipStream_t s) {
+    const int64_t want = (a.total_tiles + 3) / 4;
+    int64_t grid = want;
+#if AL_ADAMW_PERSISTENT
     static int per_cu = 0;
     if (per_cu == 0) {
         int n = 0;
@@ -444,10 +470,13 @@ static hipError_t launch_t(const AdamWLaunch& a, int grid_cap, hipStream_t s) {
             n = 2;
         per_cu = n;
     }
-    const int64_t want = (a.total_tiles + 3) / 4;
-    int64_t grid = (int64_t)per_cu * device_cu_count();
+    grid = (int64_t)per_cu * device_cu_count();
     if (grid > want) grid = want;
     if (grid > grid_cap) grid = grid_cap;
+#else
+    (void)grid_cap;
+    if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;  // waves then stride over the remaining chunks
+#endif
     hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3((unsigned)grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }

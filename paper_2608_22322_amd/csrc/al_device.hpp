@@ -325,14 +325,66 @@ __device__ __forceinline__ uint32_t load_code1(const void* c, int64_t e) {
         return reinterpret_cast<const uint16_t*>(c)[e];
 }
 
-template <int C>
+// Streaming (non-temporal) or ordinary vector loads and stores of 16, 8 and 4
+// bytes. The non-temporal builtins take clang vector types, not HIP's structs.
+typedef float nt_f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nt_u2 __attribute__((ext_vector_type(2)));
+
+template <bool NT>
+__device__ __forceinline__ float4 ld_f4(const float* p) {
+    if constexpr (NT) {
+        const nt_f4 x = __builtin_nontemporal_load(reinterpret_cast<const nt_f4*>(p));
+        return make_float4(x.x, x.y, x.z, x.w);
+    } else {
+        return *reinterpret_cast<const float4*>(p);
+    }
+}
+template <bool NT>
+__device__ __forceinline__ uint2 ld_u2(const void* p) {
+    if constexpr (NT) {
+        const nt_u2 x = __builtin_nontemporal_load(reinterpret_cast<const nt_u2*>(p));
+        return make_uint2(x.x, x.y);
+    } else {
+        return *reinterpret_cast<const uint2*>(p);
+    }
+}
+template <bool NT>
+__device__ __forceinline__ uint32_t ld_u1(const void* p) {
+    if constexpr (NT)
+        return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
+    else
+        return *reinterpret_cast<const uint32_t*>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st_f4(float* p, const float4& x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(nt_f4{x.x, x.y, x.z, x.w}, reinterpret_cast<nt_f4*>(p));
+    else
+        *reinterpret_cast<float4*>(p) = x;
+}
+template <bool NT>
+__device__ __forceinline__ void st_u2(void* p, const uint2& x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(nt_u2{x.x, x.y}, reinterpret_cast<nt_u2*>(p));
+    else
+        *reinterpret_cast<uint2*>(p) = x;
+}
+template <bool NT>
+__device__ __forceinline__ void st_u1(void* p, uint32_t x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(x, reinterpret_cast<uint32_t*>(p));
+    else
+        *reinterpret_cast<uint32_t*>(p) = x;
+}
+
+template <int C, bool NT = false>
 __device__ __forceinline__ void store_codes4(void* c, int64_t e, const uint32_t q[4]) {
     if constexpr (C == AL8 || C == UF8) {
         uint32_t w = (q[0] & 0xFFu) | ((q[1] & 0xFFu) << 8) | ((q[2] & 0xFFu) << 16) | (q[3] << 24);
-        *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(c) + e) = w;
+        st_u1<NT>(reinterpret_cast<uint8_t*>(c) + e, w);
     } else {
         uint2 w = make_uint2((q[0] & 0xFFFFu) | (q[1] << 16), (q[2] & 0xFFFFu) | (q[3] << 16));
-        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(c) + e) = w;
+        st_u2<NT>(reinterpret_cast<uint16_t*>(c) + e, w);
     }
 }
 

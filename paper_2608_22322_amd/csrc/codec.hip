@@ -166,13 +166,9 @@ __global__ __launch_bounds__(256) void stream_kernel(float* __restrict__ p, cons
 hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
                               hipStream_t s) {
     const int64_t chunks = n / 2048;
-    int per_cu = 0;
-    hipError_t e = nt ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<true>, 256, 0)
-                      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, stream_kernel<false>, 256, 0);
-    if (e != hipSuccess || per_cu <= 0) per_cu = 2;
-    int64_t grid = (int64_t)per_cu * device_cu_count();
-    const int64_t want = (chunks + 3) / 4;
-    if (grid > want) grid = want;
+    // one chunk per wave, as the AdamW step launches
+    int64_t grid = (chunks + 3) / 4;
+    if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;
     if (grid <= 0) return hipSuccess;
     if (nt)
         hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, chunks);

@@ -273,7 +273,7 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
 
 hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
     const int grid = (int)(a.total_units < cap ? a.total_units : cap);
     if (grad_dtype == G_BF16)
         hipLaunchKernelGGL(fac_marg_g2_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
@@ -391,7 +391,7 @@ __global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a) {
 
 hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
     const int64_t want = (a.total_units + 3) / 4;
     const int grid = (int)(want < cap ? want : cap);
     if (grad_dtype == G_BF16)
@@ -482,7 +482,7 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
 
 hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
     const int64_t want = (a.total_units + 3) / 4;
     const int grid = (int)(want < cap ? want : cap);
     if (grad_dtype == G_BF16)
@@ -671,7 +671,7 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
 
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = (int64_t)device_cu_count() * 4;
+    const int64_t cap = int64_t(1) << 30;  // one unit per wave; waves stride beyond this
     const int grid = (int)(a.total_units < cap ? a.total_units : cap);
     if (grad_dtype == G_BF16)
         hipLaunchKernelGGL(came_res_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
@@ -809,7 +809,7 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
 
 hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_chunks == 0) return hipSuccess;
-    const int64_t cap = (int64_t)device_cu_count() * 8;
+    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
     const int64_t want = (a.total_chunks + 3) / 4;
     const int grid = (int)(want < cap ? want : cap);
     if (grad_dtype == G_BF16)
