@@ -275,7 +275,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--block", type=int, default=2048, help="headline B_V (2048: the paper's AdamW configuration)")
-    ap.add_argument("--sweep", default="64,128,256,2048", help="B_V values to time ('' for headline only)")
+X
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paths", action="store_true", help="skip the Adafactor / CAME timings")
     args = ap.parse_args()

@@ -223,9 +223,10 @@ al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void
 /* Diagnostic: the streaming ceiling of the fused AdamW access pattern. Reads
  * p (n fp32), g (n bf16), m and v (n bytes each) and writes p, m, v with no
  * optimizer arithmetic (the values written are meaningless), using the same
- * lane mapping as al_adamw_step (2048-element chunks); nontemporal != 0
- * uses non-temporal loads and stores. n must be a multiple of 2048. Timing it gives the achievable HBM
- * bandwidth for the step's exact byte mix. */
+ * lane mapping and launch shape as al_adamw_step (one 1024-element chunk per
+ * wavefront); nontemporal != 0 uses non-temporal loads and stores. n must be
+ * a multiple of 2048. Timing it gives the achievable HBM bandwidth for the
+ * step's exact byte mix. */
 al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n,
                          void* stream);
 

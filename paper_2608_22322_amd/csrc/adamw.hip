@@ -219,6 +219,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
     }
 
     // ------------------------------------------------ 2. per sub-tile: decode, moments, parameter, momentum code
+    // the new second moment waits in registers for its block's interval
     float vk[K][4];
     uint32_t vmn[Q::NSLOT], vmx[Q::NSLOT];
 #pragma unroll
@@ -231,7 +232,10 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         const int rel = k * kSub + 4 * lane;
         const int64_t e = e0 + rel;
         const int kk = k % R::P;  // slot of this sub-tile in the current load phase
-        if (k > 0 && kk == 0) load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, k / R::P);
+        if (k > 0 && kk == 0) {
+            __builtin_amdgcn_sched_barrier(0);  // keep the next phase's loads after this phase's arithmetic
+            load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, k / R::P);
+        }
         float mh[4], vh[4], mn[4], vn[4], pn[4];
         if constexpr (MC == UF8) {
             const double mstep = readlane_d(q1, k);
@@ -398,13 +402,14 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
     }
 }
 
-// Waves per SIMD the register allocator targets: 3 (at most 168 VGPRs) where
-// the chunk is 1024 elements, which hides more memory latency behind the
-// per-element decode/encode; 2 for 2048-element chunks, whose registers do not
-// fit 168 without spilling.
-template <int BV>
+// At least 4 waves per SIMD (at most 128 VGPRs) with a UF8 momentum: with one
+// chunk per wave the step needs about 95-127 registers, and the extra resident
+// waves hide HBM latency behind the per-element decode/encode arithmetic. An
+// fp32 momentum carries 12 more registers per sub-tile and gets 3 (168), or 2
+// with 2048-element AL16 chunks.
+template <int MC, int VC, int BV>
 constexpr int adamw_waves_per_eu() {
-    return BV >= 2048 ? 2 : 3;
+    return MC == UF8 ? 4 : (VC == AL16 && BV >= 2048 ? 2 : 3);
 }
 
 // largest ti with t[ti].tile_begin <= chunk
@@ -420,29 +425,26 @@ __device__ __forceinline__ int locate(const AdamWLaunch& a, int64_t chunk) {
     return lo;
 }
 
-// One chunk per wave (waves stride only if a launch exceeds 2^30 workgroups);
-// each wave issues the loads of up to 4 sub-tiles (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it
-// computes on them. A chunk that ends a tensor takes the guarded path.
+// One chunk per wave; each wave issues the loads of up to 4 sub-tiles
+// (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it computes on
+// them. A chunk that ends a tensor takes the guarded path.
 template <int G, int MC, int VC, int BV>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(adamw_waves_per_eu<BV>())))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(adamw_waves_per_eu<MC, VC, BV>())))
 void adamw_kernel(const AdamWLaunch a) {
     constexpr int C = Geo<MC, VC, BV>::C;
     const int lane = threadIdx.x & 63;
-    const int64_t wpb = blockDim.x >> 6;
-    const int64_t wave = (int64_t)blockIdx.x * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t nwaves = (int64_t)gridDim.x * wpb;
+    const int64_t chunk = a.chunk_base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
     __shared__ float lut_all[4][NT];
     float* lut = lut_all[threadIdx.x >> 6];
-    for (int64_t chunk = wave; chunk < a.total_tiles; chunk += nwaves) {
-        const AdamWDesc& d = a.t[locate(a, chunk)];
-        const int64_t e0 = (chunk - d.tile_begin) * C;
-        const int64_t valid = d.n - e0;
-        if (valid >= C)
-            adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut);
-        else
-            adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut);
-    }
+    if (chunk >= a.total_tiles) return;
+    const AdamWDesc& d = a.t[locate(a, chunk)];
+    const int64_t e0 = (chunk - d.tile_begin) * C;
+    const int64_t valid = d.n - e0;
+    if (valid >= C)
+        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut);
+    else
+        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut);
 }
 
 int adamw_tile_elems(int v_codec, int v_block) {
@@ -450,77 +452,64 @@ int adamw_tile_elems(int v_codec, int v_block) {
     return v_block > 1024 ? v_block : 1024;
 }
 
-#ifndef AL_ADAMW_PERSISTENT
-#define AL_ADAMW_PERSISTENT 0
-#endif
-
-// One chunk per wave: the grid covers every chunk of the launch, and the
+// One wave per chunk: the grid covers every chunk of the launch and the
 // hardware dispatcher refills each CU as its waves retire. (A persistent grid
-// sized by occupancy moves the same byte mix about 6% slower on gfx950.)
+// sized by occupancy moves the same byte mix about 6% slower on gfx950, and a
+// chunk loop lets the compiler hoist per-chunk constants into spilled
+// registers.) Lists beyond 2^32 chunks take several launches.
 template <int G, int MC, int VC, int BV>
-static hipError_t launch_t(const AdamWLaunch& a, int grid_cap, hipStream_t s) {
-    const int64_t want = (a.total_tiles + 3) / 4;
-    int64_t grid = want;
-#if AL_ADAMW_PERSISTENT
-    static int per_cu = 0;
-    if (per_cu == 0) {
-        int n = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, adamw_kernel<G, MC, VC, BV>, 256, 0) != hipSuccess ||
-            n <= 0)
-            n = 2;
-        per_cu = n;
+static hipError_t launch_t(const AdamWLaunch& a, hipStream_t s) {
+    constexpr int64_t kMaxGrid = int64_t(1) << 30;  // workgroups (4 waves each) per launch
+    AdamWLaunch b = a;
+    for (b.chunk_base = 0; b.chunk_base < a.total_tiles; b.chunk_base += 4 * kMaxGrid) {
+        const int64_t left = (a.total_tiles - b.chunk_base + 3) / 4;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3((unsigned)grid), dim3(256), 0, s, b);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    grid = (int64_t)per_cu * device_cu_count();
-    if (grid > want) grid = want;
-    if (grid > grid_cap) grid = grid_cap;
-#else
-    (void)grid_cap;
-    if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;  // waves then stride over the remaining chunks
-#endif
-    hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3((unsigned)grid), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 template <int G, int MC, int VC>
-static hipError_t launch_bv(const AdamWLaunch& a, int bv, int grid, hipStream_t s) {
+static hipError_t launch_bv(const AdamWLaunch& a, int bv, hipStream_t s) {
     if constexpr (VC == FP32) {
-        return launch_t<G, MC, VC, 256>(a, grid, s);
+        return launch_t<G, MC, VC, 256>(a, s);
     } else {
         switch (bv) {
-            case 64: return launch_t<G, MC, VC, 64>(a, grid, s);
-            case 128: return launch_t<G, MC, VC, 128>(a, grid, s);
-            case 256: return launch_t<G, MC, VC, 256>(a, grid, s);
-            case 512: return launch_t<G, MC, VC, 512>(a, grid, s);
-            case 1024: return launch_t<G, MC, VC, 1024>(a, grid, s);
-            case 2048: return launch_t<G, MC, VC, 2048>(a, grid, s);
+            case 64: return launch_t<G, MC, VC, 64>(a, s);
+            case 128: return launch_t<G, MC, VC, 128>(a, s);
+            case 256: return launch_t<G, MC, VC, 256>(a, s);
+            case 512: return launch_t<G, MC, VC, 512>(a, s);
+            case 1024: return launch_t<G, MC, VC, 1024>(a, s);
+            case 2048: return launch_t<G, MC, VC, 2048>(a, s);
         }
         return hipErrorInvalidValue;
     }
 }
 
 template <int G, int MC>
-static hipError_t launch_vc(const AdamWLaunch& a, int vc, int bv, int grid, hipStream_t s) {
+static hipError_t launch_vc(const AdamWLaunch& a, int vc, int bv, hipStream_t s) {
     switch (vc) {
-        case AL8: return launch_bv<G, MC, AL8>(a, bv, grid, s);
-        case AL16: return launch_bv<G, MC, AL16>(a, bv, grid, s);
-        case FP32: return launch_bv<G, MC, FP32>(a, bv, grid, s);
+        case AL8: return launch_bv<G, MC, AL8>(a, bv, s);
+        case AL16: return launch_bv<G, MC, AL16>(a, bv, s);
+        case FP32: return launch_bv<G, MC, FP32>(a, bv, s);
     }
     return hipErrorInvalidValue;
 }
 
 template <int G>
-static hipError_t launch_mc(const AdamWLaunch& a, int mc, int vc, int bv, int grid, hipStream_t s) {
+static hipError_t launch_mc(const AdamWLaunch& a, int mc, int vc, int bv, hipStream_t s) {
     switch (mc) {
-        case UF8: return launch_vc<G, UF8>(a, vc, bv, grid, s);
-        case FP32: return launch_vc<G, FP32>(a, vc, bv, grid, s);
+        case UF8: return launch_vc<G, UF8>(a, vc, bv, s);
+        case FP32: return launch_vc<G, FP32>(a, vc, bv, s);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block, int grid,
-                        hipStream_t s) {
-    if (grad_dtype == G_BF16) return launch_mc<G_BF16>(a, m_codec, v_codec, v_block, grid, s);
-    return launch_mc<G_F32>(a, m_codec, v_codec, v_block, grid, s);
+hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block, hipStream_t s) {
+    if (grad_dtype == G_BF16) return launch_mc<G_BF16>(a, m_codec, v_codec, v_block, s);
+    return launch_mc<G_F32>(a, m_codec, v_codec, v_block, s);
 }
 
 }  // namespace al

@@ -382,12 +382,11 @@ al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg
     a.v_floor = cfg->v.log_floor;
     a.cf = al::exp2_coef();
     const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
-    const int grid_cap = al::device_cu_count() * 16;
     hipStream_t s = as_stream(stream);
 
     auto flush = [&]() -> al_status {
         if (a.nt == 0) return AL_OK;
-        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, grid_cap, s);
+        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, s);
         a.nt = 0;
         a.total_tiles = 0;
         return e == hipSuccess ? AL_OK : hip_fail(e, "al_adamw_step launch");

@@ -35,13 +35,14 @@ struct AdamWLaunch {
     Exp2Coef cf;                      // decode polynomial
     int32_t nt;
     int64_t total_tiles;
+    int64_t chunk_base;  // first chunk of this launch (one wave per chunk)
     AdamWDesc t[kAdamWMaxTensors];
 };
 
 // Elements per tile: max(block of v, 256).
 int adamw_tile_elems(int v_codec, int v_block);
 hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block,
-                        int grid, hipStream_t s);
+                        hipStream_t s);
 
 // ------------------------------------------------------------------ codec
 hipError_t launch_quantize(int codec, const float* x, int64_t n, int block, float log_floor, void* codes,

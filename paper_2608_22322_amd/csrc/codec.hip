@@ -110,71 +110,55 @@ hipError_t launch_diag_math(int fn, const double* x, int64_t n, double* out, int
 
 // Streaming ceiling of the fused AdamW access pattern: per element read p
 // (fp32), g (bf16), m and v (1 byte each), write p, m, v -- the same bytes,
-// chunking and lane mapping as the AdamW kernel, with no optimizer
-// arithmetic, 2048 elements per wavefront chunk. NT selects non-temporal
-// loads and stores.
-typedef float f4v __attribute__((ext_vector_type(4)));
-typedef uint32_t u2v __attribute__((ext_vector_type(2)));
-
+// lane mapping and launch shape as the AdamW kernel (one 1024-element chunk
+// per wavefront, 4 consecutive elements per lane in each 256-element
+// sub-tile), with no optimizer arithmetic. NT selects non-temporal loads and
+// stores.
 template <bool NT>
 __global__ __launch_bounds__(256) void stream_kernel(float* __restrict__ p, const uint16_t* __restrict__ g,
                                                       uint8_t* __restrict__ m, uint8_t* __restrict__ v,
-                                                      int64_t chunks) {
+                                                      int64_t chunk_base, int64_t chunks) {
     const int lane = threadIdx.x & 63;
-    const int64_t wpb = blockDim.x >> 6;
-    const int64_t wave = (int64_t)blockIdx.x * wpb + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t nwaves = (int64_t)gridDim.x * wpb;
-    for (int64_t c = wave; c < chunks; c += nwaves) {
-        f4v pv[8];
-        u2v gv[8];
-        uint32_t mv[8], vv[8];
+    const int64_t c = chunk_base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (c >= chunks) return;
+    float4 pv[4];
+    uint2 gv[4];
+    uint32_t mv[4], vv[4];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int64_t e = c * 2048 + k * 256 + 4 * lane;
-            if constexpr (NT) {
-                pv[k] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p + e));
-                gv[k] = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(g + e));
-                mv[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(m + e));
-                vv[k] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(v + e));
-            } else {
-                pv[k] = *reinterpret_cast<const f4v*>(p + e);
-                gv[k] = *reinterpret_cast<const u2v*>(g + e);
-                mv[k] = *reinterpret_cast<const uint32_t*>(m + e);
-                vv[k] = *reinterpret_cast<const uint32_t*>(v + e);
-            }
-        }
+    for (int k = 0; k < 4; ++k) {
+        const int64_t e = c * 1024 + k * 256 + 4 * lane;
+        pv[k] = ld_f4<NT>(p + e);
+        gv[k] = ld_u2<NT>(g + e);
+        mv[k] = ld_u1<NT>(m + e);
+        vv[k] = ld_u1<NT>(v + e);
+    }
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int64_t e = c * 2048 + k * 256 + 4 * lane;
-            f4v o = pv[k];
-            o.x += bf16_to_f32(gv[k].x & 0xFFFFu);
-            o.w += bf16_to_f32(gv[k].y >> 16);
-            const uint32_t mo = mv[k] ^ vv[k], vo = vv[k] + 0x01010101u;
-            if constexpr (NT) {
-                __builtin_nontemporal_store(o, reinterpret_cast<f4v*>(p + e));
-                __builtin_nontemporal_store(mo, reinterpret_cast<uint32_t*>(m + e));
-                __builtin_nontemporal_store(vo, reinterpret_cast<uint32_t*>(v + e));
-            } else {
-                *reinterpret_cast<f4v*>(p + e) = o;
-                *reinterpret_cast<uint32_t*>(m + e) = mo;
-                *reinterpret_cast<uint32_t*>(v + e) = vo;
-            }
-        }
+    for (int k = 0; k < 4; ++k) {
+        const int64_t e = c * 1024 + k * 256 + 4 * lane;
+        float4 o = pv[k];
+        o.x += bf16_to_f32(gv[k].x & 0xFFFFu);
+        o.w += bf16_to_f32(gv[k].y >> 16);
+        st_f4<NT>(p + e, o);
+        st_u1<NT>(m + e, mv[k] ^ vv[k]);
+        st_u1<NT>(v + e, vv[k] + 0x01010101u);
     }
 }
 
 hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
                               hipStream_t s) {
-    const int64_t chunks = n / 2048;
-    // one chunk per wave, as the AdamW step launches
-    int64_t grid = (chunks + 3) / 4;
-    if (grid > (int64_t(1) << 30)) grid = int64_t(1) << 30;
-    if (grid <= 0) return hipSuccess;
-    if (nt)
-        hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, chunks);
-    else
-        hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, chunks);
-    return hipGetLastError();
+    const int64_t chunks = n / 1024;
+    constexpr int64_t kMaxGrid = int64_t(1) << 30;
+    for (int64_t base = 0; base < chunks; base += 4 * kMaxGrid) {
+        const int64_t left = (chunks - base + 3) / 4;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        if (nt)
+            hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, base, chunks);
+        else
+            hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, base, chunks);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 template <int C>
