@@ -7,7 +7,7 @@ mask (generated once, reused every step), AL8 second moment (block B_V) and
 UF8 momentum (block 256), all resident in HBM. W warm-up steps, then K timed
 steps with HIP events on the launch stream. The headline is B_V = 2048, the
 second-moment block of the paper's AdamW configuration (Table 4); the
-block-size sweep {64, 128, 256, 2048} is reported alongside, as is the
+block-size sweep {64, 128, 256, 512, 1024, 2048} is reported alongside, as is the
 measured streaming ceiling of the same byte mix (al_diag_stream).
 
 Prints ONE JSON line on stdout (progress goes to stderr).
@@ -275,7 +275,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--block", type=int, default=2048, help="headline B_V (2048: the paper's AdamW configuration)")
-X
+    ap.add_argument("--sweep", default="64,128,256,512,1024,2048", help="B_V values to time ('' for headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paths", action="store_true", help="skip the Adafactor / CAME timings")
     args = ap.parse_args()
