@@ -192,6 +192,21 @@ __device__ __forceinline__ uint32_t al_encode_fast(float x, const ALEnc& p) {
     return x > 0.0f ? 1u + (uint32_t)r : 0u;
 }
 
+// fl32(x / d) from a precomputed rd = fl64(1 / d). q = fl64(x * rd) lies
+// within 2.5 binary64 ulps of fl64(x / d), so the two round to the same fp32
+// value unless q is that close to an fp32 rounding midpoint (its 29 low
+// mantissa bits near 2^28) or outside the normal fp32 range; those rare
+// cases take the binary64 division.
+__device__ __forceinline__ float div_to_f32(double x, double d, double rd) {
+    const double q = x * rd;
+    const uint64_t b = __builtin_bit_cast(uint64_t, q);
+    const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
+    const uint32_t low = (uint32_t)b & 0x1FFFFFFFu;
+    const bool ok = (ex - (1023u - 125u) <= 251u && low - 0x0FFFFFF8u > 16u) || q == 0.0;
+    if (__builtin_expect(ok, 1)) return (float)q;
+    return (float)(x / d);
+}
+
 // Cross-lane moves of 64-bit values.
 __device__ __forceinline__ double shfl_d(double v, int src) { return __shfl(v, src); }
 __device__ __forceinline__ double readlane_d(double v, int lane) {

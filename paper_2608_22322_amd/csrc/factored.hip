@@ -13,12 +13,13 @@
 // CAME adds: res (sums of (uhat - m)^2 + eps2 with the in-step momentum),
 // fin over the confidence, and apply (recompute uhat and m, encode m, update p).
 //
-// Marginal sums. A wavefront owns a 256x256 unit as 4x4 tiles of 64x64. It
-// loads a tile in the natural layout (16 lanes x 4 columns x 4 rows per
-// instruction, coalesced 128-byte row segments), adds each term to in-lane
-// column accumulators, and writes the tile to LDS; each lane then sums one
-// tile row out of LDS. All sums are double-double and every partial is
-// merged in a fixed order, so the means are the exactly rounded ones.
+// Marginal sums. A wavefront owns a 256x256 unit, walked as 16 groups of 16
+// rows x 4 tiles of 64 columns. It loads a 16x64 tile in the natural layout
+// (16 lanes x 4 columns x 4 rows, coalesced row segments), adds each term to
+// in-lane column accumulators, and stages the tile in LDS (4-8 KB per wave,
+// so LDS does not limit occupancy); 4 lanes then sum each tile row out of LDS.
+// All sums are double-double and every partial is merged in a fixed order, so
+// the means are the exactly rounded ones.
 #include "al_codec_dev.hpp"
 #include "al_device.hpp"
 #include "al_internal.hpp"
@@ -178,108 +179,130 @@ hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream
 }
 
 // ------------------------------------------------------- marginal sums of G2
+// Lane roles in a 16x64 tile of a 256x256 unit. Load layout: lane (lr, lc) =
+// (lane / 16, lane % 16) holds rows lr + 4i (i < 4), columns 4 lc .. 4 lc + 3
+// (16 lanes cover a coalesced 64-column row segment). Row layout: lane
+// (rrow, rq) = (lane / 4, lane % 4) sums row rrow, columns 16 rq .. 16 rq + 15
+// of the tile out of LDS. Column sums stay in the loading lanes across the
+// unit's rows; a row's partial is merged over its 4 lanes after the unit's 4
+// column tiles. Every wave owns one unit, so the kernel has no unit loop.
+constexpr int kTileRows = 16;
+
 template <int G>
-__global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a) {
-    __shared__ float tile[64][68];
-    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4;
-    for (int64_t unit = blockIdx.x; unit < a.total_units; unit += gridDim.x) {
-        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-        const int64_t u = unit - d.unit_begin;
-        const int64_t ru = u / d.ncu, cu = u % d.ncu;
-        const int64_t r0 = ru * 256, c0 = cu * 256;
-        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-        const bool vec = (d.cols & 3) == 0;
-        DD racc[4];
+__global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
+    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
+    const int64_t unit = base + blockIdx.x;
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+    const bool vec = (d.cols & 3) == 0;
+    const double eps1 = a.eps1;
+    DD cacc[4][4];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) racc[rt] = DD{0.0, 0.0};
-        for (int ct = 0; ct < 4 && ct * 64 < nc; ++ct) {
-            const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
-            DD cacc[4];
+    for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
+        for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
+    for (int rg = 0; rg * kTileRows < nr; ++rg) {
+        DD rsum{0.0, 0.0};
 #pragma unroll
-            for (int rt = 0; rt < 4; ++rt) {
-                if (rt * 64 >= nr) break;
-#pragma unroll 4
-                for (int i = 0; i < 16; ++i) {
-                    const int rr = rt * 64 + lr + 4 * i;
-                    const int cc = ct * 64 + 4 * lc;
+        for (int ct = 0; ct < 4; ++ct) {
+            if (ct * 64 >= nc) break;
+            const int cc = ct * 64 + 4 * lc;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int rr = rg * kTileRows + lr + 4 * i;
+                float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                if (rr < nr) {
                     const int64_t e = (r0 + rr) * d.cols + c0 + cc;
-                    float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                    if (rr < nr) {
-                        if (vec && cc + 4 <= nc) {
-                            grad4<G>(d.g, e, gv);
-                        } else {
-#pragma unroll
-                            for (int j = 0; j < 4; ++j)
-                                if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
-                        }
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (cc + j < nc) {
-                                const double x = (double)gv[j];
-                                dd_add(cacc[j], x * x + a.eps1);
-                            }
-                        }
-                    }
-                    *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
-                }
-                __syncthreads();
-                if (rt * 64 + lane < nr) {
-                    if (ncol == 64) {
-#pragma unroll 4
-                        for (int c = 0; c < 64; c += 4) {
-                            const float4 t = *reinterpret_cast<const float4*>(&tile[lane][c]);
-                            const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
-                            dd_add(racc[rt], x0 * x0 + a.eps1);
-                            dd_add(racc[rt], x1 * x1 + a.eps1);
-                            dd_add(racc[rt], x2 * x2 + a.eps1);
-                            dd_add(racc[rt], x3 * x3 + a.eps1);
-                        }
+                    if (vec && cc + 4 <= nc) {
+                        grad4<G>(d.g, e, gv);
                     } else {
-                        for (int c = 0; c < ncol; ++c) {
-                            const double x = tile[lane][c];
-                            dd_add(racc[rt], x * x + a.eps1);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (cc + j < nc) {
+                            const double x = (double)gv[j];
+                            dd_add(cacc[ct][j], x * x + eps1);
                         }
                     }
                 }
-                __syncthreads();
+                *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
             }
+            __syncthreads();
+            const int rr = rg * kTileRows + rrow;
+            const int cq = ct * 64 + 16 * rq;  // first column of this lane's quarter
+            if (rr < nr && cq < nc) {
+                if (cq + 16 <= nc) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                DD v = cacc[j];
-                v = dd_merge(v, dd_shfl_xor(v, 16));
-                v = dd_merge(v, dd_shfl_xor(v, 32));
-                const int col = ct * 64 + 4 * lc + j;
-                if (lr == 0 && col < nc) {
-                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
-                    cp[0] = v.hi;
-                    cp[1] = v.lo;
+                    for (int c = 0; c < 16; c += 4) {
+                        const float4 t = *reinterpret_cast<const float4*>(&tile[rrow][16 * rq + c]);
+                        const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
+                        dd_add(rsum, x0 * x0 + eps1);
+                        dd_add(rsum, x1 * x1 + eps1);
+                        dd_add(rsum, x2 * x2 + eps1);
+                        dd_add(rsum, x3 * x3 + eps1);
+                    }
+                } else {
+                    for (int c = 0; c < nc - cq; ++c) {
+                        const double x = tile[rrow][16 * rq + c];
+                        dd_add(rsum, x * x + eps1);
+                    }
                 }
             }
+            __syncthreads();
         }
+        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
+        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
+        const int rr = rg * kTileRows + rrow;
+        if (rq == 0 && rr < nr) {
+            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + rr);
+            rp[0] = rsum.hi;
+            rp[1] = rsum.lo;
+        }
+    }
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-            const int row = rt * 64 + lane;
-            if (row < nr) {
-                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
-                rp[0] = racc[rt].hi;
-                rp[1] = racc[rt].lo;
+    for (int ct = 0; ct < 4; ++ct) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            DD v = cacc[ct][j];
+            v = dd_merge(v, dd_shfl_xor(v, 16));
+            v = dd_merge(v, dd_shfl_xor(v, 32));
+            const int col = ct * 64 + 4 * lc + j;
+            if (lr == 0 && col < nc) {
+                double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                cp[0] = v.hi;
+                cp[1] = v.lo;
             }
         }
     }
 }
 
+// One 64-thread workgroup per unit; lists beyond 2^31 units take several launches.
+template <class K>
+static hipError_t launch_per_unit(K kernel, const FacArgs& a, hipStream_t s) {
+    constexpr int64_t kMaxGrid = int64_t(1) << 31;
+    for (int64_t base = 0; base < a.total_units; base += kMaxGrid) {
+        const int64_t left = a.total_units - base;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(64), 0, s, a, base);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
-    const int grid = (int)(a.total_units < cap ? a.total_units : cap);
-    if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(fac_marg_g2_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
-    else
-        hipLaunchKernelGGL(fac_marg_g2_kernel<G_F32>, dim3(grid), dim3(64), 0, s, a);
-    return hipGetLastError();
+    return grad_dtype == G_BF16 ? launch_per_unit(fac_marg_g2_kernel<G_BF16>, a, s)
+                                : launch_per_unit(fac_marg_g2_kernel<G_F32>, a, s);
 }
 
 // ------------------------------------------------- finalize (one WG / tensor)
@@ -438,7 +461,7 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
         const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
         const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
         const bool vec = (d.cols & 3) == 0 && 4 * lane + 4 <= nc;
-        const double clip = d.scal[0];
+        const double rclip = 1.0 / d.scal[0];
         double cf[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) cf[j] = 4 * lane + j < nc ? d.cfac[c0 + 4 * lane + j] : 0.0;
@@ -467,7 +490,7 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
             for (int j = 0; j < 4; ++j) {
                 const double uu = (ri * cf[j]) * (double)gv[j];
                 const double pd = (double)pv[j] * a.decay;
-                out[j] = (float)(pd - a.lr * (uu / clip));
+                out[j] = (float)(pd - a.lr * (uu * rclip));  // p carries a tolerance: multiply by 1 / clip
             }
             if (vec) {
                 *reinterpret_cast<float4*>(d.p + e) = make_float4(out[0], out[1], out[2], out[3]);
@@ -551,119 +574,131 @@ __device__ __forceinline__ float came_momentum(const FacArgs& a, const FacDesc& 
 
 // --------------------------- CAME residual marginal sums (tile layout, fp64)
 // Term (uhat - m)^2 + eps2 with uhat = fl32(u / clip), m the in-step
-// momentum; row sums through an fp64 LDS tile.
+// momentum; the same lane roles and 16x64 tiles as the marginals of G2, with
+// the binary64 terms staged in LDS for the row sums.
 template <int G>
-__global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
-    __shared__ double tile[64][66];
-    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4;
-    for (int64_t unit = blockIdx.x; unit < a.total_units; unit += gridDim.x) {
-        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-        const int64_t u = unit - d.unit_begin;
-        const int64_t ru = u / d.ncu, cu = u % d.ncu;
-        const int64_t r0 = ru * 256, c0 = cu * 256;
-        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-        const bool vec = (d.cols & 3) == 0;
-        const double clip = d.scal[0];
-        DD racc[4];
+__global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
+    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
+    const int64_t unit = base + blockIdx.x;
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+    const bool vec = (d.cols & 3) == 0;
+    const double clip = d.scal[0], rclip = 1.0 / clip;
+    const bool uf8 = a.m_codec == UF8;
+    DD cacc[4][4];
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) racc[rt] = DD{0.0, 0.0};
-        for (int ct = 0; ct < 4 && ct * 64 < nc; ++ct) {
-            const int ncol = nc - ct * 64 < 64 ? nc - ct * 64 : 64;
-            const int cc = ct * 64 + 4 * lc;  // column of this lane's first element within the unit
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
+    for (int rg = 0; rg * kTileRows < nr; ++rg) {
+        DD rsum{0.0, 0.0};
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+            if (ct * 64 >= nc) break;
+            const int cc = ct * 64 + 4 * lc;
+            const bool full = vec && cc + 4 <= nc;
             double cf[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) cf[j] = cc + j < nc ? d.cfac[c0 + cc + j] : 0.0;
-            DD cacc[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
+            for (int i = 0; i < 4; ++i) {
+                const int rr = rg * kTileRows + lr + 4 * i;
+                double term[4] = {0.0, 0.0, 0.0, 0.0};
+                if (rr < nr) {
+                    const double ri = d.rfac[r0 + rr];
+                    const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+                    float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    float mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (full) {
+                        grad4<G>(d.g, e, gv);
+                        if (uf8) {
+                            // e % 4 == 0: the 4 elements share one momentum block
+                            const double st = (double)d.mm[e / 256] / 127.0;
+                            const uint32_t w =
+                                *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
 #pragma unroll
-            for (int rt = 0; rt < 4; ++rt) {
-                if (rt * 64 >= nr) break;
-#pragma unroll 2
-                for (int i = 0; i < 16; ++i) {
-                    const int rr = rt * 64 + lr + 4 * i;
-                    double term[4] = {0.0, 0.0, 0.0, 0.0};
-                    if (rr < nr) {
-                        const double ri = d.rfac[r0 + rr];
-                        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
-                        float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                        float mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                        const bool full = vec && cc + 4 <= nc;
-                        if (full) {
-                            grad4<G>(d.g, e, gv);
+                            for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
                         } else {
-#pragma unroll
-                            for (int j = 0; j < 4; ++j)
-                                if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
+                            const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
+                            mh[0] = t.x;
+                            mh[1] = t.y;
+                            mh[2] = t.z;
+                            mh[3] = t.w;
                         }
-                        if (a.m_codec == UF8) {
-                            // the lane's 4 elements share a momentum block unless they straddle one
-                            const int64_t b0 = e / 256, b3 = (e + 3) / 256;
-                            const double st0 = (double)d.mm[b0] / 127.0;
-                            const double st3 = b3 == b0 ? st0 : (double)d.mm[b3] / 127.0;
-                            uint32_t w;
-                            if (full && (e & 3) == 0) {
-                                w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
-                            } else {
-                                w = 0u;
-#pragma unroll
-                                for (int j = 0; j < 4; ++j)
-                                    if (cc + j < nc) w |= (uint32_t)reinterpret_cast<const uint8_t*>(d.m)[e + j] << (8 * j);
-                            }
-#pragma unroll
-                            for (int j = 0; j < 4; ++j) {
-                                const double st = (e + j) / 256 == b0 ? st0 : st3;
-                                mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
-                            }
-                        } else {
-#pragma unroll
-                            for (int j = 0; j < 4; ++j)
-                                if (cc + j < nc) mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
-                        }
+                    } else {
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
                             if (cc + j < nc) {
-                                const double uu = (ri * cf[j]) * (double)gv[j];
-                                const float uh = (float)(uu / clip);
-                                const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
-                                const double df = (double)uh - (double)m;
-                                term[j] = df * df + a.eps2;
-                                dd_add(cacc[j], term[j]);
+                                gv[j] = grad1<G>(d.g, e + j);
+                                if (uf8)
+                                    mh[j] = uf8_decode(reinterpret_cast<const int8_t*>(d.m)[e + j],
+                                                       (double)d.mm[(e + j) / 256] / 127.0);
+                                else
+                                    mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
                             }
                         }
                     }
-                    double* tp = &tile[lr + 4 * i][4 * lc];
-                    tp[0] = term[0];
-                    tp[1] = term[1];
-                    tp[2] = term[2];
-                    tp[3] = term[3];
-                }
-                __syncthreads();
-                if (rt * 64 + lane < nr)
-                    for (int c = 0; c < ncol; ++c) dd_add(racc[rt], tile[lane][c]);
-                __syncthreads();
-            }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                DD v = cacc[j];
-                v = dd_merge(v, dd_shfl_xor(v, 16));
-                v = dd_merge(v, dd_shfl_xor(v, 32));
-                const int col = cc + j;
-                if (lr == 0 && col < nc) {
-                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
-                    cp[0] = v.hi;
-                    cp[1] = v.lo;
+                    for (int j = 0; j < 4; ++j) {
+                        if (cc + j < nc) {
+                            const double uu = (ri * cf[j]) * (double)gv[j];
+                            const float uh = div_to_f32(uu, clip, rclip);
+                            const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
+                            const double df = (double)uh - (double)m;
+                            term[j] = df * df + a.eps2;
+                            dd_add(cacc[ct][j], term[j]);
+                        }
+                    }
+                }
+                double* tp = &tile[lr + 4 * i][4 * lc];
+                *reinterpret_cast<double2*>(tp) = make_double2(term[0], term[1]);
+                *reinterpret_cast<double2*>(tp + 2) = make_double2(term[2], term[3]);
+            }
+            __syncthreads();
+            const int rr = rg * kTileRows + rrow;
+            const int cq = ct * 64 + 16 * rq;
+            if (rr < nr && cq < nc) {
+                const int cnt = nc - cq < 16 ? nc - cq : 16;
+                if (cnt == 16) {
+#pragma unroll
+                    for (int c = 0; c < 16; c += 2) {
+                        const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
+                        dd_add(rsum, t.x);
+                        dd_add(rsum, t.y);
+                    }
+                } else {
+                    for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
                 }
             }
+            __syncthreads();
         }
+        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
+        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
+        const int rr = rg * kTileRows + rrow;
+        if (rq == 0 && rr < nr) {
+            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + rr);
+            rp[0] = rsum.hi;
+            rp[1] = rsum.lo;
+        }
+    }
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
-            const int row = rt * 64 + lane;
-            if (row < nr) {
-                double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
-                rp[0] = racc[rt].hi;
-                rp[1] = racc[rt].lo;
+    for (int ct = 0; ct < 4; ++ct) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            DD v = cacc[ct][j];
+            v = dd_merge(v, dd_shfl_xor(v, 16));
+            v = dd_merge(v, dd_shfl_xor(v, 32));
+            const int col = ct * 64 + 4 * lc + j;
+            if (lr == 0 && col < nc) {
+                double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                cp[0] = v.hi;
+                cp[1] = v.lo;
             }
         }
     }
@@ -671,13 +706,8 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a) {
 
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = int64_t(1) << 30;  // one unit per wave; waves stride beyond this
-    const int grid = (int)(a.total_units < cap ? a.total_units : cap);
-    if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(came_res_kernel<G_BF16>, dim3(grid), dim3(64), 0, s, a);
-    else
-        hipLaunchKernelGGL(came_res_kernel<G_F32>, dim3(grid), dim3(64), 0, s, a);
-    return hipGetLastError();
+    return grad_dtype == G_BF16 ? launch_per_unit(came_res_kernel<G_BF16>, a, s)
+                                : launch_per_unit(came_res_kernel<G_F32>, a, s);
 }
 
 // ------------------------------------------------------ CAME apply (2-D)
@@ -693,7 +723,7 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
         const FacDesc& d = a.D[locate_chunk(a.D, a.n2, chunk)];
         const int64_t n = d.rows * d.cols;
         const int64_t e0 = (chunk - d.chunk_begin) * 1024;
-        const double clip = d.scal[0];
+        const double clip = d.scal[0], rclip = 1.0 / clip;
         if ((d.cols & 255) == 0 && e0 + 1024 <= n) {
             // every 256-element sub-tile lies in one row: row factors are uniform,
             // column factors are 4 consecutive values per lane, loads are vectors
@@ -729,7 +759,7 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const double uu = (ri * cfj[j]) * (double)gv[j];
-                    const float uh = (float)(uu / clip);
+                    const float uh = div_to_f32(uu, clip, rclip);
                     mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
                     const double upd = (si * sfj[j]) * (double)mnew[j];
                     pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
@@ -774,7 +804,7 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
                 const int64_t e = eb + j;
                 if (e < n) {
                     const double uu = (d.rfac[i] * d.cfac[jc]) * (double)grad1<G>(d.g, e);
-                    const float uh = (float)(uu / clip);
+                    const float uh = div_to_f32(uu, clip, rclip);
                     const float m = came_momentum(a, d, e, uh);
                     mnew[j] = m;
                     const double upd = (d.sr[i] * d.sc[jc]) * (double)m;
