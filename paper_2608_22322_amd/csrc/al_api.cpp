@@ -127,6 +127,7 @@ struct FacPlan {
     std::vector<al::FacDesc> desc;  // 2-D tensors first, then 1-D
     int n2 = 0, n1 = 0;
     int64_t total_units = 0, total_chunks = 0;
+    int64_t total_blk[2] = {0, 0};
     size_t bytes = 0;
     size_t rms_off = 0;
 };
@@ -188,6 +189,11 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
         P.total_units += (int64_t)d.nru * d.ncu;
         d.chunk_begin = P.total_chunks;
         P.total_chunks += (t.rows * t.cols + 1023) / 1024;
+        const int64_t bv = vs.block, bc = came ? cs.block : vs.block;
+        d.blk_begin[0] = P.total_blk[0];
+        P.total_blk[0] += (t.rows + bv - 1) / bv + (t.cols + bv - 1) / bv;
+        d.blk_begin[1] = P.total_blk[1];
+        P.total_blk[1] += (t.rows + bc - 1) / bc + (t.cols + bc - 1) / bc;
     }
     size_t off = align256((size_t)ntot * sizeof(al::FacDesc));
     P.rms_off = off;
@@ -228,6 +234,8 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
             }
             d.rtmp = reinterpret_cast<float*>(take((size_t)t.rows * 4));
             d.ctmp = reinterpret_cast<float*>(take((size_t)t.cols * 4));
+            const int64_t bmin = came && cs.block < vs.block ? cs.block : vs.block;
+            d.rsum = reinterpret_cast<double*>(take((size_t)((t.rows + bmin - 1) / bmin) * 16));
         } else {
             d.nru = d.ncu = 0;
             const size_t n = (size_t)(t.rows * t.cols);
@@ -249,6 +257,8 @@ al::FacArgs fac_args(const FacPlan& P, char* ws) {
     a.n1 = P.n1;
     a.total_units = P.total_units;
     a.total_chunks = P.total_chunks;
+    a.total_blk[0] = P.total_blk[0];
+    a.total_blk[1] = P.total_blk[1];
     a.cf = al::exp2_coef();
     a.m_block = 256;
     return a;

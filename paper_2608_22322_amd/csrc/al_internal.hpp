@@ -91,9 +91,12 @@ struct FacDesc {
     float* rtmp;      // staging: R (2-D) or V (1-D)
     float* ctmp;      // staging: C (2-D) or momentum (1-D)
     double* scal;     // [0] = clip divisor max(1, RMS / d)
+    double* rsum;     // (hi, lo) per block of the row factor: partial sums of R (or R')
     int64_t unit_begin;   // first 256x256 unit of this tensor (2-D)
     int64_t chunk_begin;  // first 1024-element chunk of this tensor (2-D)
+    int64_t blk_begin[2];  // first code block of this tensor's R then C (role 0: V, role 1: confidence)
     int32_t nru, ncu;     // units along rows / columns
+    int32_t pad_;
 };
 
 constexpr int kFacCopyBatch = 16;
@@ -107,6 +110,7 @@ struct FacArgs {
     double* rmspart;      // [total_units] (hi, lo): partial sums of u^2
     int32_t n2, n1;       // 2-D tensors, 1-D tensors (D[n2 .. n2 + n1))
     int64_t total_units, total_chunks;
+    int64_t total_blk[2];  // code blocks over all 2-D tensors' R and C, per role
     double beta, omb;     // second-moment EMA: Adafactor beta2_t / CAME beta2, and 1 - beta
     double beta1, omb1;   // CAME momentum
     double beta3, omb3;   // CAME confidence

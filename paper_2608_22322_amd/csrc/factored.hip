@@ -4,8 +4,9 @@
 //
 // Kernel sequence of one Adafactor step (2-D tensors):
 //   marg   row and column sums of G2 = g^2 + eps1, exact (double-double)
-//   fin    one workgroup per tensor: R, C = EMA of the means, rounded to fp32,
-//          re-encoded; mean(R); factors r_i = (R_i / mean R)^-1/2, c_j = C_j^-1/2
+//   fin    one wavefront per code block of R and C: EMA of the exact means,
+//          rounded to fp32, re-encoded; then per tensor mean(R) and the
+//          factors r_i = (R_i / mean R)^-1/2, c_j = C_j^-1/2
 //   rms    partial sums of u^2, u_ij = (r_i c_j) g_ij, per 256x256 unit
 //   clip   per tensor: max(1, RMS(u) / d)
 //   apply  p <- p (1 - lr wd) - lr u / clip
@@ -305,62 +306,148 @@ hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
                                 : launch_per_unit(fac_marg_g2_kernel<G_F32>, a, s);
 }
 
-// ------------------------------------------------- finalize (one WG / tensor)
+// ------------------------------------------------------------- finalize
 // role 0: second moment (EMA beta, codes vr/vc, factors rfac/cfac);
 // role 1: CAME confidence (EMA beta3, codes cr/cc, factors sr/sc).
-__global__ __launch_bounds__(256) void fac_fin_kernel(const FacArgs a, int role) {
-    __shared__ DD sh[4];
-    __shared__ double mean_r;
-    const FacDesc& d = a.D[blockIdx.x];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int codec = role ? a.c_codec : a.v_codec;
-    const int B = role ? a.c_block : a.v_block;
-    void* rc = role ? d.cr : d.vr;
-    float* rm = role ? d.crm : d.vrm;
-    void* ccd = role ? d.cc : d.vc;
-    float* cm = role ? d.ccm : d.vcm;
-    double* fr = role ? d.sr : d.rfac;
-    double* fc = role ? d.sc : d.cfac;
-    const double beta = role ? a.beta3 : a.beta, omb = role ? a.omb3 : a.omb;
-    const float lf = role ? a.c_floor : a.v_floor;
-    const int64_t rows = d.rows, cols = d.cols;
+// fin_block: one wavefront per code block of a factor vector (R blocks, then C
+// blocks, of every 2-D tensor): merge the unit partials of each element into
+// its mean, EMA with the decoded old value, round to fp32, re-encode the
+// block; R blocks also leave their double-double sum for mean(R), C blocks
+// their factors C_j^-1/2. fin_rows: one workgroup per tensor merges the R
+// block sums in order into mean(R) and writes r_i = (R_i / mean R)^-1/2.
+struct FinRole {
+    int codec, B;
+    void *rc, *cc;
+    float *rm, *cm;
+    double *fr, *fc;
+    double beta, omb;
+    float lf;
+};
 
-    for (int64_t i = tid; i < rows; i += blockDim.x) {
-        DD s{0.0, 0.0};
-        for (int cu = 0; cu < d.ncu; ++cu) {
-            const double* rp = d.rowpart + 2 * ((int64_t)cu * rows + i);
-            s = dd_merge(s, DD{rp[0], rp[1]});
-        }
-        const double mean = dd_value(s) / (double)cols;
-        const float old = vec_decode(codec, B, rc, rm, i, a.cf);
-        d.rtmp[i] = (float)(beta * (double)old + omb * mean);
+__device__ __forceinline__ FinRole fin_role(const FacArgs& a, const FacDesc& d, int role) {
+    FinRole r;
+    r.codec = role ? a.c_codec : a.v_codec;
+    r.B = role ? a.c_block : a.v_block;
+    r.rc = role ? d.cr : d.vr;
+    r.rm = role ? d.crm : d.vrm;
+    r.cc = role ? d.cc : d.vc;
+    r.cm = role ? d.ccm : d.vcm;
+    r.fr = role ? d.sr : d.rfac;
+    r.fc = role ? d.sc : d.cfac;
+    r.beta = role ? a.beta3 : a.beta;
+    r.omb = role ? a.omb3 : a.omb;
+    r.lf = role ? a.c_floor : a.v_floor;
+    return r;
+}
+
+__device__ __forceinline__ int locate_blk(const FacDesc* D, int n, int64_t blk, int role) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (D[mid].blk_begin[role] <= blk)
+            lo = mid;
+        else
+            hi = mid - 1;
     }
-    for (int64_t j = tid; j < cols; j += blockDim.x) {
-        DD s{0.0, 0.0};
-        for (int ru = 0; ru < d.nru; ++ru) {
-            const double* cp = d.colpart + 2 * ((int64_t)ru * cols + j);
-            s = dd_merge(s, DD{cp[0], cp[1]});
+    return lo;
+}
+
+__global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int role) {
+    const int lane = threadIdx.x & 63;
+    const int64_t blk = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (blk >= a.total_blk[role]) return;
+    const FacDesc& d = a.D[locate_blk(a.D, a.n2, blk, role)];
+    const FinRole R = fin_role(a, d, role);
+    const int64_t lb = blk - d.blk_begin[role];
+    const int64_t nbr = (d.rows + R.B - 1) / R.B;
+    const bool isrow = lb < nbr;
+    const int64_t n = isrow ? d.rows : d.cols;
+    const int64_t b = isrow ? lb : lb - nbr;
+    const int64_t s = b * R.B, e = s + R.B < n ? s + R.B : n;
+    void* codes = isrow ? R.rc : R.cc;
+    float* meta = isrow ? R.rm : R.cm;
+    float* x = isrow ? d.rtmp : d.ctmp;
+    // 1. EMA of the exact means (each lane handles the elements it encodes)
+    for (int64_t i = s + lane; i < e; i += 64) {
+        DD acc{0.0, 0.0};
+        double mean;
+        if (isrow) {
+            for (int cu = 0; cu < d.ncu; ++cu) {
+                const double* rp = d.rowpart + 2 * ((int64_t)cu * d.rows + i);
+                acc = dd_merge(acc, DD{rp[0], rp[1]});
+            }
+            mean = dd_value(acc) / (double)d.cols;
+        } else {
+            for (int ru = 0; ru < d.nru; ++ru) {
+                const double* cp = d.colpart + 2 * ((int64_t)ru * d.cols + i);
+                acc = dd_merge(acc, DD{cp[0], cp[1]});
+            }
+            mean = dd_value(acc) / (double)d.rows;
         }
-        const double mean = dd_value(s) / (double)rows;
-        const float old = vec_decode(codec, B, ccd, cm, j, a.cf);
-        d.ctmp[j] = (float)(beta * (double)old + omb * mean);
+        const float old = vec_decode(R.codec, R.B, codes, meta, i, a.cf);
+        x[i] = (float)(R.beta * (double)old + R.omb * mean);
     }
-    __syncthreads();
-    vec_encode(codec, B, d.rtmp, rows, lf, rc, rm, wave, 4, lane);
-    vec_encode(codec, B, d.ctmp, cols, lf, ccd, cm, wave, 4, lane);
-    DD s{0.0, 0.0};
-    for (int64_t i = tid; i < rows; i += blockDim.x) dd_add(s, (double)d.rtmp[i]);
-    s = block_dd_sum(s, sh);
-    if (tid == 0) mean_r = dd_value(s) / (double)rows;
-    __syncthreads();
-    const double mr = mean_r;
-    for (int64_t i = tid; i < rows; i += blockDim.x) fr[i] = 1.0 / sqrt((double)d.rtmp[i] / mr);
-    for (int64_t j = tid; j < cols; j += blockDim.x) fc[j] = 1.0 / sqrt((double)d.ctmp[j]);
+    __threadfence_block();  // the encode below reads x[] back (each lane its own elements)
+    // 2. re-encode the block
+    if (R.codec == FP32) {
+        for (int64_t i = s + lane; i < e; i += 64) reinterpret_cast<float*>(codes)[i] = x[i];
+    } else {
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+        for (int64_t i = s + lane; i < e; i += 64) {
+            mn = OpMin::f(mn, pos_min_key(x[i]));
+            mx = OpMax::f(mx, pos_max_key(x[i]));
+        }
+        mn = group_reduce<OpMin, 64>(mn);
+        mx = group_reduce<OpMax, 64>(mx);
+        const ALFit f = al_fit(mn, mx, R.lf);
+        if (lane == 0) {
+            meta[2 * b] = f.any ? (float)f.lmin : 0.0f;
+            meta[2 * b + 1] = f.any ? (float)f.delta : 0.0f;
+        }
+        const int levels = R.codec == AL16 ? 65534 : 254;
+        const ALEnc enc = al_enc_params(f.lmin, f.any ? (double)levels / f.delta : 1.0);
+        for (int64_t i = s + lane; i < s + R.B; i += 64) {
+            const float v = i < e ? x[i] : 0.0f;
+            if (R.codec == AL16)
+                reinterpret_cast<uint16_t*>(codes)[i] = (uint16_t)al_encode_fast<65534>(v, enc);
+            else
+                reinterpret_cast<uint8_t*>(codes)[i] = (uint8_t)al_encode_fast<254>(v, enc);
+        }
+    }
+    // 3. R: block sum for mean(R); C: factors
+    if (isrow) {
+        DD acc{0.0, 0.0};
+        for (int64_t i = s + lane; i < e; i += 64) dd_add(acc, (double)x[i]);
+        acc = dd_wave_sum(acc);
+        if (lane == 0) {
+            d.rsum[2 * b] = acc.hi;
+            d.rsum[2 * b + 1] = acc.lo;
+        }
+    } else {
+        for (int64_t i = s + lane; i < e; i += 64) R.fc[i] = 1.0 / sqrt((double)x[i]);
+    }
+}
+
+__global__ __launch_bounds__(256) void fac_fin_rows_kernel(const FacArgs a, int role) {
+    __shared__ DD sh[4];
+    const FacDesc& d = a.D[blockIdx.x];
+    const FinRole R = fin_role(a, d, role);
+    const int tid = threadIdx.x;
+    const int64_t nbr = (d.rows + R.B - 1) / R.B;
+    DD acc{0.0, 0.0};
+    for (int64_t k = tid; k < nbr; k += blockDim.x) acc = dd_merge(acc, DD{d.rsum[2 * k], d.rsum[2 * k + 1]});
+    acc = block_dd_sum(acc, sh);
+    const double mr = dd_value(acc) / (double)d.rows;
+    for (int64_t i = tid; i < d.rows; i += blockDim.x) R.fr[i] = 1.0 / sqrt((double)d.rtmp[i] / mr);
 }
 
 hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
     if (a.n2 == 0) return hipSuccess;
-    hipLaunchKernelGGL(fac_fin_kernel, dim3(a.n2), dim3(256), 0, s, a, role);
+    const int64_t grid = (a.total_blk[role] + 3) / 4;
+    hipLaunchKernelGGL(fac_fin_block_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, role);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fac_fin_rows_kernel, dim3(a.n2), dim3(256), 0, s, a, role);
     return hipGetLastError();
 }
 
