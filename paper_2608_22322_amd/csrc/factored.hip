@@ -189,9 +189,74 @@ hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream
 // column tiles. Every wave owns one unit, so the kernel has no unit loop.
 constexpr int kTileRows = 16;
 
+// Raw gradient words of one lane's 4 rows x 4 columns of a tile (bf16 pairs or
+// fp32), loaded one tile ahead of the arithmetic; absent elements read as 0.
+template <int G>
+struct GRaw {
+    uint2 w[4];
+};
+template <>
+struct GRaw<G_F32> {
+    float4 w[4];
+};
+
+template <int G>
+__device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t r0, int64_t c0, int nr, int nc,
+                                          int rg, int ct, int lr, int lc, bool vec) {
+    const int cc = ct * 64 + 4 * lc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = rg * kTileRows + lr + 4 * i;
+        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+        if constexpr (G == G_BF16) {
+            const uint16_t* g = reinterpret_cast<const uint16_t*>(d.g);
+            if (rr < nr && vec && cc + 4 <= nc) {
+                r.w[i] = *reinterpret_cast<const uint2*>(g + e);
+            } else {
+                uint32_t h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (rr < nr && cc + j < nc) h[j] = g[e + j];
+                r.w[i] = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+            }
+        } else {
+            const float* g = reinterpret_cast<const float*>(d.g);
+            if (rr < nr && vec && cc + 4 <= nc) {
+                r.w[i] = *reinterpret_cast<const float4*>(g + e);
+            } else {
+                float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (rr < nr && cc + j < nc) h[j] = g[e + j];
+                r.w[i] = make_float4(h[0], h[1], h[2], h[3]);
+            }
+        }
+    }
+}
+
+template <int G>
+__device__ __forceinline__ void unpack_graw(const GRaw<G>& r, int i, float gv[4]) {
+    if constexpr (G == G_BF16) {
+        gv[0] = bf16_to_f32(r.w[i].x & 0xFFFFu);
+        gv[1] = bf16_to_f32(r.w[i].x >> 16);
+        gv[2] = bf16_to_f32(r.w[i].y & 0xFFFFu);
+        gv[3] = bf16_to_f32(r.w[i].y >> 16);
+    } else {
+        gv[0] = r.w[i].x;
+        gv[1] = r.w[i].y;
+        gv[2] = r.w[i].z;
+        gv[3] = r.w[i].w;
+    }
+}
+
+// Column tiles outermost, 16-row groups inside: the column sums of the current
+// 64-column tile stay in registers, each row's running sum over the column
+// tiles in LDS (owned by one lane), and the next tile's gradients are loaded
+// while the current one is summed.
 template <int G>
 __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
+    __shared__ DD racc[256];
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
     const int64_t unit = base + blockIdx.x;
     if (unit >= a.total_units) return;
@@ -203,85 +268,88 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
     const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
     const bool vec = (d.cols & 3) == 0;
     const double eps1 = a.eps1;
-    DD cacc[4][4];
+    const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int k = 0; k < 4; ++k) racc[lane + 64 * k] = DD{0.0, 0.0};
+    DD cacc[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
-    for (int rg = 0; rg * kTileRows < nr; ++rg) {
+    for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
+    GRaw<G> cur;
+    load_graw<G>(cur, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    for (int it = 0; it < total; ++it) {
+        const int ct = it / nrg, rg = it - ct * nrg;
+        GRaw<G> nxt = cur;
+        if (it + 1 < total) {
+            const int ct1 = (it + 1) / nrg;
+            load_graw<G>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+        }
+        const int cc = ct * 64 + 4 * lc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float gv[4];
+            unpack_graw<G>(cur, i, gv);
+            if (rg * kTileRows + lr + 4 * i < nr) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (cc + j < nc) {
+                        const double x = (double)gv[j];
+                        dd_add(cacc[j], x * x + eps1);
+                    }
+                }
+            }
+            *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
+        }
+        __syncthreads();
         DD rsum{0.0, 0.0};
+        const int rr = rg * kTileRows + rrow;
+        const int cq = ct * 64 + 16 * rq;  // first column of this lane's quarter
+        if (rr < nr && cq < nc) {
+            if (cq + 16 <= nc) {
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
-            if (ct * 64 >= nc) break;
-            const int cc = ct * 64 + 4 * lc;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int rr = rg * kTileRows + lr + 4 * i;
-                float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                if (rr < nr) {
-                    const int64_t e = (r0 + rr) * d.cols + c0 + cc;
-                    if (vec && cc + 4 <= nc) {
-                        grad4<G>(d.g, e, gv);
-                    } else {
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            if (cc + j < nc) gv[j] = grad1<G>(d.g, e + j);
-                    }
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        if (cc + j < nc) {
-                            const double x = (double)gv[j];
-                            dd_add(cacc[ct][j], x * x + eps1);
-                        }
-                    }
+                for (int c = 0; c < 16; c += 4) {
+                    const float4 t = *reinterpret_cast<const float4*>(&tile[rrow][16 * rq + c]);
+                    const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
+                    dd_add(rsum, x0 * x0 + eps1);
+                    dd_add(rsum, x1 * x1 + eps1);
+                    dd_add(rsum, x2 * x2 + eps1);
+                    dd_add(rsum, x3 * x3 + eps1);
                 }
-                *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
-            }
-            __syncthreads();
-            const int rr = rg * kTileRows + rrow;
-            const int cq = ct * 64 + 16 * rq;  // first column of this lane's quarter
-            if (rr < nr && cq < nc) {
-                if (cq + 16 <= nc) {
-#pragma unroll
-                    for (int c = 0; c < 16; c += 4) {
-                        const float4 t = *reinterpret_cast<const float4*>(&tile[rrow][16 * rq + c]);
-                        const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
-                        dd_add(rsum, x0 * x0 + eps1);
-                        dd_add(rsum, x1 * x1 + eps1);
-                        dd_add(rsum, x2 * x2 + eps1);
-                        dd_add(rsum, x3 * x3 + eps1);
-                    }
-                } else {
-                    for (int c = 0; c < nc - cq; ++c) {
-                        const double x = tile[rrow][16 * rq + c];
-                        dd_add(rsum, x * x + eps1);
-                    }
+            } else {
+                for (int c = 0; c < nc - cq; ++c) {
+                    const double x = tile[rrow][16 * rq + c];
+                    dd_add(rsum, x * x + eps1);
                 }
             }
-            __syncthreads();
         }
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
-        const int rr = rg * kTileRows + rrow;
-        if (rq == 0 && rr < nr) {
-            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + rr);
-            rp[0] = rsum.hi;
-            rp[1] = rsum.lo;
+        if (rq == 0 && rr < nr) racc[rr] = dd_merge(racc[rr], rsum);
+        __syncthreads();
+        if (rg == nrg - 1) {
+            // column tile done: its column partials over the unit's rows
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                DD v = cacc[j];
+                v = dd_merge(v, dd_shfl_xor(v, 16));
+                v = dd_merge(v, dd_shfl_xor(v, 32));
+                const int col = cc + j;
+                if (lr == 0 && col < nc) {
+                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    cp[0] = v.hi;
+                    cp[1] = v.lo;
+                }
+                cacc[j] = DD{0.0, 0.0};
+            }
         }
+        cur = nxt;
     }
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            DD v = cacc[ct][j];
-            v = dd_merge(v, dd_shfl_xor(v, 16));
-            v = dd_merge(v, dd_shfl_xor(v, 32));
-            const int col = ct * 64 + 4 * lc + j;
-            if (lr == 0 && col < nc) {
-                double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
-                cp[0] = v.hi;
-                cp[1] = v.lo;
-            }
+    for (int k = 0; k < 4; ++k) {
+        const int row = lane + 64 * k;
+        if (row < nr) {
+            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+            rp[0] = racc[row].hi;
+            rp[1] = racc[row].lo;
         }
     }
 }
