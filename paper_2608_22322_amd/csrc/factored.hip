@@ -729,11 +729,44 @@ __device__ __forceinline__ float came_momentum(const FacArgs& a, const FacDesc& 
 
 // --------------------------- CAME residual marginal sums (tile layout, fp64)
 // Term (uhat - m)^2 + eps2 with uhat = fl32(u / clip), m the in-step
-// momentum; the same lane roles and 16x64 tiles as the marginals of G2, with
-// the binary64 terms staged in LDS for the row sums.
+// momentum; the lane roles, loop order and one-tile-ahead loads of the
+// marginals of G2, with the binary64 terms staged in LDS for the row sums.
+// A lane's raw inputs of one tile: gradients, momentum words, and per row
+// the factor r_i and the momentum block scale.
+template <int G>
+struct ResRaw {
+    GRaw<G> g;
+    uint32_t mw[4];  // UF8 codes of the 4 columns (fp32 momentum: read directly)
+    double ri[4];
+    float ms[4];
+};
+
+template <int G>
+__device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const FacDesc& d, int64_t r0,
+                                            int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec) {
+    load_graw<G>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
+    const int cc = ct * 64 + 4 * lc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = rg * kTileRows + lr + 4 * i;
+        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+        r.ri[i] = rr < nr ? d.rfac[r0 + rr] : 0.0;
+        r.mw[i] = 0u;
+        r.ms[i] = 0.0f;
+        if (a.m_codec == UF8 && rr < nr) {
+            if (vec && cc + 4 <= nc) {
+                // e % 4 == 0: the 4 codes are one word of one momentum block
+                r.mw[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                r.ms[i] = d.mm[e / 256];
+            }
+        }
+    }
+}
+
 template <int G>
 __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
+    __shared__ DD racc[256];
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
     const int64_t unit = base + blockIdx.x;
     if (unit >= a.total_units) return;
@@ -746,115 +779,121 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
     const bool vec = (d.cols & 3) == 0;
     const double clip = d.scal[0], rclip = 1.0 / clip;
     const bool uf8 = a.m_codec == UF8;
-    DD cacc[4][4];
+    const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int k = 0; k < 4; ++k) racc[lane + 64 * k] = DD{0.0, 0.0};
+    DD cacc[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) cacc[ct][j] = DD{0.0, 0.0};
-    for (int rg = 0; rg * kTileRows < nr; ++rg) {
-        DD rsum{0.0, 0.0};
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) {
-            if (ct * 64 >= nc) break;
-            const int cc = ct * 64 + 4 * lc;
-            const bool full = vec && cc + 4 <= nc;
-            double cf[4];
+    for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
+    double cf[4] = {0.0, 0.0, 0.0, 0.0};
+    ResRaw<G> cur;
+    load_resraw<G>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    for (int it = 0; it < total; ++it) {
+        const int ct = it / nrg, rg = it - ct * nrg;
+        const int cc = ct * 64 + 4 * lc;
+        if (rg == 0) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) cf[j] = cc + j < nc ? d.cfac[c0 + cc + j] : 0.0;
+        }
+        ResRaw<G> nxt = cur;
+        if (it + 1 < total) {
+            const int ct1 = (it + 1) / nrg;
+            load_resraw<G>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+        }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int rr = rg * kTileRows + lr + 4 * i;
-                double term[4] = {0.0, 0.0, 0.0, 0.0};
-                if (rr < nr) {
-                    const double ri = d.rfac[r0 + rr];
-                    const int64_t e = (r0 + rr) * d.cols + c0 + cc;
-                    float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                    float mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-                    if (full) {
-                        grad4<G>(d.g, e, gv);
-                        if (uf8) {
-                            // e % 4 == 0: the 4 elements share one momentum block
-                            const double st = (double)d.mm[e / 256] / 127.0;
-                            const uint32_t w =
-                                *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+        for (int i = 0; i < 4; ++i) {
+            const int rr = rg * kTileRows + lr + 4 * i;
+            double term[4] = {0.0, 0.0, 0.0, 0.0};
+            if (rr < nr) {
+                const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+                float gv[4], mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                unpack_graw<G>(cur.g, i, gv);
+                if (vec && cc + 4 <= nc) {
+                    if (uf8) {
+                        const double st = (double)cur.ms[i] / 127.0;
 #pragma unroll
-                            for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
-                        } else {
-                            const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
-                            mh[0] = t.x;
-                            mh[1] = t.y;
-                            mh[2] = t.z;
-                            mh[3] = t.w;
-                        }
+                        for (int j = 0; j < 4; ++j)
+                            mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(cur.mw[i] >> (8 * j)), st);
                     } else {
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (cc + j < nc) {
-                                gv[j] = grad1<G>(d.g, e + j);
-                                if (uf8)
-                                    mh[j] = uf8_decode(reinterpret_cast<const int8_t*>(d.m)[e + j],
-                                                       (double)d.mm[(e + j) / 256] / 127.0);
-                                else
-                                    mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
-                            }
-                        }
+                        const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
+                        mh[0] = t.x;
+                        mh[1] = t.y;
+                        mh[2] = t.z;
+                        mh[3] = t.w;
                     }
+                } else {
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         if (cc + j < nc) {
-                            const double uu = (ri * cf[j]) * (double)gv[j];
-                            const float uh = div_to_f32(uu, clip, rclip);
-                            const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
-                            const double df = (double)uh - (double)m;
-                            term[j] = df * df + a.eps2;
-                            dd_add(cacc[ct][j], term[j]);
+                            if (uf8)
+                                mh[j] = uf8_decode(reinterpret_cast<const int8_t*>(d.m)[e + j],
+                                                   (double)d.mm[(e + j) / 256] / 127.0);
+                            else
+                                mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
                         }
                     }
                 }
-                double* tp = &tile[lr + 4 * i][4 * lc];
-                *reinterpret_cast<double2*>(tp) = make_double2(term[0], term[1]);
-                *reinterpret_cast<double2*>(tp + 2) = make_double2(term[2], term[3]);
-            }
-            __syncthreads();
-            const int rr = rg * kTileRows + rrow;
-            const int cq = ct * 64 + 16 * rq;
-            if (rr < nr && cq < nc) {
-                const int cnt = nc - cq < 16 ? nc - cq : 16;
-                if (cnt == 16) {
 #pragma unroll
-                    for (int c = 0; c < 16; c += 2) {
-                        const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
-                        dd_add(rsum, t.x);
-                        dd_add(rsum, t.y);
+                for (int j = 0; j < 4; ++j) {
+                    if (cc + j < nc) {
+                        const double uu = (cur.ri[i] * cf[j]) * (double)gv[j];
+                        const float uh = div_to_f32(uu, clip, rclip);
+                        const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
+                        const double df = (double)uh - (double)m;
+                        term[j] = df * df + a.eps2;
+                        dd_add(cacc[j], term[j]);
                     }
-                } else {
-                    for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
                 }
             }
-            __syncthreads();
+            double* tp = &tile[lr + 4 * i][4 * lc];
+            *reinterpret_cast<double2*>(tp) = make_double2(term[0], term[1]);
+            *reinterpret_cast<double2*>(tp + 2) = make_double2(term[2], term[3]);
+        }
+        __syncthreads();
+        DD rsum{0.0, 0.0};
+        const int rr = rg * kTileRows + rrow;
+        const int cq = ct * 64 + 16 * rq;
+        if (rr < nr && cq < nc) {
+            const int cnt = nc - cq < 16 ? nc - cq : 16;
+            if (cnt == 16) {
+#pragma unroll
+                for (int c = 0; c < 16; c += 2) {
+                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
+                    dd_add(rsum, t.x);
+                    dd_add(rsum, t.y);
+                }
+            } else {
+                for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
+            }
         }
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
-        const int rr = rg * kTileRows + rrow;
-        if (rq == 0 && rr < nr) {
-            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + rr);
-            rp[0] = rsum.hi;
-            rp[1] = rsum.lo;
+        if (rq == 0 && rr < nr) racc[rr] = dd_merge(racc[rr], rsum);
+        __syncthreads();
+        if (rg == nrg - 1) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                DD v = cacc[j];
+                v = dd_merge(v, dd_shfl_xor(v, 16));
+                v = dd_merge(v, dd_shfl_xor(v, 32));
+                const int col = cc + j;
+                if (lr == 0 && col < nc) {
+                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    cp[0] = v.hi;
+                    cp[1] = v.lo;
+                }
+                cacc[j] = DD{0.0, 0.0};
+            }
         }
+        cur = nxt;
     }
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            DD v = cacc[ct][j];
-            v = dd_merge(v, dd_shfl_xor(v, 16));
-            v = dd_merge(v, dd_shfl_xor(v, 32));
-            const int col = ct * 64 + 4 * lc + j;
-            if (lr == 0 && col < nc) {
-                double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
-                cp[0] = v.hi;
-                cp[1] = v.lo;
-            }
+    for (int k = 0; k < 4; ++k) {
+        const int row = lane + 64 * k;
+        if (row < nr) {
+            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+            rp[0] = racc[row].hi;
+            rp[1] = racc[row].lo;
         }
     }
 }
