@@ -521,62 +521,111 @@ hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
 
 // ------------------------------------------------ RMS partials (per unit)
 // Natural layout: lane = 4 consecutive columns of a 256-column segment; the
-// wave walks the unit's rows. u_ij = (r_i c_j) g_ij, exactly the reference
-// operation order; u^2 summed double-double.
+// wave walks the unit's rows, kRowBatch rows at a time with all their loads
+// issued before the arithmetic. u_ij = (r_i c_j) g_ij, exactly the reference
+// operation order; u^2 summed double-double. One wave per unit.
+constexpr int kRowBatch = 8;
+
 template <int G>
-__global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a) {
-    const int lane = threadIdx.x & 63;
-    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int64_t nw = (int64_t)gridDim.x * 4;
-    for (int64_t unit = wave; unit < a.total_units; unit += nw) {
-        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-        const int64_t u = unit - d.unit_begin;
-        const int64_t ru = u / d.ncu, cu = u % d.ncu;
-        const int64_t r0 = ru * 256, c0 = cu * 256;
-        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-        const bool vec = (d.cols & 3) == 0 && 4 * lane + 4 <= nc;
-        double cf[4];
+__device__ __forceinline__ void load_row4(const FacDesc& d, int64_t e, bool vec, int nc, int c, GRaw<G>& r, int k) {
+    if constexpr (G == G_BF16) {
+        const uint16_t* g = reinterpret_cast<const uint16_t*>(d.g);
+        if (vec) {
+            r.w[k] = ld_u2<true>(g + e);
+        } else {
+            uint32_t h[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) cf[j] = 4 * lane + j < nc ? d.cfac[c0 + 4 * lane + j] : 0.0;
-        DD acc{0.0, 0.0};
-        for (int r = 0; r < nr; ++r) {
-            const double ri = d.rfac[r0 + r];
-            const int64_t e = (r0 + r) * d.cols + c0 + 4 * lane;
-            float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (vec) {
-                grad4<G>(d.g, e, gv);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (4 * lane + j < nc) gv[j] = grad1<G>(d.g, e + j);
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (4 * lane + j < nc) {
-                    const double uu = (ri * cf[j]) * (double)gv[j];
-                    dd_add(acc, uu * uu);
-                }
-            }
+            for (int j = 0; j < 4; ++j)
+                if (c + j < nc) h[j] = g[e + j];
+            r.w[k] = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
         }
-        acc = dd_wave_sum(acc);
-        if (lane == 0) {
-            a.rmspart[2 * unit] = acc.hi;
-            a.rmspart[2 * unit + 1] = acc.lo;
+    } else {
+        const float* g = reinterpret_cast<const float*>(d.g);
+        if (vec) {
+            r.w[k] = ld_f4<true>(g + e);
+        } else {
+            float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (c + j < nc) h[j] = g[e + j];
+            r.w[k] = make_float4(h[0], h[1], h[2], h[3]);
         }
     }
 }
 
+// Gradient words of kRowBatch rows (the GRaw layout, 2 x 4 rows).
+template <int G>
+struct GRows {
+    GRaw<G> h[kRowBatch / 4];
+};
+
+template <int G>
+__global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a, int64_t base) {
+    const int lane = threadIdx.x & 63;
+    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+    const int c = 4 * lane;
+    const bool vec = (d.cols & 3) == 0 && c + 4 <= nc;
+    const bool live = c < nc;
+    double cf[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cf[j] = c + j < nc ? d.cfac[c0 + c + j] : 0.0;
+    DD acc{0.0, 0.0};
+    for (int r = 0; r < nr; r += kRowBatch) {
+        GRows<G> g;
+        double ri[kRowBatch];
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            const int rr = r + k < nr ? r + k : nr - 1;  // rows past the end repeat the last one, unused
+            ri[k] = d.rfac[r0 + rr];
+            if (live) load_row4<G>(d, (r0 + rr) * d.cols + c0 + c, vec, nc, c, g.h[k / 4], k % 4);
+        }
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            if (r + k >= nr || !live) continue;
+            float gv[4];
+            unpack_graw<G>(g.h[k / 4], k % 4, gv);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (c + j < nc) {
+                    const double uu = (ri[k] * cf[j]) * (double)gv[j];
+                    dd_add(acc, uu * uu);
+                }
+            }
+        }
+    }
+    acc = dd_wave_sum(acc);
+    if (lane == 0) {
+        a.rmspart[2 * unit] = acc.hi;
+        a.rmspart[2 * unit + 1] = acc.lo;
+    }
+}
+
+// One wavefront per unit (4 per 256-thread workgroup); lists beyond 2^33 units
+// take several launches.
+template <class K>
+static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, hipStream_t s) {
+    constexpr int64_t kMaxGrid = int64_t(1) << 31;
+    for (int64_t base = 0; base < a.total_units; base += 4 * kMaxGrid) {
+        const int64_t left = (a.total_units - base + 3) / 4;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, s, a, base);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
-    const int64_t want = (a.total_units + 3) / 4;
-    const int grid = (int)(want < cap ? want : cap);
-    if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(fac_rms_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(fac_rms_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return grad_dtype == G_BF16 ? launch_wave_per_unit(fac_rms_kernel<G_BF16>, a, s)
+                                : launch_wave_per_unit(fac_rms_kernel<G_F32>, a, s);
 }
 
 // ------------------------------------------------ clip divisor (wave / tensor)
@@ -603,56 +652,65 @@ hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s) {
 }
 
 // --------------------------------------------------- Adafactor apply (2-D)
+// The RMS pass's layout and row batches; p <- p (1 - lr wd) - lr u / clip.
 template <int G>
-__global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
+__global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
-    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int64_t nw = (int64_t)gridDim.x * 4;
-    for (int64_t unit = wave; unit < a.total_units; unit += nw) {
-        const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-        const int64_t u = unit - d.unit_begin;
-        const int64_t ru = u / d.ncu, cu = u % d.ncu;
-        const int64_t r0 = ru * 256, c0 = cu * 256;
-        const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-        const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-        const bool vec = (d.cols & 3) == 0 && 4 * lane + 4 <= nc;
-        const double rclip = 1.0 / d.scal[0];
-        double cf[4];
+    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
+    const int c = 4 * lane;
+    const bool vec = (d.cols & 3) == 0 && c + 4 <= nc;
+    if (c >= nc) return;
+    const double rclip = 1.0 / d.scal[0];
+    double cf[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) cf[j] = 4 * lane + j < nc ? d.cfac[c0 + 4 * lane + j] : 0.0;
-        for (int r = 0; r < nr; ++r) {
-            const double ri = d.rfac[r0 + r];
-            const int64_t e = (r0 + r) * d.cols + c0 + 4 * lane;
-            float gv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-            float pv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int j = 0; j < 4; ++j) cf[j] = c + j < nc ? d.cfac[c0 + c + j] : 0.0;
+    for (int r = 0; r < nr; r += kRowBatch) {
+        GRows<G> g;
+        double ri[kRowBatch];
+        float4 pv[kRowBatch];
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            const int rr = r + k < nr ? r + k : nr - 1;
+            const int64_t e = (r0 + rr) * d.cols + c0 + c;
+            ri[k] = d.rfac[r0 + rr];
+            load_row4<G>(d, e, vec, nc, c, g.h[k / 4], k % 4);
             if (vec) {
-                grad4<G>(d.g, e, gv);
-                const float4 t = *reinterpret_cast<const float4*>(d.p + e);
-                pv[0] = t.x;
-                pv[1] = t.y;
-                pv[2] = t.z;
-                pv[3] = t.w;
+                pv[k] = ld_f4<true>(d.p + e);
             } else {
+                float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (4 * lane + j < nc) {
-                        gv[j] = grad1<G>(d.g, e + j);
-                        pv[j] = d.p[e + j];
-                    }
+                    if (c + j < nc) h[j] = d.p[e + j];
+                pv[k] = make_float4(h[0], h[1], h[2], h[3]);
             }
+        }
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            if (r + k >= nr) continue;
+            const int64_t e = (r0 + r + k) * d.cols + c0 + c;
+            float gv[4];
+            unpack_graw<G>(g.h[k / 4], k % 4, gv);
+            const float pin[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
             float out[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const double uu = (ri * cf[j]) * (double)gv[j];
-                const double pd = (double)pv[j] * a.decay;
+                const double uu = (ri[k] * cf[j]) * (double)gv[j];
+                const double pd = (double)pin[j] * a.decay;
                 out[j] = (float)(pd - a.lr * (uu * rclip));  // p carries a tolerance: multiply by 1 / clip
             }
             if (vec) {
-                *reinterpret_cast<float4*>(d.p + e) = make_float4(out[0], out[1], out[2], out[3]);
+                st_f4<true>(d.p + e, make_float4(out[0], out[1], out[2], out[3]));
             } else {
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (4 * lane + j < nc) d.p[e + j] = out[j];
+                    if (c + j < nc) d.p[e + j] = out[j];
             }
         }
     }
@@ -660,14 +718,8 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a) {
 
 hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
-    const int64_t want = (a.total_units + 3) / 4;
-    const int grid = (int)(want < cap ? want : cap);
-    if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(ada_apply_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(ada_apply_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return grad_dtype == G_BF16 ? launch_wave_per_unit(ada_apply_kernel<G_BF16>, a, s)
+                                : launch_wave_per_unit(ada_apply_kernel<G_F32>, a, s);
 }
 
 // ------------------------------------------- Adafactor 1-D tensors (WG each)
