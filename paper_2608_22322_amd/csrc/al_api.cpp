@@ -187,8 +187,8 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
         d.ncu = (int32_t)((t.cols + 255) / 256);
         d.unit_begin = P.total_units;
         P.total_units += (int64_t)d.nru * d.ncu;
-        d.chunk_begin = P.total_chunks;
-        P.total_chunks += (t.rows * t.cols + 1023) / 1024;
+        d.chunk_begin = P.total_chunks;  // chunks only for widths that are not a multiple of 256
+        if (t.cols % 256 != 0) P.total_chunks += (t.rows * t.cols + 1023) / 1024;
         const int64_t bv = vs.block, bc = came ? cs.block : vs.block;
         d.blk_begin[0] = P.total_blk[0];
         P.total_blk[0] += (t.rows + bv - 1) / bv + (t.cols + bv - 1) / bv;

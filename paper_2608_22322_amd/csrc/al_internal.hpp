@@ -93,7 +93,7 @@ struct FacDesc {
     double* scal;     // [0] = clip divisor max(1, RMS / d)
     double* rsum;     // (hi, lo) per block of the row factor: partial sums of R (or R')
     int64_t unit_begin;   // first 256x256 unit of this tensor (2-D)
-    int64_t chunk_begin;  // first 1024-element chunk of this tensor (2-D)
+    int64_t chunk_begin;  // first 1024-element chunk of this tensor (2-D, cols not a multiple of 256)
     int64_t blk_begin[2];  // first code block of this tensor's R then C (role 0: V, role 1: confidence)
     int32_t nru, ncu;     // units along rows / columns
     int32_t pad_;

@@ -957,11 +957,101 @@ hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
 }
 
 // ------------------------------------------------------ CAME apply (2-D)
-// Flattened 1024-element chunks, 4 sub-tiles of 256 per wave, so each
-// momentum block (256) is one sub-tile: recompute uhat and m, encode m, and
-// p <- p (1 - lr wd) - lr (s_i s_j) m.
+// Recompute uhat and m, encode m, and p <- p (1 - lr wd) - lr (s_i s_j) m.
+// Widths that are a multiple of 256: one wave per unit in the RMS pass's
+// layout, so each unit row is exactly one 256-element momentum block (one
+// wave-wide absmax per row); rows in batches with their loads issued first.
+template <int G, bool UF>
+__global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, int64_t base) {
+    const int lane = threadIdx.x & 63;
+    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    if (d.cols & 255) return;  // other widths: the chunk kernel
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int c = 4 * lane;
+    const double clip = d.scal[0], rclip = 1.0 / clip;
+    constexpr bool uf8 = UF;
+    const double2 c01 = *reinterpret_cast<const double2*>(d.cfac + c0 + c);
+    const double2 c23 = *reinterpret_cast<const double2*>(d.cfac + c0 + c + 2);
+    const double2 s01 = *reinterpret_cast<const double2*>(d.sc + c0 + c);
+    const double2 s23 = *reinterpret_cast<const double2*>(d.sc + c0 + c + 2);
+    const double cf[4] = {c01.x, c01.y, c23.x, c23.y};
+    const double sf[4] = {s01.x, s01.y, s23.x, s23.y};
+    for (int r = 0; r < nr; r += kRowBatch) {
+        GRows<G> g;
+        float4 pv[kRowBatch];
+        uint32_t mw[UF ? kRowBatch : 1];
+        float4 mf[UF ? 1 : kRowBatch];
+        double ri[kRowBatch], si[kRowBatch];
+        float ms[kRowBatch];
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            const int rr = r + k < nr ? r + k : nr - 1;  // rows past the end repeat the last one, unused
+            const int64_t e = (r0 + rr) * d.cols + c0 + c;
+            ri[k] = d.rfac[r0 + rr];
+            si[k] = d.sr[r0 + rr];
+            load_row4<G>(d, e, true, 256, c, g.h[k / 4], k % 4);
+            pv[k] = ld_f4<true>(d.p + e);
+            if constexpr (uf8) {
+                mw[k] = ld_u1<true>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                ms[k] = d.mm[(e - c) / 256];
+            } else {
+                mf[k] = ld_f4<true>(reinterpret_cast<const float*>(d.m) + e);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            if (r + k >= nr) break;
+            const int64_t e = (r0 + r + k) * d.cols + c0 + c;
+            float gv[4], mh[4];
+            unpack_graw<G>(g.h[k / 4], k % 4, gv);
+            if constexpr (uf8) {
+                const double st = (double)ms[k] / 127.0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[k] >> (8 * j)), st);
+            } else {
+                mh[0] = mf[k].x;
+                mh[1] = mf[k].y;
+                mh[2] = mf[k].z;
+                mh[3] = mf[k].w;
+            }
+            const float pin[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
+            float mnew[4], pout[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const double uu = (ri[k] * cf[j]) * (double)gv[j];
+                const float uh = div_to_f32(uu, clip, rclip);
+                mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
+                const double upd = (si[k] * sf[j]) * (double)mnew[j];
+                pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+            }
+            st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
+            if constexpr (uf8) {
+                uint32_t am = 0u;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
+                am = group_reduce<OpMax, 64>(am);
+                const double rs = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+                uint32_t q[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * rs) & 0xFFu;
+                store_codes4<UF8, true>(d.m, e, q);
+                if (lane == 0) d.mm[(e - c) / 256] = u2f(am);
+            } else {
+                st_f4<true>(reinterpret_cast<float*>(d.m) + e, make_float4(mnew[0], mnew[1], mnew[2], mnew[3]));
+            }
+        }
+    }
+}
+
+// Other widths: flattened 1024-element chunks, 4 sub-tiles of 256 per wave,
+// so each momentum block (256) is one sub-tile; element by element.
 template <int G>
-__global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
+__global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) {
     const int lane = threadIdx.x & 63;
     const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int64_t nw = (int64_t)gridDim.x * 4;
@@ -970,65 +1060,6 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
         const int64_t n = d.rows * d.cols;
         const int64_t e0 = (chunk - d.chunk_begin) * 1024;
         const double clip = d.scal[0], rclip = 1.0 / clip;
-        if ((d.cols & 255) == 0 && e0 + 1024 <= n) {
-            // every 256-element sub-tile lies in one row: row factors are uniform,
-            // column factors are 4 consecutive values per lane, loads are vectors
-            for (int k = 0; k < 4; ++k) {
-                const int64_t sb = e0 + 256 * k;
-                const int64_t i = sb / d.cols;
-                const int64_t jc = sb - i * d.cols + 4 * lane;
-                const int64_t eb = sb + 4 * lane;
-                const double ri = d.rfac[i], si = d.sr[i];
-                const double2 c01 = *reinterpret_cast<const double2*>(d.cfac + jc);
-                const double2 c23 = *reinterpret_cast<const double2*>(d.cfac + jc + 2);
-                const double2 s01 = *reinterpret_cast<const double2*>(d.sc + jc);
-                const double2 s23 = *reinterpret_cast<const double2*>(d.sc + jc + 2);
-                const double cfj[4] = {c01.x, c01.y, c23.x, c23.y};
-                const double sfj[4] = {s01.x, s01.y, s23.x, s23.y};
-                float gv[4], mh[4];
-                grad4<G>(d.g, eb, gv);
-                const float4 pv = *reinterpret_cast<const float4*>(d.p + eb);
-                const float pin[4] = {pv.x, pv.y, pv.z, pv.w};
-                if (a.m_codec == UF8) {
-                    const double st = (double)d.mm[sb / 256] / 127.0;
-                    const uint32_t w = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + eb);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w >> (8 * j)), st);
-                } else {
-                    const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + eb);
-                    mh[0] = t.x;
-                    mh[1] = t.y;
-                    mh[2] = t.z;
-                    mh[3] = t.w;
-                }
-                float mnew[4], pout[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const double uu = (ri * cfj[j]) * (double)gv[j];
-                    const float uh = div_to_f32(uu, clip, rclip);
-                    mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
-                    const double upd = (si * sfj[j]) * (double)mnew[j];
-                    pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
-                }
-                *reinterpret_cast<float4*>(d.p + eb) = make_float4(pout[0], pout[1], pout[2], pout[3]);
-                if (a.m_codec == UF8) {
-                    uint32_t am = 0u;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
-                    am = group_reduce<OpMax, 64>(am);
-                    const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
-                    uint32_t q[4];
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * r) & 0xFFu;
-                    store_codes4<UF8>(d.m, eb, q);
-                    if (lane == 0) d.mm[sb / 256] = u2f(am);
-                } else {
-                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(d.m) + eb) =
-                        make_float4(mnew[0], mnew[1], mnew[2], mnew[3]);
-                }
-            }
-            continue;
-        }
         for (int k = 0; k < 4; ++k) {
             const int64_t sb = e0 + 256 * k;
             if (sb >= n) break;
@@ -1084,14 +1115,21 @@ __global__ __launch_bounds__(256) void came_apply_kernel(const FacArgs a) {
 }
 
 hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
-    if (a.total_chunks == 0) return hipSuccess;
-    const int64_t cap = int64_t(1) << 30;  // one unit (or chunk) per wave; waves stride beyond this
+    if (a.total_units == 0) return hipSuccess;
+    const bool uf = a.m_codec == UF8;
+    hipError_t e = grad_dtype == G_BF16
+                       ? (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_BF16, true>, a, s)
+                             : launch_wave_per_unit(came_apply_unit_kernel<G_BF16, false>, a, s))
+                       : (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_F32, true>, a, s)
+                             : launch_wave_per_unit(came_apply_unit_kernel<G_F32, false>, a, s));
+    if (e != hipSuccess || a.total_chunks == 0) return e;
+    const int64_t cap = int64_t(1) << 30;
     const int64_t want = (a.total_chunks + 3) / 4;
     const int grid = (int)(want < cap ? want : cap);
     if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(came_apply_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(came_apply_chunk_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL(came_apply_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(came_apply_chunk_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
