@@ -981,20 +981,21 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
     const double2 s23 = *reinterpret_cast<const double2*>(d.sc + c0 + c + 2);
     const double cf[4] = {c01.x, c01.y, c23.x, c23.y};
     const double sf[4] = {s01.x, s01.y, s23.x, s23.y};
-    for (int r = 0; r < nr; r += kRowBatch) {
-        GRows<G> g;
-        float4 pv[kRowBatch];
-        uint32_t mw[UF ? kRowBatch : 1];
-        float4 mf[UF ? 1 : kRowBatch];
-        double ri[kRowBatch], si[kRowBatch];
-        float ms[kRowBatch];
+    constexpr int RB = 4;  // rows per batch (more would spill at 3 waves per SIMD)
+    for (int r = 0; r < nr; r += RB) {
+        GRaw<G> g;
+        float4 pv[RB];
+        uint32_t mw[UF ? RB : 1];
+        float4 mf[UF ? 1 : RB];
+        double ri[RB], si[RB];
+        float ms[RB];
 #pragma unroll
-        for (int k = 0; k < kRowBatch; ++k) {
+        for (int k = 0; k < RB; ++k) {
             const int rr = r + k < nr ? r + k : nr - 1;  // rows past the end repeat the last one, unused
             const int64_t e = (r0 + rr) * d.cols + c0 + c;
             ri[k] = d.rfac[r0 + rr];
             si[k] = d.sr[r0 + rr];
-            load_row4<G>(d, e, true, 256, c, g.h[k / 4], k % 4);
+            load_row4<G>(d, e, true, 256, c, g, k);
             pv[k] = ld_f4<true>(d.p + e);
             if constexpr (uf8) {
                 mw[k] = ld_u1<true>(reinterpret_cast<const uint8_t*>(d.m) + e);
@@ -1004,11 +1005,11 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
             }
         }
 #pragma unroll
-        for (int k = 0; k < kRowBatch; ++k) {
+        for (int k = 0; k < RB; ++k) {
             if (r + k >= nr) break;
             const int64_t e = (r0 + r + k) * d.cols + c0 + c;
             float gv[4], mh[4];
-            unpack_graw<G>(g.h[k / 4], k % 4, gv);
+            unpack_graw<G>(g, k, gv);
             if constexpr (uf8) {
                 const double st = (double)ms[k] / 127.0;
 #pragma unroll
