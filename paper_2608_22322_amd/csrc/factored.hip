@@ -200,7 +200,7 @@ struct GRaw<G_F32> {
     float4 w[4];
 };
 
-template <int G>
+template <int G, bool FULL>
 __device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t r0, int64_t c0, int nr, int nc,
                                           int rg, int ct, int lr, int lc, bool vec) {
     const int cc = ct * 64 + 4 * lc;
@@ -210,7 +210,7 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t 
         const int64_t e = (r0 + rr) * d.cols + c0 + cc;
         if constexpr (G == G_BF16) {
             const uint16_t* g = reinterpret_cast<const uint16_t*>(d.g);
-            if (rr < nr && vec && cc + 4 <= nc) {
+            if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
                 r.w[i] = *reinterpret_cast<const uint2*>(g + e);
             } else {
                 uint32_t h[4] = {0u, 0u, 0u, 0u};
@@ -221,7 +221,7 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t 
             }
         } else {
             const float* g = reinterpret_cast<const float*>(d.g);
-            if (rr < nr && vec && cc + 4 <= nc) {
+            if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
                 r.w[i] = *reinterpret_cast<const float4*>(g + e);
             } else {
                 float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -253,20 +253,13 @@ __device__ __forceinline__ void unpack_graw(const GRaw<G>& r, int i, float gv[4]
 // 64-column tile stay in registers, each row's running sum over the column
 // tiles in LDS (owned by one lane), and the next tile's gradients are loaded
 // while the current one is summed.
-template <int G>
-__global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
-    __shared__ DD racc[256];
+template <int G, bool FULL>
+__device__ __forceinline__ void marg_unit(const FacArgs& a, const FacDesc& d, int64_t ru, int64_t cu, int nr_, int nc_,
+                                          bool vec_, float (*tile)[68], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
-    const int64_t unit = base + blockIdx.x;
-    if (unit >= a.total_units) return;
-    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-    const int64_t u = unit - d.unit_begin;
-    const int64_t ru = u / d.ncu, cu = u % d.ncu;
     const int64_t r0 = ru * 256, c0 = cu * 256;
-    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-    const bool vec = (d.cols & 3) == 0;
+    const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
+    const bool vec = FULL || vec_;
     const double eps1 = a.eps1;
     const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
 #pragma unroll
@@ -275,23 +268,23 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
 #pragma unroll
     for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
     GRaw<G> cur;
-    load_graw<G>(cur, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    load_graw<G, FULL>(cur, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
         GRaw<G> nxt = cur;
         if (it + 1 < total) {
             const int ct1 = (it + 1) / nrg;
-            load_graw<G>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+            load_graw<G, FULL>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
         }
         const int cc = ct * 64 + 4 * lc;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             float gv[4];
             unpack_graw<G>(cur, i, gv);
-            if (rg * kTileRows + lr + 4 * i < nr) {
+            if (FULL || rg * kTileRows + lr + 4 * i < nr) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    if (cc + j < nc) {
+                    if (FULL || cc + j < nc) {
                         const double x = (double)gv[j];
                         dd_add(cacc[j], x * x + eps1);
                     }
@@ -303,8 +296,8 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
         DD rsum{0.0, 0.0};
         const int rr = rg * kTileRows + rrow;
         const int cq = ct * 64 + 16 * rq;  // first column of this lane's quarter
-        if (rr < nr && cq < nc) {
-            if (cq + 16 <= nc) {
+        if (FULL || (rr < nr && cq < nc)) {
+            if (FULL || cq + 16 <= nc) {
 #pragma unroll
                 for (int c = 0; c < 16; c += 4) {
                     const float4 t = *reinterpret_cast<const float4*>(&tile[rrow][16 * rq + c]);
@@ -323,7 +316,7 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
         }
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
-        if (rq == 0 && rr < nr) racc[rr] = dd_merge(racc[rr], rsum);
+        if (rq == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
         __syncthreads();
         if (rg == nrg - 1) {
             // column tile done: its column partials over the unit's rows
@@ -333,7 +326,7 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
                 v = dd_merge(v, dd_shfl_xor(v, 16));
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = cc + j;
-                if (lr == 0 && col < nc) {
+                if (lr == 0 && (FULL || col < nc)) {
                     double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
                     cp[0] = v.hi;
                     cp[1] = v.lo;
@@ -346,12 +339,31 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int row = lane + 64 * k;
-        if (row < nr) {
+        if (FULL || row < nr) {
             double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
             rp[0] = racc[row].hi;
             rp[1] = racc[row].lo;
         }
     }
+}
+
+// Interior units (256x256, width a multiple of 4) take a guard-free body.
+template <int G>
+__global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
+    __shared__ DD racc[256];
+    const int64_t unit = base + blockIdx.x;
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int nr = (int)(d.rows - ru * 256 < 256 ? d.rows - ru * 256 : 256);
+    const int nc = (int)(d.cols - cu * 256 < 256 ? d.cols - cu * 256 : 256);
+    const bool vec = (d.cols & 3) == 0;
+    if (nr == 256 && nc == 256 && vec)
+        marg_unit<G, true>(a, d, ru, cu, nr, nc, vec, tile, racc);
+    else
+        marg_unit<G, false>(a, d, ru, cu, nr, nc, vec, tile, racc);
 }
 
 // One 64-thread workgroup per unit; lists beyond 2^31 units take several launches.
@@ -793,20 +805,20 @@ struct ResRaw {
     float ms[4];
 };
 
-template <int G>
+template <int G, bool FULL>
 __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const FacDesc& d, int64_t r0,
                                             int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec) {
-    load_graw<G>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
+    load_graw<G, FULL>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
     const int cc = ct * 64 + 4 * lc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int rr = rg * kTileRows + lr + 4 * i;
         const int64_t e = (r0 + rr) * d.cols + c0 + cc;
-        r.ri[i] = rr < nr ? d.rfac[r0 + rr] : 0.0;
+        r.ri[i] = (FULL || rr < nr) ? d.rfac[r0 + rr] : 0.0;
         r.mw[i] = 0u;
         r.ms[i] = 0.0f;
-        if (a.m_codec == UF8 && rr < nr) {
-            if (vec && cc + 4 <= nc) {
+        if (a.m_codec == UF8 && (FULL || rr < nr)) {
+            if (FULL || (vec && cc + 4 <= nc)) {
                 // e % 4 == 0: the 4 codes are one word of one momentum block
                 r.mw[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
                 r.ms[i] = d.mm[e / 256];
@@ -815,20 +827,13 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
     }
 }
 
-template <int G>
-__global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
-    __shared__ DD racc[256];
+template <int G, bool FULL>
+__device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int64_t ru, int64_t cu, int nr_, int nc_,
+                                         bool vec_, double (*tile)[66], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
-    const int64_t unit = base + blockIdx.x;
-    if (unit >= a.total_units) return;
-    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
-    const int64_t u = unit - d.unit_begin;
-    const int64_t ru = u / d.ncu, cu = u % d.ncu;
     const int64_t r0 = ru * 256, c0 = cu * 256;
-    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
-    const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-    const bool vec = (d.cols & 3) == 0;
+    const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
+    const bool vec = FULL || vec_;
     const double clip = d.scal[0], rclip = 1.0 / clip;
     const bool uf8 = a.m_codec == UF8;
     const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
@@ -839,28 +844,28 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
     for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
     double cf[4] = {0.0, 0.0, 0.0, 0.0};
     ResRaw<G> cur;
-    load_resraw<G>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    load_resraw<G, FULL>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
         const int cc = ct * 64 + 4 * lc;
         if (rg == 0) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) cf[j] = cc + j < nc ? d.cfac[c0 + cc + j] : 0.0;
+            for (int j = 0; j < 4; ++j) cf[j] = (FULL || cc + j < nc) ? d.cfac[c0 + cc + j] : 0.0;
         }
         ResRaw<G> nxt = cur;
         if (it + 1 < total) {
             const int ct1 = (it + 1) / nrg;
-            load_resraw<G>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+            load_resraw<G, FULL>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rr = rg * kTileRows + lr + 4 * i;
             double term[4] = {0.0, 0.0, 0.0, 0.0};
-            if (rr < nr) {
+            if (FULL || rr < nr) {
                 const int64_t e = (r0 + rr) * d.cols + c0 + cc;
                 float gv[4], mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                 unpack_graw<G>(cur.g, i, gv);
-                if (vec && cc + 4 <= nc) {
+                if (FULL || (vec && cc + 4 <= nc)) {
                     if (uf8) {
                         const double st = (double)cur.ms[i] / 127.0;
 #pragma unroll
@@ -887,7 +892,7 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
                 }
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    if (cc + j < nc) {
+                    if (FULL || cc + j < nc) {
                         const double uu = (cur.ri[i] * cf[j]) * (double)gv[j];
                         const float uh = div_to_f32(uu, clip, rclip);
                         const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
@@ -905,9 +910,9 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
         DD rsum{0.0, 0.0};
         const int rr = rg * kTileRows + rrow;
         const int cq = ct * 64 + 16 * rq;
-        if (rr < nr && cq < nc) {
+        if (FULL || (rr < nr && cq < nc)) {
             const int cnt = nc - cq < 16 ? nc - cq : 16;
-            if (cnt == 16) {
+            if (FULL || cnt == 16) {
 #pragma unroll
                 for (int c = 0; c < 16; c += 2) {
                     const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
@@ -920,7 +925,7 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
         }
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
         rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
-        if (rq == 0 && rr < nr) racc[rr] = dd_merge(racc[rr], rsum);
+        if (rq == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
         __syncthreads();
         if (rg == nrg - 1) {
 #pragma unroll
@@ -929,7 +934,7 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
                 v = dd_merge(v, dd_shfl_xor(v, 16));
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = cc + j;
-                if (lr == 0 && col < nc) {
+                if (lr == 0 && (FULL || col < nc)) {
                     double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
                     cp[0] = v.hi;
                     cp[1] = v.lo;
@@ -942,12 +947,30 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int row = lane + 64 * k;
-        if (row < nr) {
+        if (FULL || row < nr) {
             double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
             rp[0] = racc[row].hi;
             rp[1] = racc[row].lo;
         }
     }
+}
+
+template <int G>
+__global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
+    __shared__ DD racc[256];
+    const int64_t unit = base + blockIdx.x;
+    if (unit >= a.total_units) return;
+    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int nr = (int)(d.rows - ru * 256 < 256 ? d.rows - ru * 256 : 256);
+    const int nc = (int)(d.cols - cu * 256 < 256 ? d.cols - cu * 256 : 256);
+    const bool vec = (d.cols & 3) == 0;
+    if (nr == 256 && nc == 256 && vec)
+        res_unit<G, true>(a, d, ru, cu, nr, nc, vec, tile, racc);
+    else
+        res_unit<G, false>(a, d, ru, cu, nr, nc, vec, tile, racc);
 }
 
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
