@@ -392,6 +392,62 @@ __device__ __forceinline__ void st_u1(void* p, uint32_t x) {
         *reinterpret_cast<uint32_t*>(p) = x;
 }
 
+// Pointers in the global address space. Pointers read from a workspace table
+// are generic to the compiler, which then issues flat loads; those also count
+// against the LDS wait counter, so an LDS read would wait for every load in
+// flight. Kernels that read their pointers from memory convert them once.
+template <class T>
+using gp = __attribute__((address_space(1))) T*;
+
+template <class T>
+__device__ __forceinline__ gp<T> to_g(T* p) {
+    return (gp<T>)p;
+}
+template <class U, class T>
+__device__ __forceinline__ gp<U> g_as(gp<T> p) {
+    return (gp<U>)p;
+}
+
+template <bool NT>
+__device__ __forceinline__ float4 ld_f4(gp<const float> p) {
+    if constexpr (NT) {
+        const nt_f4 x = __builtin_nontemporal_load(g_as<const nt_f4>(p));
+        return make_float4(x.x, x.y, x.z, x.w);
+    } else {
+        return *g_as<const float4>(p);
+    }
+}
+template <bool NT>
+__device__ __forceinline__ uint2 ld_u2(gp<const void> p) {
+    if constexpr (NT) {
+        const nt_u2 x = __builtin_nontemporal_load(g_as<const nt_u2>(p));
+        return make_uint2(x.x, x.y);
+    } else {
+        return *g_as<const uint2>(p);
+    }
+}
+template <bool NT>
+__device__ __forceinline__ uint32_t ld_u1(gp<const void> p) {
+    if constexpr (NT)
+        return __builtin_nontemporal_load(g_as<const uint32_t>(p));
+    else
+        return *g_as<const uint32_t>(p);
+}
+template <bool NT>
+__device__ __forceinline__ void st_f4(gp<float> p, const float4& x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(nt_f4{x.x, x.y, x.z, x.w}, g_as<nt_f4>(p));
+    else
+        *g_as<float4>(p) = x;
+}
+template <bool NT>
+__device__ __forceinline__ void st_u1(gp<void> p, uint32_t x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(x, g_as<uint32_t>(p));
+    else
+        *g_as<uint32_t>(p) = x;
+}
+
 template <int C, bool NT = false>
 __device__ __forceinline__ void store_codes4(void* c, int64_t e, const uint32_t q[4]) {
     if constexpr (C == AL8 || C == UF8) {

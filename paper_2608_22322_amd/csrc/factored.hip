@@ -52,6 +52,42 @@ __device__ __forceinline__ int locate_chunk(const FacDesc* D, int n, int64_t chu
     return lo;
 }
 
+// Global-address-space view of the data pointers of a descriptor (the
+// descriptors are read from the workspace, so their pointers are generic to
+// the compiler; see gp in al_device.hpp).
+struct GD {
+    gp<float> p;
+    gp<const void> g;
+    gp<void> m;
+    gp<float> mm;
+    gp<double> colpart, rowpart;
+    gp<const double> rfac, cfac, sr, sc;
+    gp<const double> scal;
+    int64_t rows, cols, unit_begin;
+    int32_t nru, ncu;
+};
+
+__device__ __forceinline__ GD gview(const FacDesc& d) {
+    GD v;
+    v.p = to_g(d.p);
+    v.g = to_g(d.g);
+    v.m = to_g(d.m);
+    v.mm = to_g(d.mm);
+    v.colpart = to_g(d.colpart);
+    v.rowpart = to_g(d.rowpart);
+    v.rfac = to_g((const double*)d.rfac);
+    v.cfac = to_g((const double*)d.cfac);
+    v.sr = to_g((const double*)d.sr);
+    v.sc = to_g((const double*)d.sc);
+    v.scal = to_g((const double*)d.scal);
+    v.rows = d.rows;
+    v.cols = d.cols;
+    v.unit_begin = d.unit_begin;
+    v.nru = d.nru;
+    v.ncu = d.ncu;
+    return v;
+}
+
 template <int G>
 __device__ __forceinline__ float grad1(const void* g, int64_t e) {
     if constexpr (G == G_BF16)
@@ -201,7 +237,7 @@ struct GRaw<G_F32> {
 };
 
 template <int G, bool FULL>
-__device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t r0, int64_t c0, int nr, int nc,
+__device__ __forceinline__ void load_graw(GRaw<G>& r, const GD& d, int64_t r0, int64_t c0, int nr, int nc,
                                           int rg, int ct, int lr, int lc, bool vec) {
     const int cc = ct * 64 + 4 * lc;
 #pragma unroll
@@ -209,9 +245,9 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t 
         const int rr = rg * kTileRows + lr + 4 * i;
         const int64_t e = (r0 + rr) * d.cols + c0 + cc;
         if constexpr (G == G_BF16) {
-            const uint16_t* g = reinterpret_cast<const uint16_t*>(d.g);
+            const gp<const uint16_t> g = g_as<const uint16_t>(d.g);
             if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
-                r.w[i] = *reinterpret_cast<const uint2*>(g + e);
+                r.w[i] = *g_as<const uint2>(g + e);
             } else {
                 uint32_t h[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -220,9 +256,9 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const FacDesc& d, int64_t 
                 r.w[i] = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
             }
         } else {
-            const float* g = reinterpret_cast<const float*>(d.g);
+            const gp<const float> g = g_as<const float>(d.g);
             if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
-                r.w[i] = *reinterpret_cast<const float4*>(g + e);
+                r.w[i] = *g_as<const float4>(g + e);
             } else {
                 float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -254,7 +290,7 @@ __device__ __forceinline__ void unpack_graw(const GRaw<G>& r, int i, float gv[4]
 // tiles in LDS (owned by one lane), and the next tile's gradients are loaded
 // while the current one is summed.
 template <int G, bool FULL>
-__device__ __forceinline__ void marg_unit(const FacArgs& a, const FacDesc& d, int64_t ru, int64_t cu, int nr_, int nc_,
+__device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t ru, int64_t cu, int nr_, int nc_,
                                           bool vec_, float (*tile)[68], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
     const int64_t r0 = ru * 256, c0 = cu * 256;
@@ -327,7 +363,7 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const FacDesc& d, in
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = cc + j;
                 if (lr == 0 && (FULL || col < nc)) {
-                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    const gp<double> cp = d.colpart + 2 * (ru * d.cols + c0 + col);
                     cp[0] = v.hi;
                     cp[1] = v.lo;
                 }
@@ -340,7 +376,7 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const FacDesc& d, in
     for (int k = 0; k < 4; ++k) {
         const int row = lane + 64 * k;
         if (FULL || row < nr) {
-            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+            const gp<double> rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
             rp[0] = racc[row].hi;
             rp[1] = racc[row].lo;
         }
@@ -361,9 +397,9 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
     const int nc = (int)(d.cols - cu * 256 < 256 ? d.cols - cu * 256 : 256);
     const bool vec = (d.cols & 3) == 0;
     if (nr == 256 && nc == 256 && vec)
-        marg_unit<G, true>(a, d, ru, cu, nr, nc, vec, tile, racc);
+        marg_unit<G, true>(a, gview(d), ru, cu, nr, nc, vec, tile, racc);
     else
-        marg_unit<G, false>(a, d, ru, cu, nr, nc, vec, tile, racc);
+        marg_unit<G, false>(a, gview(d), ru, cu, nr, nc, vec, tile, racc);
 }
 
 // One 64-thread workgroup per unit; lists beyond 2^31 units take several launches.
@@ -539,11 +575,11 @@ hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
 constexpr int kRowBatch = 8;
 
 template <int G>
-__device__ __forceinline__ void load_row4(const FacDesc& d, int64_t e, bool vec, int nc, int c, GRaw<G>& r, int k) {
+__device__ __forceinline__ void load_row4(const GD& d, int64_t e, bool vec, int nc, int c, GRaw<G>& r, int k) {
     if constexpr (G == G_BF16) {
-        const uint16_t* g = reinterpret_cast<const uint16_t*>(d.g);
+        const gp<const uint16_t> g = g_as<const uint16_t>(d.g);
         if (vec) {
-            r.w[k] = ld_u2<true>(g + e);
+            r.w[k] = ld_u2<true>(g_as<const void>(g + e));
         } else {
             uint32_t h[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -552,7 +588,7 @@ __device__ __forceinline__ void load_row4(const FacDesc& d, int64_t e, bool vec,
             r.w[k] = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
         }
     } else {
-        const float* g = reinterpret_cast<const float*>(d.g);
+        const gp<const float> g = g_as<const float>(d.g);
         if (vec) {
             r.w[k] = ld_f4<true>(g + e);
         } else {
@@ -576,7 +612,7 @@ __global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a, int64_t b
     const int lane = threadIdx.x & 63;
     const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
-    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const int64_t u = unit - d.unit_begin;
     const int64_t ru = u / d.ncu, cu = u % d.ncu;
     const int64_t r0 = ru * 256, c0 = cu * 256;
@@ -670,7 +706,7 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t
     const int lane = threadIdx.x & 63;
     const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
-    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const int64_t u = unit - d.unit_begin;
     const int64_t ru = u / d.ncu, cu = u % d.ncu;
     const int64_t r0 = ru * 256, c0 = cu * 256;
@@ -806,7 +842,7 @@ struct ResRaw {
 };
 
 template <int G, bool FULL>
-__device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const FacDesc& d, int64_t r0,
+__device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const GD& d, int64_t r0,
                                             int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec) {
     load_graw<G, FULL>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
     const int cc = ct * 64 + 4 * lc;
@@ -820,7 +856,7 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
         if (a.m_codec == UF8 && (FULL || rr < nr)) {
             if (FULL || (vec && cc + 4 <= nc)) {
                 // e % 4 == 0: the 4 codes are one word of one momentum block
-                r.mw[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                r.mw[i] = *g_as<const uint32_t>(g_as<const uint8_t>(d.m) + e);
                 r.ms[i] = d.mm[e / 256];
             }
         }
@@ -828,13 +864,13 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
 }
 
 template <int G, bool FULL>
-__device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int64_t ru, int64_t cu, int nr_, int nc_,
-                                         bool vec_, double (*tile)[66], DD* racc) {
+__device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double clip, int64_t ru, int64_t cu, int nr_,
+                                         int nc_, bool vec_, double (*tile)[66], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
     const int64_t r0 = ru * 256, c0 = cu * 256;
     const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
     const bool vec = FULL || vec_;
-    const double clip = d.scal[0], rclip = 1.0 / clip;
+    const double rclip = 1.0 / clip;
     const bool uf8 = a.m_codec == UF8;
     const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
 #pragma unroll
@@ -872,7 +908,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int
                         for (int j = 0; j < 4; ++j)
                             mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(cur.mw[i] >> (8 * j)), st);
                     } else {
-                        const float4 t = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.m) + e);
+                        const float4 t = ld_f4<false>(g_as<const float>(d.m) + e);
                         mh[0] = t.x;
                         mh[1] = t.y;
                         mh[2] = t.z;
@@ -883,10 +919,10 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int
                     for (int j = 0; j < 4; ++j) {
                         if (cc + j < nc) {
                             if (uf8)
-                                mh[j] = uf8_decode(reinterpret_cast<const int8_t*>(d.m)[e + j],
+                                mh[j] = uf8_decode(g_as<const int8_t>(d.m)[e + j],
                                                    (double)d.mm[(e + j) / 256] / 127.0);
                             else
-                                mh[j] = reinterpret_cast<const float*>(d.m)[e + j];
+                                mh[j] = g_as<const float>(d.m)[e + j];
                         }
                     }
                 }
@@ -935,7 +971,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = cc + j;
                 if (lr == 0 && (FULL || col < nc)) {
-                    double* cp = d.colpart + 2 * (ru * d.cols + c0 + col);
+                    const gp<double> cp = d.colpart + 2 * (ru * d.cols + c0 + col);
                     cp[0] = v.hi;
                     cp[1] = v.lo;
                 }
@@ -948,7 +984,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const FacDesc& d, int
     for (int k = 0; k < 4; ++k) {
         const int row = lane + 64 * k;
         if (FULL || row < nr) {
-            double* rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
+            const gp<double> rp = d.rowpart + 2 * (cu * d.rows + r0 + row);
             rp[0] = racc[row].hi;
             rp[1] = racc[row].lo;
         }
@@ -968,9 +1004,9 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
     const int nc = (int)(d.cols - cu * 256 < 256 ? d.cols - cu * 256 : 256);
     const bool vec = (d.cols & 3) == 0;
     if (nr == 256 && nc == 256 && vec)
-        res_unit<G, true>(a, d, ru, cu, nr, nc, vec, tile, racc);
+        res_unit<G, true>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
     else
-        res_unit<G, false>(a, d, ru, cu, nr, nc, vec, tile, racc);
+        res_unit<G, false>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
 }
 
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
@@ -989,7 +1025,7 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
     const int lane = threadIdx.x & 63;
     const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
-    const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     if (d.cols & 255) return;  // other widths: the chunk kernel
     const int64_t u = unit - d.unit_begin;
     const int64_t ru = u / d.ncu, cu = u % d.ncu;
