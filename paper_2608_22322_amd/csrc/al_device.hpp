@@ -207,6 +207,27 @@ __device__ __forceinline__ float div_to_f32(double x, double d, double rd) {
     return (float)(x / d);
 }
 
+// Four quotients at once, with one (rarely taken) branch for the fallbacks.
+__device__ __forceinline__ void div4_to_f32(const double x[4], double d, double rd, float out[4]) {
+    bool all = true;
+    bool ok[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const double q = x[j] * rd;
+        const uint64_t b = __builtin_bit_cast(uint64_t, q);
+        const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
+        const uint32_t low = (uint32_t)b & 0x1FFFFFFFu;
+        ok[j] = (ex - (1023u - 125u) <= 251u && low - 0x0FFFFFF8u > 16u) || q == 0.0;
+        out[j] = (float)q;
+        all = all && ok[j];
+    }
+    if (__builtin_expect(!all, 0)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (!ok[j]) out[j] = (float)(x[j] / d);
+    }
+}
+
 // Cross-lane moves of 64-bit values.
 __device__ __forceinline__ double shfl_d(double v, int src) { return __shfl(v, src); }
 __device__ __forceinline__ double readlane_d(double v, int lane) {
@@ -248,6 +269,16 @@ __device__ __forceinline__ DD dd_merge(DD a, DD b) {
 __device__ __forceinline__ double dd_value(DD a) { return a.hi + a.lo; }
 
 __device__ __forceinline__ DD dd_shfl_xor(DD a, int m) { return DD{__shfl_xor(a.hi, m), __shfl_xor(a.lo, m)}; }
+
+// Double-double of the partner lane within a quad (DPP, no LDS traffic):
+// CTRL = kDppQuadXor1 or kDppQuadXor2.
+template <int CTRL>
+__device__ __forceinline__ DD dd_quad_xor(DD a) {
+    const uint64_t h = __builtin_bit_cast(uint64_t, a.hi), l = __builtin_bit_cast(uint64_t, a.lo);
+    const uint64_t h2 = ((uint64_t)dpp<CTRL>((uint32_t)(h >> 32)) << 32) | dpp<CTRL>((uint32_t)h);
+    const uint64_t l2 = ((uint64_t)dpp<CTRL>((uint32_t)(l >> 32)) << 32) | dpp<CTRL>((uint32_t)l);
+    return DD{__builtin_bit_cast(double, h2), __builtin_bit_cast(double, l2)};
+}
 
 // Wave-wide merge; every lane gets the total (fixed butterfly order).
 __device__ __forceinline__ DD dd_wave_sum(DD a) {
@@ -414,7 +445,8 @@ __device__ __forceinline__ float4 ld_f4(gp<const float> p) {
         const nt_f4 x = __builtin_nontemporal_load(g_as<const nt_f4>(p));
         return make_float4(x.x, x.y, x.z, x.w);
     } else {
-        return *g_as<const float4>(p);
+        const nt_f4 x = *g_as<const nt_f4>(p);
+        return make_float4(x.x, x.y, x.z, x.w);
     }
 }
 template <bool NT>
@@ -423,7 +455,8 @@ __device__ __forceinline__ uint2 ld_u2(gp<const void> p) {
         const nt_u2 x = __builtin_nontemporal_load(g_as<const nt_u2>(p));
         return make_uint2(x.x, x.y);
     } else {
-        return *g_as<const uint2>(p);
+        const nt_u2 x = *g_as<const nt_u2>(p);
+        return make_uint2(x.x, x.y);
     }
 }
 template <bool NT>
@@ -438,7 +471,7 @@ __device__ __forceinline__ void st_f4(gp<float> p, const float4& x) {
     if constexpr (NT)
         __builtin_nontemporal_store(nt_f4{x.x, x.y, x.z, x.w}, g_as<nt_f4>(p));
     else
-        *g_as<float4>(p) = x;
+        *g_as<nt_f4>(p) = nt_f4{x.x, x.y, x.z, x.w};
 }
 template <bool NT>
 __device__ __forceinline__ void st_u1(gp<void> p, uint32_t x) {

@@ -247,7 +247,7 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const GD& d, int64_t r0, i
         if constexpr (G == G_BF16) {
             const gp<const uint16_t> g = g_as<const uint16_t>(d.g);
             if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
-                r.w[i] = *g_as<const uint2>(g + e);
+                r.w[i] = ld_u2<false>(g_as<const void>(g + e));
             } else {
                 uint32_t h[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -258,7 +258,7 @@ __device__ __forceinline__ void load_graw(GRaw<G>& r, const GD& d, int64_t r0, i
         } else {
             const gp<const float> g = g_as<const float>(d.g);
             if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
-                r.w[i] = *g_as<const float4>(g + e);
+                r.w[i] = ld_f4<false>(g + e);
             } else {
                 float h[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
@@ -350,8 +350,8 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
                 }
             }
         }
-        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
-        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
+        rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor1>(rsum));
+        rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor2>(rsum));
         if (rq == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
         __syncthreads();
         if (rg == nrg - 1) {
@@ -926,13 +926,16 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                         }
                     }
                 }
+                double uu[4];
+                float uh[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) uu[j] = (cur.ri[i] * cf[j]) * (double)gv[j];
+                div4_to_f32(uu, clip, rclip, uh);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     if (FULL || cc + j < nc) {
-                        const double uu = (cur.ri[i] * cf[j]) * (double)gv[j];
-                        const float uh = div_to_f32(uu, clip, rclip);
-                        const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
-                        const double df = (double)uh - (double)m;
+                        const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
+                        const double df = (double)uh[j] - (double)m;
                         term[j] = df * df + a.eps2;
                         dd_add(cacc[j], term[j]);
                     }
@@ -959,8 +962,8 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                 for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
             }
         }
-        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 1));
-        rsum = dd_merge(rsum, dd_shfl_xor(rsum, 2));
+        rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor1>(rsum));
+        rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor2>(rsum));
         if (rq == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
         __syncthreads();
         if (rg == nrg - 1) {
@@ -1034,12 +1037,12 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
     const int c = 4 * lane;
     const double clip = d.scal[0], rclip = 1.0 / clip;
     constexpr bool uf8 = UF;
-    const double2 c01 = *reinterpret_cast<const double2*>(d.cfac + c0 + c);
-    const double2 c23 = *reinterpret_cast<const double2*>(d.cfac + c0 + c + 2);
-    const double2 s01 = *reinterpret_cast<const double2*>(d.sc + c0 + c);
-    const double2 s23 = *reinterpret_cast<const double2*>(d.sc + c0 + c + 2);
-    const double cf[4] = {c01.x, c01.y, c23.x, c23.y};
-    const double sf[4] = {s01.x, s01.y, s23.x, s23.y};
+    double cf[4], sf[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        cf[j] = d.cfac[c0 + c + j];
+        sf[j] = d.sc[c0 + c + j];
+    }
     constexpr int RB = 4;  // rows per batch (more would spill at 3 waves per SIMD)
     for (int r = 0; r < nr; r += RB) {
         GRaw<G> g;
@@ -1057,10 +1060,10 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
             load_row4<G>(d, e, true, 256, c, g, k);
             pv[k] = ld_f4<true>(d.p + e);
             if constexpr (uf8) {
-                mw[k] = ld_u1<true>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                mw[k] = ld_u1<true>(g_as<const void>(g_as<const uint8_t>(d.m) + e));
                 ms[k] = d.mm[(e - c) / 256];
             } else {
-                mf[k] = ld_f4<true>(reinterpret_cast<const float*>(d.m) + e);
+                mf[k] = ld_f4<true>(g_as<const float>(d.m) + e);
             }
         }
 #pragma unroll
@@ -1080,12 +1083,14 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
                 mh[3] = mf[k].w;
             }
             const float pin[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
-            float mnew[4], pout[4];
+            float mnew[4], pout[4], uh[4];
+            double uu[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) uu[j] = (ri[k] * cf[j]) * (double)gv[j];
+            div4_to_f32(uu, clip, rclip, uh);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const double uu = (ri[k] * cf[j]) * (double)gv[j];
-                const float uh = div_to_f32(uu, clip, rclip);
-                mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh);
+                mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
                 const double upd = (si[k] * sf[j]) * (double)mnew[j];
                 pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
             }
@@ -1099,10 +1104,11 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
                 uint32_t q[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * rs) & 0xFFu;
-                store_codes4<UF8, true>(d.m, e, q);
+                const uint32_t w = (q[0] & 0xFFu) | ((q[1] & 0xFFu) << 8) | ((q[2] & 0xFFu) << 16) | (q[3] << 24);
+                st_u1<true>(g_as<void>(g_as<uint8_t>(d.m) + e), w);
                 if (lane == 0) d.mm[(e - c) / 256] = u2f(am);
             } else {
-                st_f4<true>(reinterpret_cast<float*>(d.m) + e, make_float4(mnew[0], mnew[1], mnew[2], mnew[3]));
+                st_f4<true>(g_as<float>(d.m) + e, make_float4(mnew[0], mnew[1], mnew[2], mnew[3]));
             }
         }
     }
