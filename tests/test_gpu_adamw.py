@@ -158,6 +158,20 @@ def test_adamw_100_steps_tinyllama_shapes(dev, block):
 
 def _sampled_full_size(dev, shapes, w, block, n_samples, steps, seed):
     """Run the full list on the GPU; recompute sampled whole tiles with the oracle from regenerated inputs."""
+    T = max(block, 256)
+    rng = np.random.default_rng(seed)
+    picks = []
+    for _ in range(n_samples):
+        i = int(rng.integers(len(shapes)))
+        ntiles = (shapes[i].n + T - 1) // T
+        k = int(rng.integers(ntiles))
+        picks.append((i, k))
+    picks += [(0, 0), (len(shapes) - 1, (shapes[-1].n + T - 1) // T - 1)]
+    return _sampled_full_size_picks(dev, shapes, w, block, steps, picks)
+
+
+def _sampled_full_size_picks(dev, shapes, w, block, steps, picks):
+    """As _sampled_full_size, for the given (tensor, tile) picks; a tile is max(B_V, 256) elements."""
     import torch
 
     import paper_2608_22322_amd as al
@@ -173,14 +187,6 @@ def _sampled_full_size(dev, shapes, w, block, n_samples, steps, seed):
         states.append(al.ParamState(p, g, s.rows, s.cols, m=m, m_meta=mm, v=v, v_meta=vm))
     cfg = al.adamw_cfg(grad_bf16=True, m=mspec, v=vspec)
     arr = al.tensor_array(states)
-    rng = np.random.default_rng(seed)
-    picks = []
-    for _ in range(n_samples):
-        i = int(rng.integers(len(shapes)))
-        ntiles = (shapes[i].n + T - 1) // T
-        k = int(rng.integers(ntiles))
-        picks.append((i, k))
-    picks += [(0, 0), (len(shapes) - 1, (shapes[-1].n + T - 1) // T - 1)]
     host = {}
     for (i, k) in picks:
         s = shapes[i]
@@ -220,12 +226,30 @@ def test_adamw_full_size_tinyllama_sampled(dev, block):
     log(f"near-boundary code differences: {near}")
 
 
-@pytest.mark.parametrize("block", [64, 256])
+@pytest.mark.parametrize("block", [64, 256, 2048])
 def test_adamw_full_size_llama7b_sampled(dev, block):
     import torch
 
     w = Workload("llama-7b", llama7b_shapes(), zero_frac=0.01, steps=2)
     log(f"Llama-7B full size, B_V {block}")
     near = _sampled_full_size(dev, w.shapes, w, block, 32, 2, 9)
+    log(f"near-boundary code differences: {near}")
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("block", [64, 2048])
+def test_adamw_tensor_beyond_2_31_elements(dev, block):
+    """One tensor of 2^31 + 3 * 2048 + 778 elements (64-bit offsets, ragged last chunk); sampled
+    tiles below and above 2^31 recomputed by the oracle."""
+    import torch
+
+    cols = 2**30 + 3 * 1024 + 389
+    n = 2 * cols
+    shapes = [Shape("huge", 2, cols)]
+    w = Workload("huge", shapes, zero_frac=0.01, steps=2)
+    log(f"one tensor of {n} elements, B_V {block}")
+    T = max(block, 256)
+    near = _sampled_full_size_picks(dev, shapes, w, block, 2, [(0, 0), (0, 2**31 // T - 1), (0, 2**31 // T),
+                                                               (0, 2**31 // T + 1), (0, (n + T - 1) // T - 1)])
     log(f"near-boundary code differences: {near}")
     torch.cuda.empty_cache()

@@ -131,3 +131,48 @@ def test_degenerate_blocks(dev):
         compare_bits(g_meta, o_meta, codec + " degenerate meta")
         compare_bits(g_out, oracle.al_dequantize(bits, o_codes, o_meta, x.shape[0], B), codec + " degenerate decode")
         assert np.array_equal(g_codes[: x.shape[0]] == 0, x == 0)
+
+
+@pytest.mark.parametrize("codec", ["AL8", "UF8"])
+def test_quantize_beyond_2_31_elements(dev, codec):
+    """al_quantize / al_dequantize over 2^31 + 2048 + 333 elements (64-bit offsets, partial last
+    block); blocks below and above 2^31 recomputed by the oracle from regenerated inputs."""
+    import torch
+
+    import paper_2608_22322_amd as al
+
+    B = 256
+    n = 2**31 + 2048 + 333
+    key = synth.grad_key(77, 1)
+    xd = torch.empty(n + 4, dtype=torch.float32, device=dev)
+    al.synth_normal(xd[:n], key, 1e-3)
+    if codec == "AL8":
+        xd.abs_()
+    c = CODECS[codec]
+    codes, meta = al.alloc_state(n, al.Spec(c, B), dev)
+    al.quantize(c, xd[:n], B, -53.0, codes, meta)
+    out = torch.empty(n + 4, dtype=torch.float32, device=dev)
+    al.dequantize(c, codes, meta, n, B, out)
+    torch.cuda.synchronize()
+    nb = (n + B - 1) // B
+    near = 0
+    for b in (0, 2**31 // B - 1, 2**31 // B, 2**31 // B + 1, nb - 1):
+        lo, hi = b * B, min(n, (b + 1) * B)
+        x = synth.normal_f32(key, np.arange(lo, hi), 1e-3)
+        if codec == "AL8":
+            x = np.abs(x)
+        g_codes = to_np(codes[lo:lo + B])
+        if codec == "UF8":
+            o_codes, o_meta, y = oracle.uf8_quantize(x, B)
+            g_codes = g_codes.astype(np.int8)
+            compare_bits(to_np(meta[b:b + 1]), o_meta, f"{codec} block {b} meta")
+            ref = oracle.uf8_dequantize(g_codes, o_meta, hi - lo, B)
+        else:
+            o_codes, o_meta, y = oracle.al_quantize(8, x, B, -53.0)
+            compare_bits(to_np(meta[2 * b:2 * b + 2]), o_meta, f"{codec} block {b} meta")
+            ref = oracle.al_dequantize(8, g_codes, o_meta, hi - lo, B)
+        near += compare_codes(g_codes, o_codes, y, f"{codec} block {b}")
+        compare_bits(to_np(out[lo:hi]), ref, f"{codec} block {b} decode")
+    log(f"{codec} beyond 2^31: near-boundary code differences {near}")
+    del xd, out, codes, meta
+    torch.cuda.empty_cache()
