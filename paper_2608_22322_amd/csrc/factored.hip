@@ -236,13 +236,16 @@ struct GRaw<G_F32> {
     float4 w[4];
 };
 
-template <int G, bool FULL>
+// Tile width TC = 64: 16 lanes per row, lane rows lr + 4i of a 16-row group;
+// TC = 128: 32 lanes per row, lane rows lr + 2i of an 8-row group.
+template <int G, bool FULL, int TC = 64>
 __device__ __forceinline__ void load_graw(GRaw<G>& r, const GD& d, int64_t r0, int64_t c0, int nr, int nc,
                                           int rg, int ct, int lr, int lc, bool vec) {
-    const int cc = ct * 64 + 4 * lc;
+    constexpr int LS = 256 / TC, TR = 4 * LS;
+    const int cc = ct * TC + 4 * lc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int rr = rg * kTileRows + lr + 4 * i;
+        const int rr = rg * TR + lr + LS * i;
         const int64_t e = (r0 + rr) * d.cols + c0 + cc;
         if constexpr (G == G_BF16) {
             const gp<const uint16_t> g = g_as<const uint16_t>(d.g);
@@ -829,10 +832,13 @@ __device__ __forceinline__ float came_momentum(const FacArgs& a, const FacDesc& 
 
 // --------------------------- CAME residual marginal sums (tile layout, fp64)
 // Term (uhat - m)^2 + eps2 with uhat = fl32(u / clip), m the in-step
-// momentum; the lane roles, loop order and one-tile-ahead loads of the
-// marginals of G2, with the binary64 terms staged in LDS for the row sums.
-// A lane's raw inputs of one tile: gradients, momentum words, and per row
-// the factor r_i and the momentum block scale.
+// momentum; the loop order and one-tile-ahead loads of the marginals of G2,
+// on 8x128 tiles: lane (lr, lc) = (lane / 32, lane % 32) holds rows lr + 2i
+// (i < 4), columns 4 lc .. 4 lc + 3, so each row's 128 momentum codes are one
+// full 128-byte line; the binary64 terms are staged in LDS and 8 lanes sum
+// each tile row (16 columns each, merged with DPP).
+constexpr int kResRows = 8, kResCols = 128;
+
 template <int G>
 struct ResRaw {
     GRaw<G> g;
@@ -844,11 +850,11 @@ struct ResRaw {
 template <int G, bool FULL>
 __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const GD& d, int64_t r0,
                                             int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec) {
-    load_graw<G, FULL>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
-    const int cc = ct * 64 + 4 * lc;
+    load_graw<G, FULL, kResCols>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
+    const int cc = ct * kResCols + 4 * lc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int rr = rg * kTileRows + lr + 4 * i;
+        const int rr = rg * kResRows + lr + 2 * i;
         const int64_t e = (r0 + rr) * d.cols + c0 + cc;
         r.ri[i] = (FULL || rr < nr) ? d.rfac[r0 + rr] : 0.0;
         r.mw[i] = 0u;
@@ -865,14 +871,14 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
 
 template <int G, bool FULL>
 __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double clip, int64_t ru, int64_t cu, int nr_,
-                                         int nc_, bool vec_, double (*tile)[66], DD* racc) {
-    const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
+                                         int nc_, bool vec_, double (*tile)[kResCols + 2], DD* racc) {
+    const int lane = threadIdx.x, lc = lane & 31, lr = lane >> 5, rrow = lane >> 3, re = lane & 7;
     const int64_t r0 = ru * 256, c0 = cu * 256;
     const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
     const bool vec = FULL || vec_;
     const double rclip = 1.0 / clip;
     const bool uf8 = a.m_codec == UF8;
-    const int nrg = (nr + kTileRows - 1) / kTileRows, nct = (nc + 63) / 64, total = nrg * nct;
+    const int nrg = (nr + kResRows - 1) / kResRows, nct = (nc + kResCols - 1) / kResCols, total = nrg * nct;
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[lane + 64 * k] = DD{0.0, 0.0};
     DD cacc[4];
@@ -883,7 +889,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
     load_resraw<G, FULL>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
-        const int cc = ct * 64 + 4 * lc;
+        const int cc = ct * kResCols + 4 * lc;
         if (rg == 0) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) cf[j] = (FULL || cc + j < nc) ? d.cfac[c0 + cc + j] : 0.0;
@@ -895,7 +901,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int rr = rg * kTileRows + lr + 4 * i;
+            const int rr = rg * kResRows + lr + 2 * i;
             double term[4] = {0.0, 0.0, 0.0, 0.0};
             if (FULL || rr < nr) {
                 const int64_t e = (r0 + rr) * d.cols + c0 + cc;
@@ -941,36 +947,37 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                     }
                 }
             }
-            double* tp = &tile[lr + 4 * i][4 * lc];
+            double* tp = &tile[lr + 2 * i][4 * lc];
             *reinterpret_cast<double2*>(tp) = make_double2(term[0], term[1]);
             *reinterpret_cast<double2*>(tp + 2) = make_double2(term[2], term[3]);
         }
         __syncthreads();
         DD rsum{0.0, 0.0};
-        const int rr = rg * kTileRows + rrow;
-        const int cq = ct * 64 + 16 * rq;
+        const int rr = rg * kResRows + rrow;
+        const int cq = ct * kResCols + 16 * re;  // first column of this lane's sixteenth
         if (FULL || (rr < nr && cq < nc)) {
             const int cnt = nc - cq < 16 ? nc - cq : 16;
             if (FULL || cnt == 16) {
 #pragma unroll
                 for (int c = 0; c < 16; c += 2) {
-                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
+                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * re + c]);
                     dd_add(rsum, t.x);
                     dd_add(rsum, t.y);
                 }
             } else {
-                for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
+                for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * re + c]);
             }
         }
         rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor1>(rsum));
         rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor2>(rsum));
-        if (rq == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
+        rsum = dd_merge(rsum, dd_quad_xor<kDppRowHalfMirror>(rsum));  // the other quad of the 8 lanes
+        if (re == 0 && (FULL || rr < nr)) racc[rr] = dd_merge(racc[rr], rsum);
         __syncthreads();
         if (rg == nrg - 1) {
+            // column tile done: merge the two lanes of each column
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 DD v = cacc[j];
-                v = dd_merge(v, dd_shfl_xor(v, 16));
                 v = dd_merge(v, dd_shfl_xor(v, 32));
                 const int col = cc + j;
                 if (lr == 0 && (FULL || col < nc)) {
@@ -996,7 +1003,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
 
 template <int G>
 __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
+    __shared__ __attribute__((aligned(16))) double tile[kResRows][kResCols + 2];
     __shared__ DD racc[256];
     const int64_t unit = base + blockIdx.x;
     if (unit >= a.total_units) return;
