@@ -285,3 +285,27 @@ def test_tinyllama_workspace_sizes():
         need = _fac_ws(ts, came)
         two_d = sum(s.n for s in shapes if s.rows > 1)
         assert two_d / 8 <= need <= two_d / 8 * 1.2, (came, need)
+
+
+def test_g1_grouping_reproduces_table4_adafactor_memory():
+    """Section 6: G1 keeps 1-D, norm, embedding and LM-head states FP32; Table 4 lists 1.4 / 1.5 MiB of
+    Adafactor state under G1 at B = 256 / 2048 (against 1.2 / 1.3 under G0)."""
+    from paper_2608_22322_amd import grouping
+
+    sh = tinyllama_shapes()
+    prot = grouping.protected_flags(sh, "G1")
+    names = {s.name for s, p in zip(sh, prot) if p and s.is_2d}
+    assert names == {"embed", "lm_head"}
+    assert all(p for s, p in zip(sh, prot) if not s.is_2d)
+    for B, g0, g1 in ((256, 1.2, 1.4), (2048, 1.3, 1.5)):
+        specs = {"v": al.Spec(al.AL8, B)}
+        assert round(grouping.grouped_state_bytes(sh, "adafactor", specs, "G0") / MiB, 1) == g0
+        assert round(grouping.grouped_state_bytes(sh, "adafactor", specs, "G1") / MiB, 1) == g1
+    # the G0 AdamW and CAME rows of Table 4 through the same accounting
+    assert round(grouping.grouped_state_bytes(sh, "adamw", {"m": al.Spec(al.UF8, 256), "v": al.Spec(al.AL8, 2048)},
+                                              "G0") / MiB, 1) == 2119.2
+    assert round(grouping.grouped_state_bytes(sh, "came", {"m": al.Spec(al.UF8, 256), "v": al.Spec(al.AL16, 2048),
+                                                           "conf": al.Spec(al.AL16, 2048)}, "G0") / MiB, 1) == 1069.8
+    assert not any(grouping.protected_flags(sh, "G0"))
+    with pytest.raises(ValueError):
+        grouping.protected_flags(sh, "G2")
