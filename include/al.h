@@ -220,6 +220,17 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
  * (factored second-moment reconstruction). x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
+/* Sums of squares behind the relative update error of section 3.2 (Eq.
+ * update_error): with U = a, U_ref = b (two updates of the same n elements,
+ * fp32 device arrays), writes out[0] = sum_i (a_i - b_i)^2 and out[1] =
+ * sum_i b_i^2, each term formed in binary64 and summed double-double (fixed
+ * order: the result is reproducible and within an ulp of the exact sum).
+ * out: device buffer of at least AL_DIFF_NORMS_OUT doubles, 16-byte aligned;
+ * out[2 ..] is scratch. n = 0 writes zeros. Enqueued on stream; allocates
+ * nothing. The error is sqrt(out[0]) / (sqrt(out[1]) + eps). */
+#define AL_DIFF_NORMS_OUT 4098
+al_status al_diff_norms(const float* a, const float* b, int64_t n, double* out, void* stream);
+
 /* Diagnostic: the streaming ceiling of the fused AdamW access pattern. Reads
  * p (n fp32), g (n bf16), m and v (n bytes each) and writes p, m, v with no
  * optimizer arithmetic (the values written are meaningless), using the same

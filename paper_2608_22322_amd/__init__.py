@@ -67,7 +67,7 @@ _lib = None
 # every symbol include/al.h and include/al_synth.h declare
 EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al_state_bytes", "al_quantize",
            "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
-           "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream",
+           "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream", "al_diff_norms",
            "al_synth_normal")
 
 
@@ -98,9 +98,10 @@ def lib():
         L.al_synth_normal.argtypes = [vp, i32, i64, u64, f, u64, u64, vp]
         L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
         L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
+        L.al_diff_norms.argtypes = [vp, vp, i64, vp, vp]
         for name in ("al_quantize", "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes",
                      "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream",
-           "al_synth_normal"):
+                     "al_diff_norms", "al_synth_normal"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -183,6 +184,17 @@ def diag_math(fn: int, x, out, stream=None) -> None:
 
 def diag_stream(nontemporal: bool, p, g, m, v, stream=None) -> None:
     check(lib().al_diag_stream(int(nontemporal), _ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), _stream(stream)))
+
+
+DIFF_NORMS_OUT = 4098  # doubles of the al_diff_norms output / scratch buffer
+
+
+def diff_norms(a, b, out, stream=None) -> None:
+    """out[0] = sum (a - b)^2, out[1] = sum b^2 (float32 device tensors of equal size; out: float64
+    device tensor of at least DIFF_NORMS_OUT elements)."""
+    if a.numel() != b.numel() or out.numel() < DIFF_NORMS_OUT:
+        raise ValueError("diff_norms: sizes")
+    check(lib().al_diff_norms(_ptr(a), _ptr(b), a.numel(), _ptr(out), _stream(stream)))
 
 
 def synth_normal(out, key: int, sigma: float, mask_key: int = 0, mask_frac: float = 0.0, stream=None) -> None:

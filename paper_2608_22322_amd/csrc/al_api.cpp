@@ -431,6 +431,17 @@ al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_math launch");
 }
 
+al_status al_diff_norms(const float* a, const float* b, int64_t n, double* out, void* stream) {
+    g_err[0] = 0;
+    if (n < 0) return fail(AL_EINVAL, "al_diff_norms: n < 0");
+    if (!out) return fail(AL_EINVAL, "al_diff_norms: out is NULL");
+    if (n > 0 && (!a || !b)) return fail(AL_EINVAL, "al_diff_norms: NULL buffer");
+    if (!aligned16(out) || (n > 0 && (!aligned16(a) || !aligned16(b))))
+        return fail(AL_EALIGN, "al_diff_norms: alignment");
+    hipError_t e = al::launch_diff_norms(a, b, n, out, as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_diff_norms launch");
+}
+
 al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n, void* stream) {
     g_err[0] = 0;
     if (n < 0 || n % 2048 != 0) return fail(AL_EINVAL, "al_diag_stream: n must be a non-negative multiple of 2048");

@@ -108,6 +108,70 @@ hipError_t launch_diag_math(int fn, const double* x, int64_t n, double* out, int
     return hipGetLastError();
 }
 
+// Sums of squares for the relative update error (section 3.2, Eq.
+// update_error): out[0] = sum (a_i - b_i)^2, out[1] = sum b_i^2 over binary64
+// terms, double-double partials per workgroup (fixed count and order), then
+// one workgroup merges them; out[2 ..] holds the partials.
+__global__ __launch_bounds__(256) void diff_norms_partial_kernel(const float* __restrict__ a,
+                                                                 const float* __restrict__ b, int64_t n,
+                                                                 double* __restrict__ part) {
+    __shared__ DD sh[2][4];
+    DD s0{0.0, 0.0}, s1{0.0, 0.0};
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const double bi = (double)b[i];
+        const double d = (double)a[i] - bi;
+        dd_add(s0, d * d);
+        dd_add(s1, bi * bi);
+    }
+    s0 = dd_wave_sum(s0);
+    s1 = dd_wave_sum(s1);
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (lane == 0) {
+        sh[0][w] = s0;
+        sh[1][w] = s1;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        DD t0 = sh[0][0], t1 = sh[1][0];
+        for (int k = 1; k < 4; ++k) {
+            t0 = dd_merge(t0, sh[0][k]);
+            t1 = dd_merge(t1, sh[1][k]);
+        }
+        double* o = part + 4 * blockIdx.x;
+        o[0] = t0.hi;
+        o[1] = t0.lo;
+        o[2] = t1.hi;
+        o[3] = t1.lo;
+    }
+}
+
+__global__ __launch_bounds__(64) void diff_norms_final_kernel(const double* __restrict__ part, int np,
+                                                              double* __restrict__ out) {
+    DD s0{0.0, 0.0}, s1{0.0, 0.0};
+    for (int k = threadIdx.x; k < np; k += 64) {
+        s0 = dd_merge(s0, DD{part[4 * k], part[4 * k + 1]});
+        s1 = dd_merge(s1, DD{part[4 * k + 2], part[4 * k + 3]});
+    }
+    s0 = dd_wave_sum(s0);
+    s1 = dd_wave_sum(s1);
+    if (threadIdx.x == 0) {
+        out[0] = dd_value(s0);
+        out[1] = dd_value(s1);
+    }
+}
+
+hipError_t launch_diff_norms(const float* a, const float* b, int64_t n, double* out, hipStream_t s) {
+    constexpr int kParts = kDiffNormParts;
+    const int64_t want = (n + 255) / 256;
+    const int np = (int)(want < kParts ? (want > 0 ? want : 1) : kParts);
+    hipLaunchKernelGGL(diff_norms_partial_kernel, dim3(np), dim3(256), 0, s, a, b, n, out + 2);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(diff_norms_final_kernel, dim3(1), dim3(64), 0, s, out + 2, np, out);
+    return hipGetLastError();
+}
+
 // Streaming ceiling of the fused AdamW access pattern: per element read p
 // (fp32), g (bf16), m and v (1 byte each), write p, m, v -- the same bytes,
 // lane mapping and launch shape as the AdamW kernel (one 1024-element chunk

@@ -309,3 +309,12 @@ def test_g1_grouping_reproduces_table4_adafactor_memory():
     assert not any(grouping.protected_flags(sh, "G0"))
     with pytest.raises(ValueError):
         grouping.protected_flags(sh, "G2")
+
+
+def test_diff_norms_validation():
+    L = al.lib()
+    assert _status(lambda: al.check(L.al_diff_norms(A, A, -1, A, None))) == 1
+    assert _status(lambda: al.check(L.al_diff_norms(A, A, 10, None, None))) == 1
+    assert _status(lambda: al.check(L.al_diff_norms(None, A, 10, A, None))) == 1
+    assert _status(lambda: al.check(L.al_diff_norms(A + 4, A, 10, A, None))) == 2
+    assert _status(lambda: al.check(L.al_diff_norms(A, A, 10, A + 8, None))) == 2
