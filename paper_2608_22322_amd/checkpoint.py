@@ -1,0 +1,105 @@
+"""Optimizer-state checkpoints and state-precision migration (section 7.1).
+
+A checkpoint keeps every state in its coded form -- codes, block metadata and the code
+type (codec, block size, log floor) -- so saving and loading is exact and training resumes
+bit for bit. Migration re-codes a state under another spec (for instance AL8 -> AL16) by
+decoding it with al_dequantize and encoding the values with al_quantize.
+
+File format: one safetensors file. Tensor "t{i}.{role}" holds the codes (or FP32 values),
+"t{i}.{role}.meta" the block metadata; the JSON header metadata holds, per tensor, its name,
+shape and per-role spec, plus the optimizer kind and step.
+"""
+from __future__ import annotations
+
+import json
+
+from . import AL8, AL16, FP32, UF8, Spec, alloc_state, dequantize, quantize
+
+ROLES = ("m", "v", "vr", "vc", "cr", "cc")
+_CODECS = {FP32: "FP32", AL8: "AL8", AL16: "AL16", UF8: "UF8"}
+_BY_NAME = {v: k for k, v in _CODECS.items()}
+
+
+def _role_len(st, role: str) -> int:
+    if role in ("m", "v"):
+        return st.rows * st.cols
+    return st.rows if role in ("vr", "cr") else st.cols
+
+
+def save(path: str, states, specs, names, kind: str, step: int) -> None:
+    """Write the coded states of a tensor list.
+
+    states: ParamState list; specs: per tensor, a dict role -> Spec for the roles it holds;
+    names: tensor names; kind: optimizer kind; step: the last completed step."""
+    from safetensors.torch import save_file
+
+    tensors, info = {}, []
+    for i, (st, sp, name) in enumerate(zip(states, specs, names)):
+        roles = {}
+        for role in ROLES:
+            buf = getattr(st, role)
+            if buf is None:
+                continue
+            s = sp[role]
+            tensors[f"t{i}.{role}"] = buf.detach().contiguous().cpu()
+            meta = getattr(st, role + "_meta")
+            if meta is not None:
+                tensors[f"t{i}.{role}.meta"] = meta.detach().contiguous().cpu()
+            roles[role] = {"codec": _CODECS[s.codec], "block": int(s.block), "log_floor": float(s.log_floor),
+                           "n": _role_len(st, role)}
+        info.append({"name": name, "rows": int(st.rows), "cols": int(st.cols), "roles": roles})
+    header = {"format": "al-optimizer-state/1", "kind": kind, "step": str(int(step)), "tensors": json.dumps(info)}
+    save_file(tensors, path, metadata=header)
+
+
+def load(path: str, states, device="cuda"):
+    """Load coded states into a ParamState list of the same tensors (shapes checked); returns
+    (kind, step, specs) with specs per tensor as dicts role -> Spec."""
+    from safetensors import safe_open
+
+    with safe_open(path, framework="pt") as f:
+        header = f.metadata()
+        if header.get("format") != "al-optimizer-state/1":
+            raise ValueError(f"{path}: not an optimizer-state checkpoint")
+        info = json.loads(header["tensors"])
+        if len(info) != len(states):
+            raise ValueError(f"{path}: {len(info)} tensors, expected {len(states)}")
+        specs = []
+        for i, (st, ti) in enumerate(zip(states, info)):
+            if (ti["rows"], ti["cols"]) != (st.rows, st.cols):
+                raise ValueError(f"{path}: tensor {i} ({ti['name']}) shape {ti['rows']}x{ti['cols']} "
+                                 f"!= {st.rows}x{st.cols}")
+            sp = {}
+            for role, r in ti["roles"].items():
+                setattr(st, role, f.get_tensor(f"t{i}.{role}").to(device))
+                key = f"t{i}.{role}.meta"
+                setattr(st, role + "_meta", f.get_tensor(key).to(device) if key in f.keys() else None)
+                sp[role] = Spec(_BY_NAME[r["codec"]], r["block"], r["log_floor"])
+            specs.append(sp)
+    return header["kind"], int(header["step"]), specs
+
+
+def migrate(st, role: str, old: Spec, new: Spec, stream=None) -> None:
+    """Re-code one state of a ParamState from spec old to spec new (e.g. AL8 -> AL16, AL16 -> AL8,
+    FP32 <-> AL). Values are decoded to fp32 and encoded again; FP32 states are taken as is."""
+    import torch
+
+    n = _role_len(st, role)
+    buf, meta = getattr(st, role), getattr(st, role + "_meta")
+    device = buf.device
+    if old.codec == FP32:
+        x = buf
+    else:
+        x = torch.empty(max(n, 4), dtype=torch.float32, device=device)
+        dequantize(old.codec, buf, meta, n, old.block, x, stream=stream)
+    if new.codec == FP32:
+        setattr(st, role, x if old.codec != FP32 else buf)
+        setattr(st, role + "_meta", None)
+        return
+    codes, nmeta = alloc_state(n, new, device)
+    quantize(new.codec, x[:n], new.block, new.log_floor, codes, nmeta, stream=stream)
+    setattr(st, role, codes)
+    setattr(st, role + "_meta", nmeta)
+
+
+__all__ = ["save", "load", "migrate"]
