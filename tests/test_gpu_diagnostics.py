@@ -135,3 +135,94 @@ def test_factored_update_error_ordering(dev):
         errs[codec] = update_error("adafactor", [st], cfg, t=5)
     log(f"Adafactor E_upd: AL8 {errs[al.AL8]:.3e} AL16 {errs[al.AL16]:.3e}")
     assert 0 < errs[al.AL16] < errs[al.AL8] / 50
+
+
+# ---------------------------------------------------------------- controlled probes (section 5)
+from . import probe_util as pu  # noqa: E402
+
+
+def _dev_vec(x, dev):
+    import torch
+
+    return torch.from_numpy(np.concatenate([x, np.zeros(8, np.float32)])).to(dev)
+
+
+@pytest.mark.parametrize("case", ["narrow", "medium", "wide", "sparse"])
+def test_probe_state_and_operator_error_match_oracle(dev, case):
+    """state_error and the inverse-square-root E_upd from the library against the oracle on the
+    same block (2048 elements, AL8 and AL16, B 2048)."""
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd.diagnostics import state_error, update_error
+
+    seed = 8 if case == "sparse" else 7
+    v = pu.sparse_state(seed) if case == "sparse" else pu.regime_state(case, seed)
+    g = pu.operator_grad(v, seed)
+    n = v.shape[0]
+    vd = _dev_vec(v, dev)
+    for bits, codec in ((8, al.AL8), (16, al.AL16)):
+        spec = al.Spec(codec, 2048, pu.PROBE_FLOOR)
+        s_gpu = state_error(vd[:n], spec)
+        s_orc = pu.oracle_state_error(v, bits, 2048)
+        st = al.ParamState(None, _dev_vec(g, dev), 1, n, m=_dev_vec(np.zeros(n, np.float32), dev), v=vd)
+        cfg = al.adamw_cfg(lr=1.0, beta1=0.0, weight_decay=0.0, grad_bf16=False, m=al.Spec(al.FP32), v=spec)
+        e_gpu = update_error("adamw", [st], cfg, t=pu.OPERATOR_T)
+        e_orc = pu.oracle_operator_error(v, g, bits, 2048)
+        log(f"{case} AL{bits}: state {s_gpu:.6e} (oracle {s_orc:.6e}) operator {e_gpu:.6e} (oracle {e_orc:.6e})")
+        assert abs(s_gpu - s_orc) <= 1e-9 * s_orc  # same codes, same decoded values
+        # the parameter update is fp32 on the GPU: E_upd agrees to the update's own rounding
+        tol = 5e-3 if bits == 8 else 0.1
+        assert abs(e_gpu - e_orc) <= tol * e_orc
+        if bits == 8:
+            assert e_gpu < 0.01
+
+
+@pytest.mark.parametrize("block", [256, 2048])
+def test_ema_drift_5k_steps_matches_oracle(dev, block):
+    """Temporal probe: 5000 AdamW steps (FP32 m, AL8 v, beta2 0.999) over i.i.d. gradients drawn
+    by the device generator; drift and E_upd of step 5000 against the oracle's trajectories."""
+    import torch
+
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import synth
+    from paper_2608_22322_amd.diagnostics import ema_drift
+
+    n, steps, seed, sigma = 4096, 5000, 5, 1e-3
+    floor = float(np.float32(2 * math.log2(1e-8)))
+    grad = torch.zeros(n + 8, dtype=torch.float32, device=dev)
+    fill = lambda t: al.synth_normal(grad[:n], synth.grad_key(seed, t), sigma)
+    cfg = al.adamw_cfg(lr=1e-3, weight_decay=0.0, grad_bf16=False, m=al.Spec(al.FP32),
+                       v=al.Spec(al.AL8, block, floor))
+    res = ema_drift("adamw", [(1, n)], cfg, steps, fill, [grad])
+    d_orc, u_orc = pu.oracle_adamw_drift(n, steps, block, seed=seed, sigma=sigma)
+    log(f"B {block}: drift {res['drift']['v']:.6e} (oracle {d_orc:.6e}) "
+        f"E_upd {res['update_error']:.6e} (oracle {u_orc:.6e})")
+    assert set(res["drift"]) == {"v"}
+    assert abs(res["drift"]["v"] - d_orc) <= 2e-3 * d_orc
+    assert abs(res["update_error"] - u_orc) <= 1e-2 * u_orc
+    cfg32 = al.adamw_cfg(lr=1e-3, weight_decay=0.0, grad_bf16=False, m=al.Spec(al.FP32), v=al.Spec(al.FP32))
+    res32 = ema_drift("adamw", [(1, n)], cfg32, 50, fill, [grad])
+    assert res32["drift"] == {} and res32["update_error"] == 0.0
+
+
+def test_ema_drift_factored_matches_oracle(dev):
+    """Temporal probe on factored states (Adafactor, 48 x 160, 200 steps, AL8 and AL16 B 128)."""
+    import torch
+
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import synth
+    from paper_2608_22322_amd.diagnostics import ema_drift
+
+    rows, cols, steps, seed, sigma = 48, 160, 200, 6, 1e-3
+    n = rows * cols
+    grad = torch.zeros(n + 8, dtype=torch.float32, device=dev)
+    fill = lambda t: al.synth_normal(grad[:n], synth.grad_key(seed, t), sigma)
+    floor = float(np.float32(math.log2(1e-30)))
+    for bits, codec in ((8, al.AL8), (16, al.AL16)):
+        cfg = al.adafactor_cfg(lr=1e-3, grad_bf16=False, v=al.Spec(codec, 128, floor))
+        res = ema_drift("adafactor", [(rows, cols)], cfg, steps, fill, [grad])
+        d_orc, u_orc = pu.oracle_adafactor_drift(rows, cols, steps, bits, 128, seed=seed, sigma=sigma)
+        log(f"Adafactor AL{bits}: drift {res['drift']} (oracle {d_orc}) E_upd {res['update_error']:.6e} "
+            f"(oracle {u_orc:.6e})")
+        for r in ("vr", "vc"):
+            assert abs(res["drift"][r] - d_orc[r]) <= 1e-6 * d_orc[r]
+        assert abs(res["update_error"] - u_orc) <= (2e-2 if bits == 8 else 0.2) * u_orc
