@@ -7,20 +7,22 @@
 // corrections; codes per section 4 (Eq. al_bounds, al_quant, al_dequant,
 // exact_zero) and the uniform signed momentum code of section 4.3.
 //
-// Work decomposition. A chunk is max(1024, B_V) consecutive elements of one
-// tensor, owned by one wavefront: 4 consecutive elements per lane in each of
-// K = chunk/256 sub-tiles, so every load and store is a coalesced 16/8/4-byte
-// access and every block reduction stays inside the wavefront (DPP, swizzle,
-// readlane). The momentum block (256) is one sub-tile and is encoded as soon
-// as that sub-tile's moments are computed; the second moment is held in
-// registers until its block is complete. Per-block scalar work of the second
+// Work decomposition. A chunk is max(2048, B_V) consecutive elements of one
+// tensor for AL8 blocks of 256+, else max(1024, B_V), owned by one wavefront:
+// 4 consecutive elements per lane in each of K = chunk/256 sub-tiles, so every
+// load and store is a coalesced 16/8/4-byte access and every block reduction
+// stays inside the wavefront (DPP, swizzle, readlane). The momentum block
+// (256) is one sub-tile and is encoded as soon as that sub-tile's moments are
+// computed; the second moment is held in registers until its block is
+// complete, and a block of whole sub-tiles has its min/max keys reduced as
+// soon as its last sub-tile is done. Per-block scalar work of the second
 // moment (the binary64 divisions and endpoint logarithms of up to 16 blocks)
-// runs once per chunk with one block per lane, and the results are broadcast
-// back (readlane for blocks that span whole sub-tiles, ds_bpermute for
-// smaller ones). The grid holds one wave per chunk, and the chunk -> tensor
-// map is a binary search over the descriptor table held in the kernel
-// arguments. Full chunks use non-temporal loads and stores: every byte of
-// the step is touched exactly once.
+// runs once per chunk with one block per lane pair, and the results are
+// broadcast back (readlane for blocks that span whole sub-tiles, ds_bpermute
+// for smaller ones). The grid holds one wave per chunk, and the chunk ->
+// tensor map is a binary search over the descriptor table held in the kernel
+// arguments. Full chunks use non-temporal loads and stores: every byte of the
+// step is touched exactly once.
 #include "al_device.hpp"
 #include "al_internal.hpp"
 
@@ -38,10 +40,17 @@ namespace al {
 constexpr bool kNtLoad = AL_ADAMW_NT_LOAD != 0;
 constexpr bool kNtStore = AL_ADAMW_NT_STORE != 0;
 
+__host__ __device__ constexpr int chunk_elems(int vc, int bv) {
+    return vc == FP32 ? 1024 : (vc == AL8 && bv >= kSub) ? (bv > 2048 ? bv : 2048) : (bv > 1024 ? bv : 1024);
+}
+
 template <int MC, int VC, int BV>
 struct Geo {
     static constexpr bool VQ = (VC == AL8 || VC == AL16);
-    static constexpr int C = (VQ && BV > 1024) ? BV : 1024;  // elements per chunk
+    // elements per chunk: AL8 blocks of 256+ take 2048 (the per-chunk work amortised over twice
+    // the elements); smaller AL8 blocks (their per-sub-tile min/max slots), AL16 (wider codes)
+    // and an fp32 second moment would not fit in 128 registers at 2048 and take max(1024, B_V)
+    static constexpr int C = chunk_elems(VC, BV);
     static constexpr int K = C / kSub;                       // sub-tiles per chunk
     static constexpr int NB = VQ ? C / BV : 1;               // v blocks per chunk
     static constexpr int GL = BV < kSub ? BV / 4 : 64;       // lanes per v block within a sub-tile
@@ -222,6 +231,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
     // the new second moment waits in registers for its block's interval
     float vk[K][4];
     uint32_t vmn[Q::NSLOT], vmx[Q::NSLOT];
+    uint32_t pmn = 0xFFFFFFFFu, pmx = 0u;
 #pragma unroll
     for (int s = 0; s < Q::NSLOT; ++s) {
         vmn[s] = 0xFFFFFFFFu;
@@ -316,14 +326,31 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 if (rel + j < valid) reinterpret_cast<float*>(d.m)[e + j] = mn[j];
         }
         if constexpr (VQ) {
-            const int s = BV < kSub ? k : k * kSub / BV;
+            // vn >= 0 here, so its bit pattern orders it; bits - 1 sends +0 to
+            // the largest key, out of the positive minimum
+            if constexpr (BV >= kSub) {
+                // a block of whole sub-tiles: one running key pair, reduced over
+                // the wavefront (to wave-uniform values) as soon as the block ends
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                // vn >= 0 here, so its bit pattern orders it; bits - 1 sends
-                // +0 to the largest key, out of the positive minimum
-                vk[k][j] = vn[j];
-                vmn[s] = OpMin::f(vmn[s], f2u(vn[j]) - 1u);
-                vmx[s] = OpMax::f(vmx[s], f2u(vn[j]));
+                for (int j = 0; j < 4; ++j) {
+                    vk[k][j] = vn[j];
+                    pmn = OpMin::f(pmn, f2u(vn[j]) - 1u);
+                    pmx = OpMax::f(pmx, f2u(vn[j]));
+                }
+                if ((k + 1) * kSub % BV == 0) {
+                    const int s = k * kSub / BV;
+                    vmn[s] = group_reduce<OpMin, 64>(pmn) + 1u;  // back to bits; 0 when no positive
+                    vmx[s] = group_reduce<OpMax, 64>(pmx);
+                    pmn = 0xFFFFFFFFu;
+                    pmx = 0u;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    vk[k][j] = vn[j];
+                    vmn[k] = OpMin::f(vmn[k], f2u(vn[j]) - 1u);
+                    vmx[k] = OpMax::f(vmx[k], f2u(vn[j]));
+                }
             }
         } else if constexpr (FULL) {
             st_f4<kNtStore>(reinterpret_cast<float*>(d.v) + e, make_float4(vn[0], vn[1], vn[2], vn[3]));
@@ -334,11 +361,14 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         }
     }
     if constexpr (VQ) {
-        // -------------------------------------------- 3. second-moment block reductions
+        // -------------------------------------------- 3. second-moment block reductions (blocks
+        // smaller than a sub-tile: GL-lane groups of every sub-tile)
+        if constexpr (BV < kSub) {
 #pragma unroll
-        for (int s = 0; s < Q::NSLOT; ++s) {
-            vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]) + 1u;  // back to bits; 0 when no positive
-            vmx[s] = group_reduce<OpMax, Q::GL>(vmx[s]);
+            for (int s = 0; s < Q::NSLOT; ++s) {
+                vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]) + 1u;
+                vmx[s] = group_reduce<OpMax, Q::GL>(vmx[s]);
+            }
         }
 
         // -------------------------------------------- 4. block fits, one block per lane pair
@@ -409,7 +439,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 // with 2048-element AL16 chunks.
 template <int MC, int VC, int BV>
 constexpr int adamw_waves_per_eu() {
-    return MC == UF8 ? 4 : (VC == AL16 && BV >= 2048 ? 2 : 3);
+    return MC == UF8 ? 4 : (VC == AL16 && Geo<MC, VC, BV>::C >= 2048 ? 2 : 3);
 }
 
 // largest ti with t[ti].tile_begin <= chunk
@@ -447,10 +477,7 @@ void adamw_kernel(const AdamWLaunch a) {
         adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut);
 }
 
-int adamw_tile_elems(int v_codec, int v_block) {
-    if (v_codec == FP32) return Geo<UF8, FP32, 256>::C;
-    return v_block > 1024 ? v_block : 1024;
-}
+int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
 
 // One wave per chunk: the grid covers every chunk of the launch and the
 // hardware dispatcher refills each CU as its waves retire. (A persistent grid
