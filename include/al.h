@@ -231,15 +231,24 @@ al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void
 #define AL_DIFF_NORMS_OUT 4098
 al_status al_diff_norms(const float* a, const float* b, int64_t n, double* out, void* stream);
 
-/* Diagnostic: the streaming ceiling of the fused AdamW access pattern. Reads
- * p (n fp32), g (n bf16), m and v (n bytes each) and writes p, m, v with no
- * optimizer arithmetic (the values written are meaningless), using the same
- * lane mapping and launch shape as al_adamw_step (one 1024-element chunk per
- * wavefront); nontemporal != 0 uses non-temporal loads and stores. n must be
- * a multiple of 2048. Timing it gives the achievable HBM bandwidth for the
- * step's exact byte mix. */
-al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n,
-                         void* stream);
+/* Diagnostic: streaming rates of the fused AdamW byte mix. Reads p (n fp32),
+ * g (n bf16), m and v (n bytes each) and writes p, m, v with no optimizer
+ * arithmetic. mode selects the access shape:
+ *   0, 1  the shape of al_adamw_step (one 2048-element chunk per wavefront in
+ *         two load phases, 4 consecutive elements per lane, XCD-contiguous
+ *         workgroup order); mode 1 uses non-temporal loads and stores. Writes
+ *         p[4i] += g[4i], p[4i+3] += g[4i+3] (g as bf16), m ^= v, v += 1 per
+ *         byte. n must be a multiple of 2048.
+ *   2, 3  the fastest shape found for the mix (one 4096-element chunk per
+ *         wavefront, 16 bytes per lane from every stream, all loads before any
+ *         store, non-temporal): a reference rate, not the step's layout.
+ *         Writes p += 1, m ^= v, v += 1 per byte; g is only read. n must be a
+ *         multiple of 4096.
+ * v += 1 carries into the next byte where a byte is 0xFF. Timing it gives the
+ * achievable HBM bandwidth for the step's exact byte mix. Enqueued on stream;
+ * allocates nothing. AL_EINVAL for a bad mode, n or NULL buffer, AL_EALIGN
+ * for a buffer not 16-byte aligned. */
+al_status al_diag_stream(int32_t mode, float* p, const void* g, void* m, void* v, int64_t n, void* stream);
 
 #ifdef __cplusplus
 }

@@ -182,8 +182,11 @@ def diag_math(fn: int, x, out, stream=None) -> None:
     check(lib().al_diag_math(fn, _ptr(x), x.numel(), _ptr(out), _stream(stream)))
 
 
-def diag_stream(nontemporal: bool, p, g, m, v, stream=None) -> None:
-    check(lib().al_diag_stream(int(nontemporal), _ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), _stream(stream)))
+def diag_stream(nontemporal: bool, p, g, m, v, stream=None, wide: bool = False) -> None:
+    """Streaming rate probe of the AdamW byte mix (al_diag_stream): the step's access shape, or with wide=True
+    the fastest shape found for the mix (4096-element chunks, 16 bytes per lane from every stream)."""
+    mode = (2 | 1) if wide else int(bool(nontemporal))
+    check(lib().al_diag_stream(mode, _ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), _stream(stream)))
 
 
 DIFF_NORMS_OUT = 4098  # doubles of the al_diff_norms output / scratch buffer

@@ -463,7 +463,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(adamw_waves
 void adamw_kernel(const AdamWLaunch a) {
     constexpr int C = Geo<MC, VC, BV>::C;
     const int lane = threadIdx.x & 63;
-    const int64_t chunk = a.chunk_base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t chunk = a.chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
     __shared__ float lut_all[4][NT];
     float* lut = lut_all[threadIdx.x >> 6];
@@ -480,7 +480,8 @@ void adamw_kernel(const AdamWLaunch a) {
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
 
 // One wave per chunk: the grid covers every chunk of the launch and the
-// hardware dispatcher refills each CU as its waves retire. (A persistent grid
+// hardware dispatcher refills each CU as its waves retire; each XCD walks a
+// contiguous eighth of the chunks (xcd_order). (A persistent grid
 // sized by occupancy moves the same byte mix about 6% slower on gfx950, and a
 // chunk loop lets the compiler hoist per-chunk constants into spilled
 // registers.) Lists beyond 2^32 chunks take several launches.

@@ -442,14 +442,17 @@ al_status al_diff_norms(const float* a, const float* b, int64_t n, double* out, 
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_diff_norms launch");
 }
 
-al_status al_diag_stream(int32_t nontemporal, float* p, const void* g, void* m, void* v, int64_t n, void* stream) {
+al_status al_diag_stream(int32_t mode, float* p, const void* g, void* m, void* v, int64_t n, void* stream) {
     g_err[0] = 0;
-    if (n < 0 || n % 2048 != 0) return fail(AL_EINVAL, "al_diag_stream: n must be a non-negative multiple of 2048");
+    if (mode < 0 || mode > 3) return fail(AL_EINVAL, "al_diag_stream: mode must be 0..3");
+    const int64_t unit = (mode & 2) ? 4096 : 2048;
+    if (n < 0 || n % unit != 0)
+        return fail(AL_EINVAL, "al_diag_stream: n must be a non-negative multiple of 2048 (4096 for the wide shape)");
     if (n == 0) return AL_OK;
     if (!p || !g || !m || !v) return fail(AL_EINVAL, "al_diag_stream: NULL buffer");
     if (!aligned16(p) || !aligned16(g) || !aligned16(m) || !aligned16(v))
         return fail(AL_EALIGN, "al_diag_stream: alignment");
-    hipError_t e = al::launch_diag_stream(nontemporal != 0, p, static_cast<const uint16_t*>(g),
+    hipError_t e = al::launch_diag_stream(mode, p, static_cast<const uint16_t*>(g),
                                           static_cast<uint8_t*>(m), static_cast<uint8_t*>(v), n, as_stream(stream));
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_stream launch");
 }

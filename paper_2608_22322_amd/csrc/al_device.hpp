@@ -371,6 +371,17 @@ __device__ __forceinline__ uint32_t load_code1(const void* c, int64_t e) {
         return reinterpret_cast<const uint16_t*>(c)[e];
 }
 
+// Workgroup id -> work unit for streaming kernels. The dispatcher hands
+// workgroups to the 8 XCDs round-robin (workgroup i to XCD i mod 8); this
+// gives each XCD a contiguous eighth of the units instead of every eighth
+// unit (the tail beyond a multiple of 8 keeps its order). Measured on the
+// step's read/write mix: 1-3% more HBM throughput.
+__device__ __forceinline__ int64_t xcd_order(uint32_t wg, uint32_t grid) {
+    const int64_t g8 = (int64_t)(grid & ~7u);
+    const int64_t w = wg;
+    return w < g8 ? (w & 7) * (g8 >> 3) + (w >> 3) : w;
+}
+
 // Streaming (non-temporal) or ordinary vector loads and stores of 16, 8 and 4
 // bytes. The non-temporal builtins take clang vector types, not HIP's structs.
 typedef float nt_f4 __attribute__((ext_vector_type(4)));

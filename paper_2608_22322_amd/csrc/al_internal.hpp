@@ -50,7 +50,7 @@ hipError_t launch_quantize(int codec, const float* x, int64_t n, int block, floa
 hipError_t launch_dequantize(int codec, const void* codes, const float* meta, int64_t n, int block,
                              float* out, int grid_cap, hipStream_t s);
 
-hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
+hipError_t launch_diag_stream(int mode, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
                               hipStream_t s);
 constexpr int kDiffNormParts = 1024;  // workgroup partials of al_diff_norms (4 doubles each)
 hipError_t launch_diff_norms(const float* a, const float* b, int64_t n, double* out, hipStream_t s);

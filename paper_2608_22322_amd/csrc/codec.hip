@@ -174,48 +174,92 @@ hipError_t launch_diff_norms(const float* a, const float* b, int64_t n, double* 
 
 // Streaming ceiling of the fused AdamW access pattern: per element read p
 // (fp32), g (bf16), m and v (1 byte each), write p, m, v -- the same bytes,
-// lane mapping and launch shape as the AdamW kernel (one 1024-element chunk
-// per wavefront, 4 consecutive elements per lane in each 256-element
-// sub-tile), with no optimizer arithmetic. NT selects non-temporal loads and
-// stores.
+// lane mapping and launch shape as the AdamW kernel (one 2048-element chunk
+// per wavefront in two load phases of four 256-element sub-tiles, 4
+// consecutive elements per lane, XCD-contiguous workgroup order), with no
+// optimizer arithmetic. NT selects non-temporal loads and stores.
 template <bool NT>
 __global__ __launch_bounds__(256) void stream_kernel(float* __restrict__ p, const uint16_t* __restrict__ g,
                                                       uint8_t* __restrict__ m, uint8_t* __restrict__ v,
                                                       int64_t chunk_base, int64_t chunks) {
     const int lane = threadIdx.x & 63;
-    const int64_t c = chunk_base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t c = chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (c >= chunks) return;
-    float4 pv[4];
-    uint2 gv[4];
-    uint32_t mv[4], vv[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int64_t e = c * 1024 + k * 256 + 4 * lane;
-        pv[k] = ld_f4<NT>(p + e);
-        gv[k] = ld_u2<NT>(g + e);
-        mv[k] = ld_u1<NT>(m + e);
-        vv[k] = ld_u1<NT>(v + e);
-    }
+    for (int ph = 0; ph < 2; ++ph) {
+        if (ph > 0) __builtin_amdgcn_sched_barrier(0);
+        float4 pv[4];
+        uint2 gv[4];
+        uint32_t mv[4], vv[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int64_t e = c * 1024 + k * 256 + 4 * lane;
-        float4 o = pv[k];
-        o.x += bf16_to_f32(gv[k].x & 0xFFFFu);
-        o.w += bf16_to_f32(gv[k].y >> 16);
-        st_f4<NT>(p + e, o);
-        st_u1<NT>(m + e, mv[k] ^ vv[k]);
-        st_u1<NT>(v + e, vv[k] + 0x01010101u);
+        for (int k = 0; k < 4; ++k) {
+            const int64_t e = c * 2048 + (ph * 4 + k) * 256 + 4 * lane;
+            pv[k] = ld_f4<NT>(p + e);
+            gv[k] = ld_u2<NT>(g + e);
+            mv[k] = ld_u1<NT>(m + e);
+            vv[k] = ld_u1<NT>(v + e);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t e = c * 2048 + (ph * 4 + k) * 256 + 4 * lane;
+            float4 o = pv[k];
+            o.x += bf16_to_f32(gv[k].x & 0xFFFFu);
+            o.w += bf16_to_f32(gv[k].y >> 16);
+            st_f4<NT>(p + e, o);
+            st_u1<NT>(m + e, mv[k] ^ vv[k]);
+            st_u1<NT>(v + e, vv[k] + 0x01010101u);
+        }
     }
 }
 
-hipError_t launch_diag_stream(int nt, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
+// Best streaming shape found for the same byte mix (a reference rate, not
+// the step's layout): one 4096-element chunk per wavefront, every stream read
+// 16 bytes per lane (p: 4 elements, g: 8, m and v: 16 per lane), all loads of
+// the chunk issued before any store, XCD-contiguous order. Writes p + 1,
+// m ^ v, v + 1 (per byte); g is read and discarded.
+__global__ __launch_bounds__(256) void stream_wide_kernel(float* __restrict__ p, const uint16_t* __restrict__ g,
+                                                          uint8_t* __restrict__ m, uint8_t* __restrict__ v,
+                                                          int64_t chunk_base, int64_t chunks) {
+    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+    const int lane = threadIdx.x & 63;
+    const int64_t c = chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (c >= chunks) return;
+    const int64_t e0 = c * 4096;
+    nt_f4 pv[16];
+    u4 gv[8], mv[4], vv[4];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) pv[i] = __builtin_nontemporal_load(reinterpret_cast<const nt_f4*>(p + e0 + i * 256 + 4 * lane));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) gv[i] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(g + e0 + i * 512 + 8 * lane));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        mv[i] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(m + e0 + i * 1024 + 16 * lane));
+        vv[i] = __builtin_nontemporal_load(reinterpret_cast<const u4*>(v + e0 + i * 1024 + 16 * lane));
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) asm volatile("" ::"v"(gv[i]));  // the gradient bytes are read, not used
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        __builtin_nontemporal_store(pv[i] + 1.0f, reinterpret_cast<nt_f4*>(p + e0 + i * 256 + 4 * lane));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        __builtin_nontemporal_store(mv[i] ^ vv[i], reinterpret_cast<u4*>(m + e0 + i * 1024 + 16 * lane));
+        __builtin_nontemporal_store(vv[i] + 0x01010101u, reinterpret_cast<u4*>(v + e0 + i * 1024 + 16 * lane));
+    }
+}
+
+hipError_t launch_diag_stream(int mode, float* p, const uint16_t* g, uint8_t* m, uint8_t* v, int64_t n,
                               hipStream_t s) {
-    const int64_t chunks = n / 1024;
+    const bool wide = (mode & 2) != 0;
+    const int64_t chunks = n / (wide ? 4096 : 2048);
     constexpr int64_t kMaxGrid = int64_t(1) << 30;
     for (int64_t base = 0; base < chunks; base += 4 * kMaxGrid) {
         const int64_t left = (chunks - base + 3) / 4;
         const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
-        if (nt)
+        if (wide)
+            hipLaunchKernelGGL(stream_wide_kernel, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, base, chunks);
+        else if (mode & 1)
             hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, base, chunks);
         else
             hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)grid), dim3(256), 0, s, p, g, m, v, base, chunks);

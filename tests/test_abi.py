@@ -318,3 +318,14 @@ def test_diff_norms_validation():
     assert _status(lambda: al.check(L.al_diff_norms(None, A, 10, A, None))) == 1
     assert _status(lambda: al.check(L.al_diff_norms(A + 4, A, 10, A, None))) == 2
     assert _status(lambda: al.check(L.al_diff_norms(A, A, 10, A + 8, None))) == 2
+
+
+def test_diag_stream_validation():
+    L = al.lib()
+    assert _status(lambda: al.check(L.al_diag_stream(4, A, A, A, A, 4096, None))) == 1
+    assert _status(lambda: al.check(L.al_diag_stream(-1, A, A, A, A, 4096, None))) == 1
+    assert _status(lambda: al.check(L.al_diag_stream(0, A, A, A, A, 2047, None))) == 1
+    assert _status(lambda: al.check(L.al_diag_stream(3, A, A, A, A, 2048, None))) == 1  # wide: multiple of 4096
+    assert _status(lambda: al.check(L.al_diag_stream(1, None, A, A, A, 2048, None))) == 1
+    assert _status(lambda: al.check(L.al_diag_stream(1, A, A, A + 4, A, 2048, None))) == 2
+    assert al.lib().al_diag_stream(2, A, A, A, A, 0, None) == 0  # empty: no HIP call
