@@ -44,6 +44,7 @@ TAG_PARAM = 1
 TAG_GRAD = 2
 TAG_MASK = 3
 TAG_STATE = 4
+TAG_PROJ = 5
 
 
 def mix64_int(z: int) -> int:
@@ -147,3 +148,13 @@ def mask_key(tensor: int, seed: int = BASE_SEED) -> int:
 
 def state_key(tensor: int, which: int, seed: int = BASE_SEED) -> int:
     return stream_key(seed, TAG_STATE, tensor, which)
+
+
+def proj_key(tensor: int, epoch: int, seed: int = BASE_SEED) -> int:
+    """Stream of the APOLLO projection matrix of a tensor for one refresh period (epoch = (t - 1) // gap)."""
+    return stream_key(seed, TAG_PROJ, tensor, epoch)
+
+
+def proj_matrix(tensor: int, epoch: int, L: int, rank: int, seed: int = BASE_SEED) -> np.ndarray:
+    """L x rank projection with entries N(0, 1/rank) (float32, row-major)."""
+    return normal_f32(proj_key(tensor, epoch, seed), L * rank, 1.0 / math.sqrt(rank)).reshape(L, rank)
