@@ -162,6 +162,48 @@ typedef struct al_came_cfg {
     al_state_spec m, v, conf;
 } al_came_cfg;
 
+/* APOLLO, the projected-state path (section 3.1: first and second moments
+ * kept in a low-rank projection of the gradient derive a channel-wise scale
+ * of the original gradient; section 6 setup: rank 256, channel-wise scaling,
+ * projection refreshed every 200 steps; Table 4: UF8 momentum, AL8 second
+ * moment). A rows x cols tensor has C = max(rows, cols) channels of
+ * L = min(rows, cols) inputs: rows >= cols projects the columns (channel c is
+ * row c), otherwise the rows (channel c is column c). Per step:
+ *   R   = fl32(A Pi) in binary64, A = G (rows >= cols) or G^T as C x L,
+ *         Pi = proj (L x rank, row-major fp32; the caller draws it, N(0, 1/rank),
+ *         and refreshes it every gap steps);
+ *   m, v: the AdamW moments of R (rank * C elements, channel-major: element
+ *         c * rank + k), with AdamW's codes, bias corrections and eps; the
+ *         direction Rt = (m / bc1) / (sqrt(v / bc2) + eps) is fp32;
+ *   s_c = ||Rt_c|| / (||R_c|| + 1e-8), G~ = G with channel c scaled by s_c;
+ *   limiter (gamma > 0): from step 2, lam = max(||G~|| / (*norm_state + 1e-8),
+ *         gamma) / gamma and *norm_state = fl32(||G~|| / lam); at step 1
+ *         lam = 1 and *norm_state = fl32(||G~||);
+ *   param = fl32(param (1 - lr wd) - lr g (s_c / lam)), binary64.
+ * The token embedding, LM head and 1-D tensors are not projected: they take
+ * al_adamw_step with the same codes. */
+typedef struct al_apollo_tensor {
+    float* param;
+    const void* grad;
+    int64_t rows;
+    int64_t cols;
+    const float* proj; /* L x rank fp32 */
+    void* m;           /* projected momentum, rank * C elements */
+    float* m_meta;
+    void* v;           /* projected second moment, rank * C elements */
+    float* v_meta;
+    float* norm_state; /* 1 float: the limiter's last update norm (unused when gamma <= 0) */
+} al_apollo_tensor;
+
+/* rank: 64, 128 or 256. gamma: the limiter's growth bound (<= 0: no limiter).
+ * m: UF8 (block 256) or FP32; v: AL8, AL16 or FP32. */
+typedef struct al_apollo_cfg {
+    double lr, beta1, beta2, eps, weight_decay, gamma;
+    int32_t rank;
+    int32_t grad_dtype;
+    al_state_spec m, v;
+} al_apollo_cfg;
+
 /* Library version string, e.g. "0.1.0 gfx950". */
 const char* al_version(void);
 
@@ -211,6 +253,21 @@ al_status al_adafactor_step(const al_tensor* tensors, int32_t nt, const al_adafa
  * (rows > 1) vr, vc, cr, cc with metadata or (rows == 1) v, v_meta. */
 al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* cfg,
                        int64_t step, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace size (bytes) that al_apollo_step needs for this list and config:
+ * per tensor R and Rt (rank * C floats each) and per-channel binary64 sums. */
+al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,
+                                    size_t* bytes);
+
+/* One APOLLO step over nt projected tensors (rows, cols >= 1). Kernels, in
+ * stream order: the binary64 projection on the matrix cores (also sums of
+ * squares per channel of G), the fused AdamW step over the projected moments
+ * (fp32 R as its gradient, Rt in the workspace as its parameter, lr 1, no
+ * weight decay), the channel scales, the limiter per tensor, and the
+ * parameter update. ws: device workspace of at least the queried size,
+ * 256-byte aligned. */
+al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg, int64_t step,
+                         void* ws, size_t ws_bytes, void* stream);
 
 /* Diagnostic: evaluate, elementwise on the device, a math primitive the
  * codes rely on, so tests can bound it against the host: fn 0 = hardware

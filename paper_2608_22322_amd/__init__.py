@@ -62,13 +62,26 @@ class CAMECfg(ctypes.Structure):
                 ("m", StateSpec), ("v", StateSpec), ("conf", StateSpec)]
 
 
+class ApolloTensor(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("rows", ctypes.c_int64),
+                ("cols", ctypes.c_int64), ("proj", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("m_meta", ctypes.c_void_p), ("v", ctypes.c_void_p), ("v_meta", ctypes.c_void_p),
+                ("norm_state", ctypes.c_void_p)]
+
+
+class ApolloCfg(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double), ("gamma", ctypes.c_double),
+                ("rank", ctypes.c_int32), ("grad_dtype", ctypes.c_int32), ("m", StateSpec), ("v", StateSpec)]
+
+
 _lib = None
 
 # every symbol include/al.h and include/al_synth.h declare
 EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al_state_bytes", "al_quantize",
            "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
-           "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream", "al_diff_norms",
-           "al_synth_normal")
+           "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes", "al_apollo_step", "al_diag_math",
+           "al_diag_stream", "al_diff_norms", "al_synth_normal")
 
 
 def lib():
@@ -95,12 +108,16 @@ def lib():
                                               ctypes.POINTER(sz)]
         L.al_adafactor_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdafactorCfg), i64, vp, sz, vp]
         L.al_came_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(CAMECfg), i64, vp, sz, vp]
+        L.al_apollo_workspace_bytes.argtypes = [ctypes.POINTER(ApolloTensor), i32, ctypes.POINTER(ApolloCfg),
+                                                ctypes.POINTER(sz)]
+        L.al_apollo_step.argtypes = [ctypes.POINTER(ApolloTensor), i32, ctypes.POINTER(ApolloCfg), i64, vp, sz, vp]
         L.al_synth_normal.argtypes = [vp, i32, i64, u64, f, u64, u64, vp]
         L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
         L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
         L.al_diff_norms.argtypes = [vp, vp, i64, vp, vp]
         for name in ("al_quantize", "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes",
-                     "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_diag_math", "al_diag_stream",
+                     "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes",
+                     "al_apollo_step", "al_diag_math", "al_diag_stream",
                      "al_diff_norms", "al_synth_normal"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -299,3 +316,31 @@ def came_step(states, cfg: CAMECfg, step: int, ws, stream=None, arr=None) -> Non
     arr = arr if arr is not None else tensor_array(states)
     check(lib().al_came_step(arr, len(states), ctypes.byref(cfg), step, _ptr(ws),
                              0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+
+
+# ------------------------------------------------------------------ APOLLO (projected states)
+def apollo_cfg(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, gamma=1.01, rank=256, grad_bf16=True,
+               m: Spec = None, v: Spec = None) -> ApolloCfg:
+    m = m or Spec(UF8, 256)
+    v = v or Spec(AL8, 2048, log2_floor_of(eps * eps))
+    return ApolloCfg(lr, beta1, beta2, eps, weight_decay, gamma, rank, 1 if grad_bf16 else 0, m.c(), v.c())
+
+
+def apollo_tensor_array(items) -> ctypes.Array:
+    """items: (param, grad, rows, cols, proj, m, m_meta, v, v_meta, norm_state) tuples of device tensors."""
+    arr = (ApolloTensor * max(len(items), 1))()
+    for i, (p, g, rows, cols, proj, m, mm, v, vm, ns) in enumerate(items):
+        arr[i] = ApolloTensor(_ptr(p), _ptr(g), rows, cols, _ptr(proj), _ptr(m), _ptr(mm), _ptr(v), _ptr(vm),
+                              _ptr(ns))
+    return arr
+
+
+def apollo_workspace_bytes(arr, nt: int, cfg: ApolloCfg) -> int:
+    out = ctypes.c_size_t(0)
+    check(lib().al_apollo_workspace_bytes(arr, nt, ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def apollo_step(arr, nt: int, cfg: ApolloCfg, step: int, ws, stream=None) -> None:
+    check(lib().al_apollo_step(arr, nt, ctypes.byref(cfg), step, _ptr(ws), 0 if ws is None else ws.numel(),
+                               _stream(stream)))

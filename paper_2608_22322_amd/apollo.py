@@ -12,6 +12,8 @@ N(0, 1/r); it is an input of the step (seeded, refreshed every `gap` steps by th
 """
 from __future__ import annotations
 
+import math
+
 from . import FP32, Spec, state_bytes as _codec_bytes
 
 RANK = 256
@@ -51,3 +53,68 @@ def state_bytes(shapes, rank: int = RANK, m: Spec = Spec(FP32, 256), v: Spec = S
         else:
             total += _codec_bytes(full_m.codec, s.n, full_m.block) + _codec_bytes(full_v.codec, s.n, full_v.block)
     return total
+
+
+class ApolloStep:
+    """One APOLLO step per call over a list of ParamState (param, grad, rows, cols) with names: projected
+    tensors take al_apollo_step (projected moments, projection matrix and limiter state allocated here),
+    the others al_adamw_step with the same codes (their ParamState m, v are allocated here too). The
+    projection of tensor i for steps (e - 1) * gap + 1 .. e * gap is drawn from the seeded stream
+    (seed, projection, i, e - 1) with entries N(0, 1/rank)."""
+
+    def __init__(self, states, names, cfg=None, gap: int = GAP, seed: int | None = None, device="cuda"):
+        import torch
+
+        from . import (Spec, adamw_cfg, alloc_state, apollo_cfg, apollo_tensor_array, apollo_workspace_bytes, synth,
+                       tensor_array)
+
+        self.cfg = cfg or apollo_cfg()
+        self.gap = gap
+        self.seed = synth.BASE_SEED if seed is None else seed
+        r = self.cfg.rank
+        mspec = Spec(self.cfg.m.codec, self.cfg.m.block, self.cfg.m.log_floor)
+        vspec = Spec(self.cfg.v.codec, self.cfg.v.block, self.cfg.v.log_floor)
+        self.proj_idx, self.full_idx = [], []
+        self.items, self.proj = [], []
+        for i, (st, name) in enumerate(zip(states, names)):
+            if projected(name, st.rows, st.cols):
+                right, C, L = layout(st.rows, st.cols)
+                m, mm = alloc_state(C * r, mspec, device)
+                v, vm = alloc_state(C * r, vspec, device)
+                pj = torch.empty(L * r, dtype=torch.float32, device=device)
+                ns = torch.zeros(4, dtype=torch.float32, device=device)
+                self.items.append((st.param, st.grad, st.rows, st.cols, pj, m, mm, v, vm, ns))
+                self.proj.append((i, L, pj))
+                self.proj_idx.append(i)
+            else:
+                st.m, st.m_meta = alloc_state(st.rows * st.cols, mspec, device)
+                st.v, st.v_meta = alloc_state(st.rows * st.cols, vspec, device)
+                self.full_idx.append(i)
+        self.arr = apollo_tensor_array(self.items)
+        nbytes = apollo_workspace_bytes(self.arr, len(self.items), self.cfg)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        self.full_states = [states[i] for i in self.full_idx]
+        self.full_arr = tensor_array(self.full_states)
+        self.full_cfg = adamw_cfg(lr=self.cfg.lr, beta1=self.cfg.beta1, beta2=self.cfg.beta2, eps=self.cfg.eps,
+                                  weight_decay=self.cfg.weight_decay, grad_bf16=self.cfg.grad_dtype == 1,
+                                  m=mspec, v=vspec)
+        self._epoch = None
+
+    def refresh(self, step: int, stream=None) -> None:
+        """Draw the projections of the refresh period holding `step` (no-op within a period)."""
+        from . import synth, synth_normal
+
+        e = (step - 1) // self.gap
+        if e == self._epoch:
+            return
+        for i, L, pj in self.proj:
+            synth_normal(pj, synth.proj_key(i, e, self.seed), 1.0 / math.sqrt(self.cfg.rank), stream=stream)
+        self._epoch = e
+
+    def step(self, t: int, stream=None) -> None:
+        from . import adamw_step, apollo_step
+
+        self.refresh(t, stream)
+        apollo_step(self.arr, len(self.items), self.cfg, t, self.ws, stream)
+        if self.full_states:
+            adamw_step(self.full_states, self.full_cfg, t, stream=stream, arr=self.full_arr)

@@ -266,6 +266,100 @@ al::FacArgs fac_args(const FacPlan& P, char* ws) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// ------------------------------------------------------------ APOLLO plan
+al_status check_apollo_cfg(const al_apollo_cfg* cfg) {
+    if (!cfg) return fail(AL_EINVAL, "apollo: cfg is NULL");
+    if (cfg->grad_dtype != AL_DTYPE_F32 && cfg->grad_dtype != AL_DTYPE_BF16)
+        return fail(AL_EINVAL, "apollo: grad_dtype %d", cfg->grad_dtype);
+    if (cfg->rank != 64 && cfg->rank != 128 && cfg->rank != 256)
+        return fail(AL_EINVAL, "apollo: rank %d must be 64, 128 or 256", cfg->rank);
+    if (!is_fin(cfg->lr) || cfg->lr < 0 || !is_fin(cfg->eps) || cfg->eps < 0 || !is_fin(cfg->weight_decay) ||
+        cfg->weight_decay < 0 || !is_fin(cfg->gamma) || !(cfg->beta1 >= 0 && cfg->beta1 < 1) ||
+        !(cfg->beta2 >= 0 && cfg->beta2 < 1))
+        return fail(AL_EINVAL, "apollo: hyperparameters out of range");
+    al_status st;
+    if ((st = check_spec(cfg->m, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_UF8), "m")) != AL_OK) return st;
+    if ((st = check_spec(cfg->v, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16), "v")) !=
+        AL_OK)
+        return st;
+    if (cfg->m.codec == AL_CODEC_UF8 && cfg->m.block != 256)
+        return fail(AL_EUNSUPPORTED, "apollo: UF8 momentum block must be 256 (got %d)", cfg->m.block);
+    return AL_OK;
+}
+
+struct ApolloPlan {
+    std::vector<al::ApolloDesc> desc;
+    std::vector<int> idx;  // tensor index of each descriptor (empty tensors are skipped)
+    int64_t total_tiles = 0, total_chans = 0, total_units = 0;
+    size_t bytes = 0;
+};
+
+// Validate the list and lay out the workspace: descriptor table, then per
+// tensor R, Rt (C x rank fp32), gn2, s, sg (C doubles) and the limiter slot.
+al_status apollo_plan(const al_apollo_tensor* ts, int nt, const al_apollo_cfg* cfg, char* ws, ApolloPlan& P) {
+    if (nt < 0) return fail(AL_EINVAL, "apollo: nt < 0");
+    if (nt > 0 && !ts) return fail(AL_EINVAL, "apollo: tensors is NULL");
+    P = ApolloPlan();
+    const int64_t r = cfg->rank;
+    for (int i = 0; i < nt; ++i) {
+        const al_apollo_tensor& t = ts[i];
+        if (t.rows < 0 || t.cols < 0) return fail(AL_EINVAL, "tensor %d: negative shape", i);
+        if (t.rows > 0 && t.cols > (int64_t(1) << 40) / t.rows) return fail(AL_EINVAL, "tensor %d: shape too large", i);
+        if (t.rows * t.cols == 0) continue;
+        if (!t.param || !t.grad || !t.proj) return fail(AL_EINVAL, "tensor %d: param, grad or proj is NULL", i);
+        if (!aligned16(t.param) || !aligned16(t.grad) || !aligned16(t.proj))
+            return fail(AL_EALIGN, "tensor %d: param, grad or proj not 16-byte aligned", i);
+        const int64_t C = t.rows >= t.cols ? t.rows : t.cols;
+        al_status st;
+        if ((st = check_state(t.m, t.m_meta, cfg->m, C * r, "m", i)) != AL_OK) return st;
+        if ((st = check_state(t.v, t.v_meta, cfg->v, C * r, "v", i)) != AL_OK) return st;
+        if (cfg->gamma > 0) {
+            if (!t.norm_state) return fail(AL_EINVAL, "tensor %d: norm_state is NULL (the limiter is on)", i);
+            if (!aligned16(t.norm_state)) return fail(AL_EALIGN, "tensor %d: norm_state not 16-byte aligned", i);
+        }
+        al::ApolloDesc d;
+        std::memset(&d, 0, sizeof(d));
+        d.p = t.param;
+        d.g = t.grad;
+        d.proj = t.proj;
+        d.norm_state = t.norm_state;
+        d.rows = t.rows;
+        d.cols = t.cols;
+        d.right = t.rows >= t.cols;
+        d.C = C;
+        d.L = d.right ? t.cols : t.rows;
+        d.nru = (int32_t)((t.rows + 255) / 256);
+        d.ncu = (int32_t)((t.cols + 255) / 256);
+        d.tile_begin = P.total_tiles;
+        P.total_tiles += (C + al::kApolloTileCh - 1) / al::kApolloTileCh;
+        d.chan_begin = P.total_chans;
+        P.total_chans += C;
+        d.unit_begin = P.total_units;
+        P.total_units += (int64_t)d.nru * d.ncu;
+        P.desc.push_back(d);
+        P.idx.push_back(i);
+    }
+    if (P.total_tiles >= (int64_t(1) << 31) || P.total_chans / 4 >= (int64_t(1) << 31) ||
+        P.total_units / 4 >= (int64_t(1) << 31))
+        return fail(AL_EUNSUPPORTED, "apollo: tensor list too large for one launch");
+    size_t off = align256(P.desc.size() * sizeof(al::ApolloDesc));
+    auto take = [&](size_t nbytes) -> char* {
+        char* ptr = ws ? ws + off : nullptr;
+        off += align256(nbytes);
+        return ptr;
+    };
+    for (auto& d : P.desc) {
+        d.R = reinterpret_cast<float*>(take((size_t)(d.C * r) * 4));
+        d.Rt = reinterpret_cast<float*>(take((size_t)(d.C * r) * 4));
+        d.gn2 = reinterpret_cast<double*>(take((size_t)d.C * 8));
+        d.s = reinterpret_cast<double*>(take((size_t)d.C * 8));
+        d.sg = reinterpret_cast<double*>(take((size_t)d.C * 8));
+        d.lam = reinterpret_cast<double*>(take(16));
+    }
+    P.bytes = P.desc.empty() ? 0 : off;
+    return AL_OK;
+}
+
 }  // namespace
 
 namespace al {
@@ -418,6 +512,92 @@ al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg
             if ((st = flush()) != AL_OK) return st;
     }
     return flush();
+}
+
+al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,
+                                    size_t* bytes) {
+    g_err[0] = 0;
+    if (!bytes) return fail(AL_EINVAL, "al_apollo_workspace_bytes: bytes is NULL");
+    al_status st = check_apollo_cfg(cfg);
+    if (st != AL_OK) return st;
+    ApolloPlan P;
+    if ((st = apollo_plan(tensors, nt, cfg, nullptr, P)) != AL_OK) return st;
+    *bytes = P.bytes;
+    return AL_OK;
+}
+
+al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg, int64_t step,
+                         void* ws, size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    al_status st = check_apollo_cfg(cfg);
+    if (st != AL_OK) return st;
+    if (step < 1) return fail(AL_EINVAL, "al_apollo_step: step must be >= 1");
+    ApolloPlan P;
+    if ((st = apollo_plan(tensors, nt, cfg, nullptr, P)) != AL_OK) return st;
+    if (P.desc.empty()) return AL_OK;
+    if ((st = check_ws(ws, ws_bytes, P.bytes, "al_apollo_step")) != AL_OK) return st;
+    if ((st = apollo_plan(tensors, nt, cfg, static_cast<char*>(ws), P)) != AL_OK) return st;
+
+    al::ApolloArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.D = reinterpret_cast<const al::ApolloDesc*>(ws);
+    a.nt = (int32_t)P.desc.size();
+    a.rank = cfg->rank;
+    a.total_tiles = P.total_tiles;
+    a.total_chans = P.total_chans;
+    a.total_units = P.total_units;
+    a.lr = cfg->lr;
+    a.decay = 1.0 - cfg->lr * cfg->weight_decay;
+    a.gamma = cfg->gamma;
+    a.step = step;
+
+    // the fused AdamW step over the projected moments: gradient R, parameter Rt
+    // (cleared by the projection), lr 1, no weight decay -> Rt = -direction
+    al::AdamWLaunch w;
+    std::memset(&w, 0, sizeof(w));
+    const double bc1 = 1.0 - std::pow(cfg->beta1, (double)step);
+    const double bc2 = 1.0 - std::pow(cfg->beta2, (double)step);
+    w.beta1 = cfg->beta1;
+    w.omb1 = 1.0 - cfg->beta1;
+    w.beta2 = cfg->beta2;
+    w.omb2 = 1.0 - cfg->beta2;
+    w.step_size = (float)(1.0 / bc1);
+    w.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+    w.eps = (float)cfg->eps;
+    w.decay = 1.0f;
+    w.v_floor = cfg->v.log_floor;
+    w.cf = al::exp2_coef();
+    const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
+
+    hipStream_t s = as_stream(stream);
+    hipError_t e;
+    if ((e = al::apollo_copy_desc(P.desc.data(), a.nt, const_cast<al::ApolloDesc*>(a.D), s)) != hipSuccess ||
+        (e = al::launch_apollo_proj(a, cfg->grad_dtype, s)) != hipSuccess)
+        return hip_fail(e, "al_apollo_step launch");
+    for (size_t k = 0; k < P.desc.size(); ++k) {
+        const al::ApolloDesc& d = P.desc[k];
+        const al_apollo_tensor& t = tensors[P.idx[k]];
+        al::AdamWDesc& x = w.t[w.nt++];
+        x.p = d.Rt;
+        x.g = d.R;
+        x.m = t.m;
+        x.ms = t.m_meta;
+        x.v = t.v;
+        x.vm = t.v_meta;
+        x.n = d.C * cfg->rank;
+        x.tile_begin = w.total_tiles;
+        w.total_tiles += (x.n + T - 1) / T;
+        if (w.nt == al::kAdamWMaxTensors || k + 1 == P.desc.size()) {
+            if ((e = al::launch_adamw(w, AL_DTYPE_F32, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
+                return hip_fail(e, "al_apollo_step launch");
+            w.nt = 0;
+            w.total_tiles = 0;
+        }
+    }
+    if ((e = al::launch_apollo_scale(a, s)) != hipSuccess || (e = al::launch_apollo_norm(a, s)) != hipSuccess ||
+        (e = al::launch_apollo_update(a, cfg->grad_dtype, s)) != hipSuccess)
+        return hip_fail(e, "al_apollo_step launch");
+    return AL_OK;
 }
 
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream) {

@@ -133,6 +133,52 @@ hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s);
 hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s);
 hipError_t launch_came_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s);
 
+// ------------------------------------------------------------------ APOLLO
+// One descriptor per projected tensor, held in the caller's workspace. A
+// tensor has C channels of L inputs (A = G or G^T as C x L) and rank r; its
+// workspace regions hold R and Rt (C x r fp32, channel-major) and per-channel
+// binary64 sums.
+constexpr int kApolloTileCh = 64;  // channels per projection workgroup
+struct ApolloDesc {
+    float* p;
+    const void* g;
+    const float* proj;   // L x r
+    float* norm_state;   // limiter state (1 float), or NULL
+    float* R;            // C x r: fl32(A Pi)
+    float* Rt;           // C x r: the AdamW direction on R (written negated by the AdamW kernel)
+    double* gn2;         // C: sum over the channel of g^2
+    double* s;           // C: channel scale
+    double* sg;          // C: s_c^2 gn2_c
+    double* lam;         // [0]: limiter divisor
+    int64_t rows, cols, C, L;
+    int64_t tile_begin;  // first projection tile (kApolloTileCh channels)
+    int64_t chan_begin;  // first channel over the list
+    int64_t unit_begin;  // first 256x256 update unit
+    int32_t right;       // channels are rows (rows >= cols)
+    int32_t nru, ncu;
+    int32_t pad_;
+};
+
+constexpr int kApolloCopyBatch = 16;
+struct ApolloDescBatch {
+    int32_t count, offset;
+    ApolloDesc d[kApolloCopyBatch];
+};
+
+struct ApolloArgs {
+    const ApolloDesc* D;
+    int32_t nt, rank;
+    int64_t total_tiles, total_chans, total_units;
+    double lr, decay, gamma;
+    int64_t step;
+};
+
+hipError_t apollo_copy_desc(const ApolloDesc* host, int count, ApolloDesc* dev, hipStream_t s);
+hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s);
+hipError_t launch_apollo_scale(const ApolloArgs& a, hipStream_t s);
+hipError_t launch_apollo_norm(const ApolloArgs& a, hipStream_t s);
+hipError_t launch_apollo_update(const ApolloArgs& a, int grad_dtype, hipStream_t s);
+
 // Taylor coefficients of the binary64 exp2 used by every decode.
 const Exp2Coef& exp2_coef();
 

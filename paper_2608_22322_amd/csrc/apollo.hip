@@ -1,0 +1,324 @@
+// APOLLO projected-state step on gfx950 (section 3.1: moments kept in a
+// low-rank projection of the gradient derive a channel-wise scale of the
+// original gradient; section 6 setup: rank 256, channel-wise scaling).
+//
+// Kernel sequence of one step (the fused AdamW step over the projected
+// moments runs between proj and scale, launched by the C ABI):
+//   proj    R = fl32(A Pi) for a tile of 64 channels and all r columns, in
+//           binary64 on the matrix cores (v_mfma_f64_16x16x4f64): A (bf16 or
+//           fp32 gradient, as C x L) and Pi (fp32) are staged through LDS in
+//           slices of 32 inputs and widened to binary64; the products are
+//           exact and the accumulation is binary64, so fl32 of the result is
+//           the exactly rounded value except within ~L ulps of binary64 of an
+//           fp32 midpoint. Also sums g^2 per channel and clears Rt.
+//   scale   one wavefront per channel: s_c = ||Rt_c|| / (||R_c|| + 1e-8).
+//   norm    one wavefront per tensor: ||G~||^2 = sum_c s_c^2 ||G_c||^2 and the
+//           norm-growth limiter.
+//   update  p = fl32(p (1 - lr wd) - lr g (s_c / lam)) over 256x256 units,
+//           one wavefront per unit, 4 columns per lane, rows in batches.
+// The projection is the one dense contraction of the path (2 r flops per
+// parameter); everything else streams.
+#include "al_device.hpp"
+#include "al_internal.hpp"
+
+namespace al {
+
+typedef double d4v __attribute__((ext_vector_type(4)));
+
+template <int64_t ApolloDesc::*F>
+__device__ __forceinline__ int apollo_locate(const ApolloDesc* D, int n, int64_t x) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (D[mid].*F <= x)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// Fixed-order butterfly sum of a double over the wavefront (every lane gets the total).
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+    return x;
+}
+
+template <int G>
+__device__ __forceinline__ double grad_d(const void* g, int64_t e) {
+    if constexpr (G == G_BF16)
+        return (double)bf16_to_f32(reinterpret_cast<const uint16_t*>(g)[e]);
+    else
+        return (double)reinterpret_cast<const float*>(g)[e];
+}
+
+// --------------------------------------------------------------- descriptors
+__global__ void apollo_desc_copy_kernel(const ApolloDescBatch b, ApolloDesc* dst) {
+    constexpr int W = sizeof(ApolloDesc) / 8;
+    const int total = b.count * W;
+    const uint64_t* src = reinterpret_cast<const uint64_t*>(b.d);
+    uint64_t* out = reinterpret_cast<uint64_t*>(dst + b.offset);
+    for (int i = threadIdx.x; i < total; i += blockDim.x) out[i] = src[i];
+}
+
+hipError_t apollo_copy_desc(const ApolloDesc* host, int count, ApolloDesc* dev, hipStream_t s) {
+    static_assert(sizeof(ApolloDesc) % 8 == 0, "descriptor size");
+    for (int off = 0; off < count; off += kApolloCopyBatch) {
+        ApolloDescBatch b;
+        b.count = count - off < kApolloCopyBatch ? count - off : kApolloCopyBatch;
+        b.offset = off;
+        for (int i = 0; i < b.count; ++i) b.d[i] = host[off + i];
+        hipLaunchKernelGGL(apollo_desc_copy_kernel, dim3(1), dim3(256), 0, s, b, dev);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// ---------------------------------------------------------------- projection
+constexpr int kLK = 32;  // inputs per LDS slice
+
+// One workgroup per tile of 64 channels; wave w computes output columns
+// [64 w, 64 w + 64) of the tile (4 x 4 MFMA tiles of 16 x 16) when 64 w < r.
+// MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
+template <int G>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void apollo_proj_kernel(const ApolloArgs a) {
+    __shared__ double As[kApolloTileCh][kLK + 1];
+    __shared__ __attribute__((aligned(16))) float Bs[kLK][256];
+    const int64_t tile = blockIdx.x;
+    const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::tile_begin>(a.D, a.nt, tile)];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int r = a.rank, r4 = a.rank / 4;
+    const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
+    const int64_t C = d.C, L = d.L, cols = d.cols;
+    const bool right = d.right != 0;
+    const bool active = 64 * w < r;
+    d4v acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
+    double gsum = 0.0;
+    for (int64_t l0 = 0; l0 < L; l0 += kLK) {
+        // A slice: consecutive threads walk the contiguous direction of G
+        for (int e = tid; e < kApolloTileCh * kLK; e += 256) {
+            const int c = right ? e / kLK : e % kApolloTileCh;
+            const int l = right ? e % kLK : e / kApolloTileCh;
+            double x = 0.0;
+            if (c0 + c < C && l0 + l < L) {
+                const int64_t idx = right ? (c0 + c) * cols + (l0 + l) : (l0 + l) * cols + (c0 + c);
+                x = grad_d<G>(d.g, idx);
+            }
+            As[c][l] = x;
+        }
+        // Pi slice: rows l0 .. l0 + 31, all r columns (16-byte loads)
+        for (int e = tid; e < kLK * r4; e += 256) {
+            const int l = e / r4, k4 = e - l * r4;
+            float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (l0 + l < L) x = *reinterpret_cast<const float4*>(d.proj + (l0 + l) * r + 4 * k4);
+            *reinterpret_cast<float4*>(&Bs[l][4 * k4]) = x;
+        }
+        __syncthreads();
+        if (tid < kApolloTileCh) {
+#pragma unroll 8
+            for (int l = 0; l < kLK; ++l) {
+                const double x = As[tid][l];
+                gsum += x * x;
+            }
+        }
+        if (active) {
+#pragma unroll 2
+            for (int kk = 0; kk < kLK; kk += 4) {
+                double af[4], bf[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) af[i] = As[16 * i + (lane & 15)][kk + (lane >> 4)];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bf[j] = (double)Bs[kk + (lane >> 4)][64 * w + 16 * j + (lane & 15)];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+    if (active) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t c = c0 + 16 * i + (lane >> 4) + 4 * v;
+                    const int k = 64 * w + 16 * j + (lane & 15);
+                    if (c < C) {
+                        d.R[c * r + k] = (float)acc[i][j][v];
+                        d.Rt[c * r + k] = 0.0f;
+                    }
+                }
+    }
+    if (tid < kApolloTileCh && c0 + tid < C) d.gn2[c0 + tid] = gsum;
+}
+
+hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_tiles == 0) return hipSuccess;
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(apollo_proj_kernel<G_BF16>, dim3((unsigned)a.total_tiles), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(apollo_proj_kernel<G_F32>, dim3((unsigned)a.total_tiles), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ channel scales
+// One wavefront per channel (4 per workgroup). Rt holds the negated direction
+// (the AdamW kernel's parameter output from zero); only squares are used.
+__global__ __launch_bounds__(256) void apollo_scale_kernel(const ApolloArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t ch = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (ch >= a.total_chans) return;
+    const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::chan_begin>(a.D, a.nt, ch)];
+    const int64_t c = ch - d.chan_begin;
+    const int r = a.rank;
+    double st = 0.0, sr = 0.0;
+    for (int k = lane; k < r; k += 64) {
+        const double x = (double)d.Rt[c * r + k];
+        const double y = (double)d.R[c * r + k];
+        st += x * x;
+        sr += y * y;
+    }
+    st = wave_sum_d(st);
+    sr = wave_sum_d(sr);
+    if (lane == 0) {
+        const double sc = sqrt(st) / (sqrt(sr) + 1e-8);
+        d.s[c] = sc;
+        d.sg[c] = sc * sc * d.gn2[c];
+    }
+}
+
+hipError_t launch_apollo_scale(const ApolloArgs& a, hipStream_t s) {
+    if (a.total_chans == 0) return hipSuccess;
+    hipLaunchKernelGGL(apollo_scale_kernel, dim3((unsigned)((a.total_chans + 3) / 4)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+// --------------------------------------------------------- limiter per tensor
+__global__ __launch_bounds__(64) void apollo_norm_kernel(const ApolloArgs a) {
+    const ApolloDesc& d = a.D[blockIdx.x];
+    const int lane = threadIdx.x;
+    double acc = 0.0;
+    for (int64_t c = lane; c < d.C; c += 64) acc += d.sg[c];
+    acc = wave_sum_d(acc);
+    if (lane == 0) {
+        const double n = sqrt(acc);
+        double lam = 1.0;
+        if (a.gamma > 0.0) {
+            if (a.step >= 2) {
+                const double q = n / ((double)d.norm_state[0] + 1e-8);
+                lam = (q > a.gamma ? q : a.gamma) / a.gamma;
+                d.norm_state[0] = (float)(n / lam);
+            } else {
+                d.norm_state[0] = (float)n;
+            }
+        }
+        d.lam[0] = lam;
+    }
+}
+
+hipError_t launch_apollo_norm(const ApolloArgs& a, hipStream_t s) {
+    if (a.nt == 0) return hipSuccess;
+    hipLaunchKernelGGL(apollo_norm_kernel, dim3(a.nt), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------ parameter update
+constexpr int kUpdRows = 4;
+
+template <int G>
+__global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t unit = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (unit >= a.total_units) return;
+    const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::unit_begin>(a.D, a.nt, unit)];
+    const int64_t u = unit - d.unit_begin;
+    const int64_t ru = u / d.ncu, cu = u % d.ncu;
+    const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
+    const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
+    const int nc = (int)(cols - c0 < 256 ? cols - c0 : 256);
+    const int c = 4 * lane;
+    if (c >= nc) return;
+    const bool vec = (cols & 3) == 0 && c + 4 <= nc;
+    const bool right = d.right != 0;
+    const double lam = d.lam[0];
+    double sc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sc[j] = (!right && c + j < nc) ? d.s[c0 + c + j] / lam : 0.0;
+    for (int rb = 0; rb < nr; rb += kUpdRows) {
+        float pv[kUpdRows][4], gv[kUpdRows][4];
+        double sr[kUpdRows];
+#pragma unroll
+        for (int k = 0; k < kUpdRows; ++k) {
+            const int rr = rb + k < nr ? rb + k : nr - 1;  // rows past the end repeat the last one, unused
+            const int64_t e = (r0 + rr) * cols + c0 + c;
+            sr[k] = right ? d.s[r0 + rr] / lam : 0.0;
+            if (vec) {
+                const float4 x = *reinterpret_cast<const float4*>(d.p + e);
+                pv[k][0] = x.x;
+                pv[k][1] = x.y;
+                pv[k][2] = x.z;
+                pv[k][3] = x.w;
+                if constexpr (G == G_BF16) {
+                    const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.g) + e);
+                    gv[k][0] = bf16_to_f32(w.x & 0xFFFFu);
+                    gv[k][1] = bf16_to_f32(w.x >> 16);
+                    gv[k][2] = bf16_to_f32(w.y & 0xFFFFu);
+                    gv[k][3] = bf16_to_f32(w.y >> 16);
+                } else {
+                    const float4 y = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.g) + e);
+                    gv[k][0] = y.x;
+                    gv[k][1] = y.y;
+                    gv[k][2] = y.z;
+                    gv[k][3] = y.w;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    pv[k][j] = c + j < nc ? d.p[e + j] : 0.0f;
+                    gv[k][j] = c + j < nc ? (float)grad_d<G>(d.g, e + j) : 0.0f;
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < kUpdRows; ++k) {
+            if (rb + k >= nr) continue;
+            const int64_t e = (r0 + rb + k) * cols + c0 + c;
+            float out[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const double upd = (double)gv[k][j] * (right ? sr[k] : sc[j]);
+                out[j] = (float)((double)pv[k][j] * a.decay - a.lr * upd);
+            }
+            if (vec) {
+                *reinterpret_cast<float4*>(d.p + e) = make_float4(out[0], out[1], out[2], out[3]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (c + j < nc) d.p[e + j] = out[j];
+            }
+        }
+    }
+}
+
+hipError_t launch_apollo_update(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
+    if (a.total_units == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((a.total_units + 3) / 4);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(apollo_update_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(apollo_update_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace al
