@@ -170,17 +170,18 @@ def factored_bytes_per_param(shapes, came: bool):
     return alg, sched
 
 
-def time_factored(came: bool, steps: int, warmup: int):
+def time_factored(came: bool, steps: int, warmup: int, llama7b: bool = False):
     """One Adafactor (AL8 B256 factored + 1-D, no zero mask) or CAME (AL16 B128 V and confidence, UF8 m,
-    2% zeros) step over the TinyLlama-1.1B list, grads generated once."""
+    2% zeros) step over the TinyLlama-1.1B list (or the Llama-7B list), grads generated once."""
     import torch
 
     import paper_2608_22322_amd as al
     from paper_2608_22322_amd import data
-    from paper_2608_22322_amd.workloads import tinyllama_shapes, workload_tinyllama
+    from paper_2608_22322_amd.workloads import Workload, llama7b_shapes, tinyllama_shapes, workload_tinyllama
 
-    shapes = tinyllama_shapes()
-    w = workload_tinyllama(zero_frac=0.02 if came else 0.0)
+    shapes = llama7b_shapes() if llama7b else tinyllama_shapes()
+    w = (Workload("llama-7b", shapes, zero_frac=0.02 if came else 0.0, steps=20) if llama7b else
+         workload_tinyllama(zero_frac=0.02 if came else 0.0))
     dev = torch.device("cuda:0")
     if came:
         cfg = al.came_cfg()
@@ -226,9 +227,9 @@ def time_factored(came: bool, steps: int, warmup: int):
     mean = sum(ms_) / len(ms_)
     n = sum(s.n for s in shapes)
     alg, sched = factored_bytes_per_param(shapes, came)
-    rec = {"workload": "tinyllama-1.1b list (201 tensors), " + ("CAME: AL16 B128 V and confidence, UF8 m B256, "
-                                                               "2% zero grads" if came else
-                                                               "Adafactor: AL8 B256 factored V and 1-D v"),
+    rec = {"workload": ("llama-7b list (291 tensors), " if llama7b else "tinyllama-1.1b list (201 tensors), ") +
+                       ("CAME: AL16 B128 V and confidence, UF8 m B256, 2% zero grads" if came else
+                        "Adafactor: AL8 B256 factored V and 1-D v"),
            "params": n, "ms_mean": round(mean, 4), "ms_min": round(min(ms_), 4),
            "gparams_s": round(n / (mean * 1e-3) / 1e9, 2),
            "algorithmic_bytes_per_param": round(alg, 4), "schedule_bytes_per_param": round(sched, 4),
@@ -236,6 +237,60 @@ def time_factored(came: bool, steps: int, warmup: int):
            "frac_of_peak": round(alg * n / (mean * 1e-3) / 1e9 / PEAK_GBS, 4),
            "workspace_bytes": nbytes}
     del states, ws
+    torch.cuda.empty_cache()
+    return rec
+
+
+def time_apollo(steps: int, warmup: int):
+    """One APOLLO step (rank 256, channel-wise scales, limiter 1.01; UF8 m B256 + AL8 v B2048) over the
+    TinyLlama-1.1B list: the 154 layer matrices projected, the embedding, LM head and norms under AdamW with
+    the same codes; bf16 grads N(0, 1e-3) with 2% zeros, generated once. The projection is the dense
+    contraction of the step: 2 * rank flops per projected parameter, binary64 on the matrix cores."""
+    import torch
+
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import apollo, data
+    from paper_2608_22322_amd.workloads import tinyllama_shapes, workload_tinyllama
+
+    shapes = tinyllama_shapes()
+    w = workload_tinyllama(zero_frac=0.02)
+    dev = torch.device("cuda:0")
+    states = []
+    for i, s in enumerate(shapes):
+        st = al.ParamState(data.device_param(i, s, dev), data.device_grad_buffer(s, w, dev), s.rows, s.cols)
+        data.fill_grad(st.grad, i, s, w, 1)
+        states.append(st)
+    cfg = al.apollo_cfg(rank=apollo.RANK, gamma=apollo.GAMMA)
+    drv = apollo.ApolloStep(states, [s.name for s in shapes], cfg, device=dev)
+    stream = torch.cuda.current_stream()
+    t = 0
+    for _ in range(warmup):
+        t += 1
+        drv.step(t, stream)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        t += 1
+        evs[k][0].record(stream)
+        drv.step(t, stream)
+        evs[k][1].record(stream)
+    torch.cuda.synchronize()
+    ms_ = [a.elapsed_time(b) for a, b in evs]
+    mean = sum(ms_) / len(ms_)
+    n = sum(s.n for s in shapes)
+    nproj = sum(s.n for s in shapes if apollo.projected(s.name, s.rows, s.cols))
+    flops = 2.0 * apollo.RANK * nproj
+    rec = {"workload": "tinyllama-1.1b list (201 tensors), APOLLO rank 256: 154 layer matrices projected "
+                       "(UF8 m B256 + AL8 v B2048 on the projected moments), embedding/head/norms AdamW "
+                       "with the same codes, 2% zero grads",
+           "params": n, "projected_params": nproj, "ms_mean": round(mean, 4), "ms_min": round(min(ms_), 4),
+           "gparams_s": round(n / (mean * 1e-3) / 1e9, 2), "projection_gflop": round(flops / 1e9, 1),
+           "projection_fp64_tflops_lower_bound": round(flops / (mean * 1e-3) / 1e12, 2),
+           "fp64_mfma_peak_tflops": 78.6,
+           "state_mib": round(apollo.state_bytes(shapes, apollo.RANK, al.Spec(al.UF8, 256),
+                                                 al.Spec(al.AL8, 2048)) / 2**20, 1),
+           "workspace_bytes": int(drv.ws.numel())}
+    del states, drv
     torch.cuda.empty_cache()
     return rec
 
@@ -362,6 +417,11 @@ def main():
         for name, came in (("adafactor", False), ("came", True)):
             paths[name] = time_factored(came, args.steps, args.warmup)
             log(name + ": " + json.dumps(paths[name]))
+        for name, came in (("adafactor_7b", False), ("came_7b", True)):
+            paths[name] = time_factored(came, args.steps, args.warmup, llama7b=True)
+            log(name + ": " + json.dumps(paths[name]))
+        paths["apollo"] = time_apollo(args.steps, args.warmup)
+        log("apollo: " + json.dumps(paths["apollo"]))
         out["paths"] = paths
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")

@@ -77,12 +77,45 @@ hipError_t apollo_copy_desc(const ApolloDesc* host, int count, ApolloDesc* dev, 
 }
 
 // ---------------------------------------------------------------- projection
-constexpr int kLK = 32;  // inputs per LDS slice
+constexpr int kLK = 16;  // inputs per LDS slice
 
 // One workgroup per tile of 64 channels; wave w computes output columns
 // [64 w, 64 w + 64) of the tile (4 x 4 MFMA tiles of 16 x 16) when 64 w < r.
-// MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16] and
-// B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
+// The next slice's global loads are issued into registers before the matrix
+// work on the current slice (software prefetch; one LDS buffer, two barriers
+// per slice). MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16]
+// and B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
+constexpr int kAPer = kApolloTileCh * kLK / 256;  // A values per thread and slice
+constexpr int kBPer = kLK * 256 / 4 / 256;        // Pi float4 per thread and slice at rank 256
+
+template <int G>
+__device__ __forceinline__ void proj_fetch(const ApolloDesc& d, int64_t c0, int64_t l0, int r4, bool right, int tid,
+                                           float (&ra)[kAPer], float4 (&rb)[kBPer]) {
+#pragma unroll
+    for (int q = 0; q < kAPer; ++q) {
+        const int e = tid + 256 * q;
+        const int c = right ? e / kLK : e % kApolloTileCh;
+        const int l = right ? e % kLK : e / kApolloTileCh;
+        float x = 0.0f;
+        if (c0 + c < d.C && l0 + l < d.L) {
+            const int64_t idx = right ? (c0 + c) * d.cols + (l0 + l) : (l0 + l) * d.cols + (c0 + c);
+            if constexpr (G == G_BF16)
+                x = bf16_to_f32(reinterpret_cast<const uint16_t*>(d.g)[idx]);
+            else
+                x = reinterpret_cast<const float*>(d.g)[idx];
+        }
+        ra[q] = x;
+    }
+#pragma unroll
+    for (int q = 0; q < kBPer; ++q) {
+        const int e = tid + 256 * q;
+        const int l = e / r4, k4 = e - l * r4;
+        float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        if (e < kLK * r4 && l0 + l < d.L) x = *reinterpret_cast<const float4*>(d.proj + (l0 + l) * (4 * r4) + 4 * k4);
+        rb[q] = x;
+    }
+}
+
 template <int G>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void apollo_proj_kernel(const ApolloArgs a) {
     __shared__ double As[kApolloTileCh][kLK + 1];
@@ -92,7 +125,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int r = a.rank, r4 = a.rank / 4;
     const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
-    const int64_t C = d.C, L = d.L, cols = d.cols;
+    const int64_t C = d.C, L = d.L;
     const bool right = d.right != 0;
     const bool active = 64 * w < r;
     d4v acc[4][4];
@@ -101,26 +134,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
     double gsum = 0.0;
+    float ra[kAPer];
+    float4 rb[kBPer];
+    proj_fetch<G>(d, c0, 0, r4, right, tid, ra, rb);
     for (int64_t l0 = 0; l0 < L; l0 += kLK) {
-        // A slice: consecutive threads walk the contiguous direction of G
-        for (int e = tid; e < kApolloTileCh * kLK; e += 256) {
+#pragma unroll
+        for (int q = 0; q < kAPer; ++q) {
+            const int e = tid + 256 * q;
             const int c = right ? e / kLK : e % kApolloTileCh;
             const int l = right ? e % kLK : e / kApolloTileCh;
-            double x = 0.0;
-            if (c0 + c < C && l0 + l < L) {
-                const int64_t idx = right ? (c0 + c) * cols + (l0 + l) : (l0 + l) * cols + (c0 + c);
-                x = grad_d<G>(d.g, idx);
-            }
-            As[c][l] = x;
+            As[c][l] = (double)ra[q];
         }
-        // Pi slice: rows l0 .. l0 + 31, all r columns (16-byte loads)
-        for (int e = tid; e < kLK * r4; e += 256) {
-            const int l = e / r4, k4 = e - l * r4;
-            float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-            if (l0 + l < L) x = *reinterpret_cast<const float4*>(d.proj + (l0 + l) * r + 4 * k4);
-            *reinterpret_cast<float4*>(&Bs[l][4 * k4]) = x;
+#pragma unroll
+        for (int q = 0; q < kBPer; ++q) {
+            const int e = tid + 256 * q;
+            if (e < kLK * r4) {
+                const int l = e / r4, k4 = e - l * r4;
+                *reinterpret_cast<float4*>(&Bs[l][4 * k4]) = rb[q];
+            }
         }
         __syncthreads();
+        if (l0 + kLK < L) proj_fetch<G>(d, c0, l0 + kLK, r4, right, tid, ra, rb);
         if (tid < kApolloTileCh) {
 #pragma unroll 8
             for (int l = 0; l < kLK; ++l) {
