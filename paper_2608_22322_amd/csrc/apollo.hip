@@ -273,7 +273,8 @@ constexpr int kUpdRows = 4;
 template <int G>
 __global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) {
     const int lane = threadIdx.x & 63;
-    const int64_t unit = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = xcd_order(blockIdx.x, gridDim.x) * 4 +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
     const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::unit_begin>(a.D, a.nt, unit)];
     const int64_t u = unit - d.unit_begin;

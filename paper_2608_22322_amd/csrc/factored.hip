@@ -391,7 +391,7 @@ template <int G>
 __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
     __shared__ DD racc[256];
-    const int64_t unit = base + blockIdx.x;
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
     if (unit >= a.total_units) return;
     const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
     const int64_t u = unit - d.unit_begin;
@@ -613,7 +613,8 @@ struct GRows {
 template <int G>
 __global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
-    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x) * 4 +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const int64_t u = unit - d.unit_begin;
@@ -707,7 +708,8 @@ hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s) {
 template <int G>
 __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
-    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x) * 4 +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const int64_t u = unit - d.unit_begin;
@@ -1005,7 +1007,7 @@ template <int G>
 __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) double tile[kResRows][kResCols + 2];
     __shared__ DD racc[256];
-    const int64_t unit = base + blockIdx.x;
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
     if (unit >= a.total_units) return;
     const FacDesc& d = a.D[locate_unit(a.D, a.n2, unit)];
     const int64_t u = unit - d.unit_begin;
@@ -1033,7 +1035,8 @@ hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
 template <int G, bool UF>
 __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
-    const int64_t unit = base + (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x) * 4 +
+                         __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     if (d.cols & 255) return;  // other widths: the chunk kernel
@@ -1126,7 +1129,7 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
 template <int G>
 __global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) {
     const int lane = threadIdx.x & 63;
-    const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t wave = xcd_order(blockIdx.x, gridDim.x) * 4 + (threadIdx.x >> 6);
     const int64_t nw = (int64_t)gridDim.x * 4;
     for (int64_t chunk = wave; chunk < a.total_chunks; chunk += nw) {
         const FacDesc& d = a.D[locate_chunk(a.D, a.n2, chunk)];

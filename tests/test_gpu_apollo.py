@@ -171,3 +171,58 @@ def test_apollo_driver_mixed_list(dev):
         torch.cuda.synchronize()
         for i in range(len(shapes)):
             compare_params(to_np(states[i].param)[:host[i].shape[0]], host[i], 1e-5, f"{names[i]} t{t}")
+
+
+def test_apollo_full_tinyllama_list_sampled(dev):
+    """The whole 201-tensor TinyLlama list through ApolloStep (the bench's configuration: 154 projected
+    layer matrices at rank 256, embedding/head/norms under AdamW); whole small tensors recomputed by the
+    oracle -- projected ones (left and right) and 1-D ones -- after each of two steps."""
+    import torch
+
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import apollo, data
+    from paper_2608_22322_amd.workloads import tinyllama_shapes, workload_tinyllama
+
+    shapes = tinyllama_shapes()
+    w = workload_tinyllama(zero_frac=0.02)
+    states = []
+    for i, s in enumerate(shapes):
+        states.append(al.ParamState(data.device_param(i, s, dev), data.device_grad_buffer(s, w, dev), s.rows, s.cols))
+    drv = apollo.ApolloStep(states, [s.name for s in shapes], al.apollo_cfg(), device=dev)
+    names = ("layer0.k", "layer7.v", "layer3.q", "layer0.attn_norm", "norm")
+    sample = [i for i, s in enumerate(shapes) if s.name in names]
+    host = {}
+    for i in sample:
+        s = shapes[i]
+        p0 = data.host_param(i, s, np.arange(s.n))
+        if apollo.projected(s.name, s.rows, s.cols):
+            right, C, L = oap.layout(s.rows, s.cols)
+            host[i] = dict(p=p0.copy(), P=synth.proj_matrix(i, 0, L, 256), m=oracle.State(oracle.UF8, C * 256, 256),
+                           v=oracle.State(oracle.AL8, C * 256, 2048, FLOOR), prev=np.zeros(1, np.float32),
+                           k=drv.proj_idx.index(i))
+        else:
+            host[i] = dict(p=p0.copy(), m=oracle.State(oracle.UF8, s.n, 256), v=oracle.State(oracle.AL8, s.n, 2048, FLOOR))
+    log(f"APOLLO full TinyLlama list, sampled tensors {[shapes[i].name for i in sample]}")
+    for t in (1, 2):
+        for i, s in enumerate(shapes):
+            data.fill_grad(states[i].grad, i, s, w, t)
+        drv.step(t)
+        torch.cuda.synchronize()
+        for i in sample:
+            s, h = shapes[i], host[i]
+            gh = data.host_grad(i, w, t, np.arange(s.n))
+            what = f"{s.name} t{t}"
+            if "P" in h:
+                oap.apollo_step(h["p"], gh, s.rows, s.cols, h["P"], h["m"], h["v"], t, h["prev"], lr=1e-4)
+                it = drv.items[h["k"]]
+                n = oap.layout(s.rows, s.cols)[1] * 256
+                compare_codes(to_np(it[5], n), h["m"].codes[:n], h["m"].y, f"{what} m codes")
+                compare_codes(to_np(it[7], n), h["v"].codes[:n], h["v"].y, f"{what} v codes")
+                assert math.isclose(float(to_np(it[9])[0]), float(h["prev"][0]), rel_tol=1e-5), what
+            else:
+                oracle.adamw_step(h["p"], gh, h["m"], h["v"], t, lr=1e-4, wd=0.0)
+                compare_codes(to_np(states[i].m, s.n), h["m"].codes[:s.n], h["m"].y, f"{what} m codes")
+                compare_codes(to_np(states[i].v, s.n), h["v"].codes[:s.n], h["v"].y, f"{what} v codes")
+            compare_params(to_np(states[i].param)[:s.n], h["p"], 1e-5, f"{what} param")
+    del drv, states
+    torch.cuda.empty_cache()
