@@ -329,3 +329,67 @@ def test_diag_stream_validation():
     assert _status(lambda: al.check(L.al_diag_stream(1, None, A, A, A, 2048, None))) == 1
     assert _status(lambda: al.check(L.al_diag_stream(1, A, A, A + 4, A, 2048, None))) == 2
     assert al.lib().al_diag_stream(2, A, A, A, A, 0, None) == 0  # empty: no HIP call
+
+
+# ----------------------------------------------------------------- APOLLO
+def _at(rows=40, cols=96, **kw):
+    base = dict(param=A, grad=A, rows=rows, cols=cols, proj=A, m=A, m_meta=A, v=A, v_meta=A, norm_state=A)
+    base.update(kw)
+    return al.ApolloTensor(**base)
+
+
+def _ap_ws(ts, cfg=None):
+    arr = (al.ApolloTensor * max(len(ts), 1))(*ts)
+    return al.apollo_workspace_bytes(arr, len(ts), cfg or al.apollo_cfg(rank=64))
+
+
+def _ap_step(ts, cfg=None, step=1, ws=A, ws_bytes=None, nt=None):
+    cfg = cfg or al.apollo_cfg(rank=64)
+    arr = (al.ApolloTensor * max(len(ts), 1))(*ts)
+    if ws_bytes is None:
+        ws_bytes = _ap_ws(ts, cfg) if ts else 0
+    al.check(al.lib().al_apollo_step(arr, len(ts) if nt is None else nt, ctypes.byref(cfg), step, ws, ws_bytes,
+                                     None))
+
+
+def test_apollo_workspace_layout():
+    # descriptors, then per tensor R and Rt (C x rank fp32), three C-double vectors and a 16-byte slot,
+    # each region 256-byte aligned
+    def al256(x):
+        return (x + 255) // 256 * 256
+
+    C, r = 96, 64  # 40 x 96: the rows are projected, 96 channels
+    per = 2 * al256(C * r * 4) + 3 * al256(C * 8) + al256(16)
+    one = _ap_ws([_at()])
+    assert one - per in (256, 512)  # the descriptor table of one tensor
+    two = _ap_ws([_at(), _at(rows=96, cols=40)])  # the transposed shape has the same 96 channels
+    assert two - one - per in (0, 256)  # a second descriptor may spill into one more 256-byte line
+    big = _ap_ws([_at(rows=5632, cols=2048)])  # 5632 channels (rows >= cols), same one-descriptor table
+    assert big - one == 2 * (al256(5632 * r * 4) - al256(C * r * 4)) + 3 * (al256(5632 * 8) - al256(C * 8))
+    assert _ap_ws([_at(rows=0)]) == 0 and _ap_ws([]) == 0
+
+
+def test_apollo_validation():
+    assert _status(lambda: _ap_step([_at()], step=0)) == 1
+    assert _status(lambda: _ap_step([_at()], nt=-1)) == 1
+    assert _status(lambda: _ap_step([_at(rows=-1)])) == 1
+    assert _status(lambda: _ap_step([_at(proj=None)])) == 1
+    assert _status(lambda: _ap_step([_at(param=A + 4)])) == 2
+    assert _status(lambda: _ap_step([_at(proj=A + 8)])) == 2
+    assert _status(lambda: _ap_step([_at(v_meta=None)])) == 1
+    assert _status(lambda: _ap_step([_at(norm_state=None)])) == 1  # the limiter is on by default
+    assert _status(lambda: _ap_step([_at()], cfg=al.apollo_cfg(rank=96))) == 1
+    assert _status(lambda: _ap_step([_at()], cfg=al.apollo_cfg(rank=64, beta2=1.0))) == 1
+    assert _status(lambda: _ap_step([_at()], cfg=al.apollo_cfg(rank=64, m=al.Spec(al.AL8, 256)))) == 1
+    assert _status(lambda: _ap_step([_at()], cfg=al.apollo_cfg(rank=64, v=al.Spec(al.UF8, 256)))) == 1
+    assert _status(lambda: _ap_step([_at()], cfg=al.apollo_cfg(rank=64, m=al.Spec(al.UF8, 512)))) == 4
+    need = _ap_ws([_at()])
+    assert _status(lambda: _ap_step([_at()], ws=None)) == 3
+    assert _status(lambda: _ap_step([_at()], ws_bytes=need - 1)) == 3
+    assert _status(lambda: _ap_step([_at()], ws=A + 16)) == 2
+    cfg = al.apollo_cfg(rank=64)
+    cfg.grad_dtype = 7
+    assert _status(lambda: _ap_step([_at()], cfg=cfg)) == 1
+    # empty tensors and empty lists enqueue nothing
+    _ap_step([_at(rows=0, param=None, grad=None, proj=None, m=None, v=None, m_meta=None, v_meta=None)])
+    _ap_step([])
