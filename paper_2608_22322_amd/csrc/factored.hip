@@ -490,13 +490,17 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
     for (int64_t i = s + lane; i < e; i += 64) {
         DD acc{0.0, 0.0};
         double mean;
+        // the partials' loads do not depend on the running sum: unrolled, they are issued ahead
+        // (the embedding's column blocks merge 125 row-unit partials per element)
         if (isrow) {
+#pragma unroll 8
             for (int cu = 0; cu < d.ncu; ++cu) {
                 const double* rp = d.rowpart + 2 * ((int64_t)cu * d.rows + i);
                 acc = dd_merge(acc, DD{rp[0], rp[1]});
             }
             mean = dd_value(acc) / (double)d.cols;
         } else {
+#pragma unroll 8
             for (int ru = 0; ru < d.nru; ++ru) {
                 const double* cp = d.colpart + 2 * ((int64_t)ru * d.cols + i);
                 acc = dd_merge(acc, DD{cp[0], cp[1]});
