@@ -7,7 +7,7 @@
 //   proj    R = fl32(A Pi) for a tile of 64 channels and all r columns, in
 //           binary64 on the matrix cores (v_mfma_f64_16x16x4f64): A (bf16 or
 //           fp32 gradient, as C x L) and Pi (fp32) are staged through LDS in
-//           slices of 32 inputs and widened to binary64; the products are
+//           slices of 16 inputs and widened to binary64; the products are
 //           exact and the accumulation is binary64, so fl32 of the result is
 //           the exactly rounded value except within ~L ulps of binary64 of an
 //           fp32 midpoint. Also sums g^2 per channel and clears Rt.
@@ -79,21 +79,28 @@ hipError_t apollo_copy_desc(const ApolloDesc* host, int count, ApolloDesc* dev, 
 // ---------------------------------------------------------------- projection
 constexpr int kLK = 16;  // inputs per LDS slice
 
-// One workgroup per tile of 64 channels; wave w computes output columns
-// [64 w, 64 w + 64) of the tile (4 x 4 MFMA tiles of 16 x 16) when 64 w < r.
-// The next slice's global loads are issued into registers before the matrix
-// work on the current slice (software prefetch; one LDS buffer, two barriers
-// per slice). MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16]
-// and B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
-constexpr int kAPer = kApolloTileCh * kLK / 256;  // A values per thread and slice
-constexpr int kBPer = kLK * 256 / 4 / 256;        // Pi float4 per thread and slice at rank 256
+// One workgroup of 8 wavefronts per tile of 64 channels; wave w computes output
+// columns [32 w, 32 w + 32) of the tile (4 x 2 MFMA tiles of 16 x 16, eight
+// binary64 accumulators: 124 VGPRs, 4 waves per SIMD) when 32 w < r. (Four
+// wavefronts of 64 x 64 outputs -- 16 accumulators, 230 VGPRs, 2 waves per SIMD
+// -- ran the projection 14% slower.) The next slice's global loads are issued
+// into registers before the matrix work on the current slice (software
+// prefetch; one LDS buffer, two barriers per slice). MFMA f64 16x16x4 operand
+// layout: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]; result
+// register v of lane l is D[l / 16 + 4 v][l % 16].
+constexpr int kProjWaves = 8;                                     // wavefronts per workgroup
+constexpr int kProjThreads = 64 * kProjWaves;
+constexpr int kProjCW = 256 / kProjWaves;                         // output columns per wavefront
+constexpr int kProjJT = kProjCW / 16;                             // 16-column MFMA tiles per wavefront
+constexpr int kAPer = kApolloTileCh * kLK / kProjThreads;         // A values per thread and slice
+constexpr int kBPer = kLK * 256 / 4 / kProjThreads;               // Pi float4 per thread and slice at rank 256
 
 template <int G>
 __device__ __forceinline__ void proj_fetch(const ApolloDesc& d, int64_t c0, int64_t l0, int r4, bool right, int tid,
                                            float (&ra)[kAPer], float4 (&rb)[kBPer]) {
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
-        const int e = tid + 256 * q;
+        const int e = tid + kProjThreads * q;
         const int c = right ? e / kLK : e % kApolloTileCh;
         const int l = right ? e % kLK : e / kApolloTileCh;
         float x = 0.0f;
@@ -108,7 +115,7 @@ __device__ __forceinline__ void proj_fetch(const ApolloDesc& d, int64_t c0, int6
     }
 #pragma unroll
     for (int q = 0; q < kBPer; ++q) {
-        const int e = tid + 256 * q;
+        const int e = tid + kProjThreads * q;
         const int l = e / r4, k4 = e - l * r4;
         float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         if (e < kLK * r4 && l0 + l < d.L) x = *reinterpret_cast<const float4*>(d.proj + (l0 + l) * (4 * r4) + 4 * k4);
@@ -117,7 +124,8 @@ __device__ __forceinline__ void proj_fetch(const ApolloDesc& d, int64_t c0, int6
 }
 
 template <int G>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void apollo_proj_kernel(const ApolloArgs a) {
+__global__ __launch_bounds__(kProjThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void apollo_proj_kernel(const ApolloArgs a) {
     __shared__ double As[kApolloTileCh][kLK + 1];
     __shared__ __attribute__((aligned(16))) float Bs[kLK][256];
     const int64_t tile = blockIdx.x;
@@ -127,12 +135,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
     const int64_t C = d.C, L = d.L;
     const bool right = d.right != 0;
-    const bool active = 64 * w < r;
-    d4v acc[4][4];
+    const bool active = kProjCW * w < r;
+    d4v acc[4][kProjJT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
+        for (int j = 0; j < kProjJT; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
     double gsum = 0.0;
     float ra[kAPer];
     float4 rb[kBPer];
@@ -140,14 +148,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
     for (int64_t l0 = 0; l0 < L; l0 += kLK) {
 #pragma unroll
         for (int q = 0; q < kAPer; ++q) {
-            const int e = tid + 256 * q;
+            const int e = tid + kProjThreads * q;
             const int c = right ? e / kLK : e % kApolloTileCh;
             const int l = right ? e % kLK : e / kApolloTileCh;
             As[c][l] = (double)ra[q];
         }
 #pragma unroll
         for (int q = 0; q < kBPer; ++q) {
-            const int e = tid + 256 * q;
+            const int e = tid + kProjThreads * q;
             if (e < kLK * r4) {
                 const int l = e / r4, k4 = e - l * r4;
                 *reinterpret_cast<float4*>(&Bs[l][4 * k4]) = rb[q];
@@ -165,15 +173,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
         if (active) {
 #pragma unroll 2
             for (int kk = 0; kk < kLK; kk += 4) {
-                double af[4], bf[4];
+                double af[4], bf[kProjJT];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) af[i] = As[16 * i + (lane & 15)][kk + (lane >> 4)];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) bf[j] = (double)Bs[kk + (lane >> 4)][64 * w + 16 * j + (lane & 15)];
+                for (int j = 0; j < kProjJT; ++j)
+                    bf[j] = (double)Bs[kk + (lane >> 4)][kProjCW * w + 16 * j + (lane & 15)];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
+                    for (int j = 0; j < kProjJT; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
             }
         }
@@ -183,11 +192,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < kProjJT; ++j)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int64_t c = c0 + 16 * i + (lane >> 4) + 4 * v;
-                    const int k = 64 * w + 16 * j + (lane & 15);
+                    const int k = kProjCW * w + 16 * j + (lane & 15);
                     if (c < C) {
                         d.R[c * r + k] = (float)acc[i][j][v];
                         d.Rt[c * r + k] = 0.0f;
@@ -200,9 +209,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void a
 hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_tiles == 0) return hipSuccess;
     if (grad_dtype == G_BF16)
-        hipLaunchKernelGGL(apollo_proj_kernel<G_BF16>, dim3((unsigned)a.total_tiles), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(apollo_proj_kernel<G_BF16>, dim3((unsigned)a.total_tiles), dim3(kProjThreads), 0, s, a);
     else
-        hipLaunchKernelGGL(apollo_proj_kernel<G_F32>, dim3((unsigned)a.total_tiles), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(apollo_proj_kernel<G_F32>, dim3((unsigned)a.total_tiles), dim3(kProjThreads), 0, s, a);
     return hipGetLastError();
 }
 
