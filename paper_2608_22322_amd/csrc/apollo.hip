@@ -216,34 +216,43 @@ hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s
 }
 
 // ------------------------------------------------------------ channel scales
-// One wavefront per channel (4 per workgroup). Rt holds the negated direction
+// A wavefront takes kScaleCh consecutive channels of the list (one tensor's
+// channels are consecutive, so a group may span two tensors), 4 elements per
+// lane with 16-byte loads; each channel's two sums of squares reduce over
+// the wavefront in a fixed butterfly order. Rt holds the negated direction
 // (the AdamW kernel's parameter output from zero); only squares are used.
+constexpr int kScaleCh = 4;
+
 __global__ __launch_bounds__(256) void apollo_scale_kernel(const ApolloArgs a) {
     const int lane = threadIdx.x & 63;
-    const int64_t ch = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (ch >= a.total_chans) return;
-    const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::chan_begin>(a.D, a.nt, ch)];
-    const int64_t c = ch - d.chan_begin;
+    const int64_t ch0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kScaleCh;
     const int r = a.rank;
-    double st = 0.0, sr = 0.0;
-    for (int k = lane; k < r; k += 64) {
-        const double x = (double)d.Rt[c * r + k];
-        const double y = (double)d.R[c * r + k];
-        st += x * x;
-        sr += y * y;
-    }
-    st = wave_sum_d(st);
-    sr = wave_sum_d(sr);
-    if (lane == 0) {
-        const double sc = sqrt(st) / (sqrt(sr) + 1e-8);
-        d.s[c] = sc;
-        d.sg[c] = sc * sc * d.gn2[c];
+    for (int q = 0; q < kScaleCh; ++q) {
+        const int64_t ch = ch0 + q;
+        if (ch >= a.total_chans) return;
+        const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::chan_begin>(a.D, a.nt, ch)];
+        const int64_t c = ch - d.chan_begin;
+        double st = 0.0, sr = 0.0;
+        for (int k = 4 * lane; k < r; k += 256) {
+            const float4 x = *reinterpret_cast<const float4*>(d.Rt + c * r + k);
+            const float4 y = *reinterpret_cast<const float4*>(d.R + c * r + k);
+            st += (double)x.x * x.x + (double)x.y * x.y + (double)x.z * x.z + (double)x.w * x.w;
+            sr += (double)y.x * y.x + (double)y.y * y.y + (double)y.z * y.z + (double)y.w * y.w;
+        }
+        st = wave_sum_d(st);
+        sr = wave_sum_d(sr);
+        if (lane == 0) {
+            const double sc = sqrt(st) / (sqrt(sr) + 1e-8);
+            d.s[c] = sc;
+            d.sg[c] = sc * sc * d.gn2[c];
+        }
     }
 }
 
 hipError_t launch_apollo_scale(const ApolloArgs& a, hipStream_t s) {
     if (a.total_chans == 0) return hipSuccess;
-    hipLaunchKernelGGL(apollo_scale_kernel, dim3((unsigned)((a.total_chans + 3) / 4)), dim3(256), 0, s, a);
+    const int64_t waves = (a.total_chans + kScaleCh - 1) / kScaleCh;
+    hipLaunchKernelGGL(apollo_scale_kernel, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
