@@ -8,6 +8,11 @@ decoding it with al_dequantize and encoding the values with al_quantize.
 File format: one safetensors file. Tensor "t{i}.{role}" holds the codes (or FP32 values),
 "t{i}.{role}.meta" the block metadata; the JSON header metadata holds, per tensor, its name,
 shape and per-role spec, plus the optimizer kind and step.
+
+APOLLO (save_apollo / load_apollo) keeps the projected moments "p{i}.m", "p{i}.v" (+ ".meta") and
+the limiter state "p{i}.norm" of every projected tensor, the full AdamW states "t{i}.m", "t{i}.v" of
+the others, and in the header the rank, codes, refresh gap and seed: the projection itself is not
+stored, it is drawn again from the seeded stream of its refresh period.
 """
 from __future__ import annotations
 
@@ -102,4 +107,80 @@ def migrate(st, role: str, old: Spec, new: Spec, stream=None) -> None:
     setattr(st, role + "_meta", nmeta)
 
 
-__all__ = ["save", "load", "migrate"]
+def _spec_json(ss) -> dict:
+    return {"codec": _CODECS[ss.codec], "block": int(ss.block), "log_floor": float(ss.log_floor)}
+
+
+def save_apollo(path: str, drv, names, step: int) -> None:
+    """Write the state of an apollo.ApolloStep after `step` completed steps."""
+    from safetensors.torch import save_file
+
+    tensors, proj, full = {}, [], []
+    for k, (i, L, pj) in enumerate(drv.proj):
+        _, _, rows, cols, _, m, mm, v, vm, ns = drv.items[k]
+        tensors[f"p{i}.m"] = m.detach().cpu()
+        tensors[f"p{i}.v"] = v.detach().cpu()
+        if mm is not None:
+            tensors[f"p{i}.m.meta"] = mm.detach().cpu()
+        if vm is not None:
+            tensors[f"p{i}.v.meta"] = vm.detach().cpu()
+        tensors[f"p{i}.norm"] = ns.detach().cpu()
+        proj.append({"index": i, "name": names[i], "rows": int(rows), "cols": int(cols)})
+    for i, st in zip(drv.full_idx, drv.full_states):
+        for role in ("m", "v"):
+            tensors[f"t{i}.{role}"] = getattr(st, role).detach().cpu()
+            meta = getattr(st, role + "_meta")
+            if meta is not None:
+                tensors[f"t{i}.{role}.meta"] = meta.detach().cpu()
+        full.append({"index": i, "name": names[i], "rows": int(st.rows), "cols": int(st.cols)})
+    c = drv.cfg
+    header = {"format": "al-apollo-state/1", "step": str(int(step)), "rank": str(int(c.rank)),
+              "gap": str(int(drv.gap)), "seed": str(int(drv.seed)), "m": json.dumps(_spec_json(c.m)),
+              "v": json.dumps(_spec_json(c.v)), "projected": json.dumps(proj), "full": json.dumps(full)}
+    save_file(tensors, path, metadata=header)
+
+
+def load_apollo(path: str, drv, names) -> int:
+    """Copy a saved APOLLO state into an ApolloStep built over the same tensor list (same names, shapes,
+    rank, codes, gap and seed); the buffers are overwritten in place. Returns the saved step; the next
+    step() draws the projection of its refresh period again."""
+    from safetensors import safe_open
+
+    c = drv.cfg
+    with safe_open(path, framework="pt") as f:
+        h = f.metadata()
+        if h.get("format") != "al-apollo-state/1":
+            raise ValueError(f"{path}: not an APOLLO optimizer-state checkpoint")
+        want = {"rank": str(int(c.rank)), "gap": str(int(drv.gap)), "seed": str(int(drv.seed)),
+                "m": json.dumps(_spec_json(c.m)), "v": json.dumps(_spec_json(c.v))}
+        for key, val in want.items():
+            if h[key] != val:
+                raise ValueError(f"{path}: {key} {h[key]} != {val}")
+        proj, full = json.loads(h["projected"]), json.loads(h["full"])
+        if [p["index"] for p in proj] != [i for i, _, _ in drv.proj] or \
+                [p["index"] for p in full] != list(drv.full_idx):
+            raise ValueError(f"{path}: the projected / full tensor sets differ")
+        for p in proj + full:
+            if p["name"] != names[p["index"]]:
+                raise ValueError(f"{path}: tensor {p['index']} is {p['name']}, expected {names[p['index']]}")
+        for k, (i, L, pj) in enumerate(drv.proj):
+            _, _, rows, cols, _, m, mm, v, vm, ns = drv.items[k]
+            if (proj[k]["rows"], proj[k]["cols"]) != (rows, cols):
+                raise ValueError(f"{path}: tensor {i} shape differs")
+            for buf, key in ((m, f"p{i}.m"), (mm, f"p{i}.m.meta"), (v, f"p{i}.v"), (vm, f"p{i}.v.meta"),
+                             (ns, f"p{i}.norm")):
+                if buf is not None:
+                    buf.copy_(f.get_tensor(key).to(buf.device))
+        for k, (i, st) in enumerate(zip(drv.full_idx, drv.full_states)):
+            if (full[k]["rows"], full[k]["cols"]) != (st.rows, st.cols):
+                raise ValueError(f"{path}: tensor {i} shape differs")
+            for role in ("m", "v"):
+                getattr(st, role).copy_(f.get_tensor(f"t{i}.{role}").to(st.param.device))
+                meta = getattr(st, role + "_meta")
+                if meta is not None:
+                    meta.copy_(f.get_tensor(f"t{i}.{role}.meta").to(st.param.device))
+    drv._epoch = None
+    return int(h["step"])
+
+
+__all__ = ["save", "load", "migrate", "save_apollo", "load_apollo"]
