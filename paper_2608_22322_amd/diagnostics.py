@@ -230,4 +230,51 @@ def ema_drift(kind: str, shapes, cfg, steps: int, grad_fn, grads, eps: float = 1
     return {"drift": {k: v.rel() for k, v in drift.items()}, "update_error": upd.rel(eps)}
 
 
-__all__ = ["update_error", "state_error", "ema_drift"]
+def apollo_update_error(tensors, cfg, t: int, eps: float = 1e-30, stream=None) -> float:
+    """E_upd of one APOLLO step (al_apollo_step) over projected tensors.
+
+    tensors: (grad, rows, cols, proj, m, v) per tensor, all device tensors: grad G, the projection
+    (L x rank fp32) and the exact projected moments m, v in FP32 (rank * C elements each). cfg: an
+    APOLLO config with the state codes under test (its FP32 counterpart is derived). Both runs start
+    from zero parameters with the limiter off (it only rescales a tensor's whole update), so the
+    parameters after the step are the two updates -lr g s_c. The inputs are not modified."""
+    import torch
+
+    from . import ApolloCfg, apollo_step, apollo_tensor_array, apollo_workspace_bytes
+
+    device = tensors[0][0].device
+    ref_cfg = ApolloCfg.from_buffer_copy(cfg)
+    ref_cfg.m = StateSpec(FP32, cfg.m.block, cfg.m.log_floor)
+    ref_cfg.v = StateSpec(FP32, cfg.v.block, cfg.v.log_floor)
+    ref_cfg.gamma = 0.0
+    q_cfg = ApolloCfg.from_buffer_copy(cfg)
+    q_cfg.gamma = 0.0
+    ref_items, q_items, keep = [], [], []
+    for g, rows, cols, proj, m, v in tensors:
+        n = rows * cols
+        pr = torch.zeros(max(n, 4), dtype=torch.float32, device=device)
+        pq = torch.zeros(max(n, 4), dtype=torch.float32, device=device)
+        ref_items.append((pr, g, rows, cols, proj, m.clone(), None, v.clone(), None, None))
+        length = m.numel()
+        coded = []
+        for buf, ss in ((m, cfg.m), (v, cfg.v)):
+            if ss.codec == FP32:
+                coded += [buf.clone(), None]
+                continue
+            codes, meta = alloc_state(length, _spec(ss), device)
+            quantize(ss.codec, buf[:length], ss.block, ss.log_floor, codes, meta, stream=stream)
+            coded += [codes, meta]
+        q_items.append((pq, g, rows, cols, proj, coded[0], coded[1], coded[2], coded[3], None))
+        keep.append((pr, pq, n))
+    for items, c in ((ref_items, ref_cfg), (q_items, q_cfg)):
+        arr = apollo_tensor_array(items)
+        nbytes = apollo_workspace_bytes(arr, len(items), c)
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        apollo_step(arr, len(items), c, t, ws, stream)
+    acc = _Norms(device)
+    for pr, pq, n in keep:
+        acc.add(pq[:n], pr[:n], stream=stream)
+    return acc.rel(eps)
+
+
+__all__ = ["update_error", "state_error", "ema_drift", "apollo_update_error"]

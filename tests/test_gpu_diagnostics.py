@@ -226,3 +226,79 @@ def test_ema_drift_factored_matches_oracle(dev):
         for r in ("vr", "vc"):
             assert abs(res["drift"][r] - d_orc[r]) <= 1e-6 * d_orc[r]
         assert abs(res["update_error"] - u_orc) <= (2e-2 if bits == 8 else 0.2) * u_orc
+
+
+def _apollo_case(dev, shapes, rank, seed):
+    """Exact projected moments (plausible magnitudes, some dormant channels), gradients and projections."""
+    import torch
+
+    from oracle import apollo as oap
+
+    out = []
+    for i, (rows, cols) in enumerate(shapes):
+        right, C, L = oap.layout(rows, cols)
+        n = C * rank
+        m = synth.normal_f32(synth.grad_key(seed + i, 1), n, 1e-4)
+        v = np.abs(synth.normal_f32(synth.grad_key(seed + i, 2), n, 1e-6)).astype(np.float32)
+        v[: 3 * rank] = 0.0  # three dormant channels
+        m[v == 0] = 0.0
+        g = synth.normal_f32(synth.grad_key(seed + i, 4), rows * cols, 1e-3)
+        P = synth.proj_matrix(seed + i, 0, L, rank)
+        pad = lambda x: torch.from_numpy(np.concatenate([x.ravel(), np.zeros(8, np.float32)])).to(dev)
+        out.append(dict(rows=rows, cols=cols, m=m, v=v, g=g, P=P, dm=pad(m), dv=pad(v), dg=pad(g), dP=pad(P)))
+    return out
+
+
+def _oracle_apollo_error(case, rank, t, mspec, vspec):
+    from oracle import apollo as oap
+
+    num = den = 0.0
+    for c in case:
+        right, C, L = oap.layout(c["rows"], c["cols"])
+        n = C * rank
+        ur = np.zeros(c["rows"] * c["cols"], np.float32)
+        uq = np.zeros_like(ur)
+        mr, vr = oracle.State(oracle.FP32, n), oracle.State(oracle.FP32, n)
+        mr.codes[:] = c["m"]
+        vr.codes[:] = c["v"]
+        mq = oracle.State(mspec[0], n, mspec[1])
+        vq = oracle.State(vspec[0], n, vspec[1], vspec[2])
+        mq.encode(c["m"])
+        vq.encode(c["v"])
+        prev = np.zeros(1, np.float32)
+        oap.apollo_step(ur, c["g"], c["rows"], c["cols"], c["P"], mr, vr, t, prev, gamma=0.0)
+        oap.apollo_step(uq, c["g"], c["rows"], c["cols"], c["P"], mq, vq, t, prev, gamma=0.0)
+        d = uq.astype(np.float64) - ur.astype(np.float64)
+        num += math.fsum((d * d).tolist())
+        den += math.fsum((ur.astype(np.float64) ** 2).tolist())
+    return math.sqrt(num) / (math.sqrt(den) + 1e-30)
+
+
+def test_apollo_update_error_matches_oracle(dev):
+    import paper_2608_22322_amd as al
+    from paper_2608_22322_amd import diagnostics
+
+    shapes, rank, t = [(96, 40), (40, 200)], 64, 5
+    case = _apollo_case(dev, shapes, rank, 40)
+    items = [(c["dg"], c["rows"], c["cols"], c["dP"], c["dm"], c["dv"]) for c in case]
+    cfg = al.apollo_cfg(rank=rank, grad_bf16=False, m=al.Spec(al.UF8, 256), v=al.Spec(al.AL8, 2048, V_FLOOR))
+    got = diagnostics.apollo_update_error(items, cfg, t)
+    want = _oracle_apollo_error(case, rank, t, (oracle.UF8, 256), (oracle.AL8, 2048, V_FLOOR))
+    log(f"APOLLO E_upd (UF8 + AL8 B2048): GPU {got:.6e}, oracle {want:.6e}")
+    assert want > 1e-5 and math.isclose(got, want, rel_tol=1e-3)
+    # FP32 codes: the two runs are the same computation
+    cfg32 = al.apollo_cfg(rank=rank, grad_bf16=False, m=al.Spec(al.FP32, 256), v=al.Spec(al.FP32, 2048))
+    assert diagnostics.apollo_update_error(items, cfg32, t) == 0.0
+    # states already on code levels: re-encoding is idempotent, the coded run sees the same values
+    lv = []
+    for c in case:
+        n = c["m"].shape[0]
+        mq = oracle.State(oracle.UF8, n, 256)
+        vq = oracle.State(oracle.AL8, n, 2048, V_FLOOR)
+        mq.encode(c["m"])
+        vq.encode(c["v"])
+        lv.append((mq.decode(), vq.decode()))
+    import torch
+    pad = lambda x: torch.from_numpy(np.concatenate([x, np.zeros(8, np.float32)])).to(dev)
+    items_lv = [(c["dg"], c["rows"], c["cols"], c["dP"], pad(m), pad(v)) for c, (m, v) in zip(case, lv)]
+    assert diagnostics.apollo_update_error(items_lv, cfg, t) == 0.0
