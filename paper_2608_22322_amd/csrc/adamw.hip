@@ -15,7 +15,8 @@
 // (256) is one sub-tile and is encoded as soon as that sub-tile's moments are
 // computed; the second moment is held in registers until its block is
 // complete, and a block of whole sub-tiles has its min/max keys reduced as
-// soon as its last sub-tile is done. Per-block scalar work of the second
+// soon as its last sub-tile is done (smaller blocks: reduced over their lane
+// group after every sub-tile and parked in LDS). Per-block scalar work of the second
 // moment (the binary64 divisions and endpoint logarithms of up to 16 blocks)
 // runs once per chunk with one block per lane pair, and the results are
 // broadcast back (readlane for blocks that span whole sub-tiles, ds_bpermute
@@ -48,16 +49,18 @@ template <int MC, int VC, int BV>
 struct Geo {
     static constexpr bool VQ = (VC == AL8 || VC == AL16);
     // elements per chunk: AL8 blocks of 256+ take 2048 (the per-chunk work amortised over twice
-    // the elements); smaller AL8 blocks (their per-sub-tile min/max slots), AL16 (wider codes)
-    // and an fp32 second moment would not fit in 128 registers at 2048 and take max(1024, B_V)
+    // the elements); smaller AL8 blocks, AL16 (wider codes) and an fp32 second moment would
+    // spill at 2048 under 128 registers and take max(1024, B_V)
     static constexpr int C = chunk_elems(VC, BV);
     static constexpr int K = C / kSub;                       // sub-tiles per chunk
     static constexpr int NB = VQ ? C / BV : 1;               // v blocks per chunk
     static constexpr int GL = BV < kSub ? BV / 4 : 64;       // lanes per v block within a sub-tile
     static constexpr int PER = kSub / BV > 0 ? kSub / BV : 1;  // v blocks per sub-tile (BV < 256)
     static constexpr int LEVELS = VQ ? levels_of<VC>() : 1;
-    static constexpr int NSLOT = BV < kSub ? K : NB;         // in-lane min/max slots
+    static constexpr int NSLOT = BV < kSub ? 1 : NB;         // wave-uniform min/max slots (blocks of 256+)
     static constexpr bool LUT = (VC == AL8) && BV >= 512;     // decode through an LDS level table
+    // decode through per-block split tables: 16 + 16 binary64 factors per block
+    static constexpr bool SPLIT = (VC == AL8) && (BV == 128 || BV == 256);
 };
 
 template <bool C_, class A, class B>
@@ -178,7 +181,7 @@ __device__ __forceinline__ float grad_at(const typename Pick<G == G_BF16, uint2,
 
 template <int G, int MC, int VC, int BV, bool FULL>
 __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWDesc& d, int64_t e0, int64_t valid,
-                                              int lane, float* lut) {
+                                              int lane, float* lut, double* stab, uint2* skey) {
     using Q = Geo<MC, VC, BV>;
     constexpr int K = Q::K;
     constexpr int NB = Q::NB;
@@ -227,6 +230,27 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         }
     }
 
+    // Blocks of 128 and 256 elements: a level table would cost one evaluation
+    // per element. Instead, with k = 16 a + b (a, b in 0..15),
+    // 2^(l_min + k step) = 2^(l_min + 16 a step) * 2^(b step): entries [0, 16)
+    // of a block's split table hold the first factor, [16, 32) the second, so a
+    // block costs 32 evaluations and an element one binary64 product (within
+    // about 2.5 binary64 ulps of 2^(l_min + k step), then rounded to fp32).
+    if constexpr (Q::SPLIT) {
+        static_assert(NB * 32 % kWave == 0, "split tables fill whole wavefront passes");
+#pragma unroll
+        for (int i = 0; i < NB * 32 / kWave; ++i) {
+            // entry lane + 64 i belongs to block 2 i (lanes < 32) or 2 i + 1
+            const double st0 = readlane_d(q1, 32 + 2 * i), st1 = readlane_d(q1, 33 + 2 * i);
+            const float l0 = u2f(readlane_u(f2u(om.l), 32 + 2 * i));
+            const float l1 = u2f(readlane_u(f2u(om.l), 33 + 2 * i));
+            const double st = lane < 32 ? st0 : st1;
+            const int j = lane & 31;
+            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
+            stab[lane + kWave * i] = exp2_d(arg, a.cf);
+        }
+    }
+
     // ------------------------------------------------ 2. per sub-tile: decode, moments, parameter, momentum code
     // the new second moment waits in registers for its block's interval
     float vk[K][4];
@@ -259,6 +283,15 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             const float* t = lut + (k * kSub / BV) * 256;
 #pragma unroll
             for (int j = 0; j < 4; ++j) vh[j] = t[(r.v[kk] >> (8 * j)) & 0xFFu];
+        } else if constexpr (Q::SPLIT) {
+            const double* t = stab + ((k * kSub + 4 * lane) / BV) * 32;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
+                const uint32_t kq = q == 0u ? 0u : q - 1u;
+                const float lv = (float)(t[kq >> 4] * t[16 + (kq & 15u)]);
+                vh[j] = q == 0u ? 0.0f : lv;
+            }
         } else if constexpr (VQ) {
             double vstep, vl32;
             if constexpr (BV >= kSub) {
@@ -345,12 +378,18 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                     pmx = 0u;
                 }
             } else {
+                // blocks inside the sub-tile: reduce each GL-lane group now and park
+                // the keys in LDS, slot = block index within the chunk
+                uint32_t tmn = 0xFFFFFFFFu, tmx = 0u;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     vk[k][j] = vn[j];
-                    vmn[k] = OpMin::f(vmn[k], f2u(vn[j]) - 1u);
-                    vmx[k] = OpMax::f(vmx[k], f2u(vn[j]));
+                    tmn = OpMin::f(tmn, f2u(vn[j]) - 1u);
+                    tmx = OpMax::f(tmx, f2u(vn[j]));
                 }
+                tmn = group_reduce<OpMin, Q::GL>(tmn) + 1u;
+                tmx = group_reduce<OpMax, Q::GL>(tmx);
+                if (lane % Q::GL == 0) skey[k * Q::PER + lane / Q::GL] = make_uint2(tmn, tmx);
             }
         } else if constexpr (FULL) {
             st_f4<kNtStore>(reinterpret_cast<float*>(d.v) + e, make_float4(vn[0], vn[1], vn[2], vn[3]));
@@ -361,17 +400,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         }
     }
     if constexpr (VQ) {
-        // -------------------------------------------- 3. second-moment block reductions (blocks
-        // smaller than a sub-tile: GL-lane groups of every sub-tile)
-        if constexpr (BV < kSub) {
-#pragma unroll
-            for (int s = 0; s < Q::NSLOT; ++s) {
-                vmn[s] = group_reduce<OpMin, Q::GL>(vmn[s]) + 1u;
-                vmx[s] = group_reduce<OpMax, Q::GL>(vmx[s]);
-            }
-        }
-
-        // -------------------------------------------- 4. block fits, one block per lane pair
+        // -------------------------------------------- 3. block fits, one block per lane pair
         // lanes 2b, 2b+1 hold block b's min / max key; both compute its interval.
         uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
         const int b = lane >> 1;
@@ -381,16 +410,10 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 kmin = (b == s) ? vmn[s] : kmin;
                 kmax = (b == s) ? vmx[s] : kmax;
             }
-        } else {
-            // block b of the chunk = sub-tile b / PER, lane group b % PER (leader lane (b % PER) * GL)
-            const int src = (b % Q::PER) * Q::GL;
-#pragma unroll
-            for (int k = 0; k < K; ++k) {
-                const uint32_t tmn = (uint32_t)__shfl((int)vmn[k], src);
-                const uint32_t tmx = (uint32_t)__shfl((int)vmx[k], src);
-                kmin = (b / Q::PER == k) ? tmn : kmin;
-                kmax = (b / Q::PER == k) ? tmx : kmax;
-            }
+        } else if (b < NB) {
+            const uint2 kk = skey[b];
+            kmin = kk.x;
+            kmax = kk.y;
         }
         const bool any = kmax != 0u && b < NB;
         const uint32_t key = (lane & 1) ? kmax : kmin;
@@ -465,16 +488,22 @@ void adamw_kernel(const AdamWLaunch a) {
     const int lane = threadIdx.x & 63;
     const int64_t chunk = a.chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
+    constexpr int NS = Geo<MC, VC, BV>::SPLIT ? Geo<MC, VC, BV>::NB * 32 : 1;
+    constexpr int NK = (Geo<MC, VC, BV>::VQ && BV < kSub) ? Geo<MC, VC, BV>::NB : 1;
     __shared__ float lut_all[4][NT];
+    __shared__ double stab_all[4][NS];
+    __shared__ uint2 skey_all[4][NK];
     float* lut = lut_all[threadIdx.x >> 6];
+    double* stab = stab_all[threadIdx.x >> 6];
+    uint2* skey = skey_all[threadIdx.x >> 6];
     if (chunk >= a.total_tiles) return;
     const AdamWDesc& d = a.t[locate(a, chunk)];
     const int64_t e0 = (chunk - d.tile_begin) * C;
     const int64_t valid = d.n - e0;
     if (valid >= C)
-        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut);
+        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut, stab, skey);
     else
-        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut);
+        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut, stab, skey);
 }
 
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }

@@ -37,9 +37,12 @@ constexpr int kDppRowMirror = 0x140;      // lane i -> 15-i within 16
 // ds_swizzle bit mode: and_mask 0x1F, xor_mask 0x10 -> lane ^ 16 within 32
 constexpr int kSwzXor16 = 0x401F;
 
+// Every control word above reads a lane of the same row, so no lane is out of
+// range and bound_ctrl changes nothing; with it set the compiler folds the move
+// into the consuming operation (v_min_u32_dpp etc.), one instruction per step.
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp(uint32_t x) {
-    return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xF, 0xF, false);
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
 }
 
 struct OpMax {
