@@ -274,7 +274,9 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * fp32 log2 of (float)x (the fast code position uses it on mantissas in
  * [1/2, 1)), 1 = the binary64 exp2 used by decoding, 2 = binary64 log2 (block
  * endpoints and near-boundary positions), 3 = binary64 sqrt, 4 = 1/sqrt(x)
- * (factored second-moment reconstruction). x, out: n doubles (device). */
+ * (factored second-moment reconstruction), 5 = x / 127 and 6 = 127 / x by
+ * the division-free sequences of the UF8 code (exact for x a finite fp32
+ * value, x > 0 for 6). x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
 /* Sums of squares behind the relative update error of section 3.2 (Eq.

@@ -343,7 +343,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 #pragma unroll
             for (int j = 1; j < 4; ++j) am = OpMax::f(am, abs_bits(mn[j]));
             am = group_reduce<OpMax, 64>(am);
-            const double rr = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+            const double rr = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
             uint32_t q[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mn[j] * rr) & 0xFFu;

@@ -38,7 +38,7 @@ __device__ __forceinline__ void quantize_tile(const float* __restrict__ x, int64
             for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(xv[k][j]));
         am = group_reduce<OpMax, GL>(am);
         const float s = u2f(am);
-        const double r = am != 0u ? 127.0 / (double)s : 0.0;
+        const double r = am != 0u ? rdiv127((double)s) : 0.0;
         if (leader && blk_live) meta[blk] = s;
 #pragma unroll
         for (int k = 0; k < K; ++k) {

@@ -301,6 +301,34 @@ __device__ __forceinline__ int32_t uf8_encode(float x, double r) {
     return (int32_t)q;
 }
 
+// fl64(x / 127) without a division, for x a finite fp32 value held in
+// binary64. q = fl64(x * R), R = fl64(1/127), is within about an ulp of the
+// quotient; the remainder x - 127 q is a small multiple of ulp(q), so the fma
+// forms it exactly, and one correction step q + rem * R gives the correctly
+// rounded quotient (Markstein's correction; R's significand is not all ones).
+// Scaling x by 2^k scales every step exactly, so the device test over all fp32
+// significands covers every such x.
+__device__ __forceinline__ double div127(double x) {
+    constexpr double R = 1.0 / 127.0;
+    const double q = x * R;
+    const double rem = __builtin_fma(-q, 127.0, x);
+    return __builtin_fma(rem, R, q);
+}
+
+// fl64(127 / x) for x a positive finite fp32 value held in binary64: the
+// hardware reciprocal, two Newton steps, and the same remainder correction
+// as div127 (a third of the instructions of the general binary64 division,
+// whose scaling steps guard ranges an fp32 x never reaches). Checked against
+// the IEEE quotient on the device over all fp32 significands.
+__device__ __forceinline__ double rdiv127(double x) {
+    double r = __builtin_amdgcn_rcp(x);
+    r = __builtin_fma(__builtin_fma(-x, r, 1.0), r, r);
+    r = __builtin_fma(__builtin_fma(-x, r, 1.0), r, r);
+    const double q = 127.0 * r;
+    const double rem = __builtin_fma(-x, q, 127.0);
+    return __builtin_fma(rem, r, q);
+}
+
 // Decode with step = absmax / 127 (binary64): fl32(q * step).
 __device__ __forceinline__ float uf8_decode(int32_t q, double step) { return (float)((double)q * step); }
 

@@ -60,7 +60,7 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
         }
         F4 o;
         if constexpr (C == UF8) {
-            const double step = (double)meta[blk] / 127.0;
+            const double step = div127((double)meta[blk]);
 #pragma unroll
             for (int j = 0; j < 4; ++j) o.v[j] = uf8_decode((int32_t)(int8_t)(uint8_t)q[j], step);
         } else {
@@ -95,6 +95,8 @@ __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __
             case 2: r = log2(v); break;
             case 3: r = sqrt(v); break;
             case 4: r = 1.0 / sqrt(v); break;
+            case 5: r = div127(v); break;
+            case 6: r = rdiv127(v); break;
         }
         out[i] = r;
     }

@@ -120,7 +120,7 @@ __device__ __forceinline__ float vec_decode(int codec, int B, const void* codes,
     if (codec == FP32) return reinterpret_cast<const float*>(codes)[i];
     if (codec == UF8) {
         const int32_t q = reinterpret_cast<const int8_t*>(codes)[i];
-        return uf8_decode(q, (double)meta[i / B] / 127.0);
+        return uf8_decode(q, div127((double)meta[i / B]));
     }
     const uint32_t q = codec == AL16 ? reinterpret_cast<const uint16_t*>(codes)[i]
                                      : reinterpret_cast<const uint8_t*>(codes)[i];
@@ -147,7 +147,7 @@ __device__ void vec_encode(int codec, int B, const float* x, int64_t n, float lo
             uint32_t am = 0u;
             for (int64_t i = s + lane; i < e; i += 64) am = OpMax::f(am, abs_bits(x[i]));
             am = group_reduce<OpMax, 64>(am);
-            const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+            const double r = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
             if (lane == 0) meta[b] = u2f(am);
             for (int64_t i = s + lane; i < s + B; i += 64) {
                 const int32_t q = i < e ? (int32_t)__builtin_rint((double)x[i] * r) : 0;
@@ -238,15 +238,17 @@ struct GRaw<G_F32> {
 
 // Tile width TC = 64: 16 lanes per row, lane rows lr + 4i of a 16-row group;
 // TC = 128: 32 lanes per row, lane rows lr + 2i of an 8-row group.
+// lane_off = lr * cols + 4 lc, the lane's part of every element index (formed
+// once per unit), so each address is a wave-uniform base plus that offset.
 template <int G, bool FULL, int TC = 64>
 __device__ __forceinline__ void load_graw(GRaw<G>& r, const GD& d, int64_t r0, int64_t c0, int nr, int nc,
-                                          int rg, int ct, int lr, int lc, bool vec) {
+                                          int rg, int ct, int lr, int lc, bool vec, int64_t lane_off) {
     constexpr int LS = 256 / TC, TR = 4 * LS;
     const int cc = ct * TC + 4 * lc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int rr = rg * TR + lr + LS * i;
-        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+        const int64_t e = (r0 + rg * TR + LS * i) * d.cols + c0 + ct * TC + lane_off;
         if constexpr (G == G_BF16) {
             const gp<const uint16_t> g = g_as<const uint16_t>(d.g);
             if (FULL || (rr < nr && vec && cc + 4 <= nc)) {
@@ -294,7 +296,7 @@ __device__ __forceinline__ void unpack_graw(const GRaw<G>& r, int i, float gv[4]
 // while the current one is summed.
 template <int G, bool FULL>
 __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t ru, int64_t cu, int nr_, int nc_,
-                                          bool vec_, float (*tile)[68], DD* racc) {
+                                          bool vec_, double (*tile)[66], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 15, lr = lane >> 4, rrow = lane >> 2, rq = lane & 3;
     const int64_t r0 = ru * 256, c0 = cu * 256;
     const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
@@ -307,29 +309,35 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
 #pragma unroll
     for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
     GRaw<G> cur;
-    load_graw<G, FULL>(cur, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    const int64_t lane_off = (int64_t)lr * d.cols + 4 * lc;
+    load_graw<G, FULL>(cur, d, r0, c0, nr, nc, 0, 0, lr, lc, vec, lane_off);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
         GRaw<G> nxt = cur;
         if (it + 1 < total) {
             const int ct1 = (it + 1) / nrg;
-            load_graw<G, FULL>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+            load_graw<G, FULL>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
         }
         const int cc = ct * 64 + 4 * lc;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             float gv[4];
             unpack_graw<G>(cur, i, gv);
+            double t[4] = {0.0, 0.0, 0.0, 0.0};
             if (FULL || rg * kTileRows + lr + 4 * i < nr) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     if (FULL || cc + j < nc) {
                         const double x = (double)gv[j];
-                        dd_add(cacc[j], x * x + eps1);
+                        t[j] = x * x + eps1;
+                        dd_add(cacc[j], t[j]);
                     }
                 }
             }
-            *reinterpret_cast<float4*>(&tile[lr + 4 * i][4 * lc]) = make_float4(gv[0], gv[1], gv[2], gv[3]);
+            // the binary64 terms are staged once for the row sums
+            double* tp = &tile[lr + 4 * i][4 * lc];
+            *reinterpret_cast<double2*>(tp) = make_double2(t[0], t[1]);
+            *reinterpret_cast<double2*>(tp + 2) = make_double2(t[2], t[3]);
         }
         __syncthreads();
         DD rsum{0.0, 0.0};
@@ -338,19 +346,13 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
         if (FULL || (rr < nr && cq < nc)) {
             if (FULL || cq + 16 <= nc) {
 #pragma unroll
-                for (int c = 0; c < 16; c += 4) {
-                    const float4 t = *reinterpret_cast<const float4*>(&tile[rrow][16 * rq + c]);
-                    const double x0 = t.x, x1 = t.y, x2 = t.z, x3 = t.w;
-                    dd_add(rsum, x0 * x0 + eps1);
-                    dd_add(rsum, x1 * x1 + eps1);
-                    dd_add(rsum, x2 * x2 + eps1);
-                    dd_add(rsum, x3 * x3 + eps1);
+                for (int c = 0; c < 16; c += 2) {
+                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
+                    dd_add(rsum, t.x);
+                    dd_add(rsum, t.y);
                 }
             } else {
-                for (int c = 0; c < nc - cq; ++c) {
-                    const double x = tile[rrow][16 * rq + c];
-                    dd_add(rsum, x * x + eps1);
-                }
+                for (int c = 0; c < nc - cq; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
             }
         }
         rsum = dd_merge(rsum, dd_quad_xor<kDppQuadXor1>(rsum));
@@ -389,7 +391,7 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
 // Interior units (256x256, width a multiple of 4) take a guard-free body.
 template <int G>
 __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) float tile[kTileRows][68];
+    __shared__ __attribute__((aligned(16))) double tile[kTileRows][66];
     __shared__ DD racc[256];
     const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
     if (unit >= a.total_units) return;
@@ -829,7 +831,7 @@ __device__ __forceinline__ float came_momentum(const FacArgs& a, const FacDesc& 
     float mh;
     if (a.m_codec == UF8) {
         const int32_t q = reinterpret_cast<const int8_t*>(d.m)[e];
-        mh = uf8_decode(q, (double)d.mm[e / a.m_block] / 127.0);
+        mh = uf8_decode(q, div127((double)d.mm[e / a.m_block]));
     } else {
         mh = reinterpret_cast<const float*>(d.m)[e];
     }
@@ -855,13 +857,14 @@ struct ResRaw {
 
 template <int G, bool FULL>
 __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const GD& d, int64_t r0,
-                                            int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec) {
-    load_graw<G, FULL, kResCols>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec);
+                                            int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec,
+                                            int64_t lane_off) {
+    load_graw<G, FULL, kResCols>(r.g, d, r0, c0, nr, nc, rg, ct, lr, lc, vec, lane_off);
     const int cc = ct * kResCols + 4 * lc;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int rr = rg * kResRows + lr + 2 * i;
-        const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+        const int64_t e = (r0 + rg * kResRows + 2 * i) * d.cols + c0 + ct * kResCols + lane_off;
         r.ri[i] = (FULL || rr < nr) ? d.rfac[r0 + rr] : 0.0;
         r.mw[i] = 0u;
         r.ms[i] = 0.0f;
@@ -869,7 +872,7 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
             if (FULL || (vec && cc + 4 <= nc)) {
                 // e % 4 == 0: the 4 codes are one word of one momentum block
                 r.mw[i] = *g_as<const uint32_t>(g_as<const uint8_t>(d.m) + e);
-                r.ms[i] = d.mm[e / 256];
+                r.ms[i] = d.mm[(uint64_t)e >> 8];
             }
         }
     }
@@ -892,7 +895,8 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
     for (int j = 0; j < 4; ++j) cacc[j] = DD{0.0, 0.0};
     double cf[4] = {0.0, 0.0, 0.0, 0.0};
     ResRaw<G> cur;
-    load_resraw<G, FULL>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec);
+    const int64_t lane_off = (int64_t)lr * d.cols + 4 * lc;
+    load_resraw<G, FULL>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec, lane_off);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
         const int cc = ct * kResCols + 4 * lc;
@@ -903,19 +907,19 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
         ResRaw<G> nxt = cur;
         if (it + 1 < total) {
             const int ct1 = (it + 1) / nrg;
-            load_resraw<G, FULL>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec);
+            load_resraw<G, FULL>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rr = rg * kResRows + lr + 2 * i;
             double term[4] = {0.0, 0.0, 0.0, 0.0};
             if (FULL || rr < nr) {
-                const int64_t e = (r0 + rr) * d.cols + c0 + cc;
+                const int64_t e = (r0 + rg * kResRows + 2 * i) * d.cols + c0 + ct * kResCols + lane_off;
                 float gv[4], mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                 unpack_graw<G>(cur.g, i, gv);
                 if (FULL || (vec && cc + 4 <= nc)) {
                     if (uf8) {
-                        const double st = (double)cur.ms[i] / 127.0;
+                        const double st = div127((double)cur.ms[i]);
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
                             mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(cur.mw[i] >> (8 * j)), st);
@@ -932,7 +936,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                         if (cc + j < nc) {
                             if (uf8)
                                 mh[j] = uf8_decode(g_as<const int8_t>(d.m)[e + j],
-                                                   (double)d.mm[(e + j) / 256] / 127.0);
+                                                   div127((double)d.mm[(e + j) / 256]));
                             else
                                 mh[j] = g_as<const float>(d.m)[e + j];
                         }
@@ -1087,7 +1091,7 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
             float gv[4], mh[4];
             unpack_graw<G>(g, k, gv);
             if constexpr (uf8) {
-                const double st = (double)ms[k] / 127.0;
+                const double st = div127((double)ms[k]);
 #pragma unroll
                 for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[k] >> (8 * j)), st);
             } else {
@@ -1114,7 +1118,7 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
 #pragma unroll
                 for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
                 am = group_reduce<OpMax, 64>(am);
-                const double rs = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+                const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
                 uint32_t q[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * rs) & 0xFFu;
@@ -1178,7 +1182,7 @@ __global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) 
 #pragma unroll
                 for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
                 am = group_reduce<OpMax, 64>(am);
-                const double r = am != 0u ? 127.0 / (double)u2f(am) : 0.0;
+                const double r = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int32_t q = (int32_t)__builtin_rint((double)mnew[j] * r);

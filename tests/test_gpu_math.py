@@ -64,3 +64,29 @@ def test_log2_sqrt_rsqrt():
     assert np.all(np.abs(lg - np.log2(x)) <= ulp)
     assert np.array_equal(_run(3, x), np.sqrt(x))
     assert np.array_equal(_run(4, x), 1.0 / np.sqrt(x))
+
+
+def _fp32_cover():
+    """Every fp32 significand (x in [1, 2)), the same significands at the ends of the fp32 range
+    (subnormals included, as values), and 2^20 random positive finite fp32 bit patterns."""
+    sig = (np.arange(1 << 23, dtype=np.uint32) | np.uint32(0x3F800000)).view(np.float32).astype(np.float64)
+    rng = np.random.default_rng(3)
+    bits = rng.integers(1, 0x7F800000, 1 << 20, dtype=np.uint32)
+    rnd = bits.view(np.float32).astype(np.float64)
+    ends = np.concatenate([sig[::97] * 2.0**-149, sig[::89] * 2.0**-127, sig[::83] * 2.0**127])
+    return np.concatenate([sig, rnd, ends, [2.0**-149, float(np.finfo(np.float32).max)]])
+
+
+def test_uf8_division_free_quotients_are_correctly_rounded():
+    """x / 127 (UF8 decode step) and 127 / x (encode scale) without the binary64 division equal the
+    IEEE quotients bit for bit; scaling x by 2^k scales every step exactly, so the significands of
+    [1, 2) cover every fp32 input (the range ends and random patterns check that)."""
+    require_gpu()
+    x = _fp32_cover()
+    q = _run(5, x)
+    assert np.array_equal(q, x / 127.0), np.count_nonzero(q != x / 127.0)
+    assert np.array_equal(_run(5, -x), -x / 127.0)
+    assert _run(5, np.zeros(1))[0] == 0.0
+    r = _run(6, x)
+    assert np.array_equal(r, 127.0 / x), np.count_nonzero(r != 127.0 / x)
+    log(f"x/127 and 127/x exact over {x.size:,} fp32 inputs")
