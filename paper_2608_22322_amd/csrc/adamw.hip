@@ -181,7 +181,7 @@ __device__ __forceinline__ float grad_at(const typename Pick<G == G_BF16, uint2,
 
 template <int G, int MC, int VC, int BV, bool FULL>
 __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWDesc& d, int64_t e0, int64_t valid,
-                                              int lane, float* lut, double* stab, uint2* skey) {
+                                              int lane, double* lut, double* stab, uint2* skey) {
     using Q = Geo<MC, VC, BV>;
     constexpr int K = Q::K;
     constexpr int NB = Q::NB;
@@ -215,7 +215,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
     // wavefront's LDS slice (4 levels per lane) -- 255 evaluations per block
     // instead of one per element. LDS traffic of one wavefront is ordered, so
     // no barrier is needed between building and reading its own table.
-    // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q.
+    // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q,
+    // kept in binary64 (the fp32 value widened) for the binary64 EMA.
     if constexpr (Q::LUT) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
@@ -225,7 +226,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             for (int i = 0; i < 4; ++i) {
                 const int k = lane + 64 * i;
                 const float lv = (float)exp2_d(l32 + (double)(k - 1) * st, a.cf);
-                lut[b * 256 + k] = k == 0 ? 0.0f : lv;
+                lut[b * 256 + k] = k == 0 ? 0.0 : (double)lv;
             }
         }
     }
@@ -271,6 +272,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, k / R::P);
         }
         float mh[4], vh[4], mn[4], vn[4], pn[4];
+        double vhd[4];  // the decoded second moment, widened for the EMA
         if constexpr (MC == UF8) {
             const double mstep = readlane_d(q1, k);
 #pragma unroll
@@ -280,9 +282,9 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             for (int j = 0; j < 4; ++j) mh[j] = f4_at(r.m[kk], j);
         }
         if constexpr (Q::LUT) {
-            const float* t = lut + (k * kSub / BV) * 256;
+            const double* t = lut + (k * kSub / BV) * 256;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) vh[j] = t[(r.v[kk] >> (8 * j)) & 0xFFu];
+            for (int j = 0; j < 4; ++j) vhd[j] = t[(r.v[kk] >> (8 * j)) & 0xFFu];
         } else if constexpr (Q::SPLIT) {
             const double* t = stab + ((k * kSub + 4 * lane) / BV) * 32;
 #pragma unroll
@@ -320,7 +322,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         for (int j = 0; j < 4; ++j) {
             const double gd = (double)grad_at<G>(r.g[kk], j);
             mn[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * gd);
-            vn[j] = (float)(a.beta2 * (double)vh[j] + a.omb2 * (gd * gd));
+            if constexpr (!Q::LUT) vhd[j] = (double)vh[j];
+            vn[j] = (float)(a.beta2 * vhd[j] + a.omb2 * (gd * gd));
             const float den_p = __builtin_fmaf(__builtin_amdgcn_sqrtf(vn[j]), a.inv_sqrt_bc2, a.eps);
             const float upd = mn[j] * __builtin_amdgcn_rcpf(den_p);
             pn[j] = __builtin_fmaf(-a.step_size, upd, f4_at(r.p[kk], j) * a.decay);
@@ -490,10 +493,10 @@ void adamw_kernel(const AdamWLaunch a) {
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
     constexpr int NS = Geo<MC, VC, BV>::SPLIT ? Geo<MC, VC, BV>::NB * 32 : 1;
     constexpr int NK = (Geo<MC, VC, BV>::VQ && BV < kSub) ? Geo<MC, VC, BV>::NB : 1;
-    __shared__ float lut_all[4][NT];
+    __shared__ double lut_all[4][NT];
     __shared__ double stab_all[4][NS];
     __shared__ uint2 skey_all[4][NK];
-    float* lut = lut_all[threadIdx.x >> 6];
+    double* lut = lut_all[threadIdx.x >> 6];
     double* stab = stab_all[threadIdx.x >> 6];
     uint2* skey = skey_all[threadIdx.x >> 6];
     if (chunk >= a.total_tiles) return;

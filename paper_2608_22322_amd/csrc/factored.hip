@@ -973,12 +973,14 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
         if (FULL || (rr < nr && cq < nc)) {
             const int cnt = nc - cq < 16 ? nc - cq : 16;
             if (FULL || cnt == 16) {
+                DD r2{0.0, 0.0};  // a second chain for the odd columns
 #pragma unroll
                 for (int c = 0; c < 16; c += 2) {
                     const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * re + c]);
                     dd_add(rsum, t.x);
-                    dd_add(rsum, t.y);
+                    dd_add(r2, t.y);
                 }
+                rsum = dd_merge(rsum, r2);
             } else {
                 for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * re + c]);
             }
