@@ -168,31 +168,34 @@ def test_came_ragged_lists(dev, grad_bf16, mc, vc, vb, cc, cb):
 TL_SUBSET = [Shape("k", 256, 2048), Shape("attn_norm", 1, 2048), Shape("down_slab", 96, 5632)]
 
 
-def test_adafactor_50_steps(dev):
+def test_adafactor_100_steps(dev):
+    """Independent 100-step trajectories (the TinyLlama Adafactor configuration's length) on a
+    subset of its shapes: states and parameters compared along the way."""
     import paper_2608_22322_amd as al
 
-    w = Workload("tl-subset", TL_SUBSET, zero_frac=0.0, steps=50)
+    w = Workload("tl-subset", TL_SUBSET, zero_frac=0.0, steps=100)
     pair = FacPair(dev, TL_SUBSET, w, False, _spec(al, "AL8", 256, F1))
     near = 0
-    for t in range(1, 51):
+    for t in range(1, 101):
         pair.step(t)
-        if t in (1, 2, 10, 25, 50):
+        if t in (1, 2, 10, 25, 50, 75, 100):
             near += pair.compare(t, 1e-5 if t == 1 else 1e-4)
-    log(f"Adafactor 50 steps: near-boundary code differences {near}")
+    log(f"Adafactor 100 steps: near-boundary code differences {near}")
 
 
-def test_came_50_steps(dev):
+def test_came_100_steps(dev):
+    """As test_adafactor_100_steps, for the TinyLlama CAME configuration."""
     import paper_2608_22322_amd as al
 
-    w = Workload("tl-subset", TL_SUBSET, zero_frac=0.02, steps=50)
+    w = Workload("tl-subset", TL_SUBSET, zero_frac=0.02, steps=100)
     pair = FacPair(dev, TL_SUBSET, w, True, _spec(al, "AL16", 128, F1), mspec=_spec(al, "UF8", 256, 0.0),
                    cspec=_spec(al, "AL16", 128, F2))
     near = 0
-    for t in range(1, 51):
+    for t in range(1, 101):
         pair.step(t)
-        if t in (1, 2, 10, 25, 50):
+        if t in (1, 2, 10, 25, 50, 75, 100):
             near += pair.compare(t, 1e-5 if t == 1 else 1e-4)
-    log(f"CAME 50 steps: near-boundary code differences {near}")
+    log(f"CAME 100 steps: near-boundary code differences {near}")
 
 
 @pytest.mark.parametrize("came", [False, True])
