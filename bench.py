@@ -326,6 +326,16 @@ def cpu_baseline(shapes, block_v):
                       f"AL8 B_V {block_v} + UF8, single-threaded binary64 C oracle; {secs:.1f} s of CPU time"}
 
 
+PATHS = ("adafactor", "came", "adafactor_7b", "came_7b", "apollo")
+
+
+def time_path(name: str, steps: int, warmup: int):
+    """The other optimizer paths: Adafactor and CAME on the TinyLlama and Llama-7B lists, APOLLO on TinyLlama."""
+    if name == "apollo":
+        return time_apollo(steps, warmup)
+    return time_factored(name.startswith("came"), steps, warmup, llama7b=name.endswith("_7b"))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -335,12 +345,17 @@ def main():
     ap.add_argument("--sweep", default="64,128,256,512,1024,2048", help="B_V values to time ('' for headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paths", action="store_true", help="skip the Adafactor / CAME timings")
+    ap.add_argument("--only-path", choices=PATHS, default=None,
+                    help="time one of the other paths alone and print its record (for profiling; no headline)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: the step needs no collective and every box here has one GPU "
-              f"(asked for --gpus {args.gpus}); a multi-GPU run would shard the tensor list with no exchange in the step.",
+        print(f"bench.py measures one GPU (asked for --gpus {args.gpus}): the optimizer step needs no collective; "
+              f"on several GPUs each would step its own shard of the tensor list with no exchange inside the step.",
               file=sys.stderr)
         sys.exit(2)
+    if args.only_path:
+        print(json.dumps({"path": args.only_path, **time_path(args.only_path, args.steps, args.warmup)}), flush=True)
+        return
 
     import torch
 
@@ -414,14 +429,9 @@ def main():
     }
     if not args.no_paths:
         paths = {}
-        for name, came in (("adafactor", False), ("came", True)):
-            paths[name] = time_factored(came, args.steps, args.warmup)
+        for name in PATHS:
+            paths[name] = time_path(name, args.steps, args.warmup)
             log(name + ": " + json.dumps(paths[name]))
-        for name, came in (("adafactor_7b", False), ("came_7b", True)):
-            paths[name] = time_factored(came, args.steps, args.warmup, llama7b=True)
-            log(name + ": " + json.dumps(paths[name]))
-        paths["apollo"] = time_apollo(args.steps, args.warmup)
-        log("apollo: " + json.dumps(paths["apollo"]))
         out["paths"] = paths
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")

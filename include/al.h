@@ -72,7 +72,7 @@ typedef enum al_status {
     AL_EINVAL = 1,       /* bad argument: NULL, n < 0, bad codec/block/dtype, rows*cols mismatch */
     AL_EALIGN = 2,       /* a device pointer is not 16-byte aligned */
     AL_EWORKSPACE = 3,   /* workspace missing or smaller than the query returned */
-    AL_EUNSUPPORTED = 4, /* a valid combination this build does not implement */
+    AL_EUNSUPPORTED = 4, /* a valid combination the library does not implement */
     AL_EHIP = 5          /* a HIP runtime call or launch failed */
 } al_status;
 

@@ -286,11 +286,18 @@ hipError_t launch_apollo_norm(const ApolloArgs& a, hipStream_t s) {
 }
 
 // ------------------------------------------------------------ parameter update
-constexpr int kUpdRows = 4;
+// One wave per 256 x 256 unit, lane = 4 consecutive columns, rows in batches of
+// kUpdRows with all their loads issued before the stores (non-temporal: p and g
+// are touched once). The row scales s_r / lambda of the unit's 256 rows are
+// divided once per unit (4 per lane) and read back from LDS as broadcasts, so a
+// row costs no binary64 division.
+constexpr int kUpdRows = 16;
 
 template <int G>
 __global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) {
+    __shared__ double srow_all[4][256];
     const int lane = threadIdx.x & 63;
+    double* srow = srow_all[threadIdx.x >> 6];
     const int64_t unit = xcd_order(blockIdx.x, gridDim.x) * 4 +
                          __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
@@ -301,64 +308,72 @@ __global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) 
     const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
     const int nc = (int)(cols - c0 < 256 ? cols - c0 : 256);
     const int c = 4 * lane;
-    if (c >= nc) return;
-    const bool vec = (cols & 3) == 0 && c + 4 <= nc;
     const bool right = d.right != 0;
     const double lam = d.lam[0];
+    const gp<const double> sv = to_g((const double*)d.s);
+    if (right) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int r = lane + 64 * k;
+            srow[r] = r < nr ? sv[r0 + r] / lam : 0.0;
+        }
+    }
+    if (c >= nc) return;
+    const bool vec = (cols & 3) == 0 && c + 4 <= nc;
+    const gp<float> pp = to_g(d.p);
     double sc[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sc[j] = (!right && c + j < nc) ? d.s[c0 + c + j] / lam : 0.0;
+    for (int j = 0; j < 4; ++j) sc[j] = (!right && c + j < nc) ? sv[c0 + c + j] / lam : 0.0;
     for (int rb = 0; rb < nr; rb += kUpdRows) {
-        float pv[kUpdRows][4], gv[kUpdRows][4];
-        double sr[kUpdRows];
+        float4 pv[kUpdRows];
+        float gv[kUpdRows][4];
 #pragma unroll
         for (int k = 0; k < kUpdRows; ++k) {
             const int rr = rb + k < nr ? rb + k : nr - 1;  // rows past the end repeat the last one, unused
             const int64_t e = (r0 + rr) * cols + c0 + c;
-            sr[k] = right ? d.s[r0 + rr] / lam : 0.0;
             if (vec) {
-                const float4 x = *reinterpret_cast<const float4*>(d.p + e);
-                pv[k][0] = x.x;
-                pv[k][1] = x.y;
-                pv[k][2] = x.z;
-                pv[k][3] = x.w;
+                pv[k] = ld_f4<true>(gp<const float>(pp + e));
                 if constexpr (G == G_BF16) {
-                    const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(d.g) + e);
+                    const uint2 w = ld_u2<true>(g_as<const void>(to_g((const uint16_t*)d.g) + e));
                     gv[k][0] = bf16_to_f32(w.x & 0xFFFFu);
                     gv[k][1] = bf16_to_f32(w.x >> 16);
                     gv[k][2] = bf16_to_f32(w.y & 0xFFFFu);
                     gv[k][3] = bf16_to_f32(w.y >> 16);
                 } else {
-                    const float4 y = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(d.g) + e);
+                    const float4 y = ld_f4<true>(to_g((const float*)d.g) + e);
                     gv[k][0] = y.x;
                     gv[k][1] = y.y;
                     gv[k][2] = y.z;
                     gv[k][3] = y.w;
                 }
             } else {
+                float h[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    pv[k][j] = c + j < nc ? d.p[e + j] : 0.0f;
+                    h[j] = c + j < nc ? pp[e + j] : 0.0f;
                     gv[k][j] = c + j < nc ? (float)grad_d<G>(d.g, e + j) : 0.0f;
                 }
+                pv[k] = make_float4(h[0], h[1], h[2], h[3]);
             }
         }
 #pragma unroll
         for (int k = 0; k < kUpdRows; ++k) {
             if (rb + k >= nr) continue;
             const int64_t e = (r0 + rb + k) * cols + c0 + c;
+            const double sr = right ? srow[rb + k] : 0.0;
+            const float pin[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
             float out[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const double upd = (double)gv[k][j] * (right ? sr[k] : sc[j]);
-                out[j] = (float)((double)pv[k][j] * a.decay - a.lr * upd);
+                const double upd = (double)gv[k][j] * (right ? sr : sc[j]);
+                out[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
             }
             if (vec) {
-                *reinterpret_cast<float4*>(d.p + e) = make_float4(out[0], out[1], out[2], out[3]);
+                st_f4<true>(pp + e, make_float4(out[0], out[1], out[2], out[3]));
             } else {
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
-                    if (c + j < nc) d.p[e + j] = out[j];
+                    if (c + j < nc) pp[e + j] = out[j];
             }
         }
     }
