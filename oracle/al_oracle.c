@@ -18,6 +18,14 @@
  *   N4 block min/max/absmax are exact; sums are exact and rounded once to
  *      binary64 (Shewchuk's partials method, as Python's math.fsum).
  *   N5 hyperparameters are binary64; derived scalars are computed here.
+ *
+ * Pin status (the CPU tests hold each function to something other than
+ * itself): the codes to worked examples, invariants and brute force; AdamW
+ * to torch.optim.AdamW; Adafactor to Hugging Face's Adafactor. CAME's
+ * official implementation is not available: the CAME step is pinned only
+ * through closed forms (beta1 = 0, uniform and rank-1 gradients, the
+ * second-moment path at t = 1); multi-step CAME with beta1 > 0 is parity
+ * unpinned beyond them.
  */
 #include "al_oracle.h"
 

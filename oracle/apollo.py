@@ -20,7 +20,10 @@ this repository reads it (each reading is listed with the design notes):
   p   = fl32(p (1 - lr wd) - lr (g s_c / lam))      (s_c / lam formed first, in binary64)
 
 The moments reuse the AdamW oracle (``oracle.adamw_step``), so the codes follow the same
-definitions (section 4). Sums are exact (``oracle.exact_sum``). Only tests, the smoke check and the
+definitions (section 4). APOLLO's own implementation is not available: against it this step is
+parity unpinned; the CPU tests pin it by brute-force projection, an identity projection (then the
+projected direction is torch.optim.AdamW's), the step-1 channel scale and the limiter in closed
+form, and the two projection sides under transposition. Sums are exact (``oracle.exact_sum``). Only tests, the smoke check and the
 benchmark's CPU baseline may import this module; it shares no code with the HIP library.
 """
 from __future__ import annotations
