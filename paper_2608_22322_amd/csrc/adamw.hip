@@ -61,6 +61,8 @@ struct Geo {
     static constexpr bool LUT = (VC == AL8) && BV >= 512;     // decode through an LDS level table
     // decode through per-block split tables: 16 + 16 binary64 factors per block
     static constexpr bool SPLIT = (VC == AL8) && (BV == 128 || BV == 256);
+    // blocks of 64: three factors (4 + 8 + 8 binary64 entries per block)
+    static constexpr bool SPLIT3 = (VC == AL8) && BV == 64;
 };
 
 template <bool C_, class A, class B>
@@ -252,6 +254,25 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         }
     }
 
+    // Blocks of 64: k = 64 a + 8 b + c (a < 4, b, c < 8) and
+    // 2^(l_min + k step) = 2^(l_min + 64 a step) * 2^(8 b step) * 2^(c step):
+    // 20 entries per block ([0, 4) first factor, [4, 12) second, [12, 20)
+    // third), 5 evaluations per lane for the chunk's 16 blocks, and two binary64
+    // products per element (within about 4 binary64 ulps, then rounded to fp32).
+    if constexpr (Q::SPLIT3) {
+        static_assert(NB * 20 % kWave == 0, "three-factor tables fill whole wavefront passes");
+#pragma unroll
+        for (int i = 0; i < NB * 20 / kWave; ++i) {
+            const int e = lane + kWave * i;
+            const int b = e / 20, j = e - 20 * b;
+            const double st = shfl_d(q1, 32 + b);
+            const double l32 = (double)__shfl(om.l, 32 + b);
+            const double arg = j < 4 ? l32 + (double)(64 * j) * st
+                                     : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
+            stab[e] = exp2_d(arg, a.cf);
+        }
+    }
+
     // ------------------------------------------------ 2. per sub-tile: decode, moments, parameter, momentum code
     // the new second moment waits in registers for its block's interval
     float vk[K][4];
@@ -292,6 +313,15 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
                 const uint32_t kq = q == 0u ? 0u : q - 1u;
                 const float lv = (float)(t[kq >> 4] * t[16 + (kq & 15u)]);
+                vh[j] = q == 0u ? 0.0f : lv;
+            }
+        } else if constexpr (Q::SPLIT3) {
+            const double* t = stab + ((k * kSub + 4 * lane) / BV) * 20;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
+                const uint32_t kq = q == 0u ? 0u : q - 1u;
+                const float lv = (float)((t[kq >> 6] * t[4 + ((kq >> 3) & 7u)]) * t[12 + (kq & 7u)]);
                 vh[j] = q == 0u ? 0.0f : lv;
             }
         } else if constexpr (VQ) {
@@ -491,7 +521,7 @@ void adamw_kernel(const AdamWLaunch a) {
     const int lane = threadIdx.x & 63;
     const int64_t chunk = a.chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
-    constexpr int NS = Geo<MC, VC, BV>::SPLIT ? Geo<MC, VC, BV>::NB * 32 : 1;
+    constexpr int NS = Geo<MC, VC, BV>::SPLIT ? Geo<MC, VC, BV>::NB * 32 : Geo<MC, VC, BV>::SPLIT3 ? Geo<MC, VC, BV>::NB * 20 : 1;
     constexpr int NK = (Geo<MC, VC, BV>::VQ && BV < kSub) ? Geo<MC, VC, BV>::NB : 1;
     __shared__ double lut_all[4][NT];
     __shared__ double stab_all[4][NS];
