@@ -211,23 +211,25 @@ __device__ __forceinline__ float div_to_f32(double x, double d, double rd) {
 }
 
 // Four quotients at once, with one (rarely taken) branch for the fallbacks.
+// The per-element conditions are combined as integers (no short-circuit
+// control flow), so the common path is straight-line vector code.
 __device__ __forceinline__ void div4_to_f32(const double x[4], double d, double rd, float out[4]) {
-    bool all = true;
-    bool ok[4];
+    uint32_t bad = 0u;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const double q = x[j] * rd;
         const uint64_t b = __builtin_bit_cast(uint64_t, q);
         const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
         const uint32_t low = (uint32_t)b & 0x1FFFFFFFu;
-        ok[j] = (ex - (1023u - 125u) <= 251u && low - 0x0FFFFFF8u > 16u) || q == 0.0;
+        // fallback: outside the normal fp32 exponent range or near a midpoint, unless q is 0
+        const uint32_t off = (uint32_t)(ex - (1023u - 125u) > 251u) | (uint32_t)(low - 0x0FFFFFF8u <= 16u);
+        bad |= (off & (uint32_t)(q != 0.0)) << j;
         out[j] = (float)q;
-        all = all && ok[j];
     }
-    if (__builtin_expect(!all, 0)) {
+    if (__builtin_expect(bad != 0u, 0)) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            if (!ok[j]) out[j] = (float)(x[j] / d);
+            if ((bad >> j) & 1u) out[j] = (float)(x[j] / d);
     }
 }
 

@@ -860,7 +860,7 @@ struct ResRaw {
     float ms[4];
 };
 
-template <int G, bool FULL>
+template <int G, bool FULL, bool UF>
 __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, const GD& d, int64_t r0,
                                             int64_t c0, int nr, int nc, int rg, int ct, int lr, int lc, bool vec,
                                             int64_t lane_off) {
@@ -873,7 +873,7 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
         r.ri[i] = (FULL || rr < nr) ? d.rfac[r0 + rr] : 0.0;
         r.mw[i] = 0u;
         r.ms[i] = 0.0f;
-        if (a.m_codec == UF8 && (FULL || rr < nr)) {
+        if (UF && (FULL || rr < nr)) {
             if (FULL || (vec && cc + 4 <= nc)) {
                 // e % 4 == 0: the 4 codes are one word of one momentum block
                 r.mw[i] = *g_as<const uint32_t>(g_as<const uint8_t>(d.m) + e);
@@ -883,7 +883,7 @@ __device__ __forceinline__ void load_resraw(ResRaw<G>& r, const FacArgs& a, cons
     }
 }
 
-template <int G, bool FULL>
+template <int G, bool FULL, bool UF>
 __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double clip, int64_t ru, int64_t cu, int nr_,
                                          int nc_, bool vec_, double (*tile)[kResCols + 2], DD* racc) {
     const int lane = threadIdx.x, lc = lane & 31, lr = lane >> 5, rrow = lane >> 3, re = lane & 7;
@@ -891,7 +891,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
     const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
     const bool vec = FULL || vec_;
     const double rclip = 1.0 / clip;
-    const bool uf8 = a.m_codec == UF8;
+    constexpr bool uf8 = UF;
     const int nrg = (nr + kResRows - 1) / kResRows, nct = (nc + kResCols - 1) / kResCols, total = nrg * nct;
 #pragma unroll
     for (int k = 0; k < 4; ++k) racc[lane + 64 * k] = DD{0.0, 0.0};
@@ -901,7 +901,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
     double cf[4] = {0.0, 0.0, 0.0, 0.0};
     ResRaw<G> cur;
     const int64_t lane_off = (int64_t)lr * d.cols + 4 * lc;
-    load_resraw<G, FULL>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec, lane_off);
+    load_resraw<G, FULL, UF>(cur, a, d, r0, c0, nr, nc, 0, 0, lr, lc, vec, lane_off);
     for (int it = 0; it < total; ++it) {
         const int ct = it / nrg, rg = it - ct * nrg;
         const int cc = ct * kResCols + 4 * lc;
@@ -912,7 +912,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
         ResRaw<G> nxt = cur;
         if (it + 1 < total) {
             const int ct1 = (it + 1) / nrg;
-            load_resraw<G, FULL>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
+            load_resraw<G, FULL, UF>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -923,7 +923,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                 float gv[4], mh[4] = {0.0f, 0.0f, 0.0f, 0.0f};
                 unpack_graw<G>(cur.g, i, gv);
                 if (FULL || (vec && cc + 4 <= nc)) {
-                    if (uf8) {
+                    if constexpr (uf8) {
                         const double st = div127((double)cur.ms[i]);
 #pragma unroll
                         for (int j = 0; j < 4; ++j)
@@ -939,7 +939,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         if (cc + j < nc) {
-                            if (uf8)
+                            if constexpr (uf8)
                                 mh[j] = uf8_decode(g_as<const int8_t>(d.m)[e + j],
                                                    div127((double)d.mm[(e + j) / 256]));
                             else
@@ -1018,7 +1018,8 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
     }
 }
 
-template <int G>
+// UF: UF8 momentum codes (else fp32 momentum).
+template <int G, bool UF>
 __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) double tile[kResRows][kResCols + 2];
     __shared__ DD racc[256];
@@ -1031,15 +1032,18 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
     const int nc = (int)(d.cols - cu * 256 < 256 ? d.cols - cu * 256 : 256);
     const bool vec = (d.cols & 3) == 0;
     if (nr == 256 && nc == 256 && vec)
-        res_unit<G, true>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
+        res_unit<G, true, UF>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
     else
-        res_unit<G, false>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
+        res_unit<G, false, UF>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
 }
 
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    return grad_dtype == G_BF16 ? launch_per_unit(came_res_kernel<G_BF16>, a, s)
-                                : launch_per_unit(came_res_kernel<G_F32>, a, s);
+    const bool uf = a.m_codec == UF8;
+    if (grad_dtype == G_BF16)
+        return uf ? launch_per_unit(came_res_kernel<G_BF16, true>, a, s)
+                  : launch_per_unit(came_res_kernel<G_BF16, false>, a, s);
+    return uf ? launch_per_unit(came_res_kernel<G_F32, true>, a, s) : launch_per_unit(came_res_kernel<G_F32, false>, a, s);
 }
 
 // ------------------------------------------------------ CAME apply (2-D)
