@@ -621,8 +621,45 @@ struct GRows {
 // SIMD) run 7% faster than 8-row ones at 4-5 waves per SIMD.
 constexpr int kApplyRows = 16;
 
+// Interior units (256 x 256, width a multiple of 4) take the guard-free body.
+template <int G, bool FULL>
+__device__ __forceinline__ DD rms_unit(const GD& d, int64_t r0, int64_t c0, int nr_, int nc_, int lane) {
+    const int nr = FULL ? 256 : nr_, nc = FULL ? 256 : nc_;
+    const int c = 4 * lane;
+    const bool vec = FULL || ((d.cols & 3) == 0 && c + 4 <= nc);
+    const bool live = FULL || c < nc;
+    double cf[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) cf[j] = (FULL || c + j < nc) ? d.cfac[c0 + c + j] : 0.0;
+    DD acc{0.0, 0.0};
+    for (int r = 0; r < nr; r += kRowBatch) {
+        GRows<G> g;
+        double ri[kRowBatch];
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            const int rr = (FULL || r + k < nr) ? r + k : nr - 1;  // rows past the end repeat the last one, unused
+            ri[k] = d.rfac[r0 + rr];
+            if (live) load_row4<G>(d, (r0 + rr) * d.cols + c0 + c, vec, nc, c, g.h[k / 4], k % 4);
+        }
+#pragma unroll
+        for (int k = 0; k < kRowBatch; ++k) {
+            if (!FULL && (r + k >= nr || !live)) continue;
+            float gv[4];
+            unpack_graw<G>(g.h[k / 4], k % 4, gv);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (FULL || c + j < nc) {
+                    const double uu = (ri[k] * cf[j]) * (double)gv[j];
+                    dd_add(acc, uu * uu);
+                }
+            }
+        }
+    }
+    return acc;
+}
+
 template <int G>
-__global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a, int64_t base) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6))) void fac_rms_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
     const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x) * 4 +
                          __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -633,36 +670,8 @@ __global__ __launch_bounds__(256) void fac_rms_kernel(const FacArgs a, int64_t b
     const int64_t r0 = ru * 256, c0 = cu * 256;
     const int nr = (int)(d.rows - r0 < 256 ? d.rows - r0 : 256);
     const int nc = (int)(d.cols - c0 < 256 ? d.cols - c0 : 256);
-    const int c = 4 * lane;
-    const bool vec = (d.cols & 3) == 0 && c + 4 <= nc;
-    const bool live = c < nc;
-    double cf[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) cf[j] = c + j < nc ? d.cfac[c0 + c + j] : 0.0;
-    DD acc{0.0, 0.0};
-    for (int r = 0; r < nr; r += kRowBatch) {
-        GRows<G> g;
-        double ri[kRowBatch];
-#pragma unroll
-        for (int k = 0; k < kRowBatch; ++k) {
-            const int rr = r + k < nr ? r + k : nr - 1;  // rows past the end repeat the last one, unused
-            ri[k] = d.rfac[r0 + rr];
-            if (live) load_row4<G>(d, (r0 + rr) * d.cols + c0 + c, vec, nc, c, g.h[k / 4], k % 4);
-        }
-#pragma unroll
-        for (int k = 0; k < kRowBatch; ++k) {
-            if (r + k >= nr || !live) continue;
-            float gv[4];
-            unpack_graw<G>(g.h[k / 4], k % 4, gv);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (c + j < nc) {
-                    const double uu = (ri[k] * cf[j]) * (double)gv[j];
-                    dd_add(acc, uu * uu);
-                }
-            }
-        }
-    }
+    DD acc = (nr == 256 && nc == 256 && (d.cols & 3) == 0) ? rms_unit<G, true>(d, r0, c0, nr, nc, lane)
+                                                           : rms_unit<G, false>(d, r0, c0, nr, nc, lane);
     acc = dd_wave_sum(acc);
     if (lane == 0) {
         a.rmspart[2 * unit] = acc.hi;
