@@ -17,8 +17,9 @@
 // Marginal sums. A wavefront owns a 256x256 unit, walked as 16 groups of 16
 // rows x 4 tiles of 64 columns. It loads a 16x64 tile in the natural layout
 // (16 lanes x 4 columns x 4 rows, coalesced row segments), adds each term to
-// in-lane column accumulators, and stages the tile in LDS (4-8 KB per wave,
-// so LDS does not limit occupancy); 4 lanes then sum each tile row out of LDS.
+// in-lane column accumulators, and stages its binary64 terms in LDS (8.4 KB
+// per wave, plus 4 KB of row accumulators: 12 waves per CU); 4 lanes then
+// sum each tile row out of LDS.
 // All sums are double-double and every partial is merged in a fixed order, so
 // the means are the exactly rounded ones.
 #include "al_codec_dev.hpp"
@@ -579,7 +580,7 @@ hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
 // ------------------------------------------------ RMS partials (per unit)
 // Natural layout: lane = 4 consecutive columns of a 256-column segment; the
 // wave walks the unit's rows, kRowBatch rows at a time with all their loads
-// issued before the arithmetic. u_ij = (r_i c_j) g_ij, exactly the reference
+// issued before the arithmetic. u_ij = (r_i c_j) g_ij, exactly the oracle's
 // operation order; u^2 summed double-double. One wave per unit.
 constexpr int kRowBatch = 8;
 
@@ -724,7 +725,7 @@ hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s) {
 }
 
 // --------------------------------------------------- Adafactor apply (2-D)
-// The RMS pass's layout and row batches; p <- p (1 - lr wd) - lr u / clip.
+// The RMS pass's layout in kApplyRows-row batches; p <- p (1 - lr wd) - lr u / clip.
 template <int G>
 __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t base) {
     const int lane = threadIdx.x & 63;
