@@ -276,7 +276,8 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * endpoints and near-boundary positions), 3 = binary64 sqrt, 4 = 1/sqrt(x)
  * (factored second-moment reconstruction), 5 = x / 127 and 6 = 127 / x by
  * the division-free sequences of the UF8 code (exact for x a finite fp32
- * value, x > 0 for 6). x, out: n doubles (device). */
+ * value, x > 0 for 6), 7 = fl32(x / 3) by the multiply-and-check quotient of
+ * the clipped updates. x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
 /* Sums of squares behind the relative update error of section 3.2 (Eq.

@@ -198,38 +198,36 @@ __device__ __forceinline__ uint32_t al_encode_fast(float x, const ALEnc& p) {
 // fl32(x / d) from a precomputed rd = fl64(1 / d). q = fl64(x * rd) lies
 // within 2.5 binary64 ulps of fl64(x / d), so the two round to the same fp32
 // value unless q is that close to an fp32 rounding midpoint (its 29 low
-// mantissa bits near 2^28) or outside the normal fp32 range; those rare
-// cases take the binary64 division.
+// mantissa bits near 2^28) or fl32(q) leaves the normal range (subnormal
+// results round on a coarser grid; FLT_MIN itself may be the rounding of a
+// subnormal-range q); those rare cases take the binary64 division. The
+// conditions combine as lane masks, with no short-circuit branches.
+__device__ __forceinline__ bool quotient_ok(double q, float f) {
+    const uint32_t low = (uint32_t)__builtin_bit_cast(uint64_t, q) & 0x1FFFFFFFu;
+    const bool normal = __builtin_amdgcn_classf(f, 0x108) & (__builtin_fabsf(f) != 0x1p-126f);  // +-normal
+    return (q == 0.0) | (normal & (low - 0x0FFFFFF8u > 16u));
+}
+
 __device__ __forceinline__ float div_to_f32(double x, double d, double rd) {
     const double q = x * rd;
-    const uint64_t b = __builtin_bit_cast(uint64_t, q);
-    const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
-    const uint32_t low = (uint32_t)b & 0x1FFFFFFFu;
-    const bool ok = (ex - (1023u - 125u) <= 251u && low - 0x0FFFFFF8u > 16u) || q == 0.0;
-    if (__builtin_expect(ok, 1)) return (float)q;
+    const float f = (float)q;
+    if (__builtin_expect(quotient_ok(q, f), 1)) return f;
     return (float)(x / d);
 }
 
 // Four quotients at once, with one (rarely taken) branch for the fallbacks.
-// The per-element conditions are combined as integers (no short-circuit
-// control flow), so the common path is straight-line vector code.
 __device__ __forceinline__ void div4_to_f32(const double x[4], double d, double rd, float out[4]) {
-    uint32_t bad = 0u;
+    bool ok[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const double q = x[j] * rd;
-        const uint64_t b = __builtin_bit_cast(uint64_t, q);
-        const uint32_t ex = (uint32_t)(b >> 52) & 0x7FFu;
-        const uint32_t low = (uint32_t)b & 0x1FFFFFFFu;
-        // fallback: outside the normal fp32 exponent range or near a midpoint, unless q is 0
-        const uint32_t off = (uint32_t)(ex - (1023u - 125u) > 251u) | (uint32_t)(low - 0x0FFFFFF8u <= 16u);
-        bad |= (off & (uint32_t)(q != 0.0)) << j;
         out[j] = (float)q;
+        ok[j] = quotient_ok(q, out[j]);
     }
-    if (__builtin_expect(bad != 0u, 0)) {
+    if (__builtin_expect(!(ok[0] & ok[1] & ok[2] & ok[3]), 0)) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            if ((bad >> j) & 1u) out[j] = (float)(x[j] / d);
+            if (!ok[j]) out[j] = (float)(x[j] / d);
     }
 }
 

@@ -97,6 +97,7 @@ __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __
             case 4: r = 1.0 / sqrt(v); break;
             case 5: r = div127(v); break;
             case 6: r = rdiv127(v); break;
+            case 7: r = (double)div_to_f32(v, 3.0, 1.0 / 3.0); break;
         }
         out[i] = r;
     }

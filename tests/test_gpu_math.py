@@ -90,3 +90,24 @@ def test_uf8_division_free_quotients_are_correctly_rounded():
     r = _run(6, x)
     assert np.array_equal(r, 127.0 / x), np.count_nonzero(r != 127.0 / x)
     log(f"x/127 and 127/x exact over {x.size:,} fp32 inputs")
+
+
+def test_clipped_quotient_matches_division():
+    """fl32(x / d) from fl64(x * fl64(1/d)) with the fallback test (the clipped updates of the factored
+    steps) equals (float)(x / d) bit for bit: random magnitudes across the fp32 range (subnormal and
+    overflowing quotients included) and quotients placed on and beside fp32 rounding midpoints."""
+    require_gpu()
+    rng = np.random.default_rng(4)
+    wide = np.exp2(rng.uniform(-160.0, 130.0, 1 << 20)) * rng.choice([-1.0, 1.0], 1 << 20)
+    f = rng.integers(1, 0x7F000000, 1 << 19, dtype=np.uint32).view(np.float32).astype(np.float64)
+    nxt = np.nextafter(f.astype(np.float32), np.float32(np.inf)).astype(np.float64)
+    mid = (f + nxt) / 2.0  # exact in binary64
+    near = np.concatenate([mid * 3.0, np.nextafter(mid * 3.0, np.inf), np.nextafter(mid * 3.0, -np.inf)])
+    sub = np.exp2(rng.uniform(-150.0, -124.0, 1 << 18)) * 3.0
+    x = np.concatenate([wide, near, sub, [0.0, -0.0, 3.0 * 2.0**-126, 3.0 * (2.0**-126 - 2.0**-150)]])
+    got = _run(7, x).astype(np.float32)
+    with np.errstate(over="ignore"):
+        ref = (x / 3.0).astype(np.float32)
+    bad = np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32))
+    log(f"clipped quotient: {x.size:,} inputs, {bad} differences")
+    assert bad == 0
