@@ -8,7 +8,7 @@
 // exact_zero) and the uniform signed momentum code of section 4.3.
 //
 // Work decomposition. A chunk is max(2048, B_V) consecutive elements of one
-// tensor for AL8 blocks of 256+, else max(1024, B_V), owned by one wavefront:
+// tensor for AL8 blocks of 128+, else max(1024, B_V), owned by one wavefront:
 // 4 consecutive elements per lane in each of K = chunk/256 sub-tiles, so every
 // load and store is a coalesced 16/8/4-byte access and every block reduction
 // stays inside the wavefront (DPP, swizzle, readlane). The momentum block
@@ -42,15 +42,16 @@ constexpr bool kNtLoad = AL_ADAMW_NT_LOAD != 0;
 constexpr bool kNtStore = AL_ADAMW_NT_STORE != 0;
 
 __host__ __device__ constexpr int chunk_elems(int vc, int bv) {
-    return vc == FP32 ? 1024 : (vc == AL8 && bv >= kSub) ? (bv > 2048 ? bv : 2048) : (bv > 1024 ? bv : 1024);
+    return vc == FP32 ? 1024 : (vc == AL8 && bv >= 128) ? (bv > 2048 ? bv : 2048) : (bv > 1024 ? bv : 1024);
 }
 
 template <int MC, int VC, int BV>
 struct Geo {
     static constexpr bool VQ = (VC == AL8 || VC == AL16);
-    // elements per chunk: AL8 blocks of 256+ take 2048 (the per-chunk work amortised over twice
-    // the elements); smaller AL8 blocks, AL16 (wider codes) and an fp32 second moment would
-    // spill at 2048 under 128 registers and take max(1024, B_V)
+    // elements per chunk: AL8 blocks of 128+ take 2048 (the per-chunk work amortised over twice
+    // the elements; blocks of 128 then need 138 registers and run 3 waves per SIMD, 1% faster
+    // than 1024-element chunks at 4); blocks of 64 (no gain at 2048), AL16 (wider codes) and an
+    // fp32 second moment take max(1024, B_V)
     static constexpr int C = chunk_elems(VC, BV);
     static constexpr int K = C / kSub;                       // sub-tiles per chunk
     static constexpr int NB = VQ ? C / BV : 1;               // v blocks per chunk
@@ -492,10 +493,10 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 // chunk per wave the step needs about 95-127 registers, and the extra resident
 // waves hide HBM latency behind the per-element decode/encode arithmetic. An
 // fp32 momentum carries 12 more registers per sub-tile and gets 3 (168), or 2
-// with 2048-element AL16 chunks.
+// with 2048-element AL16 chunks; AL8 blocks of 128 in 2048-element chunks get 3.
 template <int MC, int VC, int BV>
 constexpr int adamw_waves_per_eu() {
-    return MC == UF8 ? 4 : (VC == AL16 && Geo<MC, VC, BV>::C >= 2048 ? 2 : 3);
+    return (MC == UF8 && !(VC == AL8 && BV == 128)) ? 4 : (VC == AL16 && Geo<MC, VC, BV>::C >= 2048 ? 2 : 3);
 }
 
 // largest ti with t[ti].tile_begin <= chunk
