@@ -122,7 +122,7 @@ def _adamw_run(dev, shapes, bv, bf16):
     return _snapshot([x for st in states for x in (st.param, st.m, st.m_meta, st.v, st.v_meta)])
 
 
-@pytest.mark.parametrize("bv", [64, 256, 2048])
+@pytest.mark.parametrize("bv", [64, 128, 256, 2048])
 @pytest.mark.parametrize("bf16", [True, False])
 def test_adamw_bounds_and_determinism(dev, bv, bf16):
     shapes = [33, 1000, 2049, 70_001, 3 * 2048]
