@@ -393,3 +393,15 @@ def test_apollo_validation():
     # empty tensors and empty lists enqueue nothing
     _ap_step([_at(rows=0, param=None, grad=None, proj=None, m=None, v=None, m_meta=None, v_meta=None)])
     _ap_step([])
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus 2 exits with status 2 and says why, before touching a GPU."""
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
