@@ -215,20 +215,36 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
 
     // Blocks of 512+ elements: decode through a per-block table of the 255
     // positive levels fl32(2^(l_min + k step)), k = 0..254, built in this
-    // wavefront's LDS slice (4 levels per lane) -- 255 evaluations per block
-    // instead of one per element. LDS traffic of one wavefront is ordered, so
-    // no barrier is needed between building and reading its own table.
+    // wavefront's LDS slice (4 levels per lane) from the block's 16 + 16
+    // split factors below (32 evaluations per block instead of 255; a level is
+    // one binary64 product, within about 2.5 binary64 ulps before the fp32
+    // rounding). LDS traffic of one wavefront is ordered, so no barrier is
+    // needed between building and reading its own tables.
     // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q,
     // kept in binary64 (the fp32 value widened) for the binary64 EMA.
     if constexpr (Q::LUT) {
+        constexpr int NF = NB * 32;  // factor entries of the chunk (32 for one 2048 block)
+#pragma unroll
+        for (int i = 0; i < (NF + kWave - 1) / kWave; ++i) {
+            // entry lane + 64 i belongs to block 2 i (lanes < 32) or 2 i + 1
+            const int b0 = 2 * i, b1 = 2 * i + 1 < NB ? 2 * i + 1 : 2 * i;
+            const double st0 = readlane_d(q1, 32 + b0), st1 = readlane_d(q1, 32 + b1);
+            const float l0 = u2f(readlane_u(f2u(om.l), 32 + b0));
+            const float l1 = u2f(readlane_u(f2u(om.l), 32 + b1));
+            const double st = lane < 32 ? st0 : st1;
+            const int j = lane & 31;
+            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
+            const double v = exp2_d(arg, a.cf);
+            if (lane + kWave * i < NF) stab[lane + kWave * i] = v;
+        }
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            const double st = readlane_d(q1, 32 + b);
-            const double l32 = (double)u2f(readlane_u(f2u(om.l), 32 + b));
+            const double* t = stab + b * 32;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int k = lane + 64 * i;
-                const float lv = (float)exp2_d(l32 + (double)(k - 1) * st, a.cf);
+                const uint32_t kq = k == 0 ? 0u : (uint32_t)(k - 1);
+                const float lv = (float)(t[kq >> 4] * t[16 + (kq & 15u)]);
                 lut[b * 256 + k] = k == 0 ? 0.0 : (double)lv;
             }
         }
@@ -522,7 +538,7 @@ void adamw_kernel(const AdamWLaunch a) {
     const int lane = threadIdx.x & 63;
     const int64_t chunk = a.chunk_base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     constexpr int NT = Geo<MC, VC, BV>::LUT ? Geo<MC, VC, BV>::NB * 256 : 1;
-    constexpr int NS = Geo<MC, VC, BV>::SPLIT ? Geo<MC, VC, BV>::NB * 32 : Geo<MC, VC, BV>::SPLIT3 ? Geo<MC, VC, BV>::NB * 20 : 1;
+    constexpr int NS = (Geo<MC, VC, BV>::SPLIT || Geo<MC, VC, BV>::LUT) ? Geo<MC, VC, BV>::NB * 32 : Geo<MC, VC, BV>::SPLIT3 ? Geo<MC, VC, BV>::NB * 20 : 1;
     constexpr int NK = (Geo<MC, VC, BV>::VQ && BV < kSub) ? Geo<MC, VC, BV>::NB : 1;
     __shared__ double lut_all[4][NT];
     __shared__ double stab_all[4][NS];
