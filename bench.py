@@ -99,11 +99,12 @@ def time_adamw(states, block_v, steps, warmup):
             st.v_meta.zero_()
     cfg = al.adamw_cfg(m=al.Spec(al.UF8, 256), v=al.Spec(al.AL8, block_v, floor))
     arr = al.tensor_array(states)
+    ws = al.workspace(al.adamw_workspace_bytes(states, cfg, arr=arr))
     stream = torch.cuda.current_stream()
     t = 0
     for _ in range(warmup):
         t += 1
-        al.adamw_step(states, cfg, t, stream=stream, arr=arr)
+        al.adamw_step(states, cfg, t, ws, stream=stream, arr=arr)
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
@@ -111,7 +112,7 @@ def time_adamw(states, block_v, steps, warmup):
     for k in range(steps):
         t += 1
         evs[k][0].record(stream)
-        al.adamw_step(states, cfg, t, stream=stream, arr=arr)
+        al.adamw_step(states, cfg, t, ws, stream=stream, arr=arr)
         evs[k][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -372,7 +373,10 @@ def main():
     blocks = [b for b in blocks if b != args.block] + [args.block]  # headline last
     log(f"building Llama-7B list: {len(shapes)} tensors, {n:,} params")
     states = build_states(shapes, dev, min(blocks))  # smallest block: largest metadata
-    launches = math.ceil(len(shapes) / 48)
+    # al_adamw_step runs the whole list in one launch of the step kernel (include/al.h: several only beyond
+    # 2^32 chunks of at least 1024 elements)
+    assert n < 2**32 * 1024
+    launches = 1
     sweep = []
     head = None
     for b in blocks:

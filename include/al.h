@@ -42,8 +42,8 @@
  * read during the call. The library keeps no pointer after a call returns.
  * All device work is enqueued on `stream` (a hipStream_t; NULL = the null
  * stream) in order; calls return without synchronizing. The library never
- * allocates device memory: Adafactor and CAME take a caller workspace whose
- * size the *_workspace_bytes query returns. Calls on distinct streams with
+ * allocates device memory: each step takes a caller workspace whose size the
+ * matching *_workspace_bytes query returns. Calls on distinct streams with
  * distinct buffers may run concurrently; calls that share a workspace or
  * state buffers must be ordered by the caller.
  *
@@ -230,11 +230,25 @@ al_status al_quantize(int32_t codec, const float* x, int64_t n, int32_t block, f
 al_status al_dequantize(int32_t codec, const void* codes, const float* meta, int64_t n,
                         int32_t block, float* out, void* stream);
 
-/* One fused AdamW step over a list of nt tensors (step = the 1-based step
- * count after increment). One pass over HBM: read p, g, m, v (+meta), write
- * p, m, v (+meta). Uses per tensor: param, grad, m, m_meta, v, v_meta. */
-al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg,
-                        int64_t step, void* stream);
+/* Workspace size (bytes) that al_adamw_step needs for this tensor list and
+ * config: the step's tensor descriptor table (64 + 8 bytes per non-empty
+ * tensor, 256-byte aligned parts). 0 for a list with no elements. */
+al_status al_adamw_workspace_bytes(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, size_t* bytes);
+
+/* One fused AdamW step over a list of nt tensors (section 3.1, Eq.
+ * adam_update, with PyTorch AdamW's decoupled weight decay and bias
+ * corrections; codes of section 4). step = the 1-based step count after
+ * increment. One pass over HBM: read p, g, m, v (+meta), write p, m, v
+ * (+meta). Uses per tensor: param, grad, m, m_meta, v, v_meta; the other
+ * slots must be NULL. ws: device workspace of at least
+ * al_adamw_workspace_bytes, 256-byte aligned (AL_EWORKSPACE otherwise); the
+ * call writes the descriptor table there on the stream (small copy kernels)
+ * and runs the whole list in one launch of the step kernel (several for
+ * lists beyond 2^32 chunks of 1024-2048 elements). ws is scratch: its
+ * contents need not survive between calls, and calls that share it must be
+ * ordered on one stream. */
+al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* Workspace size (bytes) that al_adafactor_step / al_came_step need for this
  * tensor list and config. */
@@ -255,7 +269,8 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
                        int64_t step, void* ws, size_t ws_bytes, void* stream);
 
 /* Workspace size (bytes) that al_apollo_step needs for this list and config:
- * per tensor R and Rt (rank * C floats each) and per-channel binary64 sums. */
+ * per tensor R and Rt (rank * C floats each) and per-channel binary64 sums,
+ * and the descriptor tables of the step's launches. */
 al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,
                                     size_t* bytes);
 

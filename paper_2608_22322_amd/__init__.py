@@ -79,7 +79,7 @@ _lib = None
 
 # every symbol include/al.h and include/al_synth.h declare
 EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al_state_bytes", "al_quantize",
-           "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
+           "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
            "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes", "al_apollo_step", "al_diag_math",
            "al_diag_stream", "al_diff_norms", "al_synth_normal")
 
@@ -101,7 +101,9 @@ def lib():
             getattr(L, name).restype = i64
         L.al_quantize.argtypes = [i32, vp, i64, i32, f, vp, vp, vp]
         L.al_dequantize.argtypes = [i32, vp, vp, i64, i32, vp, vp]
-        L.al_adamw_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg), i64, vp]
+        L.al_adamw_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg),
+                                               ctypes.POINTER(sz)]
+        L.al_adamw_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg), i64, vp, sz, vp]
         L.al_adafactor_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdafactorCfg),
                                                    ctypes.POINTER(sz)]
         L.al_came_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(CAMECfg),
@@ -115,7 +117,8 @@ def lib():
         L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
         L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
         L.al_diff_norms.argtypes = [vp, vp, i64, vp, vp]
-        for name in ("al_quantize", "al_dequantize", "al_adamw_step", "al_adafactor_workspace_bytes",
+        for name in ("al_quantize", "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step",
+                     "al_adafactor_workspace_bytes",
                      "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes",
                      "al_apollo_step", "al_diag_math", "al_diag_stream",
                      "al_diff_norms", "al_synth_normal"):
@@ -286,10 +289,30 @@ def came_cfg(lr=1e-4, beta1=0.9, beta2=0.999, beta3=0.9999, eps1=1e-30, eps2=1e-
                    DTYPE_BF16 if grad_bf16 else DTYPE_F32, 0, m.c(), v.c(), conf.c())
 
 
-def adamw_step(states, cfg: AdamWCfg, step: int, stream=None, arr=None) -> None:
-    """One fused AdamW step over a list of ParamState (or a prebuilt tensor_array)."""
+def adamw_workspace_bytes(states, cfg: AdamWCfg, arr=None) -> int:
     arr = arr if arr is not None else tensor_array(states)
-    check(lib().al_adamw_step(arr, len(states), ctypes.byref(cfg), step, _stream(stream)))
+    out = ctypes.c_size_t(0)
+    check(lib().al_adamw_workspace_bytes(arr, len(states), ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def workspace(nbytes: int, device="cuda"):
+    """A device workspace of nbytes (at least 256 so the pointer is never NULL; torch's allocator aligns it to
+    at least 256 bytes)."""
+    import torch
+
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def _ws_args(ws):
+    return (None, 0) if ws is None else (_ptr(ws), ws.numel() * ws.element_size())
+
+
+def adamw_step(states, cfg: AdamWCfg, step: int, ws, stream=None, arr=None) -> None:
+    """One fused AdamW step over a list of ParamState (or a prebuilt tensor_array); ws: a device workspace of
+    at least adamw_workspace_bytes (the step's descriptor table)."""
+    arr = arr if arr is not None else tensor_array(states)
+    check(lib().al_adamw_step(arr, len(states), ctypes.byref(cfg), step, *_ws_args(ws), _stream(stream)))
 
 
 def adafactor_workspace_bytes(states, cfg: AdafactorCfg, arr=None) -> int:
@@ -308,14 +331,12 @@ def came_workspace_bytes(states, cfg: CAMECfg, arr=None) -> int:
 
 def adafactor_step(states, cfg: AdafactorCfg, step: int, ws, stream=None, arr=None) -> None:
     arr = arr if arr is not None else tensor_array(states)
-    check(lib().al_adafactor_step(arr, len(states), ctypes.byref(cfg), step, _ptr(ws),
-                                  0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+    check(lib().al_adafactor_step(arr, len(states), ctypes.byref(cfg), step, *_ws_args(ws), _stream(stream)))
 
 
 def came_step(states, cfg: CAMECfg, step: int, ws, stream=None, arr=None) -> None:
     arr = arr if arr is not None else tensor_array(states)
-    check(lib().al_came_step(arr, len(states), ctypes.byref(cfg), step, _ptr(ws),
-                             0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)))
+    check(lib().al_came_step(arr, len(states), ctypes.byref(cfg), step, *_ws_args(ws), _stream(stream)))
 
 
 # ------------------------------------------------------------------ APOLLO (projected states)
@@ -342,5 +363,4 @@ def apollo_workspace_bytes(arr, nt: int, cfg: ApolloCfg) -> int:
 
 
 def apollo_step(arr, nt: int, cfg: ApolloCfg, step: int, ws, stream=None) -> None:
-    check(lib().al_apollo_step(arr, nt, ctypes.byref(cfg), step, _ptr(ws), 0 if ws is None else ws.numel(),
-                               _stream(stream)))
+    check(lib().al_apollo_step(arr, nt, ctypes.byref(cfg), step, *_ws_args(ws), _stream(stream)))

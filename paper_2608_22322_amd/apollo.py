@@ -65,8 +65,8 @@ class ApolloStep:
     def __init__(self, states, names, cfg=None, gap: int = GAP, seed: int | None = None, device="cuda"):
         import torch
 
-        from . import (Spec, adamw_cfg, alloc_state, apollo_cfg, apollo_tensor_array, apollo_workspace_bytes, synth,
-                       tensor_array)
+        from . import (Spec, adamw_cfg, adamw_workspace_bytes, alloc_state, apollo_cfg, apollo_tensor_array,
+                       apollo_workspace_bytes, synth, tensor_array, workspace)
 
         self.cfg = cfg or apollo_cfg()
         self.gap = gap
@@ -98,6 +98,7 @@ class ApolloStep:
         self.full_cfg = adamw_cfg(lr=self.cfg.lr, beta1=self.cfg.beta1, beta2=self.cfg.beta2, eps=self.cfg.eps,
                                   weight_decay=self.cfg.weight_decay, grad_bf16=self.cfg.grad_dtype == 1,
                                   m=mspec, v=vspec)
+        self.full_ws = workspace(adamw_workspace_bytes(self.full_states, self.full_cfg, arr=self.full_arr), device)
         self._epoch = None
 
     def refresh(self, step: int, stream=None) -> None:
@@ -117,4 +118,4 @@ class ApolloStep:
         self.refresh(t, stream)
         apollo_step(self.arr, len(self.items), self.cfg, t, self.ws, stream)
         if self.full_states:
-            adamw_step(self.full_states, self.full_cfg, t, stream=stream, arr=self.full_arr)
+            adamw_step(self.full_states, self.full_cfg, t, self.full_ws, stream=stream, arr=self.full_arr)

@@ -20,10 +20,10 @@
 // moment (the binary64 divisions and endpoint logarithms of up to 16 blocks)
 // runs once per chunk with one block per lane pair, and the results are
 // broadcast back (readlane for blocks that span whole sub-tiles, ds_bpermute
-// for smaller ones). The grid holds one wave per chunk, and the chunk ->
-// tensor map is a binary search over the descriptor table held in the kernel
-// arguments. Full chunks use non-temporal loads and stores: every byte of the
-// step is touched exactly once.
+// for smaller ones). The grid holds one wave per chunk over the whole tensor
+// list, and the chunk -> tensor map is a binary search over the descriptor
+// table in device memory (one launch per step). Full chunks use non-temporal
+// loads and stores: every byte of the step is touched exactly once.
 #include "al_device.hpp"
 #include "al_internal.hpp"
 
@@ -35,6 +35,11 @@
 #endif
 
 namespace al {
+
+// The decode polynomial's coefficients, in constant memory: scalar loads at the
+// point of use (as kernel arguments they would be held in scalar registers for
+// the whole chunk, next to the descriptor read from the table, and spill).
+__constant__ Exp2Coef kExp2 = AL_EXP2_TAYLOR;
 
 // Every byte the step touches is read once and written once, so the full-chunk
 // path may mark its loads and stores non-temporal (streaming).
@@ -102,8 +107,34 @@ struct OldMeta {
     float l;  // v l_min (lanes 32..)
 };
 
+// A descriptor's streams as global-address-space pointers: the descriptors
+// are read from memory, so the compiler would otherwise treat their pointers
+// as generic and issue flat loads and stores.
+struct DescG {
+    gp<float> p;
+    gp<const uint8_t> g;
+    gp<uint8_t> m;
+    gp<float> ms;
+    gp<uint8_t> v;
+    gp<float> vm;
+    int64_t n;
+};
+
+// The table is read-only during the step, so it is read through the constant
+// address space: its loads are invariant and the compiler may repeat them
+// instead of holding every field in a scalar register for the whole chunk.
+template <class T>
+using cp = __attribute__((address_space(4))) T*;
+
+__device__ __forceinline__ DescG gview(cp<const AdamWDesc> D, int i) {
+    return DescG{to_g(D[i].p), (gp<const uint8_t>)to_g(D[i].g), (gp<uint8_t>)to_g(D[i].m), to_g(D[i].ms),
+                 (gp<uint8_t>)to_g(D[i].v), to_g(D[i].vm), D[i].n};
+}
+
+typedef float f2v __attribute__((ext_vector_type(2)));
+
 template <int G, int MC, int VC, int BV, bool FULL>
-__device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc& d, int64_t e0, int64_t valid,
+__device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const DescG& d, int64_t e0, int64_t valid,
                                          int lane, int ph) {
     using R = Raw<G, MC, VC, BV>;
 #pragma unroll
@@ -113,19 +144,19 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc&
         if constexpr (FULL) {
             r.p[k] = ld_f4<kNtLoad>(d.p + e);
             if constexpr (G == G_BF16)
-                r.g[k] = ld_u2<kNtLoad>(reinterpret_cast<const uint16_t*>(d.g) + e);
+                r.g[k] = ld_u2<kNtLoad>(g_as<const uint16_t>(d.g) + e);
             else
-                r.g[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.g) + e);
+                r.g[k] = ld_f4<kNtLoad>(g_as<const float>(d.g) + e);
             if constexpr (MC == UF8)
-                r.m[k] = ld_u1<kNtLoad>(reinterpret_cast<const uint8_t*>(d.m) + e);
+                r.m[k] = ld_u1<kNtLoad>(g_as<const uint8_t>(d.m) + e);
             else
-                r.m[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.m) + e);
+                r.m[k] = ld_f4<kNtLoad>(g_as<const float>(d.m) + e);
             if constexpr (VC == AL16)
-                r.v[k] = ld_u2<kNtLoad>(reinterpret_cast<const uint16_t*>(d.v) + e);
+                r.v[k] = ld_u2<kNtLoad>(g_as<const uint16_t>(d.v) + e);
             else if constexpr (VC == AL8)
-                r.v[k] = ld_u1<kNtLoad>(reinterpret_cast<const uint8_t*>(d.v) + e);
+                r.v[k] = ld_u1<kNtLoad>(g_as<const uint8_t>(d.v) + e);
             else
-                r.v[k] = ld_f4<kNtLoad>(reinterpret_cast<const float*>(d.v) + e);
+                r.v[k] = ld_f4<kNtLoad>(g_as<const float>(d.v) + e);
         } else {
             float pp[4];
             uint32_t gb[4], mb[4], vb[4];
@@ -134,13 +165,13 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc&
             for (int j = 0; j < 4; ++j) {
                 const bool ok = rel + j < valid;
                 pp[j] = ok ? d.p[e + j] : 0.0f;
-                if constexpr (G == G_BF16) gb[j] = ok ? reinterpret_cast<const uint16_t*>(d.g)[e + j] : 0u;
-                else gf[j] = ok ? reinterpret_cast<const float*>(d.g)[e + j] : 0.0f;
-                if constexpr (MC == UF8) mb[j] = ok ? reinterpret_cast<const uint8_t*>(d.m)[e + j] : 0u;
-                else mf[j] = ok ? reinterpret_cast<const float*>(d.m)[e + j] : 0.0f;
-                if constexpr (VC == AL16) vb[j] = ok ? reinterpret_cast<const uint16_t*>(d.v)[e + j] : 0u;
-                else if constexpr (VC == AL8) vb[j] = ok ? reinterpret_cast<const uint8_t*>(d.v)[e + j] : 0u;
-                else vf[j] = ok ? reinterpret_cast<const float*>(d.v)[e + j] : 0.0f;
+                if constexpr (G == G_BF16) gb[j] = ok ? g_as<const uint16_t>(d.g)[e + j] : 0u;
+                else gf[j] = ok ? g_as<const float>(d.g)[e + j] : 0.0f;
+                if constexpr (MC == UF8) mb[j] = ok ? g_as<const uint8_t>(d.m)[e + j] : 0u;
+                else mf[j] = ok ? g_as<const float>(d.m)[e + j] : 0.0f;
+                if constexpr (VC == AL16) vb[j] = ok ? g_as<const uint16_t>(d.v)[e + j] : 0u;
+                else if constexpr (VC == AL8) vb[j] = ok ? g_as<const uint8_t>(d.v)[e + j] : 0u;
+                else vf[j] = ok ? g_as<const float>(d.v)[e + j] : 0.0f;
             }
             r.p[k] = make_float4(pp[0], pp[1], pp[2], pp[3]);
             if constexpr (G == G_BF16) r.g[k] = make_uint2(gb[0] | (gb[1] << 16), gb[2] | (gb[3] << 16));
@@ -155,7 +186,7 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const AdamWDesc&
 }
 
 template <int MC, int VC, int BV, bool FULL>
-__device__ __forceinline__ OldMeta load_meta(const AdamWDesc& d, int64_t e0, int64_t valid, int lane) {
+__device__ __forceinline__ OldMeta load_meta(const DescG& d, int64_t e0, int64_t valid, int lane) {
     using Q = Geo<MC, VC, BV>;
     OldMeta r;
     r.a = 0.0f;
@@ -166,7 +197,7 @@ __device__ __forceinline__ OldMeta load_meta(const AdamWDesc& d, int64_t e0, int
     if constexpr (Q::VQ) {
         const int b = lane - 32;
         if (b >= 0 && b < Q::NB && (FULL || (int64_t)b * BV < valid)) {
-            const float2 mm = *reinterpret_cast<const float2*>(d.vm + 2 * (e0 / BV + b));
+            const f2v mm = *g_as<const f2v>(d.vm + 2 * (e0 / BV + b));
             r.l = mm.x;
             r.a = mm.y;
         }
@@ -183,7 +214,7 @@ __device__ __forceinline__ float grad_at(const typename Pick<G == G_BF16, uint2,
 }
 
 template <int G, int MC, int VC, int BV, bool FULL>
-__device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWDesc& d, int64_t e0, int64_t valid,
+__device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG& d, int64_t e0, int64_t valid,
                                               int lane, double* lut, double* stab, uint2* skey) {
     using Q = Geo<MC, VC, BV>;
     constexpr int K = Q::K;
@@ -234,7 +265,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             const double st = lane < 32 ? st0 : st1;
             const int j = lane & 31;
             const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
-            const double v = exp2_d(arg, a.cf);
+            const double v = exp2_d(arg, kExp2);
             if (lane + kWave * i < NF) stab[lane + kWave * i] = v;
         }
 #pragma unroll
@@ -267,7 +298,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             const double st = lane < 32 ? st0 : st1;
             const int j = lane & 31;
             const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
-            stab[lane + kWave * i] = exp2_d(arg, a.cf);
+            stab[lane + kWave * i] = exp2_d(arg, kExp2);
         }
     }
 
@@ -286,7 +317,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
             const double l32 = (double)__shfl(om.l, 32 + b);
             const double arg = j < 4 ? l32 + (double)(64 * j) * st
                                      : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
-            stab[e] = exp2_d(arg, a.cf);
+            stab[e] = exp2_d(arg, kExp2);
         }
     }
 
@@ -359,7 +390,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                     q = ((j < 2 ? r.v[kk].x : r.v[kk].y) >> (16 * (j & 1))) & 0xFFFFu;
                 else
                     q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                vh[j] = al_decode_fast(q, vl32, vstep, a.cf);
+                vh[j] = al_decode_fast(q, vl32, vstep, kExp2);
             }
         } else {
 #pragma unroll
@@ -402,11 +433,11 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 if (lane == 0) d.ms[e0 / kSub + k] = u2f(am);
             }
         } else if constexpr (FULL) {
-            st_f4<kNtStore>(reinterpret_cast<float*>(d.m) + e, make_float4(mn[0], mn[1], mn[2], mn[3]));
+            st_f4<kNtStore>(g_as<float>(d.m) + e, make_float4(mn[0], mn[1], mn[2], mn[3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                if (rel + j < valid) reinterpret_cast<float*>(d.m)[e + j] = mn[j];
+                if (rel + j < valid) g_as<float>(d.m)[e + j] = mn[j];
         }
         if constexpr (VQ) {
             // vn >= 0 here, so its bit pattern orders it; bits - 1 sends +0 to
@@ -442,11 +473,11 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
                 if (lane % Q::GL == 0) skey[k * Q::PER + lane / Q::GL] = make_uint2(tmn, tmx);
             }
         } else if constexpr (FULL) {
-            st_f4<kNtStore>(reinterpret_cast<float*>(d.v) + e, make_float4(vn[0], vn[1], vn[2], vn[3]));
+            st_f4<kNtStore>(g_as<float>(d.v) + e, make_float4(vn[0], vn[1], vn[2], vn[3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                if (rel + j < valid) reinterpret_cast<float*>(d.v)[e + j] = vn[j];
+                if (rel + j < valid) g_as<float>(d.v)[e + j] = vn[j];
         }
     }
     if constexpr (VQ) {
@@ -477,8 +508,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const AdamWD
         double dl = l1 - l0;
         dl = dl < 1e-12 ? 1e-12 : dl;
         if ((lane & 1) == 0 && b < NB && (FULL || (int64_t)b * BV < valid)) {
-            const float2 mm = any ? make_float2((float)l0, (float)dl) : make_float2(0.0f, 0.0f);
-            *reinterpret_cast<float2*>(d.vm + 2 * (e0 / BV + b)) = mm;
+            *g_as<f2v>(d.vm + 2 * (e0 / BV + b)) = any ? f2v{(float)l0, (float)dl} : f2v{0.0f, 0.0f};
         }
         const double q2 = any ? (double)LEVELS / dl : 1.0;  // (L - 2) / delta
 
@@ -515,12 +545,13 @@ constexpr int adamw_waves_per_eu() {
     return (MC == UF8 && !(VC == AL8 && BV == 128)) ? 4 : (VC == AL16 && Geo<MC, VC, BV>::C >= 2048 ? 2 : 3);
 }
 
-// largest ti with t[ti].tile_begin <= chunk
-__device__ __forceinline__ int locate(const AdamWLaunch& a, int64_t chunk) {
-    int lo = 0, hi = a.nt - 1;
+// largest ti with tb[ti] <= chunk (tb ascending, tb[0] = 0); wave-uniform, so
+// every probe is a scalar load of the packed offsets (a few cache lines)
+__device__ __forceinline__ int locate(cp<const int64_t> tb, int nt, int64_t chunk) {
+    int lo = 0, hi = nt - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (a.t[mid].tile_begin <= chunk)
+        if (tb[mid] <= chunk)
             lo = mid;
         else
             hi = mid - 1;
@@ -547,8 +578,12 @@ void adamw_kernel(const AdamWLaunch a) {
     double* stab = stab_all[threadIdx.x >> 6];
     uint2* skey = skey_all[threadIdx.x >> 6];
     if (chunk >= a.total_tiles) return;
-    const AdamWDesc& d = a.t[locate(a, chunk)];
-    const int64_t e0 = (chunk - d.tile_begin) * C;
+    // the descriptor's pointers come from memory: mark them global so the
+    // streams use global (not flat) loads and stores
+    const cp<const AdamWDesc> D = (cp<const AdamWDesc>)a.D;
+    const int ti = locate((cp<const int64_t>)a.tb, a.nt, chunk);
+    const DescG d = gview(D, ti);
+    const int64_t e0 = (chunk - D[ti].tile_begin) * C;
     const int64_t valid = d.n - e0;
     if (valid >= C)
         adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut, stab, skey);
@@ -557,6 +592,49 @@ void adamw_kernel(const AdamWLaunch a) {
 }
 
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
+
+// ------------------------------------------------------------ descriptor table
+// Descriptors per copy launch: 60 x 64 bytes keep the argument segment under
+// 4 KB.
+constexpr int kAdamWCopyBatch = 60;
+struct AdamWDescBatch {
+    int32_t count, offset;
+    AdamWDesc d[kAdamWCopyBatch];
+};
+
+__global__ void adamw_desc_copy_kernel(const AdamWDescBatch b, AdamWDesc* dst, int64_t* tb) {
+    constexpr int W = sizeof(AdamWDesc) / 8;
+    const uint64_t* src = reinterpret_cast<const uint64_t*>(b.d);
+    uint64_t* out = reinterpret_cast<uint64_t*>(dst + b.offset);
+    for (int i = threadIdx.x; i < b.count * W; i += blockDim.x) out[i] = src[i];
+    for (int i = threadIdx.x; i < b.count; i += blockDim.x) tb[b.offset + i] = b.d[i].tile_begin;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t adamw_table_bytes(int64_t nt) {
+    return nt <= 0 ? 0 : align256((size_t)nt * sizeof(AdamWDesc)) + align256((size_t)nt * sizeof(int64_t));
+}
+
+hipError_t adamw_write_table(const AdamWDesc* host, int nt, void* table, AdamWLaunch& a, hipStream_t s) {
+    static_assert(sizeof(AdamWDesc) % 8 == 0, "descriptor size");
+    static_assert(sizeof(AdamWDescBatch) <= 4096 - 64, "copy arguments");
+    AdamWDesc* D = static_cast<AdamWDesc*>(table);
+    int64_t* tb = reinterpret_cast<int64_t*>(static_cast<char*>(table) + align256((size_t)nt * sizeof(AdamWDesc)));
+    for (int off = 0; off < nt; off += kAdamWCopyBatch) {
+        AdamWDescBatch b;
+        b.count = nt - off < kAdamWCopyBatch ? nt - off : kAdamWCopyBatch;
+        b.offset = off;
+        for (int i = 0; i < b.count; ++i) b.d[i] = host[off + i];
+        hipLaunchKernelGGL(adamw_desc_copy_kernel, dim3(1), dim3(256), 0, s, b, D, tb);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    a.D = D;
+    a.tb = tb;
+    a.nt = nt;
+    return hipSuccess;
+}
 
 // One wave per chunk: the grid covers every chunk of the launch and the
 // hardware dispatcher refills each CU as its waves retire; each XCD walks a

@@ -291,6 +291,7 @@ struct ApolloPlan {
     std::vector<al::ApolloDesc> desc;
     std::vector<int> idx;  // tensor index of each descriptor (empty tensors are skipped)
     int64_t total_tiles = 0, total_chans = 0, total_units = 0;
+    size_t adamw_off = 0;  // descriptor table of the AdamW launch over the projected moments
     size_t bytes = 0;
 };
 
@@ -356,6 +357,8 @@ al_status apollo_plan(const al_apollo_tensor* ts, int nt, const al_apollo_cfg* c
         d.sg = reinterpret_cast<double*>(take((size_t)d.C * 8));
         d.lam = reinterpret_cast<double*>(take(16));
     }
+    P.adamw_off = off;
+    off += al::adamw_table_bytes((int64_t)P.desc.size());
     P.bytes = P.desc.empty() ? 0 : off;
     return AL_OK;
 }
@@ -439,40 +442,57 @@ al_status al_dequantize(int32_t codec, const void* codes, const float* meta, int
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_dequantize launch");
 }
 
-al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step,
-                        void* stream) {
-    g_err[0] = 0;
-    if (nt < 0) return fail(AL_EINVAL, "al_adamw_step: nt < 0");
-    if (nt > 0 && !tensors) return fail(AL_EINVAL, "al_adamw_step: tensors is NULL");
-    if (!cfg) return fail(AL_EINVAL, "al_adamw_step: cfg is NULL");
-    if (step < 1) return fail(AL_EINVAL, "al_adamw_step: step must be >= 1");
+}  // extern "C"
+
+namespace {
+
+// Validate an AdamW call and build its descriptors (non-empty tensors only)
+// and launch constants. No HIP call.
+al_status adamw_plan(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, const char* who,
+                     std::vector<al::AdamWDesc>& desc, al::AdamWLaunch& a) {
+    if (nt < 0) return fail(AL_EINVAL, "%s: nt < 0", who);
+    if (nt > 0 && !tensors) return fail(AL_EINVAL, "%s: tensors is NULL", who);
+    if (!cfg) return fail(AL_EINVAL, "%s: cfg is NULL", who);
+    if (step < 1) return fail(AL_EINVAL, "%s: step must be >= 1", who);
     if (cfg->grad_dtype != AL_DTYPE_F32 && cfg->grad_dtype != AL_DTYPE_BF16)
-        return fail(AL_EINVAL, "al_adamw_step: grad_dtype %d", cfg->grad_dtype);
+        return fail(AL_EINVAL, "%s: grad_dtype %d", who, cfg->grad_dtype);
     if (!is_fin(cfg->lr) || cfg->lr < 0 || !is_fin(cfg->eps) || cfg->eps < 0 || !is_fin(cfg->weight_decay) ||
         cfg->weight_decay < 0 || !(cfg->beta1 >= 0 && cfg->beta1 < 1) || !(cfg->beta2 >= 0 && cfg->beta2 < 1))
-        return fail(AL_EINVAL, "al_adamw_step: hyperparameters out of range");
+        return fail(AL_EINVAL, "%s: hyperparameters out of range", who);
     al_status st;
     if ((st = check_spec(cfg->m, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_UF8), "m")) != AL_OK) return st;
     if ((st = check_spec(cfg->v, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16), "v")) !=
         AL_OK)
         return st;
     if (cfg->m.codec == AL_CODEC_UF8 && cfg->m.block != 256)
-        return fail(AL_EUNSUPPORTED, "al_adamw_step: UF8 momentum block must be 256 (got %d)", cfg->m.block);
+        return fail(AL_EUNSUPPORTED, "%s: UF8 momentum block must be 256 (got %d)", who, cfg->m.block);
 
-    std::vector<int64_t> ns(nt);
+    desc.clear();
+    std::memset(&a, 0, sizeof(a));
+    const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
     for (int i = 0; i < nt; ++i) {
         const al_tensor& t = tensors[i];
-        if ((st = check_shape(t, i, &ns[i])) != AL_OK) return st;
-        if ((st = check_state(t.m, t.m_meta, cfg->m, ns[i], "m", i)) != AL_OK) return st;
-        if ((st = check_state(t.v, t.v_meta, cfg->v, ns[i], "v", i)) != AL_OK) return st;
+        int64_t n = 0;
+        if ((st = check_shape(t, i, &n)) != AL_OK) return st;
+        if ((st = check_state(t.m, t.m_meta, cfg->m, n, "m", i)) != AL_OK) return st;
+        if ((st = check_state(t.v, t.v_meta, cfg->v, n, "v", i)) != AL_OK) return st;
         if ((st = check_unused(t.vr, t.vr_meta, "vr", i)) != AL_OK) return st;
         if ((st = check_unused(t.vc, t.vc_meta, "vc", i)) != AL_OK) return st;
         if ((st = check_unused(t.cr, t.cr_meta, "cr", i)) != AL_OK) return st;
         if ((st = check_unused(t.cc, t.cc_meta, "cc", i)) != AL_OK) return st;
+        if (n == 0) continue;
+        al::AdamWDesc d;
+        d.p = t.param;
+        d.g = t.grad;
+        d.m = t.m;
+        d.ms = t.m_meta;
+        d.v = t.v;
+        d.vm = t.v_meta;
+        d.n = n;
+        d.tile_begin = a.total_tiles;
+        a.total_tiles += (n + T - 1) / T;
+        desc.push_back(d);
     }
-
-    al::AdamWLaunch a;
-    std::memset(&a, 0, sizeof(a));
     const double bc1 = 1.0 - std::pow(cfg->beta1, (double)step);
     const double bc2 = 1.0 - std::pow(cfg->beta2, (double)step);
     a.beta1 = cfg->beta1;
@@ -484,34 +504,41 @@ al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg
     a.eps = (float)cfg->eps;
     a.decay = (float)(1.0 - cfg->lr * cfg->weight_decay);
     a.v_floor = cfg->v.log_floor;
-    a.cf = al::exp2_coef();
-    const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
-    hipStream_t s = as_stream(stream);
+    return AL_OK;
+}
 
-    auto flush = [&]() -> al_status {
-        if (a.nt == 0) return AL_OK;
-        hipError_t e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, s);
-        a.nt = 0;
-        a.total_tiles = 0;
-        return e == hipSuccess ? AL_OK : hip_fail(e, "al_adamw_step launch");
-    };
-    for (int i = 0; i < nt; ++i) {
-        if (ns[i] == 0) continue;
-        const al_tensor& t = tensors[i];
-        al::AdamWDesc& d = a.t[a.nt++];
-        d.p = t.param;
-        d.g = t.grad;
-        d.m = t.m;
-        d.ms = t.m_meta;
-        d.v = t.v;
-        d.vm = t.v_meta;
-        d.n = ns[i];
-        d.tile_begin = a.total_tiles;
-        a.total_tiles += (ns[i] + T - 1) / T;
-        if (a.nt == al::kAdamWMaxTensors)
-            if ((st = flush()) != AL_OK) return st;
-    }
-    return flush();
+}  // namespace
+
+extern "C" {
+
+al_status al_adamw_workspace_bytes(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, size_t* bytes) {
+    g_err[0] = 0;
+    if (!bytes) return fail(AL_EINVAL, "al_adamw_workspace_bytes: bytes is NULL");
+    *bytes = 0;
+    std::vector<al::AdamWDesc> desc;
+    al::AdamWLaunch a;
+    const al_status st = adamw_plan(tensors, nt, cfg, 1, "al_adamw_workspace_bytes", desc, a);
+    if (st != AL_OK) return st;
+    *bytes = al::adamw_table_bytes((int64_t)desc.size());
+    return AL_OK;
+}
+
+al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, void* ws,
+                        size_t ws_bytes, void* stream) {
+    g_err[0] = 0;
+    std::vector<al::AdamWDesc> desc;
+    al::AdamWLaunch a;
+    al_status st = adamw_plan(tensors, nt, cfg, step, "al_adamw_step", desc, a);
+    if (st != AL_OK) return st;
+    if (desc.empty()) return AL_OK;
+    if ((st = check_ws(ws, ws_bytes, al::adamw_table_bytes((int64_t)desc.size()), "al_adamw_step")) != AL_OK)
+        return st;
+    hipStream_t s = as_stream(stream);
+    hipError_t e;
+    if ((e = al::adamw_write_table(desc.data(), (int)desc.size(), ws, a, s)) != hipSuccess ||
+        (e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
+        return hip_fail(e, "al_adamw_step launch");
+    return AL_OK;
 }
 
 al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,
@@ -566,18 +593,12 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
     w.eps = (float)cfg->eps;
     w.decay = 1.0f;
     w.v_floor = cfg->v.log_floor;
-    w.cf = al::exp2_coef();
     const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
-
-    hipStream_t s = as_stream(stream);
-    hipError_t e;
-    if ((e = al::apollo_copy_desc(P.desc.data(), a.nt, const_cast<al::ApolloDesc*>(a.D), s)) != hipSuccess ||
-        (e = al::launch_apollo_proj(a, cfg->grad_dtype, s)) != hipSuccess)
-        return hip_fail(e, "al_apollo_step launch");
+    std::vector<al::AdamWDesc> wd(P.desc.size());
     for (size_t k = 0; k < P.desc.size(); ++k) {
         const al::ApolloDesc& d = P.desc[k];
         const al_apollo_tensor& t = tensors[P.idx[k]];
-        al::AdamWDesc& x = w.t[w.nt++];
+        al::AdamWDesc& x = wd[k];
         x.p = d.Rt;
         x.g = d.R;
         x.m = t.m;
@@ -587,13 +608,16 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
         x.n = d.C * cfg->rank;
         x.tile_begin = w.total_tiles;
         w.total_tiles += (x.n + T - 1) / T;
-        if (w.nt == al::kAdamWMaxTensors || k + 1 == P.desc.size()) {
-            if ((e = al::launch_adamw(w, AL_DTYPE_F32, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
-                return hip_fail(e, "al_apollo_step launch");
-            w.nt = 0;
-            w.total_tiles = 0;
-        }
     }
+
+    hipStream_t s = as_stream(stream);
+    hipError_t e;
+    if ((e = al::apollo_copy_desc(P.desc.data(), a.nt, const_cast<al::ApolloDesc*>(a.D), s)) != hipSuccess ||
+        (e = al::launch_apollo_proj(a, cfg->grad_dtype, s)) != hipSuccess ||
+        (e = al::adamw_write_table(wd.data(), (int)wd.size(), static_cast<char*>(ws) + P.adamw_off, w, s)) !=
+            hipSuccess ||
+        (e = al::launch_adamw(w, AL_DTYPE_F32, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
+        return hip_fail(e, "al_apollo_step launch");
     if ((e = al::launch_apollo_scale(a, s)) != hipSuccess || (e = al::launch_apollo_norm(a, s)) != hipSuccess ||
         (e = al::launch_apollo_update(a, cfg->grad_dtype, s)) != hipSuccess)
         return hip_fail(e, "al_apollo_step launch");

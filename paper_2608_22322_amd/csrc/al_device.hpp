@@ -124,13 +124,24 @@ __device__ __forceinline__ float al_decode(uint32_t q, double lmin32, double ste
 // (ln 2)^k / k!, rounded to binary64); relative error <= 1.4e-16 over the
 // range, i.e. about one ulp, so fl32 of it equals fl32 of a faithfully
 // rounded exp2 except within ~1e-16 of an fp32 rounding midpoint.
-// The coefficients travel in the kernel arguments, so they are read with
-// scalar loads and each Horner step is one v_fma_f64 with a scalar-register
-// addend (there are no 64-bit literal operands on this ISA; as immediates the
-// compiler keeps them in vector registers and copies one per step).
+// The coefficients travel in the kernel arguments or in constant memory, so
+// they are read with scalar loads and each Horner step is one v_fma_f64 with a
+// scalar-register addend (there are no 64-bit literal operands on this ISA; as
+// immediates the compiler keeps them in vector registers and copies one per
+// step).
 struct Exp2Coef {
     double c[14];  // (ln 2)^k / k!, k = 0..13, rounded to binary64
 };
+
+// (ln 2)^k / k!, k = 0..13, rounded to binary64: the Taylor coefficients of
+// 2^f = e^(f ln 2).
+#define AL_EXP2_TAYLOR                                                                                      \
+    {                                                                                                       \
+        {1.0, 0x1.62e42fefa39efp-1, 0x1.ebfbdff82c58fp-3, 0x1.c6b08d704a0c0p-5, 0x1.3b2ab6fba4e77p-7,         \
+         0x1.5d87fe78a6731p-10, 0x1.430912f86c787p-13, 0x1.ffcbfc588b0c7p-17, 0x1.62c0223a5c824p-20,          \
+         0x1.b5253d395e7c4p-24, 0x1.e4cf5158b8ecap-28, 0x1.e8cac7351bb25p-32, 0x1.c3bd650fc2986p-36,          \
+         0x1.816193166d0f9p-40}                                                                             \
+    }
 
 __device__ __forceinline__ double exp2_d(double E, const Exp2Coef& cf) {
     const double n = __builtin_rint(E);
@@ -531,6 +542,27 @@ __device__ __forceinline__ void store_codes4(void* c, int64_t e, const uint32_t 
     } else {
         uint2 w = make_uint2((q[0] & 0xFFFFu) | (q[1] << 16), (q[2] & 0xFFFFu) | (q[3] << 16));
         st_u2<NT>(reinterpret_cast<uint16_t*>(c) + e, w);
+    }
+}
+
+template <bool NT>
+__device__ __forceinline__ void st_u2(gp<void> p, const uint2& x) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(nt_u2{x.x, x.y}, g_as<nt_u2>(p));
+    else
+        *g_as<nt_u2>(p) = nt_u2{x.x, x.y};
+}
+
+// Four codes of element e onward into a global code array (bytes for AL8/UF8,
+// 16-bit words for AL16).
+template <int C, bool NT = false>
+__device__ __forceinline__ void store_codes4(gp<uint8_t> c, int64_t e, const uint32_t q[4]) {
+    if constexpr (C == AL8 || C == UF8) {
+        uint32_t w = (q[0] & 0xFFu) | ((q[1] & 0xFFu) << 8) | ((q[2] & 0xFFu) << 16) | (q[3] << 24);
+        st_u1<NT>(c + e, w);
+    } else {
+        uint2 w = make_uint2((q[0] & 0xFFFFu) | (q[1] << 16), (q[2] & 0xFFFFu) | (q[3] << 16));
+        st_u2<NT>(g_as<uint16_t>(c) + e, w);
     }
 }
 

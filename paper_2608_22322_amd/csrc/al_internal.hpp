@@ -10,10 +10,9 @@
 namespace al {
 
 // ------------------------------------------------------------------ AdamW
-// A launch covers up to kAdamWMaxTensors tensors; their descriptors travel
-// in the kernel-argument segment, so a step needs no device-side table.
-constexpr int kAdamWMaxTensors = 48;
-
+// One launch covers the whole tensor list: the descriptors live in device
+// memory (the caller's workspace), written there on the stream by a copy
+// kernel that carries up to kAdamWCopyBatch of them in its arguments.
 struct AdamWDesc {
     float* p;
     const void* g;
@@ -22,7 +21,7 @@ struct AdamWDesc {
     void* v;
     float* vm;  // AL {l_min, delta} per block (unused for FP32 v)
     int64_t n;
-    int64_t tile_begin;  // first tile of this tensor within the launch
+    int64_t tile_begin;  // first chunk of this tensor within the launch
 };
 
 struct AdamWLaunch {
@@ -32,12 +31,19 @@ struct AdamWLaunch {
     float eps;
     float decay;                      // 1 - lr * weight_decay
     float v_floor;                    // l_floor of the second-moment code
-    Exp2Coef cf;                      // decode polynomial
+    const AdamWDesc* D;               // nt descriptors, ascending tile_begin (device memory)
+    const int64_t* tb;                // D[i].tile_begin again, packed (the chunk -> tensor search)
     int32_t nt;
     int64_t total_tiles;
     int64_t chunk_base;  // first chunk of this launch (one wave per chunk)
-    AdamWDesc t[kAdamWMaxTensors];
 };
+
+// Device bytes of the descriptor table of nt tensors (descriptors, then the
+// packed chunk offsets), each part 256-byte aligned.
+size_t adamw_table_bytes(int64_t nt);
+// Write nt descriptors (host array) into a table at `table` on the stream and
+// point a.D / a.tb at it.
+hipError_t adamw_write_table(const AdamWDesc* host, int nt, void* table, AdamWLaunch& a, hipStream_t s);
 
 // Elements per tile: max(block of v, 256).
 int adamw_tile_elems(int v_codec, int v_block);

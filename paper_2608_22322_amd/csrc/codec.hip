@@ -13,12 +13,7 @@
 namespace al {
 
 const Exp2Coef& exp2_coef() {
-    // (ln 2)^k / k!, the Taylor coefficients of 2^f = e^(f ln 2), in binary64
-    static const Exp2Coef c = {{1.0, 0x1.62e42fefa39efp-1, 0x1.ebfbdff82c58fp-3, 0x1.c6b08d704a0c0p-5,
-                                0x1.3b2ab6fba4e77p-7, 0x1.5d87fe78a6731p-10, 0x1.430912f86c787p-13,
-                                0x1.ffcbfc588b0c7p-17, 0x1.62c0223a5c824p-20, 0x1.b5253d395e7c4p-24,
-                                0x1.e4cf5158b8ecap-28, 0x1.e8cac7351bb25p-32, 0x1.c3bd650fc2986p-36,
-                                0x1.816193166d0f9p-40}};
+    static const Exp2Coef c = AL_EXP2_TAYLOR;
     return c;
 }
 

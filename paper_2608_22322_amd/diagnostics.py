@@ -18,7 +18,7 @@ from __future__ import annotations
 import math
 
 from . import (FP32, ParamState, Spec, StateSpec, adafactor_step, adafactor_workspace_bytes, adamw_step,
-               alloc_state, came_step, came_workspace_bytes, dequantize, diff_norms, DIFF_NORMS_OUT, quantize,
+               adamw_workspace_bytes,               alloc_state, came_step, came_workspace_bytes, dequantize, diff_norms, DIFF_NORMS_OUT, quantize,
                tensor_array)
 
 ROLES = ("m", "v", "vr", "vc", "cr", "cc")
@@ -66,15 +66,14 @@ class _Stepper:
 
         self.kind, self.states = kind, states
         self.arr = tensor_array(states)
-        self.ws = None
-        if kind != "adamw":
-            fn = adafactor_workspace_bytes if kind == "adafactor" else came_workspace_bytes
-            nbytes = max(fn(states, c, arr=self.arr) for c in cfgs)
-            self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        fn = {"adamw": adamw_workspace_bytes, "adafactor": adafactor_workspace_bytes,
+              "came": came_workspace_bytes}[kind]
+        nbytes = max(fn(states, c, arr=self.arr) for c in cfgs)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
     def __call__(self, cfg, t: int, stream=None) -> None:
         if self.kind == "adamw":
-            adamw_step(self.states, cfg, t, stream=stream, arr=self.arr)
+            adamw_step(self.states, cfg, t, self.ws, stream=stream, arr=self.arr)
         elif self.kind == "adafactor":
             adafactor_step(self.states, cfg, t, self.ws, stream=stream, arr=self.arr)
         else:

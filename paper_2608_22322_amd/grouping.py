@@ -11,7 +11,7 @@ from __future__ import annotations
 from dataclasses import dataclass
 
 from . import (AL8, AL16, FP32, UF8, Spec, StateSpec, adafactor_step, adafactor_workspace_bytes, adamw_step,
-               alloc_state, came_step, came_workspace_bytes, state_bytes, tensor_array)
+               adamw_workspace_bytes, alloc_state, came_step, came_workspace_bytes, state_bytes, tensor_array)
 
 POLICIES = ("G0", "G1")
 
@@ -74,11 +74,9 @@ class GroupedStep:
             sts = [states[i] for i in idx]
             gcfg = _with_fp32_states(kind, cfg) if prot else cfg
             arr = tensor_array(sts)
-            ws = None
-            if kind != "adamw":
-                nbytes = (adafactor_workspace_bytes if kind == "adafactor" else came_workspace_bytes)(sts, gcfg,
-                                                                                                     arr=arr)
-                ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
+            fn = {"adamw": adamw_workspace_bytes, "adafactor": adafactor_workspace_bytes,
+                  "came": came_workspace_bytes}[kind]
+            ws = torch.empty(max(fn(sts, gcfg, arr=arr), 256), dtype=torch.uint8, device=device or "cuda")
             self.groups.append(_Group(idx, arr, gcfg, ws))
         self.states = states
 
@@ -86,7 +84,7 @@ class GroupedStep:
         for g in self.groups:
             sts = [self.states[i] for i in g.idx]
             if self.kind == "adamw":
-                adamw_step(sts, g.cfg, t, stream=stream, arr=g.arr)
+                adamw_step(sts, g.cfg, t, g.ws, stream=stream, arr=g.arr)
             elif self.kind == "adafactor":
                 adafactor_step(sts, g.cfg, t, g.ws, stream=stream, arr=g.arr)
             else:

@@ -29,6 +29,8 @@ multiply, so host and device agree bit for bit):
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -93,16 +95,27 @@ def _indices(n_or_idx) -> np.ndarray:
     return np.asarray(n_or_idx, dtype=np.uint64)
 
 
+def _threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
 def normal_f32(key: int, n_or_idx, sigma: float, mask_key: int = 0, mask_frac: float = 0.0,
-               chunk: int = 1 << 22) -> np.ndarray:
-    """binary32 draws for element indices ``range(n)`` (or an index array)."""
+               chunk: int = 1 << 20) -> np.ndarray:
+    """binary32 draws for element indices ``range(n)`` (or an index array). Chunks of the index range are
+    drawn on a few threads (numpy's integer kernels release the interpreter lock); every element depends
+    only on its own index, so the result does not depend on the split."""
     idx = _indices(n_or_idx)
     out = np.empty(idx.shape[0], dtype=np.float32)
     c = normal_scale(sigma)
     thr = mask_threshold(mask_frac)
     g = np.uint64(GAMMA)
     kk = np.uint64(key)
-    for s in range(0, idx.shape[0], chunk):
+
+    def fill(s: int) -> None:
         e = idx[s:s + chunk]
         base = e * np.uint64(3)
         total = np.zeros(e.shape[0], dtype=np.int64)
@@ -116,6 +129,14 @@ def normal_f32(key: int, n_or_idx, sigma: float, mask_key: int = 0, mask_frac: f
             z = mix64(np.uint64(mask_key) + (e + np.uint64(1)) * g)
             v[z < np.uint64(thr)] = np.float32(0.0)
         out[s:s + chunk] = v
+
+    starts = range(0, idx.shape[0], chunk)
+    if len(starts) <= 1:
+        for s in starts:
+            fill(s)
+    else:
+        with ThreadPoolExecutor(min(_threads(), len(starts))) as ex:
+            list(ex.map(fill, starts))
     return out
 
 

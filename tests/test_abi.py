@@ -129,10 +129,19 @@ def test_dequantize_validation():
     al.check(L.al_dequantize(al.AL8, None, None, 0, 256, None, None))
 
 
-def _adamw(ts, cfg=None, step=1, nt=None):
+def _adamw_ws(ts, cfg=None):
     arr = (al.Tensor * max(len(ts), 1))(*ts)
     cfg = cfg or al.adamw_cfg()
-    al.check(al.lib().al_adamw_step(arr, len(ts) if nt is None else nt, ctypes.byref(cfg), step, None))
+    out = ctypes.c_size_t(0)
+    al.check(al.lib().al_adamw_workspace_bytes(arr, len(ts), ctypes.byref(cfg), ctypes.byref(out)))
+    return out.value
+
+
+def _adamw(ts, cfg=None, step=1, nt=None, ws=A, ws_bytes=1 << 20):
+    arr = (al.Tensor * max(len(ts), 1))(*ts)
+    cfg = cfg or al.adamw_cfg()
+    al.check(al.lib().al_adamw_step(arr, len(ts) if nt is None else nt, ctypes.byref(cfg), step, ws, ws_bytes,
+                                    None))
 
 
 def _t(**kw):
@@ -159,9 +168,24 @@ def test_adamw_validation():
     cfg.grad_dtype = 5
     assert _status(lambda: _adamw([_t()], cfg=cfg)) == 1
     # FP32 states need no metadata; empty tensors and empty lists enqueue nothing
-    _adamw([_t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None)])
-    _adamw([])
+    _adamw([_t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None)], ws=None, ws_bytes=0)
+    _adamw([], ws=None, ws_bytes=0)
     assert "NULL" not in al.lib().al_last_error().decode()
+
+
+def test_adamw_workspace():
+    """The workspace holds the descriptor table: 64 + 8 bytes per non-empty tensor in two 256-byte aligned
+    parts; a call without it (or with too little, or misaligned) is rejected before any HIP call."""
+    ts = [_t(), _t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None), _t(cols=512)]
+    assert _adamw_ws(ts) == 256 + 256
+    assert _adamw_ws([_t()] * 5) == 512 + 256
+    assert _adamw_ws([_t()] * 33) == 2304 + 512  # 64 x 33 = 2112 and 8 x 33 = 264, each rounded up to 256
+    assert _adamw_ws([]) == 0
+    need = _adamw_ws(ts)
+    assert _status(lambda: _adamw(ts, ws=None, ws_bytes=need)) == 3
+    assert _status(lambda: _adamw(ts, ws=A, ws_bytes=need - 1)) == 3
+    assert _status(lambda: _adamw(ts, ws=A + 16, ws_bytes=need)) == 2
+    assert _status(lambda: _adamw_ws([_t(rows=-1)])) == 1
 
 
 # ----------------------------------------------------------------- factored paths (Adafactor, CAME)
@@ -354,14 +378,14 @@ def _ap_step(ts, cfg=None, step=1, ws=A, ws_bytes=None, nt=None):
 
 def test_apollo_workspace_layout():
     # descriptors, then per tensor R and Rt (C x rank fp32), three C-double vectors and a 16-byte slot,
-    # each region 256-byte aligned
+    # then the AdamW launch's descriptor table (64 + 8 bytes per tensor), each region 256-byte aligned
     def al256(x):
         return (x + 255) // 256 * 256
 
     C, r = 96, 64  # 40 x 96: the rows are projected, 96 channels
     per = 2 * al256(C * r * 4) + 3 * al256(C * 8) + al256(16)
     one = _ap_ws([_at()])
-    assert one - per in (256, 512)  # the descriptor table of one tensor
+    assert one - per - 512 in (256, 512)  # the descriptor tables of one tensor
     two = _ap_ws([_at(), _at(rows=96, cols=40)])  # the transposed shape has the same 96 channels
     assert two - one - per in (0, 256)  # a second descriptor may spill into one more 256-byte line
     big = _ap_ws([_at(rows=5632, cols=2048)])  # 5632 channels (rows >= cols), same one-descriptor table

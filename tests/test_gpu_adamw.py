@@ -52,13 +52,14 @@ class Pair:
             self.hv.append(oracle.State(vspec.codec, s.n, vspec.block, vspec.log_floor))
         self.cfg = al.adamw_cfg(grad_bf16=w.grad_bf16, m=mspec, v=vspec)
         self.arr = al.tensor_array(self.states)
+        self.ws = al.workspace(al.adamw_workspace_bytes(self.states, self.cfg, arr=self.arr), dev)
 
     def step(self, t):
         import torch
 
         for i, (s, st) in enumerate(zip(self.shapes, self.states)):
             data.fill_grad(st.grad, i, s, self.w, t)
-        self.al.adamw_step(self.states, self.cfg, t, arr=self.arr)
+        self.al.adamw_step(self.states, self.cfg, t, self.ws, arr=self.arr)
         for i, s in enumerate(self.shapes):
             g = data.host_grad(i, self.w, t, np.arange(s.n))
             oracle.adamw_step(self.hp[i], g, self.hm[i], self.hv[i], t)
@@ -187,6 +188,7 @@ def _sampled_full_size_picks(dev, shapes, w, block, steps, picks):
         states.append(al.ParamState(p, g, s.rows, s.cols, m=m, m_meta=mm, v=v, v_meta=vm))
     cfg = al.adamw_cfg(grad_bf16=True, m=mspec, v=vspec)
     arr = al.tensor_array(states)
+    ws = al.workspace(al.adamw_workspace_bytes(states, cfg, arr=arr), dev)
     host = {}
     for (i, k) in picks:
         s = shapes[i]
@@ -197,7 +199,7 @@ def _sampled_full_size_picks(dev, shapes, w, block, steps, picks):
     for t in range(1, steps + 1):
         for i, (s, st) in enumerate(zip(shapes, states)):
             data.fill_grad(st.grad, i, s, w, t)
-        al.adamw_step(states, cfg, t, arr=arr)
+        al.adamw_step(states, cfg, t, ws, arr=arr)
         for (i, k), h in host.items():
             lo, hi = k * T, min(shapes[i].n, (k + 1) * T)
             oracle.adamw_step(h["p"], data.host_grad(i, w, t, np.arange(lo, hi)), h["m"], h["v"], t)
@@ -226,7 +228,7 @@ def test_adamw_full_size_tinyllama_sampled(dev, block):
     log(f"near-boundary code differences: {near}")
 
 
-@pytest.mark.parametrize("block", [64, 256, 2048])
+@pytest.mark.parametrize("block", [64, 128, 256, 512, 1024, 2048])
 def test_adamw_full_size_llama7b_sampled(dev, block):
     import torch
 

@@ -113,7 +113,8 @@ def _adamw_run(dev, shapes, bv, bf16):
     for t in (1, 2):
         for i, (st, n) in enumerate(zip(states, shapes)):
             st.grad = _grad(ar, i, t, n, bf16)
-        al.adamw_step(states, cfg, t)
+        ws = ar.alloc(al.adamw_workspace_bytes(states, cfg), torch.uint8)
+        al.adamw_step(states, cfg, t, ws)
     torch.cuda.synchronize()
     ar.check(f"adamw B_V {bv}")
     for st, n in zip(states, shapes):
@@ -122,7 +123,7 @@ def _adamw_run(dev, shapes, bv, bf16):
     return _snapshot([x for st in states for x in (st.param, st.m, st.m_meta, st.v, st.v_meta)])
 
 
-@pytest.mark.parametrize("bv", [64, 128, 256, 2048])
+@pytest.mark.parametrize("bv", [64, 128, 256, 512, 1024, 2048])
 @pytest.mark.parametrize("bf16", [True, False])
 def test_adamw_bounds_and_determinism(dev, bv, bf16):
     shapes = [33, 1000, 2049, 70_001, 3 * 2048]

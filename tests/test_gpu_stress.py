@@ -89,7 +89,7 @@ def test_adamw_stress(dev, regime, vc, block):
         gs = [_grad(i, s, t, lo, hi, 0.6, True) for i, s in enumerate(SHAPES)]
         for st, g in zip(states, gs):
             st.grad = _upload(dev, g)
-        al.adamw_step(states, cfg, t)
+        al.adamw_step(states, cfg, t, al.workspace(al.adamw_workspace_bytes(states, cfg), dev))
         torch.cuda.synchronize()
         for i, (s, h, g, st) in enumerate(zip(SHAPES, host, gs, states)):
             oracle.adamw_step(h["p"], g, h["m"], h["v"], t)

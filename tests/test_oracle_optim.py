@@ -205,26 +205,37 @@ def _came_states(rows, cols, codec=FP32, mcodec=FP32):
 
 def test_came_beta1_zero_closed_form():
     """beta1 = 0: m = clipped update, residual == eps2, so from zero confidence
-    R'_t = C'_t = (1 - beta3^t) eps2 and p -= lr * uhat / sqrt((1 - beta3^t) eps2)."""
+    R'_t = C'_t = (1 - beta3^t) eps2 and p -= lr * uhat / sqrt((1 - beta3^t) eps2). With beta2 = 0 the clipped
+    update uhat is Hugging Face Adafactor's at decay_rate 0 (beta2_t = 1 - t^0 = 0, the factors of the
+    current gradient only), so every step is held to that independent implementation."""
+    from transformers.optimization import Adafactor
+
     rows, cols = 20, 36
     n = rows * cols
     p0 = _param(n, 11)
     grads = _grads(rows, cols, 5, 12)
     st = _came_states(rows, cols)
-    beta3, eps2, lr = 0.9999, 1e-16, 1e-4
+    beta3, eps2 = 0.9999, 1e-16
+    lr = 1e-13  # the confidence scale 1/sqrt((1 - beta3^t) eps2) is about 1e10 / sqrt(t)
     p = p0.copy()
-    # reference clipped update from the Adafactor-pinned factored path: with
-    # beta1 = 0 the CAME update equals the clipped Adafactor-style update
-    # scaled by 1/sqrt((1 - beta3^t) eps2)
+    tp = torch.nn.Parameter(torch.from_numpy(p0.copy().reshape(rows, cols)))
+    hf = Adafactor([tp], lr=1e-3, eps=(1e-30, 1e-3), clip_threshold=1.0, decay_rate=0.0, beta1=None,
+                   weight_decay=0.0, scale_parameter=False, relative_step=False, warmup_init=False)
     for t, g in enumerate(grads, 1):
         before = p.copy()
-        oracle.came_step(p, g, rows, cols, t=t, beta1=0.0, lr=lr, beta3=beta3, eps2=eps2, **st)
+        oracle.came_step(p, g, rows, cols, t=t, beta1=0.0, beta2=0.0, lr=lr, beta3=beta3, eps2=eps2, **st)
         c_expect = (1 - beta3**t) * eps2
         np.testing.assert_allclose(st["cr"].codes, np.float32(c_expect), rtol=1e-6)
         np.testing.assert_allclose(st["cc"].codes, np.float32(c_expect), rtol=1e-6)
         upd = (before.astype(np.float64) - p) / lr * math.sqrt(c_expect)
-        # |uhat| has RMS <= 1 after clipping; the update is m = uhat exactly
-        np.testing.assert_allclose(upd, st["m"].codes, rtol=2e-3, atol=1e-3 * np.abs(upd).max())
+        hp = tp.detach().numpy().reshape(-1).astype(np.float64).copy()
+        tp.grad = torch.from_numpy(g.copy().reshape(rows, cols))
+        hf.step()
+        ref = (hp - tp.detach().numpy().reshape(-1)) / 1e-3  # HF's clipped update of this step
+        # both updates are read back through an fp32 parameter: ~1e-6 relative of p per read
+        tol = 4 * float(np.spacing(np.float32(np.abs(p0).max()))) / 1e-3
+        np.testing.assert_allclose(upd, ref, rtol=1e-4, atol=tol)
+        assert np.abs(ref).max() > 0.1
 
 
 def test_came_uniform_gradient_closed_form():
@@ -282,3 +293,126 @@ def test_came_second_moment_path_matches_adafactor_at_t1():
         uc = (p0.astype(np.float64) - pc) / 1e-4
         scale = math.sqrt((1 - 0.9999) * 1e-16) if fac else 1.0
         np.testing.assert_allclose(uc * scale, ua, rtol=5e-3, atol=5e-3 * np.abs(ua).max())
+
+
+# ----------------------------------------------- CAME over many steps with beta1 > 0 (closed forms)
+# A constant gradient g_ij = s_ij a_i b_j (|s| = 1; a uniform gradient is a = b = const) makes every
+# factored estimate exact: R_t = (1 - beta2^t) a_i^2 mean(b^2), C_t = (1 - beta2^t) b_j^2 mean(a^2) (plus
+# eps1), so u = g / sqrt(R_i C_j / mean R) = s / sqrt(1 - beta2^t), whose RMS exceeds the clip threshold
+# 1 for every finite t: the clipped update is exactly s. Then m_t is the EMA of s from zero, the residual
+# (s - m_t)^2 + eps2 is the same for every element, the confidence factors are uniform, and
+# p_t = p_{t-1} - lr m_t / sqrt(R'_t) with R'_t = (1 - beta3) sum_k beta3^(t-k) (r_k + eps2).
+# A sign change of the gradient at step k (s -> -s) keeps all of this (r_k then grows), and probes the
+# momentum carried across steps, including through its UF8 code.
+
+def _came_closed_form(signs_t, b1, b2, b3, e2, lr):
+    """(m_t, R'_t, p-update_t) per step for the clipped update signs_t[t-1] * s (uniform per step)."""
+    T = len(signs_t)
+    m = []
+    for t in range(1, T + 1):
+        # m_t = (1 - b1) sum_{j<=t} b1^(t-j) sigma_j
+        m.append(sum((1 - b1) * b1 ** (t - j) * signs_t[j - 1] for j in range(1, t + 1)))
+    r = [(signs_t[t - 1] - m[t - 1]) ** 2 for t in range(1, T + 1)]
+    R = [sum((1 - b3) * b3 ** (t - k) * (r[k - 1] + e2) for k in range(1, t + 1)) for t in range(1, T + 1)]
+    upd = [lr * m[t] / math.sqrt(R[t]) for t in range(T)]
+    return m, R, upd
+
+
+@pytest.mark.parametrize("kind", ["uniform", "rank1", "flip", "row1"])
+@pytest.mark.parametrize("codecs", ["fp32", "uf8_al16"])
+def test_came_multistep_closed_form(kind, codecs):
+    """20 CAME steps with beta1 = 0.9 > 0 against the closed form above: momentum, confidence factors and the
+    parameter trajectory, with FP32 states and with UF8 momentum + AL16 factors (a block of equal values is
+    coded exactly by UF8, and by AL16 up to the fp32 rounding of its l_min: ~1e-6 relative per decode)."""
+    rng = np.random.default_rng(41)
+    rows, cols, T, k_flip = (1, 300, 20, 0) if kind == "row1" else (16, 48, 20, 8 if kind == "flip" else 0)
+    n = rows * cols
+    if kind == "rank1":
+        a = np.exp2(rng.integers(-12, -8, rows)).astype(np.float64)
+        b = np.exp2(rng.integers(-2, 2, cols)).astype(np.float64)
+        s = np.where(rng.random(n) < 0.5, -1.0, 1.0)
+        mag = np.outer(a, b).reshape(-1)
+    else:
+        s = np.full(n, -1.0)
+        mag = np.full(n, 3e-4)
+    b1, b2, b3, e2, lr = 0.9, 0.999, 0.9999, 1e-16, 1e-4
+    sig = [(-1.0 if (k_flip and t >= k_flip) else 1.0) for t in range(1, T + 1)]
+    m_cf, R_cf, upd_cf = _came_closed_form(sig, b1, b2, b3, e2, lr)
+    if kind == "row1":  # 1-D semantics (rows == 1): update = lr m_t, no confidence factors
+        upd_cf = [lr * x for x in m_cf]
+    mc, fc = (FP32, FP32) if codecs == "fp32" else (UF8, AL16)
+    st = _came_states(rows, cols, codec=fc, mcodec=mc)
+    p0 = _param(n, 43)
+    p = p0.copy()
+    total = np.zeros(n)
+    tol = 2e-6 if codecs == "fp32" else 5e-5
+    for t in range(1, T + 1):
+        g = (mag * s * sig[t - 1]).astype(np.float32)
+        before = p.copy()
+        oracle.came_step(p, g, rows, cols, t=t, beta1=b1, beta2=b2, beta3=b3, eps2=e2, lr=lr, **st)
+        step_upd = before.astype(np.float64) - p
+        total += step_upd
+        # momentum: m_t s in every element
+        m_dec = st["m"].decode() if mc == UF8 else st["m"].codes[:n]
+        # m is rounded to fp32 every step (|m| <= 1): its absolute error grows by at most an ulp of 1 per step,
+        # which matters where the flipped momentum crosses zero
+        m_atol = t * 2.0**-23
+        np.testing.assert_allclose(m_dec, m_cf[t - 1] * s, rtol=tol, atol=m_atol, err_msg=f"m at t={t}")
+        if mc == UF8:
+            assert np.all(np.abs(st["m"].codes[:n]) == 127), t
+        if rows > 1:
+            for key in ("cr", "cc"):
+                dec = st[key].decode() if fc == AL16 else st[key].codes
+                np.testing.assert_allclose(dec, R_cf[t - 1], rtol=tol * t, err_msg=f"{key} at t={t}")
+        # per-step update, read back through an fp32 parameter (one rounding of |p| <= 0.1)
+        ulp = float(np.spacing(np.float32(np.abs(p0).max() + 0.1)))
+        u_atol = 2 * ulp + (lr * m_atol / math.sqrt(R_cf[t - 1]) if rows > 1 else lr * m_atol)
+        np.testing.assert_allclose(step_upd, upd_cf[t - 1] * s, rtol=tol * t, atol=u_atol,
+                                   err_msg=f"update at t={t}")
+    np.testing.assert_allclose(total, sum(upd_cf) * s, rtol=tol * T, atol=T * u_atol)
+    if kind == "flip":
+        # the momentum has turned: m_T s = -(1 - b1^(T-k+1)) + b1^(T-k+1) m_{k-1} < 0
+        assert m_cf[-1] < 0 < m_cf[k_flip - 2]
+
+
+def test_came_staggered_sign_flips_closed_form():
+    """Rank-1 magnitudes a_i b_j with per-element signs that flip at element-specific steps k_ij: the second
+    moment and the clip stay exact (|g| does not change, so uhat = the current sign), but the momentum,
+    the residual and therefore the confidence factors R'_i, C'_j now differ by row and by column. Their
+    values follow from the definitions: m = EMA(beta1) of the signs, residual (sign - m)^2 + eps2, R' / C' =
+    EMA(beta3) of its row / column means, update lr m / sqrt(R'_i C'_j / mean R'). A transposed or
+    misindexed confidence factor, a residual taken against the previous momentum, or a clip applied after
+    the momentum each fail it. FP32 states, 20 steps."""
+    rng = np.random.default_rng(47)
+    rows, cols, T = 16, 48, 20
+    b1, b2, b3, e2, lr = 0.9, 0.999, 0.9999, 1e-16, 1e-4
+    a = np.exp2(rng.integers(-12, -8, rows)).astype(np.float64)
+    b = np.exp2(rng.integers(-2, 2, cols)).astype(np.float64)
+    s0 = np.where(rng.random((rows, cols)) < 0.5, -1.0, 1.0)
+    k = rng.integers(2, 14, (rows, cols))  # the step from which element (i, j) has the opposite sign
+    sig = np.stack([np.where(t >= k, -s0, s0) for t in range(1, T + 1)])  # [T, rows, cols]
+    m = np.zeros((T, rows, cols))
+    for t in range(T):  # m_t = (1 - b1) sum_{l <= t} b1^(t - l) sigma_l
+        m[t] = sum((1 - b1) * b1 ** (t - l) * sig[l] for l in range(t + 1))
+    r = (sig - m) ** 2 + e2
+    Rp = np.stack([sum((1 - b3) * b3 ** (t - l) * r[l].mean(axis=1) for l in range(t + 1)) for t in range(T)])
+    Cp = np.stack([sum((1 - b3) * b3 ** (t - l) * r[l].mean(axis=0) for l in range(t + 1)) for t in range(T)])
+    assert np.ptp(Rp[-1]) > 1e-3 * Rp[-1].mean() and np.ptp(Cp[-1]) > 1e-3 * Cp[-1].mean()  # not uniform
+    st = _came_states(rows, cols)
+    p0 = _param(rows * cols, 49)
+    p = p0.copy()
+    mag = np.outer(a, b)
+    for t in range(1, T + 1):
+        g = (mag * sig[t - 1]).reshape(-1).astype(np.float32)
+        before = p.copy()
+        oracle.came_step(p, g, rows, cols, t=t, beta1=b1, beta2=b2, beta3=b3, eps2=e2, lr=lr, **st)
+        tol = 2e-6 * t
+        np.testing.assert_allclose(st["m"].codes[: rows * cols], m[t - 1].reshape(-1), rtol=tol, atol=t * 2.0**-23)
+        np.testing.assert_allclose(st["cr"].codes, Rp[t - 1], rtol=tol, err_msg=f"R' at t={t}")
+        np.testing.assert_allclose(st["cc"].codes, Cp[t - 1], rtol=tol, err_msg=f"C' at t={t}")
+        S = np.outer(Rp[t - 1], Cp[t - 1]) / Rp[t - 1].mean()
+        want = lr * m[t - 1] / np.sqrt(S)
+        ulp = float(np.spacing(np.float32(np.abs(p0).max() + 0.1)))
+        atol = 2 * ulp + lr * t * 2.0**-23 / np.sqrt(S.min())
+        np.testing.assert_allclose(before.astype(np.float64) - p, want.reshape(-1), rtol=tol, atol=atol,
+                                   err_msg=f"update at t={t}")
