@@ -18,11 +18,14 @@ from __future__ import annotations
 
 import json
 
+import numpy as np
+
 from . import AL8, AL16, FP32, UF8, Spec, alloc_state, dequantize, quantize
 
 ROLES = ("m", "v", "vr", "vc", "cr", "cc")
 _CODECS = {FP32: "FP32", AL8: "AL8", AL16: "AL16", UF8: "UF8"}
 _BY_NAME = {v: k for k, v in _CODECS.items()}
+_SAFE_DTYPES = {"F32": "float32", "U8": "uint8", "I16": "int16", "I8": "int8"}
 
 
 def _role_len(st, role: str) -> int:
@@ -57,31 +60,82 @@ def save(path: str, states, specs, names, kind: str, step: int) -> None:
     save_file(tensors, path, metadata=header)
 
 
-def load(path: str, states, device="cuda"):
-    """Load coded states into a ParamState list of the same tensors (shapes checked); returns
-    (kind, step, specs) with specs per tensor as dicts role -> Spec."""
+def _layout(n: int, spec: Spec):
+    """(code dtype name, code elements, meta floats) that alloc_state gives an n-element state: the sizes the
+    kernels index."""
+    from . import code_bytes, meta_floats
+
+    if spec.codec == FP32:
+        return "float32", max(n, 1), 0
+    dt = {AL8: "uint8", AL16: "int16", UF8: "int8"}[spec.codec]
+    elems = code_bytes(spec.codec, n, spec.block) // (2 if spec.codec == AL16 else 1)
+    return dt, max(elems, 1), max(meta_floats(spec.codec, n, spec.block), 4)
+
+
+def load(path: str, states, specs, kind: str | None = None):
+    """Copy a checkpoint's coded states into the existing state buffers of a ParamState list.
+
+    states: the same tensors (shapes checked), with their state buffers already allocated for `specs` (for
+    instance by alloc_state or grouping.attach_states); specs: per tensor, a dict role -> Spec the caller
+    will step with; kind: the optimizer kind expected (None: any). The checkpoint must hold exactly those
+    roles with the same codec, block and log floor, and each stored array must have the dtype and size of
+    the destination buffer, at least the size the spec needs. The buffers are overwritten in place
+    (copy_), so descriptor arrays and steppers built over them stay valid. Returns (kind, step)."""
     from safetensors import safe_open
 
     with safe_open(path, framework="pt") as f:
         header = f.metadata()
         if header.get("format") != "al-optimizer-state/1":
             raise ValueError(f"{path}: not an optimizer-state checkpoint")
+        if kind is not None and header["kind"] != kind:
+            raise ValueError(f"{path}: optimizer {header['kind']}, expected {kind}")
         info = json.loads(header["tensors"])
-        if len(info) != len(states):
-            raise ValueError(f"{path}: {len(info)} tensors, expected {len(states)}")
-        specs = []
-        for i, (st, ti) in enumerate(zip(states, info)):
+        if len(info) != len(states) or len(specs) != len(states):
+            raise ValueError(f"{path}: {len(info)} tensors, expected {len(states)} (with {len(specs)} specs)")
+        keys = set(f.keys())
+        plan = []
+        for i, (st, ti, want) in enumerate(zip(states, info, specs)):
+            tag = f"{path}: tensor {i} ({ti['name']})"
             if (ti["rows"], ti["cols"]) != (st.rows, st.cols):
-                raise ValueError(f"{path}: tensor {i} ({ti['name']}) shape {ti['rows']}x{ti['cols']} "
-                                 f"!= {st.rows}x{st.cols}")
-            sp = {}
+                raise ValueError(f"{tag} shape {ti['rows']}x{ti['cols']} != {st.rows}x{st.cols}")
+            if set(ti["roles"]) != set(want):
+                raise ValueError(f"{tag} holds roles {sorted(ti['roles'])}, expected {sorted(want)}")
             for role, r in ti["roles"].items():
-                setattr(st, role, f.get_tensor(f"t{i}.{role}").to(device))
-                key = f"t{i}.{role}.meta"
-                setattr(st, role + "_meta", f.get_tensor(key).to(device) if key in f.keys() else None)
-                sp[role] = Spec(_BY_NAME[r["codec"]], r["block"], r["log_floor"])
-            specs.append(sp)
-    return header["kind"], int(header["step"]), specs
+                w = want[role]
+                got = Spec(_BY_NAME[r["codec"]], int(r["block"]), float(r["log_floor"]))
+                same = got.codec == w.codec and (w.codec == FP32 or (
+                    got.block == w.block and np.float32(got.log_floor) == np.float32(w.log_floor)))
+                if not same:
+                    raise ValueError(f"{tag} {role}: saved as {r['codec']} block {r['block']} floor "
+                                     f"{r['log_floor']}, expected {_CODECS[w.codec]} block {w.block} floor "
+                                     f"{w.log_floor}")
+                n = _role_len(st, role)
+                if int(r["n"]) != n:
+                    raise ValueError(f"{tag} {role}: {r['n']} elements, expected {n}")
+                dt, ncode, nmeta = _layout(n, w)
+                parts = [(role, f"t{i}.{role}", ncode, dt)]
+                if nmeta:
+                    parts.append((role + "_meta", f"t{i}.{role}.meta", nmeta, "float32"))
+                elif f"t{i}.{role}.meta" in keys:
+                    raise ValueError(f"{tag} {role}: metadata stored for an FP32 state")
+                for attr, key, need, want_dt in parts:
+                    dst = getattr(st, attr)
+                    if dst is None:
+                        raise ValueError(f"{tag} {attr}: no buffer to load into (allocate the states first)")
+                    if key not in keys:
+                        raise ValueError(f"{tag}: {key} missing")
+                    sl = f.get_slice(key)
+                    shape, sdt = sl.get_shape(), sl.get_dtype()
+                    numel = int(np.prod(shape)) if shape else 1
+                    if str(dst.dtype) != "torch." + want_dt or _SAFE_DTYPES.get(sdt) != want_dt:
+                        raise ValueError(f"{tag} {attr}: dtype {sdt} / buffer {dst.dtype}, expected {want_dt}")
+                    if numel != dst.numel() or numel < need:
+                        raise ValueError(f"{tag} {attr}: {numel} stored elements, buffer {dst.numel()}, "
+                                         f"at least {need} needed")
+                    plan.append((dst, key))
+        for dst, key in plan:  # every check passed: overwrite in place
+            dst.copy_(f.get_tensor(key).to(dst.device))
+    return header["kind"], int(header["step"])
 
 
 def migrate(st, role: str, old: Spec, new: Spec, stream=None) -> None:
