@@ -250,6 +250,21 @@ al_status al_adamw_workspace_bytes(const al_tensor* tensors, int32_t nt, const a
 al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory or hand over a workspace
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): al_adamw_step without ws, same arguments otherwise and the
+ * same results bit for bit (the same kernels). The descriptor table lives in
+ * a fixed device array of the library instead, 288 KiB per GPU, held until
+ * the process ends: at most 4096 non-empty tensors per call (more:
+ * AL_EUNSUPPORTED, before any HIP call). The first call on a device looks up
+ * that array's address once (hipGetSymbolAddress). The call allocates
+ * nothing (no hipMalloc, hipFree or host heap). Every call on one GPU writes
+ * the same array: calls in order on one stream are safe, calls that may
+ * overlap on one GPU (several streams or threads) race and must be
+ * serialized by the caller. */
+al_status al_adamw_step_noalloc(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step,
+                                void* stream);
+
 /* Workspace size (bytes) that al_adafactor_step / al_came_step need for this
  * tensor list and config. */
 al_status al_adafactor_workspace_bytes(const al_tensor* tensors, int32_t nt,

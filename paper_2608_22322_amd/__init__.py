@@ -79,7 +79,8 @@ _lib = None
 
 # every symbol include/al.h and include/al_synth.h declare
 EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al_state_bytes", "al_quantize",
-           "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
+           "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adamw_step_noalloc",
+           "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
            "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes", "al_apollo_step", "al_diag_math",
            "al_diag_stream", "al_diff_norms", "al_synth_normal")
 
@@ -104,6 +105,7 @@ def lib():
         L.al_adamw_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg),
                                                ctypes.POINTER(sz)]
         L.al_adamw_step.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg), i64, vp, sz, vp]
+        L.al_adamw_step_noalloc.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdamWCfg), i64, vp]
         L.al_adafactor_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(AdafactorCfg),
                                                    ctypes.POINTER(sz)]
         L.al_came_workspace_bytes.argtypes = [ctypes.POINTER(Tensor), i32, ctypes.POINTER(CAMECfg),
@@ -117,7 +119,7 @@ def lib():
         L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
         L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
         L.al_diff_norms.argtypes = [vp, vp, i64, vp, vp]
-        for name in ("al_quantize", "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step",
+        for name in ("al_quantize", "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adamw_step_noalloc",
                      "al_adafactor_workspace_bytes",
                      "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes",
                      "al_apollo_step", "al_diag_math", "al_diag_stream",
@@ -313,6 +315,13 @@ def adamw_step(states, cfg: AdamWCfg, step: int, ws, stream=None, arr=None) -> N
     at least adamw_workspace_bytes (the step's descriptor table)."""
     arr = arr if arr is not None else tensor_array(states)
     check(lib().al_adamw_step(arr, len(states), ctypes.byref(cfg), step, *_ws_args(ws), _stream(stream)))
+
+
+def adamw_step_noalloc(states, cfg: AdamWCfg, step: int, stream=None, arr=None) -> None:
+    """al_adamw_step without a workspace (the library's fixed per-GPU table, at most 4096 tensors); for callers
+    that cannot allocate. Calls that may overlap on one GPU race."""
+    arr = arr if arr is not None else tensor_array(states)
+    check(lib().al_adamw_step_noalloc(arr, len(states), ctypes.byref(cfg), step, _stream(stream)))
 
 
 def adafactor_workspace_bytes(states, cfg: AdafactorCfg, arr=None) -> int:

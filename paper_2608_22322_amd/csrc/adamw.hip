@@ -24,6 +24,8 @@
 // list, and the chunk -> tensor map is a binary search over the descriptor
 // table in device memory (one launch per step). Full chunks use non-temporal
 // loads and stores: every byte of the step is touched exactly once.
+#include <mutex>
+
 #include "al_device.hpp"
 #include "al_internal.hpp"
 
@@ -594,9 +596,6 @@ void adamw_kernel(const AdamWLaunch a) {
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
 
 // ------------------------------------------------------------ descriptor table
-// Descriptors per copy launch: 60 x 64 bytes keep the argument segment under
-// 4 KB.
-constexpr int kAdamWCopyBatch = 60;
 struct AdamWDescBatch {
     int32_t count, offset;
     AdamWDesc d[kAdamWCopyBatch];
@@ -610,29 +609,68 @@ __global__ void adamw_desc_copy_kernel(const AdamWDescBatch b, AdamWDesc* dst, i
     for (int i = threadIdx.x; i < b.count; i += blockDim.x) tb[b.offset + i] = b.d[i].tile_begin;
 }
 
-static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+static constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 size_t adamw_table_bytes(int64_t nt) {
     return nt <= 0 ? 0 : align256((size_t)nt * sizeof(AdamWDesc)) + align256((size_t)nt * sizeof(int64_t));
 }
 
-hipError_t adamw_write_table(const AdamWDesc* host, int nt, void* table, AdamWLaunch& a, hipStream_t s) {
+static AdamWDesc* table_desc(void* table) { return static_cast<AdamWDesc*>(table); }
+static int64_t* table_tb(void* table, int64_t nt) {
+    return reinterpret_cast<int64_t*>(static_cast<char*>(table) + align256((size_t)nt * sizeof(AdamWDesc)));
+}
+
+hipError_t adamw_write_batch(const AdamWDesc* host, int count, int offset, void* table, int64_t nt, hipStream_t s) {
     static_assert(sizeof(AdamWDesc) % 8 == 0, "descriptor size");
     static_assert(sizeof(AdamWDescBatch) <= 4096 - 64, "copy arguments");
-    AdamWDesc* D = static_cast<AdamWDesc*>(table);
-    int64_t* tb = reinterpret_cast<int64_t*>(static_cast<char*>(table) + align256((size_t)nt * sizeof(AdamWDesc)));
+    AdamWDescBatch b;
+    b.count = count;
+    b.offset = offset;
+    for (int i = 0; i < count; ++i) b.d[i] = host[i];
+    hipLaunchKernelGGL(adamw_desc_copy_kernel, dim3(1), dim3(256), 0, s, b, table_desc(table), table_tb(table, nt));
+    return hipGetLastError();
+}
+
+void adamw_bind_table(void* table, int64_t nt, AdamWLaunch& a) {
+    a.D = table_desc(table);
+    a.tb = table_tb(table, nt);
+    a.nt = (int32_t)nt;
+}
+
+hipError_t adamw_write_table(const AdamWDesc* host, int nt, void* table, AdamWLaunch& a, hipStream_t s) {
     for (int off = 0; off < nt; off += kAdamWCopyBatch) {
-        AdamWDescBatch b;
-        b.count = nt - off < kAdamWCopyBatch ? nt - off : kAdamWCopyBatch;
-        b.offset = off;
-        for (int i = 0; i < b.count; ++i) b.d[i] = host[off + i];
-        hipLaunchKernelGGL(adamw_desc_copy_kernel, dim3(1), dim3(256), 0, s, b, D, tb);
-        const hipError_t e = hipGetLastError();
+        const hipError_t e = adamw_write_batch(host + off, nt - off < kAdamWCopyBatch ? nt - off : kAdamWCopyBatch,
+                                               off, table, nt, s);
         if (e != hipSuccess) return e;
     }
-    a.D = D;
-    a.tb = tb;
-    a.nt = nt;
+    adamw_bind_table(table, nt, a);
+    return hipSuccess;
+}
+
+// The descriptor table of the allocation-free entry point: a fixed device
+// array (one copy per GPU, alive until the process ends). Host code reaches
+// it only through the device address hipGetSymbolAddress returns; the array's
+// name in host code is a stand-in, not a device pointer.
+static __device__ __align__(256) unsigned char scratch[kAdamWScratchBytes];
+static_assert(kAdamWScratchBytes == align256((size_t)kAdamWStaticTensors * sizeof(AdamWDesc)) +
+                                        align256((size_t)kAdamWStaticTensors * sizeof(int64_t)),
+              "static table size");
+
+hipError_t adamw_static_table(void** table) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *table = addr[dev];
     return hipSuccess;
 }
 

@@ -446,10 +446,10 @@ al_status al_dequantize(int32_t codec, const void* codes, const float* meta, int
 
 namespace {
 
-// Validate an AdamW call and build its descriptors (non-empty tensors only)
-// and launch constants. No HIP call.
-al_status adamw_plan(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, const char* who,
-                     std::vector<al::AdamWDesc>& desc, al::AdamWLaunch& a) {
+// Validate an AdamW call, count its non-empty tensors and set the launch
+// constants (a.total_tiles included). No HIP call.
+al_status adamw_check(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, const char* who,
+                      int64_t* ndesc, al::AdamWLaunch& a) {
     if (nt < 0) return fail(AL_EINVAL, "%s: nt < 0", who);
     if (nt > 0 && !tensors) return fail(AL_EINVAL, "%s: tensors is NULL", who);
     if (!cfg) return fail(AL_EINVAL, "%s: cfg is NULL", who);
@@ -467,8 +467,8 @@ al_status adamw_plan(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* c
     if (cfg->m.codec == AL_CODEC_UF8 && cfg->m.block != 256)
         return fail(AL_EUNSUPPORTED, "%s: UF8 momentum block must be 256 (got %d)", who, cfg->m.block);
 
-    desc.clear();
     std::memset(&a, 0, sizeof(a));
+    *ndesc = 0;
     const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
     for (int i = 0; i < nt; ++i) {
         const al_tensor& t = tensors[i];
@@ -481,17 +481,8 @@ al_status adamw_plan(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* c
         if ((st = check_unused(t.cr, t.cr_meta, "cr", i)) != AL_OK) return st;
         if ((st = check_unused(t.cc, t.cc_meta, "cc", i)) != AL_OK) return st;
         if (n == 0) continue;
-        al::AdamWDesc d;
-        d.p = t.param;
-        d.g = t.grad;
-        d.m = t.m;
-        d.ms = t.m_meta;
-        d.v = t.v;
-        d.vm = t.v_meta;
-        d.n = n;
-        d.tile_begin = a.total_tiles;
+        ++*ndesc;
         a.total_tiles += (n + T - 1) / T;
-        desc.push_back(d);
     }
     const double bc1 = 1.0 - std::pow(cfg->beta1, (double)step);
     const double bc2 = 1.0 - std::pow(cfg->beta2, (double)step);
@@ -507,6 +498,43 @@ al_status adamw_plan(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* c
     return AL_OK;
 }
 
+// Write the descriptors of a validated list into an ndesc-entry table, a copy
+// launch per kAdamWCopyBatch of them (built in a stack buffer: no heap), bind
+// the table and launch the step.
+al_status adamw_run(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t ndesc, void* table,
+                    al::AdamWLaunch& a, hipStream_t s, const char* who) {
+    const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
+    al::AdamWDesc batch[al::kAdamWCopyBatch];
+    int nb = 0, off = 0;
+    int64_t tile = 0;
+    hipError_t e;
+    for (int i = 0; i < nt; ++i) {
+        const al_tensor& t = tensors[i];
+        const int64_t n = t.rows * t.cols;
+        if (n == 0) continue;
+        al::AdamWDesc& d = batch[nb++];
+        d.p = t.param;
+        d.g = t.grad;
+        d.m = t.m;
+        d.ms = t.m_meta;
+        d.v = t.v;
+        d.vm = t.v_meta;
+        d.n = n;
+        d.tile_begin = tile;
+        tile += (n + T - 1) / T;
+        if (nb == al::kAdamWCopyBatch) {
+            if ((e = al::adamw_write_batch(batch, nb, off, table, ndesc, s)) != hipSuccess) return hip_fail(e, who);
+            off += nb;
+            nb = 0;
+        }
+    }
+    if (nb > 0 && (e = al::adamw_write_batch(batch, nb, off, table, ndesc, s)) != hipSuccess) return hip_fail(e, who);
+    al::adamw_bind_table(table, ndesc, a);
+    if ((e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
+        return hip_fail(e, who);
+    return AL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -515,30 +543,43 @@ al_status al_adamw_workspace_bytes(const al_tensor* tensors, int32_t nt, const a
     g_err[0] = 0;
     if (!bytes) return fail(AL_EINVAL, "al_adamw_workspace_bytes: bytes is NULL");
     *bytes = 0;
-    std::vector<al::AdamWDesc> desc;
+    int64_t ndesc = 0;
     al::AdamWLaunch a;
-    const al_status st = adamw_plan(tensors, nt, cfg, 1, "al_adamw_workspace_bytes", desc, a);
+    const al_status st = adamw_check(tensors, nt, cfg, 1, "al_adamw_workspace_bytes", &ndesc, a);
     if (st != AL_OK) return st;
-    *bytes = al::adamw_table_bytes((int64_t)desc.size());
+    *bytes = al::adamw_table_bytes(ndesc);
     return AL_OK;
 }
 
 al_status al_adamw_step(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step, void* ws,
                         size_t ws_bytes, void* stream) {
     g_err[0] = 0;
-    std::vector<al::AdamWDesc> desc;
+    int64_t ndesc = 0;
     al::AdamWLaunch a;
-    al_status st = adamw_plan(tensors, nt, cfg, step, "al_adamw_step", desc, a);
+    al_status st = adamw_check(tensors, nt, cfg, step, "al_adamw_step", &ndesc, a);
     if (st != AL_OK) return st;
-    if (desc.empty()) return AL_OK;
-    if ((st = check_ws(ws, ws_bytes, al::adamw_table_bytes((int64_t)desc.size()), "al_adamw_step")) != AL_OK)
-        return st;
-    hipStream_t s = as_stream(stream);
-    hipError_t e;
-    if ((e = al::adamw_write_table(desc.data(), (int)desc.size(), ws, a, s)) != hipSuccess ||
-        (e = al::launch_adamw(a, cfg->grad_dtype, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
-        return hip_fail(e, "al_adamw_step launch");
-    return AL_OK;
+    if (ndesc == 0) return AL_OK;
+    if ((st = check_ws(ws, ws_bytes, al::adamw_table_bytes(ndesc), "al_adamw_step")) != AL_OK) return st;
+    return adamw_run(tensors, nt, cfg, ndesc, ws, a, as_stream(stream), "al_adamw_step launch");
+}
+
+al_status al_adamw_step_noalloc(const al_tensor* tensors, int32_t nt, const al_adamw_cfg* cfg, int64_t step,
+                                void* stream) {
+    g_err[0] = 0;
+    int64_t ndesc = 0;
+    al::AdamWLaunch a;
+    al_status st = adamw_check(tensors, nt, cfg, step, "al_adamw_step_noalloc", &ndesc, a);
+    if (st != AL_OK) return st;
+    if (ndesc == 0) return AL_OK;
+    if (ndesc > al::kAdamWStaticTensors)
+        return fail(AL_EUNSUPPORTED,
+                    "al_adamw_step_noalloc: %lld non-empty tensors exceed its fixed table of %d "
+                    "(use al_adamw_step with a workspace)",
+                    (long long)ndesc, al::kAdamWStaticTensors);
+    void* table = nullptr;
+    const hipError_t e = al::adamw_static_table(&table);
+    if (e != hipSuccess) return hip_fail(e, "al_adamw_step_noalloc: static table address");
+    return adamw_run(tensors, nt, cfg, ndesc, table, a, as_stream(stream), "al_adamw_step_noalloc launch");
 }
 
 al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,

@@ -38,12 +38,30 @@ struct AdamWLaunch {
     int64_t chunk_base;  // first chunk of this launch (one wave per chunk)
 };
 
+// Descriptors per copy launch: 60 x 64 bytes keep the argument segment under
+// 4 KB.
+constexpr int kAdamWCopyBatch = 60;
+
 // Device bytes of the descriptor table of nt tensors (descriptors, then the
 // packed chunk offsets), each part 256-byte aligned.
 size_t adamw_table_bytes(int64_t nt);
+// Copy `count` descriptors (host array) to entries offset.. of an nt-entry
+// table at `table`, on the stream.
+hipError_t adamw_write_batch(const AdamWDesc* host, int count, int offset, void* table, int64_t nt, hipStream_t s);
+// Point a.D / a.tb / a.nt at an nt-entry table.
+void adamw_bind_table(void* table, int64_t nt, AdamWLaunch& a);
 // Write nt descriptors (host array) into a table at `table` on the stream and
-// point a.D / a.tb at it.
+// bind it.
 hipError_t adamw_write_table(const AdamWDesc* host, int nt, void* table, AdamWLaunch& a, hipStream_t s);
+
+// The allocation-free AdamW entry point keeps its table in a fixed device
+// array of kAdamWScratchBytes (room for kAdamWStaticTensors descriptors) per
+// GPU; adamw_static_table returns its device address on the current device
+// (looked up once per device).
+constexpr int kAdamWStaticTensors = 4096;
+constexpr size_t kAdamWScratchBytes = 4096 * 64 + 4096 * 8;  // 288 KiB
+constexpr int kMaxDevices = 64;
+hipError_t adamw_static_table(void** table);
 
 // Elements per tile: max(block of v, 256).
 int adamw_tile_elems(int v_codec, int v_block);

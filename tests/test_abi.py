@@ -173,6 +173,25 @@ def test_adamw_validation():
     assert "NULL" not in al.lib().al_last_error().decode()
 
 
+def test_adamw_noalloc_validation():
+    """The allocation-free AdamW variant validates like al_adamw_step and rejects lists beyond its fixed table of
+    4096 non-empty tensors before any HIP call; empty tensors do not count."""
+    L = al.lib()
+
+    def call(ts, nt=None, cfg=None, step=1):
+        arr = (al.Tensor * max(len(ts), 1))(*ts)
+        cfg = cfg or al.adamw_cfg()
+        al.check(L.al_adamw_step_noalloc(arr, len(ts) if nt is None else nt, ctypes.byref(cfg), step, None))
+
+    assert _status(lambda: call([_t()], step=0)) == 1
+    assert _status(lambda: call([_t(m=A + 1)])) == 2
+    assert _status(lambda: call([_t()] * 4097)) == 4
+    assert "4096" in L.al_last_error().decode()
+    empty = _t(rows=0, param=None, grad=None, m=None, v=None, m_meta=None, v_meta=None)
+    call([empty] * 5000)
+    call([])
+
+
 def test_adamw_workspace():
     """The workspace holds the descriptor table: 64 + 8 bytes per non-empty tensor in two 256-byte aligned
     parts; a call without it (or with too little, or misaligned) is rejected before any HIP call."""
