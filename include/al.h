@@ -137,15 +137,23 @@ typedef struct al_adamw_cfg {
     al_state_spec m, v;
 } al_adamw_cfg;
 
+/* Flags of the factored steps (al_adafactor_cfg / al_came_cfg .flags).
+ * AL_FLAG_EXACT_SUMS: every row and column mean behind the factored states is
+ * recomputed with exact sums (slow). The default path already yields the same
+ * fp32 states bit for bit -- its fast sums are kept only where they provably
+ * round the same way -- so this flag is a check of that path, not a
+ * different result. */
+#define AL_FLAG_EXACT_SUMS 1
+
 /* Adafactor (factored second moment, section 3.1): beta2_t = 1 - t^decay_rate,
  * G2 = g^2 + eps1, R/C = EMA of row/column means of G2, update
  * u = g / sqrt(R_i C_j / mean(R)), clipped by max(1, RMS(u)/clip_threshold);
  * no first moment, no relative step, no parameter scaling.
- * v: AL8, AL16 or FP32 for R, C and 1-D v. */
+ * v: AL8, AL16 or FP32 for R, C and 1-D v. flags: 0 or AL_FLAG_EXACT_SUMS. */
 typedef struct al_adafactor_cfg {
     double lr, eps1, clip_threshold, decay_rate, weight_decay;
     int32_t grad_dtype;
-    int32_t reserved;
+    int32_t flags;
     al_state_spec v;
 } al_adafactor_cfg;
 
@@ -154,11 +162,12 @@ typedef struct al_adafactor_cfg {
  * uhat; m = EMA(beta1) of uhat; residual (uhat - m)^2 + eps2 feeds factored
  * confidence R', C' (EMA beta3); update m / sqrt(R'_i C'_j / mean(R')).
  * 1-D tensors: unfactored v, update = m, no confidence.
- * m: UF8 (block 256) or FP32; v and conf: AL8, AL16 or FP32. */
+ * m: UF8 (block 256) or FP32; v and conf: AL8, AL16 or FP32.
+ * flags: 0 or AL_FLAG_EXACT_SUMS. */
 typedef struct al_came_cfg {
     double lr, beta1, beta2, beta3, eps1, eps2, clip_threshold, weight_decay;
     int32_t grad_dtype;
-    int32_t reserved;
+    int32_t flags;
     al_state_spec m, v, conf;
 } al_came_cfg;
 

@@ -16,6 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libal.so")
 
 FP32, AL8, AL16, UF8 = 0, 1, 2, 3
+FLAG_EXACT_SUMS = 1  # factored steps: recompute every row / column mean exactly (a check of the fast path)
 DTYPE_F32, DTYPE_BF16 = 0, 1
 STATUS = {0: "AL_OK", 1: "AL_EINVAL", 2: "AL_EALIGN", 3: "AL_EWORKSPACE", 4: "AL_EUNSUPPORTED", 5: "AL_EHIP"}
 
@@ -51,14 +52,14 @@ class AdamWCfg(ctypes.Structure):
 class AdafactorCfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("eps1", ctypes.c_double), ("clip_threshold", ctypes.c_double),
                 ("decay_rate", ctypes.c_double), ("weight_decay", ctypes.c_double),
-                ("grad_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32), ("v", StateSpec)]
+                ("grad_dtype", ctypes.c_int32), ("flags", ctypes.c_int32), ("v", StateSpec)]
 
 
 class CAMECfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
                 ("beta3", ctypes.c_double), ("eps1", ctypes.c_double), ("eps2", ctypes.c_double),
                 ("clip_threshold", ctypes.c_double), ("weight_decay", ctypes.c_double),
-                ("grad_dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("grad_dtype", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("m", StateSpec), ("v", StateSpec), ("conf", StateSpec)]
 
 
@@ -275,20 +276,21 @@ def adamw_cfg(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, grad
 
 
 def adafactor_cfg(lr=1e-3, eps1=1e-30, clip_threshold=1.0, decay_rate=-0.8, weight_decay=0.0, grad_bf16=True,
-                  v: Spec | None = None) -> AdafactorCfg:
+                  v: Spec | None = None, exact_sums: bool = False) -> AdafactorCfg:
     v = v or Spec(AL8, 256, log2_floor_of(eps1))
     return AdafactorCfg(lr, eps1, clip_threshold, decay_rate, weight_decay,
-                        DTYPE_BF16 if grad_bf16 else DTYPE_F32, 0, v.c())
+                        DTYPE_BF16 if grad_bf16 else DTYPE_F32, FLAG_EXACT_SUMS if exact_sums else 0, v.c())
 
 
 def came_cfg(lr=1e-4, beta1=0.9, beta2=0.999, beta3=0.9999, eps1=1e-30, eps2=1e-16, clip_threshold=1.0,
              weight_decay=0.0, grad_bf16=True, m: Spec | None = None, v: Spec | None = None,
-             conf: Spec | None = None) -> CAMECfg:
+             conf: Spec | None = None, exact_sums: bool = False) -> CAMECfg:
     m = m or Spec(UF8, 256)
     v = v or Spec(AL16, 128, log2_floor_of(eps1))
     conf = conf or Spec(AL16, 128, log2_floor_of(eps2))
     return CAMECfg(lr, beta1, beta2, beta3, eps1, eps2, clip_threshold, weight_decay,
-                   DTYPE_BF16 if grad_bf16 else DTYPE_F32, 0, m.c(), v.c(), conf.c())
+                   DTYPE_BF16 if grad_bf16 else DTYPE_F32, FLAG_EXACT_SUMS if exact_sums else 0, m.c(), v.c(),
+                   conf.c())
 
 
 def adamw_workspace_bytes(states, cfg: AdamWCfg, arr=None) -> int:

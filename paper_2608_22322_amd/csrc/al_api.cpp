@@ -93,6 +93,7 @@ al_status check_adafactor_cfg(const al_adafactor_cfg* cfg) {
         !(cfg->clip_threshold > 0) || !is_fin(cfg->decay_rate) || cfg->decay_rate > 0 ||
         !is_fin(cfg->weight_decay) || cfg->weight_decay < 0)
         return fail(AL_EINVAL, "adafactor: hyperparameters out of range");
+    if (cfg->flags & ~AL_FLAG_EXACT_SUMS) return fail(AL_EINVAL, "adafactor: unknown flags 0x%x", cfg->flags);
     return check_spec(cfg->v, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16), "v");
 }
 
@@ -105,6 +106,7 @@ al_status check_came_cfg(const al_came_cfg* cfg) {
         cfg->weight_decay < 0 || !(cfg->beta1 >= 0 && cfg->beta1 < 1) || !(cfg->beta2 >= 0 && cfg->beta2 < 1) ||
         !(cfg->beta3 >= 0 && cfg->beta3 < 1))
         return fail(AL_EINVAL, "came: hyperparameters out of range");
+    if (cfg->flags & ~AL_FLAG_EXACT_SUMS) return fail(AL_EINVAL, "came: unknown flags 0x%x", cfg->flags);
     al_status st;
     const unsigned nonneg = (1u << AL_CODEC_FP32) | (1u << AL_CODEC_AL8) | (1u << AL_CODEC_AL16);
     if ((st = check_spec(cfg->m, (1u << AL_CODEC_FP32) | (1u << AL_CODEC_UF8), "m")) != AL_OK) return st;
@@ -762,11 +764,12 @@ al_status al_adafactor_step(const al_tensor* tensors, int32_t nt, const al_adafa
     a.v_codec = cfg->v.codec;
     a.v_block = cfg->v.block;
     a.v_floor = cfg->v.log_floor;
+    a.exact_all = (cfg->flags & AL_FLAG_EXACT_SUMS) != 0;
     hipStream_t s = as_stream(stream);
     const int G = cfg->grad_dtype;
     hipError_t e;
     if ((e = al::fac_copy_desc(P.desc.data(), (int)P.desc.size(), const_cast<al::FacDesc*>(a.D), s)) != hipSuccess ||
-        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, s)) != hipSuccess ||
+        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, G, s)) != hipSuccess ||
         (e = al::launch_fac_rms(a, G, s)) != hipSuccess || (e = al::launch_fac_clip(a, s)) != hipSuccess ||
         (e = al::launch_ada_apply(a, G, s)) != hipSuccess || (e = al::launch_ada_vec1d(a, G, s)) != hipSuccess)
         return hip_fail(e, "al_adafactor_step launch");
@@ -805,13 +808,14 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
     a.c_floor = cfg->conf.log_floor;
     a.m_codec = cfg->m.codec;
     a.m_block = cfg->m.codec == AL_CODEC_UF8 ? cfg->m.block : 256;
+    a.exact_all = (cfg->flags & AL_FLAG_EXACT_SUMS) != 0;
     hipStream_t s = as_stream(stream);
     const int G = cfg->grad_dtype;
     hipError_t e;
     if ((e = al::fac_copy_desc(P.desc.data(), (int)P.desc.size(), const_cast<al::FacDesc*>(a.D), s)) != hipSuccess ||
-        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, s)) != hipSuccess ||
+        (e = al::launch_fac_marg_g2(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 0, G, s)) != hipSuccess ||
         (e = al::launch_fac_rms(a, G, s)) != hipSuccess || (e = al::launch_fac_clip(a, s)) != hipSuccess ||
-        (e = al::launch_came_res(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 1, s)) != hipSuccess ||
+        (e = al::launch_came_res(a, G, s)) != hipSuccess || (e = al::launch_fac_fin(a, 1, G, s)) != hipSuccess ||
         (e = al::launch_came_apply(a, G, s)) != hipSuccess || (e = al::launch_came_vec1d(a, G, s)) != hipSuccess)
         return hip_fail(e, "al_came_step launch");
     return AL_OK;

@@ -143,12 +143,13 @@ struct FacArgs {
     double eps1, eps2, lr, decay, clip_d;
     int32_t v_codec, v_block, c_codec, c_block, m_codec, m_block;
     float v_floor, c_floor;
+    int32_t exact_all;  // recompute every factored mean exactly (AL_FLAG_EXACT_SUMS)
     Exp2Coef cf;
 };
 
 hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream_t s);
 hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s);
-hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s);
+hipError_t launch_fac_fin(const FacArgs& a, int role, int grad_dtype, hipStream_t s);
 hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s);
 hipError_t launch_fac_clip(const FacArgs& a, hipStream_t s);
 hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s);

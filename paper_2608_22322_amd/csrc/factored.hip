@@ -20,8 +20,12 @@
 // in-lane column accumulators, and stages its binary64 terms in LDS (8.4 KB
 // per wave, plus 4 KB of row accumulators: 12 waves per CU); 4 lanes then
 // sum each tile row out of LDS.
-// All sums are double-double and every partial is merged in a fixed order, so
-// the means are the exactly rounded ones.
+// Each lane sums its terms in runs of at most 4 plain binary64 additions
+// (relative error <= 3u) accumulated double-double, so every partial is within
+// 3u of its exact sum. The finalize step keeps the fast sum only where that
+// cannot change the fp32 rounding of the state's EMA and otherwise sums the
+// element's row or column again exactly, so the fp32 states (and their codes)
+// are the ones of the exactly rounded means.
 #include "al_codec_dev.hpp"
 #include "al_device.hpp"
 #include "al_internal.hpp"
@@ -87,6 +91,20 @@ __device__ __forceinline__ GD gview(const FacDesc& d) {
     v.nru = d.nru;
     v.ncu = d.ncu;
     return v;
+}
+
+// Term of the second moment's marginal sums: fl64(g^2 + eps1).
+__device__ __forceinline__ double marg_term(float g, double eps1) {
+    const double x = (double)g;
+    return x * x + eps1;
+}
+
+// Term of CAME's confidence marginal sums, from the decoded momentum and the
+// clipped update: m = fl32(beta1 mhat + (1 - beta1) uhat), (uhat - m)^2 + eps2.
+__device__ __forceinline__ double res_term(const FacArgs& a, float mh, float uh) {
+    const float m = (float)(a.beta1 * (double)mh + a.omb1 * (double)uh);
+    const double df = (double)uh - (double)m;
+    return df * df + a.eps2;
 }
 
 template <int G>
@@ -320,6 +338,7 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
             load_graw<G, FULL>(nxt, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
         }
         const int cc = ct * 64 + 4 * lc;
+        double gs[4] = {0.0, 0.0, 0.0, 0.0};  // the lane's 4 rows of each column, summed in row order
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             float gv[4];
@@ -327,19 +346,18 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
             double t[4] = {0.0, 0.0, 0.0, 0.0};
             if (FULL || rg * kTileRows + lr + 4 * i < nr) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (FULL || cc + j < nc) {
-                        const double x = (double)gv[j];
-                        t[j] = x * x + eps1;
-                        dd_add(cacc[j], t[j]);
-                    }
-                }
+                for (int j = 0; j < 4; ++j)
+                    if (FULL || cc + j < nc) t[j] = marg_term(gv[j], eps1);
             }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) gs[j] += t[j];
             // the binary64 terms are staged once for the row sums
             double* tp = &tile[lr + 4 * i][4 * lc];
             *reinterpret_cast<double2*>(tp) = make_double2(t[0], t[1]);
             *reinterpret_cast<double2*>(tp + 2) = make_double2(t[2], t[3]);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dd_add(cacc[j], gs[j]);
         __syncthreads();
         DD rsum{0.0, 0.0};
         const int rr = rg * kTileRows + rrow;
@@ -347,10 +365,10 @@ __device__ __forceinline__ void marg_unit(const FacArgs& a, const GD& d, int64_t
         if (FULL || (rr < nr && cq < nc)) {
             if (FULL || cq + 16 <= nc) {
 #pragma unroll
-                for (int c = 0; c < 16; c += 2) {
-                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
-                    dd_add(rsum, t.x);
-                    dd_add(rsum, t.y);
+                for (int c = 0; c < 16; c += 4) {
+                    const double2 t0 = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c]);
+                    const double2 t1 = *reinterpret_cast<const double2*>(&tile[rrow][16 * rq + c + 2]);
+                    dd_add(rsum, ((t0.x + t0.y) + t1.x) + t1.y);
                 }
             } else {
                 for (int c = 0; c < nc - cq; ++c) dd_add(rsum, tile[rrow][16 * rq + c]);
@@ -474,6 +492,65 @@ __device__ __forceinline__ int locate_blk(const FacDesc* D, int n, int64_t blk, 
     return lo;
 }
 
+// fl32(y) is the same for every binary64 y' within tol of y >= 0: y lies
+// farther than tol from both fp32 rounding midpoints around fl32(y) (the
+// midpoint of two adjacent fp32 values is exact in binary64).
+__device__ __forceinline__ bool f32_round_robust(double y, double tol) {
+    const float f = (float)y;
+    const uint32_t b = f2u(f);
+    if (b >= 0x7F7FFFFFu) return false;  // FLT_MAX, +inf, NaN, negative: take the exact path
+    const float up = u2f(b + 1u);
+    const float dn = b == 0u ? -u2f(1u) : u2f(b - 1u);
+    const double mhi = 0.5 * ((double)f + (double)up), mlo = 0.5 * ((double)f + (double)dn);
+    return (y - mlo > tol) & (mhi - y > tol);
+}
+
+// The decoded momentum of element e (UF8 or fp32).
+__device__ __forceinline__ float came_mhat(const FacArgs& a, const GD& v, int64_t e) {
+    if (a.m_codec == UF8) return uf8_decode(g_as<const int8_t>(v.m)[e], div127((double)v.mm[e / a.m_block]));
+    return g_as<const float>(v.m)[e];
+}
+
+// Exact (double-double) sum of the marginal terms of row idx (isrow) or
+// column idx of a 2-D tensor -- role 0: fl64(g^2 + eps1); role 1: CAME's
+// residual terms -- by the whole wavefront; each term is formed exactly as the
+// marginal kernels form it.
+template <int G>
+__device__ DD exact_line_sum(const FacArgs& a, const FacDesc& d, int role, bool isrow, int64_t idx, int lane) {
+    const GD v = gview(d);
+    const int64_t len = isrow ? d.cols : d.rows;
+    const double clip = role ? v.scal[0] : 1.0;
+    const double rclip = 1.0 / clip;
+    DD acc{0.0, 0.0};
+#pragma unroll 4
+    for (int64_t k = lane; k < len; k += 64) {
+        const int64_t i = isrow ? idx : k, j = isrow ? k : idx;
+        const int64_t e = i * d.cols + j;
+        float g;
+        if constexpr (G == G_BF16)
+            g = bf16_to_f32(g_as<const uint16_t>(v.g)[e]);
+        else
+            g = g_as<const float>(v.g)[e];
+        double t;
+        if (role == 0) {
+            t = marg_term(g, a.eps1);
+        } else {
+            const double uu = (v.rfac[i] * v.cfac[j]) * (double)g;
+            t = res_term(a, came_mhat(a, v, e), div_to_f32(uu, clip, rclip));
+        }
+        dd_add(acc, t);
+    }
+    return dd_wave_sum(acc);
+}
+
+// Relative distance from an fp32 rounding midpoint below which the EMA value
+// from the fast partial sums may round differently from the one from the exact
+// sum: the partials sum their terms in runs of at most 4 plain binary64
+// additions (relative error <= 3u, u = 2^-53) merged double-double, and the
+// mean and EMA add a few roundings; 16u bounds the total.
+constexpr double kRobustTol = 16.0 * 0x1p-53;
+
+template <int G>
 __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int role) {
     const int lane = threadIdx.x & 63;
     const int64_t blk = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -489,29 +566,46 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
     void* codes = isrow ? R.rc : R.cc;
     float* meta = isrow ? R.rm : R.cm;
     float* x = isrow ? d.rtmp : d.ctmp;
-    // 1. EMA of the exact means (each lane handles the elements it encodes)
-    for (int64_t i = s + lane; i < e; i += 64) {
-        DD acc{0.0, 0.0};
-        double mean;
-        // the partials' loads do not depend on the running sum: unrolled, they are issued ahead
-        // (the embedding's column blocks merge 125 row-unit partials per element)
-        if (isrow) {
+    const double cnt = (double)(isrow ? d.cols : d.rows);
+    // 1. EMA of the means (each lane handles the elements it encodes). The
+    // marginal kernels' partials are within 3u of the exact sums; where that
+    // could change the fp32 rounding of the EMA (or with exact_all), the
+    // wavefront sums the element's row or column again, exactly.
+    const int64_t nk = (e - s + 63) / 64;
+    for (int64_t k = 0; k < nk; ++k) {
+        const int64_t i = s + lane + 64 * k;
+        const bool act = i < e;
+        float old = 0.0f;
+        double y = 0.0;
+        if (act) {
+            DD acc{0.0, 0.0};
+            // the partials' loads do not depend on the running sum: unrolled, they are issued ahead
+            // (the embedding's column blocks merge 125 row-unit partials per element)
+            if (isrow) {
 #pragma unroll 8
-            for (int cu = 0; cu < d.ncu; ++cu) {
-                const double* rp = d.rowpart + 2 * ((int64_t)cu * d.rows + i);
-                acc = dd_merge(acc, DD{rp[0], rp[1]});
-            }
-            mean = dd_value(acc) / (double)d.cols;
-        } else {
+                for (int cu = 0; cu < d.ncu; ++cu) {
+                    const double* rp = d.rowpart + 2 * ((int64_t)cu * d.rows + i);
+                    acc = dd_merge(acc, DD{rp[0], rp[1]});
+                }
+            } else {
 #pragma unroll 8
-            for (int ru = 0; ru < d.nru; ++ru) {
-                const double* cp = d.colpart + 2 * ((int64_t)ru * d.cols + i);
-                acc = dd_merge(acc, DD{cp[0], cp[1]});
+                for (int ru = 0; ru < d.nru; ++ru) {
+                    const double* cp = d.colpart + 2 * ((int64_t)ru * d.cols + i);
+                    acc = dd_merge(acc, DD{cp[0], cp[1]});
+                }
             }
-            mean = dd_value(acc) / (double)d.rows;
+            old = vec_decode(R.codec, R.B, codes, meta, i, a.cf);
+            y = R.beta * (double)old + R.omb * (dd_value(acc) / cnt);
         }
-        const float old = vec_decode(R.codec, R.B, codes, meta, i, a.cf);
-        x[i] = (float)(R.beta * (double)old + R.omb * mean);
+        const bool robust = !act || (!a.exact_all && f32_round_robust(y, kRobustTol * y));
+        uint64_t pend = __ballot(!robust);
+        while (pend) {
+            const int src = __builtin_ctzll(pend);
+            pend &= pend - 1;
+            const DD S = exact_line_sum<G>(a, d, role, isrow, s + src + 64 * k, lane);
+            if (lane == src) y = R.beta * (double)old + R.omb * (dd_value(S) / cnt);
+        }
+        if (act) x[i] = (float)y;
     }
     __threadfence_block();  // the encode below reads x[] back (each lane its own elements)
     // 2. re-encode the block
@@ -567,10 +661,13 @@ __global__ __launch_bounds__(256) void fac_fin_rows_kernel(const FacArgs a, int 
     for (int64_t i = tid; i < d.rows; i += blockDim.x) R.fr[i] = 1.0 / sqrt((double)d.rtmp[i] / mr);
 }
 
-hipError_t launch_fac_fin(const FacArgs& a, int role, hipStream_t s) {
+hipError_t launch_fac_fin(const FacArgs& a, int role, int grad_dtype, hipStream_t s) {
     if (a.n2 == 0) return hipSuccess;
     const int64_t grid = (a.total_blk[role] + 3) / 4;
-    hipLaunchKernelGGL(fac_fin_block_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, role);
+    if (grad_dtype == G_BF16)
+        hipLaunchKernelGGL(fac_fin_block_kernel<G_BF16>, dim3((unsigned)grid), dim3(256), 0, s, a, role);
+    else
+        hipLaunchKernelGGL(fac_fin_block_kernel<G_F32>, dim3((unsigned)grid), dim3(256), 0, s, a, role);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fac_fin_rows_kernel, dim3(a.n2), dim3(256), 0, s, a, role);
@@ -924,6 +1021,7 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
             const int ct1 = (it + 1) / nrg;
             load_resraw<G, FULL, UF>(nxt, a, d, r0, c0, nr, nc, it + 1 - ct1 * nrg, ct1, lr, lc, vec, lane_off);
         }
+        double gs[4] = {0.0, 0.0, 0.0, 0.0};  // the lane's 4 rows of each column, summed in row order
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int rr = rg * kResRows + lr + 2 * i;
@@ -963,19 +1061,17 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
                 for (int j = 0; j < 4; ++j) uu[j] = (cur.ri[i] * cf[j]) * (double)gv[j];
                 div4_to_f32(uu, clip, rclip, uh);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (FULL || cc + j < nc) {
-                        const float m = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
-                        const double df = (double)uh[j] - (double)m;
-                        term[j] = df * df + a.eps2;
-                        dd_add(cacc[j], term[j]);
-                    }
-                }
+                for (int j = 0; j < 4; ++j)
+                    if (FULL || cc + j < nc) term[j] = res_term(a, mh[j], uh[j]);
             }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) gs[j] += term[j];
             double* tp = &tile[lr + 2 * i][4 * lc];
             *reinterpret_cast<double2*>(tp) = make_double2(term[0], term[1]);
             *reinterpret_cast<double2*>(tp + 2) = make_double2(term[2], term[3]);
         }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dd_add(cacc[j], gs[j]);
         __syncthreads();
         DD rsum{0.0, 0.0};
         const int rr = rg * kResRows + rrow;
@@ -983,14 +1079,12 @@ __device__ __forceinline__ void res_unit(const FacArgs& a, const GD& d, double c
         if (FULL || (rr < nr && cq < nc)) {
             const int cnt = nc - cq < 16 ? nc - cq : 16;
             if (FULL || cnt == 16) {
-                DD r2{0.0, 0.0};  // a second chain for the odd columns
 #pragma unroll
-                for (int c = 0; c < 16; c += 2) {
-                    const double2 t = *reinterpret_cast<const double2*>(&tile[rrow][16 * re + c]);
-                    dd_add(rsum, t.x);
-                    dd_add(r2, t.y);
+                for (int c = 0; c < 16; c += 4) {
+                    const double2 t0 = *reinterpret_cast<const double2*>(&tile[rrow][16 * re + c]);
+                    const double2 t1 = *reinterpret_cast<const double2*>(&tile[rrow][16 * re + c + 2]);
+                    dd_add(rsum, ((t0.x + t0.y) + t1.x) + t1.y);
                 }
-                rsum = dd_merge(rsum, r2);
             } else {
                 for (int c = 0; c < cnt; ++c) dd_add(rsum, tile[rrow][16 * re + c]);
             }

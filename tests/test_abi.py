@@ -306,6 +306,10 @@ def test_adafactor_cfg_validation():
     cfg = al.adafactor_cfg()
     cfg.grad_dtype = 9
     assert _status(lambda: _fac_step(t, False, cfg=cfg, ws_bytes=1 << 20)) == 1
+    cfg = al.adafactor_cfg()
+    cfg.flags = 2  # only AL_FLAG_EXACT_SUMS (1) is defined
+    assert _status(lambda: _fac_step(t, False, cfg=cfg, ws_bytes=1 << 20)) == 1
+    assert al.adafactor_cfg(exact_sums=True).flags == al.FLAG_EXACT_SUMS == 1
 
 
 def test_came_cfg_validation():
@@ -318,6 +322,10 @@ def test_came_cfg_validation():
                dict(conf=al.Spec(al.AL16, 4096))):
         assert _status(lambda: _fac_step(t, True, cfg=al.came_cfg(**kw), ws_bytes=1 << 20)) == 1, kw
     assert _status(lambda: _fac_step(t, True, cfg=al.came_cfg(m=al.Spec(al.UF8, 128)), ws_bytes=1 << 20)) == 4
+    cfg = al.came_cfg()
+    cfg.flags = 3
+    assert _status(lambda: _fac_step(t, True, cfg=cfg, ws_bytes=1 << 20)) == 1
+    assert al.came_cfg(exact_sums=True).flags == 1
 
 
 def test_tinyllama_workspace_sizes():

@@ -42,7 +42,7 @@ def _spec(al, codec, block, floor):
 class FacPair:
     """A tensor list held on the GPU (library) and on the host (oracle) for Adafactor or CAME."""
 
-    def __init__(self, dev, shapes, w, came, vspec, mspec=None, cspec=None, sample=None):
+    def __init__(self, dev, shapes, w, came, vspec, mspec=None, cspec=None, sample=None, exact=False):
         import torch
 
         import paper_2608_22322_amd as al
@@ -79,10 +79,10 @@ class FacPair:
                 h["m"] = st(mspec, s.n)
             self.host[i] = h
         if came:
-            self.cfg = al.came_cfg(grad_bf16=w.grad_bf16, m=mspec, v=vspec, conf=cspec)
+            self.cfg = al.came_cfg(grad_bf16=w.grad_bf16, m=mspec, v=vspec, conf=cspec, exact_sums=exact)
             nbytes = al.came_workspace_bytes(self.states, self.cfg)
         else:
-            self.cfg = al.adafactor_cfg(grad_bf16=w.grad_bf16, v=vspec)
+            self.cfg = al.adafactor_cfg(grad_bf16=w.grad_bf16, v=vspec, exact_sums=exact)
             nbytes = al.adafactor_workspace_bytes(self.states, self.cfg)
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
         self.arr = al.tensor_array(self.states)
@@ -262,3 +262,35 @@ def test_full_llama7b_list_sampled(dev, came):
     log(f"near-boundary code differences: {near}")
     del pair
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("came", [False, True])
+def test_exact_sums_flag_gives_identical_states(dev, came):
+    """The marginal kernels' fast sums are kept only where they provably round like the exact ones. Stepping
+    the same list with AL_FLAG_EXACT_SUMS (every row and column mean summed again exactly in the finalize
+    step) must give the same codes, metadata and parameters bit for bit, and both match the oracle:
+    TinyLlama-shaped tensors and ragged ones, 6 steps."""
+    import torch
+
+    import paper_2608_22322_amd as al
+
+    shapes = [Shape("k", 256, 2048), Shape("norm", 1, 2048), Shape("slab", 300, 513), Shape("tall", 1030, 64)]
+    w = Workload("exact-vs-fast", shapes, zero_frac=0.02, steps=6)
+    if came:
+        kw = dict(vspec=_spec(al, "AL16", 128, F1), mspec=_spec(al, "UF8", 256, 0.0), cspec=_spec(al, "AL16", 128, F2))
+    else:
+        kw = dict(vspec=_spec(al, "AL8", 256, F1))
+    fast = FacPair(dev, shapes, w, came, **kw)
+    exact = FacPair(dev, shapes, w, came, exact=True, sample=[], **kw)
+    for t in range(1, 7):
+        fast.step(t)
+        exact.step(t)
+        fast.compare(t, 1e-5 if t == 1 else 1e-4)
+        for i, (a, b) in enumerate(zip(fast.states, exact.states)):
+            for name in ("param", "m", "m_meta", "v", "v_meta", "vr", "vr_meta", "vc", "vc_meta", "cr", "cr_meta",
+                         "cc", "cc_meta"):
+                x, y = getattr(a, name), getattr(b, name)
+                if x is None:
+                    continue
+                assert torch.equal(x, y), f"step {t} tensor {i} {name}: exact-sums path differs"
+    log(f"{'CAME' if came else 'Adafactor'}: fast and exact-sum paths identical over 6 steps")
