@@ -296,35 +296,101 @@ def time_apollo(steps: int, warmup: int):
     return rec
 
 
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(shapes, block_v):
-    """The oracle, untuned, on a bounded sample: layer 0's seven weight matrices, five steps. Inputs for this
-    timing-only leg are drawn with numpy's generator (same shapes and distributions as the workload: params
-    N(0, 0.02), bf16 grads N(0, 1e-3) with 1% zeros); bit-reproducible inputs are only needed for parity."""
+    """The oracle, untuned, on a bounded sample of the 7B list, one thread per tensor (parallel over tensors
+    only, as the oracle's steps are per tensor): AdamW on layer 0's seven weight matrices (2 steps, AL8 B_V
+    block_v + UF8), Adafactor on layer 0's q/k/v/o (1 step, AL8 B256 factors) and CAME on layer 0's q and k
+    (1 step, AL16 B128 factors and confidence, UF8 m). Inputs for this timing-only leg are drawn with numpy's
+    generator (params N(0, 0.02), bf16 grads N(0, 1e-3) with 1% zeros); bit-reproducible inputs are only
+    needed for parity. Wall-clock throughput of each leg; ``value`` is the AdamW leg (the headline path)."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     import oracle
     from paper_2608_22322_amd import synth
 
+    host_cores = len(os.sched_getaffinity(0))
     rng = np.random.default_rng(921)
-    idx = [i for i, s in enumerate(shapes) if s.name.startswith("layer0.") and s.is_2d]
-    floor = float(np.float32(2 * math.log2(1e-8)))
-    n_total, secs = 0, 0.0
-    for i in idx:
-        s = shapes[i]
-        p = rng.standard_normal(s.n, dtype=np.float32) * np.float32(0.02)
-        g = rng.standard_normal(s.n, dtype=np.float32) * np.float32(1e-3)
-        g[rng.random(s.n, dtype=np.float32) < 0.01] = 0.0
-        g = synth.to_bf16_bits(g)
-        m = oracle.State(oracle.UF8, s.n, 256)
-        v = oracle.State(oracle.AL8, s.n, block_v, floor)
-        for t in range(1, 6):
-            t0 = time.perf_counter()
-            oracle.adamw_step(p, g, m, v, t)
-            secs += time.perf_counter() - t0
-            n_total += s.n
-    return {"value": n_total / secs / 1e9, "unit": "Gparams/s", "cores": 1, "kind": "oracle",
-            "sample": f"Llama-7B layer-0 weight matrices ({n_total // 5:,} params), 5 AdamW steps, "
-                      f"AL8 B_V {block_v} + UF8, single-threaded binary64 C oracle; {secs:.1f} s of CPU time"}
+    fl32 = lambda x: float(np.float32(x))
+    layer0 = {s.name.split(".", 1)[1]: s for s in shapes if s.name.startswith("layer0.") and s.is_2d}
+
+    # one pool of draws, sliced per tensor (gradients are only read; each tensor gets its own params)
+    pool_n = max(s.n for s in layer0.values())
+    p_pool = rng.standard_normal(pool_n, dtype=np.float32) * np.float32(0.02)
+    g_pool = rng.standard_normal(pool_n, dtype=np.float32) * np.float32(1e-3)
+    g_pool[rng.random(pool_n, dtype=np.float32) < 0.01] = 0.0
+    g_pool = synth.to_bf16_bits(g_pool)
+
+    def inputs(s):
+        return p_pool[: s.n].copy(), g_pool[: s.n]
+
+    def touched(st):
+        for a in (st.codes, st.meta, st.y):  # fault the pages in outside the timed region
+            a.fill(0)
+        return st
+
+    def adamw(s):
+        m = touched(oracle.State(oracle.UF8, s.n, 256))
+        v = touched(oracle.State(oracle.AL8, s.n, block_v, fl32(2 * math.log2(1e-8))))
+
+        def run(p, g):
+            for t in (1, 2):
+                oracle.adamw_step(p, g, m, v, t)
+            return 2 * s.n
+        return run
+
+    def adafactor(s):
+        f = fl32(math.log2(1e-30))
+        vr, vc = touched(oracle.State(oracle.AL8, s.rows, 256, f)), touched(oracle.State(oracle.AL8, s.cols, 256, f))
+
+        def run(p, g):
+            oracle.adafactor_step(p, g, s.rows, s.cols, vr, vc, None, 1)
+            return s.n
+        return run
+
+    def came(s):
+        f1, f2 = fl32(math.log2(1e-30)), fl32(math.log2(1e-16))
+        st = lambda n, f: touched(oracle.State(oracle.AL16, n, 128, f))
+        m = touched(oracle.State(oracle.UF8, s.n, 256))
+        vr, vc, cr, cc = st(s.rows, f1), st(s.cols, f1), st(s.rows, f2), st(s.cols, f2)
+
+        def run(p, g):
+            oracle.came_step(p, g, s.rows, s.cols, m, vr, vc, None, cr, cc, 1)
+            return s.n
+        return run
+
+    legs = {}
+    for name, make, names, what in (
+            ("adamw", adamw, ("q", "k", "v", "o", "gate", "up", "down"),
+             f"layer-0 weight matrices, 2 AdamW steps, AL8 B_V {block_v} + UF8"),
+            ("adafactor", adafactor, ("q", "k", "v", "o"), "layer-0 q/k/v/o, 1 Adafactor step, AL8 B256 factors"),
+            ("came", came, ("q", "k"), "layer-0 q/k, 1 CAME step, AL16 B128 factors + confidence, UF8 m")):
+        sel = [layer0[k] for k in names]
+        jobs = [(make(s), *inputs(s)) for s in sel]  # states and inputs built (and touched) before timing
+        threads = min(host_cores, len(sel))
+        t0 = time.perf_counter()
+        with ThreadPoolExecutor(threads) as ex:
+            n_done = sum(ex.map(lambda j: j[0](j[1], j[2]), jobs))
+        secs = time.perf_counter() - t0
+        legs[name] = {"value": n_done / secs / 1e9, "unit": "Gparams/s", "threads": threads,
+                      "sample": f"{what} ({sum(s.n for s in sel):,} params)", "wall_s": round(secs, 2)}
+        log(f"cpu oracle {name}: " + json.dumps(legs[name]))
+        del jobs
+    a = legs["adamw"]
+    return {"value": a["value"], "unit": "Gparams/s", "cores": a["threads"], "kind": "oracle",
+            "sample": f"Llama-7B {a['sample']}, binary64 C oracle, one thread per tensor; {a['wall_s']} s wall",
+            "host_cores": host_cores, "cpu_model": _cpu_model(), "paths": legs}
 
 
 PATHS = ("adafactor", "came", "adafactor_7b", "came_7b", "apollo")
