@@ -3,6 +3,7 @@
 // caller's stream. See include/al.h for the contract of each entry point.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -128,7 +129,7 @@ al_status check_ws(void* ws, size_t ws_bytes, size_t need, const char* who) {
 struct FacPlan {
     std::vector<al::FacDesc> desc;  // 2-D tensors first, then 1-D
     int n2 = 0, n1 = 0;
-    int64_t total_units = 0, total_chunks = 0;
+    int64_t total_units = 0, total_chunks = 0, whole_units = 0;
     int64_t total_blk[2] = {0, 0};
     size_t bytes = 0;
     size_t rms_off = 0;
@@ -178,6 +179,10 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
             if ((st = check_unused(t.m, t.m_meta, "m", i)) != AL_OK) return st;
         }
     }
+    // 2-D tensors made of whole 256x256 units first (their units take the
+    // streaming kernels' guard-free layout), in list order within each group
+    std::stable_partition(twod.begin(), twod.end(),
+                          [&](int i) { return ts[i].rows % 256 == 0 && ts[i].cols % 256 == 0; });
     P.n2 = (int)twod.size();
     P.n1 = (int)oned.size();
     const int ntot = P.n2 + P.n1;
@@ -189,6 +194,7 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
         d.ncu = (int32_t)((t.cols + 255) / 256);
         d.unit_begin = P.total_units;
         P.total_units += (int64_t)d.nru * d.ncu;
+        if (t.rows % 256 == 0 && t.cols % 256 == 0) P.whole_units = P.total_units;
         d.chunk_begin = P.total_chunks;  // chunks only for widths that are not a multiple of 256
         if (t.cols % 256 != 0) P.total_chunks += (t.rows * t.cols + 1023) / 1024;
         const int64_t bv = vs.block, bc = came ? cs.block : vs.block;
@@ -259,6 +265,7 @@ al::FacArgs fac_args(const FacPlan& P, char* ws) {
     a.n1 = P.n1;
     a.total_units = P.total_units;
     a.total_chunks = P.total_chunks;
+    a.whole_units = P.whole_units;
     a.total_blk[0] = P.total_blk[0];
     a.total_blk[1] = P.total_blk[1];
     a.cf = al::exp2_coef();
@@ -808,6 +815,7 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
     a.c_floor = cfg->conf.log_floor;
     a.m_codec = cfg->m.codec;
     a.m_block = cfg->m.codec == AL_CODEC_UF8 ? cfg->m.block : 256;
+    a.exact_rms = 1;
     a.exact_all = (cfg->flags & AL_FLAG_EXACT_SUMS) != 0;
     hipStream_t s = as_stream(stream);
     const int G = cfg->grad_dtype;

@@ -294,6 +294,14 @@ __device__ __forceinline__ DD dd_quad_xor(DD a) {
     return DD{__builtin_bit_cast(double, h2), __builtin_bit_cast(double, l2)};
 }
 
+// A binary64 value of another lane of the same DPP row (CTRL: a quad
+// permutation or a row mirror).
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double x) {
+    const uint64_t b = __builtin_bit_cast(uint64_t, x);
+    return __builtin_bit_cast(double, ((uint64_t)dpp<CTRL>((uint32_t)(b >> 32)) << 32) | dpp<CTRL>((uint32_t)b));
+}
+
 // Wave-wide merge; every lane gets the total (fixed butterfly order).
 __device__ __forceinline__ DD dd_wave_sum(DD a) {
 #pragma unroll
@@ -428,6 +436,8 @@ __device__ __forceinline__ int64_t xcd_order(uint32_t wg, uint32_t grid) {
 // bytes. The non-temporal builtins take clang vector types, not HIP's structs.
 typedef float nt_f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t nt_u2 __attribute__((ext_vector_type(2)));
+typedef uint32_t nt_u4 __attribute__((ext_vector_type(4)));
+typedef double nt_d2 __attribute__((ext_vector_type(2)));
 
 template <bool NT>
 __device__ __forceinline__ float4 ld_f4(const float* p) {
@@ -512,6 +522,19 @@ __device__ __forceinline__ uint2 ld_u2(gp<const void> p) {
         return make_uint2(x.x, x.y);
     }
 }
+template <bool NT>
+__device__ __forceinline__ uint4 ld_u4(gp<const void> p) {
+    if constexpr (NT) {
+        const nt_u4 x = __builtin_nontemporal_load(g_as<const nt_u4>(p));
+        return make_uint4(x.x, x.y, x.z, x.w);
+    } else {
+        const nt_u4 x = *g_as<const nt_u4>(p);
+        return make_uint4(x.x, x.y, x.z, x.w);
+    }
+}
+// Two binary64 values to 16-byte aligned global memory.
+__device__ __forceinline__ void st_d2(gp<double> p, double x, double y) { *g_as<nt_d2>(p) = nt_d2{x, y}; }
+
 template <bool NT>
 __device__ __forceinline__ uint32_t ld_u1(gp<const void> p) {
     if constexpr (NT)

@@ -136,6 +136,9 @@ struct FacArgs {
     double* rmspart;      // [total_units] (hi, lo): partial sums of u^2
     int32_t n2, n1;       // 2-D tensors, 1-D tensors (D[n2 .. n2 + n1))
     int64_t total_units, total_chunks;
+    // units [0, whole_units) belong to the tensors listed first, whose rows and
+    // columns are both multiples of 256 (every unit a full 256x256 tile)
+    int64_t whole_units;
     int64_t total_blk[2];  // code blocks over all 2-D tensors' R and C, per role
     double beta, omb;     // second-moment EMA: Adafactor beta2_t / CAME beta2, and 1 - beta
     double beta1, omb1;   // CAME momentum
@@ -144,6 +147,7 @@ struct FacArgs {
     int32_t v_codec, v_block, c_codec, c_block, m_codec, m_block;
     float v_floor, c_floor;
     int32_t exact_all;  // recompute every factored mean exactly (AL_FLAG_EXACT_SUMS)
+    int32_t exact_rms;  // RMS sums term by term double-double (CAME: the clip feeds its states)
     Exp2Coef cf;
 };
 

@@ -426,12 +426,13 @@ __global__ __launch_bounds__(64) void fac_marg_g2_kernel(const FacArgs a, int64_
         marg_unit<G, false>(a, gview(d), ru, cu, nr, nc, vec, tile, racc);
 }
 
-// One 64-thread workgroup per unit; lists beyond 2^31 units take several launches.
+// One 64-thread workgroup per unit of [begin, end); lists beyond 2^31 units
+// take several launches. Each kernel checks unit < end itself.
 template <class K>
-static hipError_t launch_per_unit(K kernel, const FacArgs& a, hipStream_t s) {
+static hipError_t launch_per_unit(K kernel, const FacArgs& a, int64_t begin, int64_t end, hipStream_t s) {
     constexpr int64_t kMaxGrid = int64_t(1) << 31;
-    for (int64_t base = 0; base < a.total_units; base += kMaxGrid) {
-        const int64_t left = a.total_units - base;
+    for (int64_t base = begin; base < end; base += kMaxGrid) {
+        const int64_t left = end - base;
         const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
         hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(64), 0, s, a, base);
         const hipError_t e = hipGetLastError();
@@ -440,10 +441,222 @@ static hipError_t launch_per_unit(K kernel, const FacArgs& a, hipStream_t s) {
     return hipSuccess;
 }
 
+// ------------------------------ marginal sums over whole units (streaming)
+// Units of the tensors whose rows and columns are both multiples of 256: no
+// guards, and every unit row starts 16-byte aligned. A batch is 8 unit rows.
+// Lane l = 32 h + q reads columns 8q .. 8q + 7 of rows 2k + h (k < 4) of the
+// batch: 16 bytes of bf16 gradients per lane, one load instruction per pair of
+// unit rows, the next batch's loads issued before the current batch's
+// arithmetic. Rows: each lane adds its 8 terms pairwise (relative error <= 3u
+// for non-negative terms) and stages that partial in LDS; 8 lanes then finish
+// each row from 4 partials apiece (pairwise, then a quad and a half-row DPP
+// merge), so a row's partial over the unit has relative error <= 8u and needs
+// no further merge inside the unit. Columns: the loading lanes add their terms
+// in plain runs over 16 of their rows (<= 15u) and add the 8 runs of the unit
+// (<= 7u more); the even- and odd-row halves merge at the end (1u): a column
+// partial has relative error <= 23u. The finalize step's robustness margin
+// covers these bounds.
+constexpr int kWStride = 34;  // LDS stride of a staged row, in doubles (16-byte aligned rows)
+constexpr int kWRunRows = 32; // unit rows per plain column run (16 rows of each lane)
+
+template <int G>
+struct Raw8 {
+    uint4 w;  // 8 bf16
+};
+template <>
+struct Raw8<G_F32> {
+    float4 a, b;
+};
+
+template <int G>
+__device__ __forceinline__ void unpack8(const Raw8<G>& r, float gv[8]) {
+    if constexpr (G == G_BF16) {
+        const uint32_t w[4] = {r.w.x, r.w.y, r.w.z, r.w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            gv[2 * i] = u2f(w[i] << 16);
+            gv[2 * i + 1] = u2f(w[i] & 0xFFFF0000u);
+        }
+    } else {
+        gv[0] = r.a.x, gv[1] = r.a.y, gv[2] = r.a.z, gv[3] = r.a.w;
+        gv[4] = r.b.x, gv[5] = r.b.y, gv[6] = r.b.z, gv[7] = r.b.w;
+    }
+}
+
+__device__ __forceinline__ double sum8(const double t[8]) {
+    return ((t[0] + t[1]) + (t[2] + t[3])) + ((t[4] + t[5]) + (t[6] + t[7]));
+}
+
+// Gradients of a batch of NR unit rows (NR / 2 row pairs) of one lane.
+template <int G, int NR>
+struct WBatch {
+    Raw8<G> r[NR / 2];
+};
+
+// Batch at unit row rb: the wave-uniform part of each address (row base) plus
+// the lane's 32-bit offset lo, so the loads take the scalar-base form.
+template <int G, int NR>
+__device__ __forceinline__ void load_wbatch(WBatch<G, NR>& b, gp<const void> g, int64_t rb, int64_t cols, uint32_t lo) {
+#pragma unroll
+    for (int k = 0; k < NR / 2; ++k) {
+        if constexpr (G == G_BF16) {
+            const gp<const uint16_t> row = g_as<const uint16_t>(g) + (rb + 2 * k) * cols;
+            b.r[k].w = ld_u4<false>(g_as<const void>(row + lo));
+        } else {
+            const gp<const float> row = g_as<const float>(g) + (rb + 2 * k) * cols;
+            b.r[k].a = ld_f4<false>(row + lo);
+            b.r[k].b = ld_f4<false>(row + lo + 4);
+        }
+    }
+}
+
+// Shared part of the whole-unit marginal kernels, batches of P::NR unit rows
+// (4 or 8). The policy P supplies the batch type, load(batch, rb) for the
+// rows from rb, and terms(batch, k, t): the 8 binary64 terms of the lane's
+// row 2k + h of that batch. Row partials go to rowpart (lo = 0), column
+// partials to colpart; stage holds NR x kWStride doubles.
+template <class P>
+__device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64_t ru, int64_t cu, double* stage) {
+    constexpr int NR = P::NR, NP = NR / 2, LPR = 64 / NR, PPL = 32 / LPR;  // lanes per row, partials per lane
+    static_assert(NR == 4 || NR == 8, "batch rows");
+    const int lane = threadIdx.x, h = lane >> 5, q = lane & 31;
+    const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
+    const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of the batch, partials PPL rpart ..
+    double cacc[8], crun[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        cacc[j] = 0.0;
+        crun[j] = 0.0;
+    }
+    typename P::Batch A, B;
+    pol.load(A, 0);
+    auto step = [&](const typename P::Batch& cur, int bi) {
+#pragma unroll
+        for (int k = 0; k < NP; ++k) {
+            double t[8];
+            pol.terms(cur, k, t);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                crun[j] += t[j];
+                // one row pair's terms live at a time: without this the compiler forms all terms of the
+                // batch before the column additions (many more registers, lower occupancy)
+                __asm__ volatile("" : "+v"(crun[j]));
+            }
+            stage[(2 * k + h) * kWStride + q] = sum8(t);
+        }
+        __syncthreads();
+        // row rrow of the batch: partials PPL rpart .. PPL rpart + PPL - 1 of its 32, pairwise
+        double rs;
+        const double2 p0 = *reinterpret_cast<const double2*>(&stage[rrow * kWStride + PPL * rpart]);
+        if constexpr (PPL == 4) {
+            const double2 p1 = *reinterpret_cast<const double2*>(&stage[rrow * kWStride + PPL * rpart + 2]);
+            rs = (p0.x + p0.y) + (p1.x + p1.y);
+        } else {
+            rs = p0.x + p0.y;
+        }
+        rs += dpp_d<kDppQuadXor1>(rs);
+        rs += dpp_d<kDppQuadXor2>(rs);
+        rs += dpp_d<kDppRowHalfMirror>(rs);
+        if constexpr (LPR == 16) rs += dpp_d<kDppRowMirror>(rs);
+        if (rpart == 0) {
+            const gp<double> rp = d.rowpart + 2 * (cu * d.rows + r0 + NR * bi + rrow);
+            st_d2(rp, rs, 0.0);
+        }
+        __syncthreads();
+        if ((bi + 1) % (kWRunRows / NR) == 0) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                cacc[j] += crun[j];
+                crun[j] = 0.0;
+            }
+        }
+    };
+    // The last pair of batches is peeled: with a conditional load inside the
+    // loop the compiler's wait counts would have to hold for both paths, and
+    // every odd batch would wait for the next even batch's loads.
+    constexpr int NB = 256 / NR;
+#pragma unroll 1
+    for (int bi = 0; bi < NB - 2; bi += 2) {
+        pol.load(B, (bi + 1) * NR);
+        step(A, bi);
+        pol.load(A, (bi + 2) * NR);
+        step(B, bi + 1);
+    }
+    pol.load(B, (NB - 1) * NR);
+    step(A, NB - 2);
+    step(B, NB - 1);
+    // the two halves hold the even and the odd rows of the same columns
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cacc[j] += __shfl_xor(cacc[j], 32);
+    if (h == 0) {
+        const gp<double> cp = d.colpart + 2 * (ru * cols + c0 + 8 * q);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) st_d2(cp + 2 * j, cacc[j], 0.0);
+    }
+}
+
+// The lane's place in a whole unit: the unit's first gradient element as a
+// wave-uniform byte address and the lane's element offset from it.
+struct WholeLane {
+    int64_t r0, c0, cols;
+    uint32_t lo;  // h * cols + 8 q
+    int h, q;
+};
+
+__device__ __forceinline__ WholeLane whole_lane(const GD& d, int64_t u) {
+    WholeLane w;
+    w.h = (int)threadIdx.x >> 5;
+    w.q = (int)threadIdx.x & 31;
+    w.r0 = (u / d.ncu) * 256;
+    w.c0 = (u % d.ncu) * 256;
+    w.cols = d.cols;
+    w.lo = (uint32_t)(w.h * d.cols + 8 * w.q);
+    return w;
+}
+
+template <int G>
+__device__ __forceinline__ gp<const void> unit_base(const GD& d, const WholeLane& w) {
+    return g_as<const void>(g_as<const uint8_t>(d.g) + (G == G_BF16 ? 2 : 4) * (w.r0 * w.cols + w.c0));
+}
+
+// Terms of the second moment's marginals: fl64(g^2 + eps1).
+template <int G>
+struct MargTerms {
+    static constexpr int NR = 8;
+    using Batch = WBatch<G, NR>;
+    gp<const void> gu;
+    int64_t cols;
+    uint32_t lo;
+    double eps1;
+    __device__ void load(Batch& b, int rb) const { load_wbatch<G, NR>(b, gu, rb, cols, lo); }
+    __device__ void terms(const Batch& b, int k, double t[8]) const {
+        float gv[8];
+        unpack8<G>(b.r[k], gv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t[j] = marg_term(gv[j], eps1);
+    }
+};
+
+template <int G>
+__global__ __launch_bounds__(64) void fac_marg_whole_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double stage[MargTerms<G>::NR * kWStride];
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const WholeLane w = whole_lane(d, unit - d.unit_begin);
+    const MargTerms<G> pol{unit_base<G>(d, w), w.cols, w.lo, a.eps1};
+    whole_unit_sums(pol, d, w.r0 / 256, w.c0 / 256, stage);
+}
+
 hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    return grad_dtype == G_BF16 ? launch_per_unit(fac_marg_g2_kernel<G_BF16>, a, s)
-                                : launch_per_unit(fac_marg_g2_kernel<G_F32>, a, s);
+    hipError_t e;
+    if (grad_dtype == G_BF16) {
+        if ((e = launch_per_unit(fac_marg_whole_kernel<G_BF16>, a, 0, a.whole_units, s)) != hipSuccess) return e;
+        return launch_per_unit(fac_marg_g2_kernel<G_BF16>, a, a.whole_units, a.total_units, s);
+    }
+    if ((e = launch_per_unit(fac_marg_whole_kernel<G_F32>, a, 0, a.whole_units, s)) != hipSuccess) return e;
+    return launch_per_unit(fac_marg_g2_kernel<G_F32>, a, a.whole_units, a.total_units, s);
 }
 
 // ------------------------------------------------------------- finalize
@@ -545,10 +758,13 @@ __device__ DD exact_line_sum(const FacArgs& a, const FacDesc& d, int role, bool 
 
 // Relative distance from an fp32 rounding midpoint below which the EMA value
 // from the fast partial sums may round differently from the one from the exact
-// sum: the partials sum their terms in runs of at most 4 plain binary64
-// additions (relative error <= 3u, u = 2^-53) merged double-double, and the
-// mean and EMA add a few roundings; 16u bounds the total.
-constexpr double kRobustTol = 16.0 * 0x1p-53;
+// sum. A partial is within 23u (u = 2^-53) of its exact sum: the whole-unit
+// kernels' column partials (plain runs of 16 binary64 additions of
+// non-negative terms, 8 runs added, two halves merged; their row partials:
+// 8u), the other units' runs of at most 4 (3u) accumulated double-double; the
+// partials are merged double-double, and the mean and the EMA add at most 4u.
+// 32u bounds the total.
+constexpr double kRobustTol = 32.0 * 0x1p-53;
 
 template <int G>
 __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int role) {
@@ -780,10 +996,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6))) void f
 // One wavefront per unit (4 per 256-thread workgroup); lists beyond 2^33 units
 // take several launches.
 template <class K>
-static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, hipStream_t s) {
+static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, int64_t begin, int64_t end, hipStream_t s) {
     constexpr int64_t kMaxGrid = int64_t(1) << 31;
-    for (int64_t base = 0; base < a.total_units; base += 4 * kMaxGrid) {
-        const int64_t left = (a.total_units - base + 3) / 4;
+    for (int64_t base = begin; base < end; base += 4 * kMaxGrid) {
+        const int64_t left = (end - base + 3) / 4;
         const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
         hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, s, a, base);
         const hipError_t e = hipGetLastError();
@@ -792,10 +1008,86 @@ static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, hipStream_t s
     return hipSuccess;
 }
 
+// Whole units (the marginal kernels' streaming layout): lane 32 h + q holds
+// columns 8q .. 8q + 7 of rows 2k + h of each 8-row batch, 16-byte gradient
+// loads, the next batch loaded before the current one's arithmetic. EXACT: u^2
+// summed double-double term by term, as in the other units (CAME, whose
+// clipped update feeds its momentum and confidence states); otherwise the 8
+// terms of a row are added pairwise (<= 3u) and those sums double-double
+// (Adafactor, where the clip scales only the parameter update).
+template <int G, bool EXACT>
+__global__ __launch_bounds__(64) void fac_rms_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const WholeLane w = whole_lane(d, unit - d.unit_begin);
+    const gp<const void> gu = unit_base<G>(d, w);
+    const int64_t cols = w.cols;
+    const uint32_t lo = w.lo;
+    double cf[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cf[j] = d.cfac[w.c0 + 8 * w.q + j];
+    const gp<const double> rf = d.rfac + w.r0 + w.h;  // row factor of row 2k + h of a batch: rf[rb + 2k]
+    constexpr int NR = 8;
+    DD acc{0.0, 0.0};
+    WBatch<G, NR> A, B;
+    double ra[4], rb_[4];
+    load_wbatch<G, NR>(A, gu, 0, cols, lo);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) ra[k] = rf[2 * k];
+    auto step = [&](const WBatch<G, NR>& cur, const double ri[4]) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            float gv[8];
+            unpack8<G>(cur.r[k], gv);
+            double t[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const double uu = (ri[k] * cf[j]) * (double)gv[j];
+                t[j] = uu * uu;
+                if constexpr (EXACT) dd_add(acc, t[j]);
+            }
+            if constexpr (!EXACT) dd_add(acc, sum8(t));
+        }
+    };
+    constexpr int NB = 256 / NR;
+    auto load = [&](WBatch<G, NR>& b, double ri[4], int bi) {
+        load_wbatch<G, NR>(b, gu, bi * NR, cols, lo);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) ri[k] = rf[bi * NR + 2 * k];
+    };
+    // last pair of batches peeled (see whole_unit_sums)
+#pragma unroll 1
+    for (int bi = 0; bi < NB - 2; bi += 2) {
+        load(B, rb_, bi + 1);
+        step(A, ra);
+        load(A, ra, bi + 2);
+        step(B, rb_);
+    }
+    load(B, rb_, NB - 1);
+    step(A, ra);
+    step(B, rb_);
+    acc = dd_wave_sum(acc);
+    if (threadIdx.x == 0) {
+        a.rmspart[2 * unit] = acc.hi;
+        a.rmspart[2 * unit + 1] = acc.lo;
+    }
+}
+
 hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    return grad_dtype == G_BF16 ? launch_wave_per_unit(fac_rms_kernel<G_BF16>, a, s)
-                                : launch_wave_per_unit(fac_rms_kernel<G_F32>, a, s);
+    hipError_t e;
+    const bool exact = a.exact_rms != 0;
+    if (grad_dtype == G_BF16) {
+        if ((e = exact ? launch_per_unit(fac_rms_whole_kernel<G_BF16, true>, a, 0, a.whole_units, s)
+                       : launch_per_unit(fac_rms_whole_kernel<G_BF16, false>, a, 0, a.whole_units, s)) != hipSuccess)
+            return e;
+        return launch_wave_per_unit(fac_rms_kernel<G_BF16>, a, a.whole_units, a.total_units, s);
+    }
+    if ((e = exact ? launch_per_unit(fac_rms_whole_kernel<G_F32, true>, a, 0, a.whole_units, s)
+                   : launch_per_unit(fac_rms_whole_kernel<G_F32, false>, a, 0, a.whole_units, s)) != hipSuccess)
+        return e;
+    return launch_wave_per_unit(fac_rms_kernel<G_F32>, a, a.whole_units, a.total_units, s);
 }
 
 // ------------------------------------------------ clip divisor (wave / tensor)
@@ -887,10 +1179,117 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t
     }
 }
 
+// Whole units, one wavefront per chunk of 8 unit rows (2048 elements, 32 per
+// unit, 4 per 256-thread workgroup) with no loop: the grid itself streams,
+// as in the AdamW step. Lane 32 h + q takes rows 2k + h (k < 4) of the chunk
+// and columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3, so every load and
+// store instruction covers whole contiguous row segments (a half-wave 512
+// bytes of parameters, 256 of gradients). All loads of the chunk are issued
+// before its arithmetic and stores; 16-byte non-temporal parameter accesses.
+constexpr int kChunkRows = 8;
+
+struct ChunkLane {
+    int64_t r0, c0, cols, row0;  // row0: the lane's first row (within the tensor)
+    int h, q, rb;                // rb: the chunk's first row within the unit
+};
+
+__device__ __forceinline__ ChunkLane chunk_lane(const GD& d, int64_t u, int64_t chunk_in_unit) {
+    ChunkLane c;
+    c.h = (int)(threadIdx.x >> 5) & 1;
+    c.q = (int)threadIdx.x & 31;
+    c.r0 = (u / d.ncu) * 256;
+    c.c0 = (u % d.ncu) * 256;
+    c.cols = d.cols;
+    c.rb = (int)chunk_in_unit * kChunkRows;
+    c.row0 = c.r0 + c.rb + c.h;
+    return c;
+}
+
+// Element index of (row pair k, column group s) of the lane: row row0 + 2k,
+// column c0 + 128 s + 4 q.
+__device__ __forceinline__ int64_t chunk_elem(const ChunkLane& c, int k, int s) {
+    return (c.row0 + 2 * k) * c.cols + c.c0 + 128 * s + 4 * c.q;
+}
+
+template <int G>
+__device__ __forceinline__ void load_g4(gp<const void> g, int64_t e, float gv[4]) {
+    if constexpr (G == G_BF16) {
+        const uint2 w = ld_u2<true>(g_as<const void>(g_as<const uint16_t>(g) + e));
+        gv[0] = u2f(w.x << 16), gv[1] = u2f(w.x & 0xFFFF0000u), gv[2] = u2f(w.y << 16), gv[3] = u2f(w.y & 0xFFFF0000u);
+    } else {
+        const float4 w = ld_f4<true>(g_as<const float>(g) + e);
+        gv[0] = w.x, gv[1] = w.y, gv[2] = w.z, gv[3] = w.w;
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void ada_apply_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = chunk / (256 / kChunkRows);
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const ChunkLane c = chunk_lane(d, unit - d.unit_begin, chunk % (256 / kChunkRows));
+    const double rclip = 1.0 / d.scal[0], lr = a.lr, decay = a.decay;
+    constexpr int NP = kChunkRows / 2;
+    float gv[NP][2][4];
+    float4 pv[NP][2];
+    double ri[NP], cf[2][4];
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+        ri[k] = d.rfac[c.row0 + 2 * k];
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            const int64_t e = chunk_elem(c, k, sg);
+            load_g4<G>(d.g, e, gv[k][sg]);
+            pv[k][sg] = ld_f4<true>(d.p + e);
+        }
+    }
+#pragma unroll
+    for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) cf[sg][j] = d.cfac[c.c0 + 128 * sg + 4 * c.q + j];
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            const float pin[4] = {pv[k][sg].x, pv[k][sg].y, pv[k][sg].z, pv[k][sg].w};
+            float out[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const double uu = (ri[k] * cf[sg][j]) * (double)gv[k][sg][j];
+                const double pd = (double)pin[j] * decay;
+                out[j] = (float)(pd - lr * (uu * rclip));  // p carries a tolerance: multiply by 1 / clip
+            }
+            st_f4<true>(d.p + chunk_elem(c, k, sg), make_float4(out[0], out[1], out[2], out[3]));
+        }
+    }
+}
+
+// One wavefront per whole-unit chunk, 4 per 256-thread workgroup; grids
+// beyond 2^31 workgroups take several launches.
+template <class K>
+static hipError_t launch_per_chunk(K kernel, const FacArgs& a, hipStream_t s) {
+    constexpr int64_t kMaxGrid = int64_t(1) << 31;
+    const int64_t end = a.whole_units * (256 / kChunkRows);
+    for (int64_t base = 0; base < end; base += 4 * kMaxGrid) {
+        const int64_t left = (end - base + 3) / 4;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, s, a, base);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_ada_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
-    return grad_dtype == G_BF16 ? launch_wave_per_unit(ada_apply_kernel<G_BF16>, a, s)
-                                : launch_wave_per_unit(ada_apply_kernel<G_F32>, a, s);
+    hipError_t e;
+    if (grad_dtype == G_BF16) {
+        if ((e = launch_per_chunk(ada_apply_whole_kernel<G_BF16>, a, s)) != hipSuccess) return e;
+        return launch_wave_per_unit(ada_apply_kernel<G_BF16>, a, a.whole_units, a.total_units, s);
+    }
+    if ((e = launch_per_chunk(ada_apply_whole_kernel<G_F32>, a, s)) != hipSuccess) return e;
+    return launch_wave_per_unit(ada_apply_kernel<G_F32>, a, a.whole_units, a.total_units, s);
 }
 
 // ------------------------------------------- Adafactor 1-D tensors (WG each)
@@ -1141,13 +1540,119 @@ __global__ __launch_bounds__(64) void came_res_kernel(const FacArgs a, int64_t b
         res_unit<G, false, UF>(a, gview(d), d.scal[0], ru, cu, nr, nc, vec, tile, racc);
 }
 
+// Whole units: the marginal kernels' streaming layout (whole_unit_sums) with
+// CAME's residual terms. Each unit row is one 256-element momentum block
+// (the width is a multiple of 256), so a row's codes share one scale; the
+// lane's 8 momentum values of a row are one 8-byte word of codes (or two
+// 16-byte fp32 loads), loaded with the gradients one batch ahead.
+constexpr int kResNR = 4;  // unit rows per batch of the residual kernel (its terms need more registers)
+template <int G, bool UF>
+struct ResBatch;
+template <int G>
+struct ResBatch<G, true> {
+    WBatch<G, kResNR> g;
+    uint2 mc[kResNR / 2];  // 8 UF8 codes of the lane's row in each row pair
+    float ms[kResNR / 2];  // their block's absmax
+    double ri[kResNR / 2];
+};
+template <int G>
+struct ResBatch<G, false> {
+    WBatch<G, kResNR> g;
+    float4 ma[kResNR / 2], mb[kResNR / 2];  // fp32 momentum
+    double ri[kResNR / 2];
+};
+
+template <int G, bool UF>
+struct ResTerms {
+    static constexpr int NR = kResNR;
+    using Batch = ResBatch<G, UF>;
+    const FacArgs* a;
+    gp<const void> gu;   // the unit's first gradient
+    gp<const void> mu;   // the unit's first momentum element (codes or fp32)
+    gp<const float> msu;  // absmax of the unit's first row's block (UF8)
+    gp<const double> rf;  // row factor of the lane's first row
+    int64_t cols, hcols;  // hcols = h * cols: the lane's row within a pair
+    uint32_t lo;
+    double cf[8];
+    double clip, rclip;
+    __device__ void load(Batch& b, int rb) const {
+        load_wbatch<G, NR>(b.g, gu, rb, cols, lo);
+#pragma unroll
+        for (int k = 0; k < NR / 2; ++k) {
+            const int64_t off = (int64_t)(rb + 2 * k) * cols;  // row rb + 2k + h, with lo
+            b.ri[k] = rf[rb + 2 * k];
+            if constexpr (UF) {
+                b.mc[k] = ld_u2<false>(g_as<const void>(g_as<const uint8_t>(mu) + off + lo));
+                b.ms[k] = msu[(off + hcols) >> 8];  // the row's momentum block
+            } else {
+                const gp<const float> m = g_as<const float>(mu) + off + lo;
+                b.ma[k] = ld_f4<false>(m);
+                b.mb[k] = ld_f4<false>(m + 4);
+            }
+        }
+    }
+    __device__ void terms(const Batch& b, int k, double t[8]) const {
+        float gv[8], mh[8], uh[8];
+        unpack8<G>(b.g.r[k], gv);
+        if constexpr (UF) {
+            const double st = div127((double)b.ms[k]);
+            const uint32_t w[2] = {b.mc[k].x, b.mc[k].y};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(w[j >> 2] >> (8 * (j & 3))), st);
+        } else {
+            mh[0] = b.ma[k].x, mh[1] = b.ma[k].y, mh[2] = b.ma[k].z, mh[3] = b.ma[k].w;
+            mh[4] = b.mb[k].x, mh[5] = b.mb[k].y, mh[6] = b.mb[k].z, mh[7] = b.mb[k].w;
+        }
+        double uu[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) uu[j] = (b.ri[k] * cf[j]) * (double)gv[j];
+        div4_to_f32(uu, clip, rclip, uh);
+        div4_to_f32(uu + 4, clip, rclip, uh + 4);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t[j] = res_term(*a, mh[j], uh[j]);
+    }
+};
+
+template <int G, bool UF>
+__global__ __launch_bounds__(64) void came_res_whole_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double stage[kResNR * kWStride];
+    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const WholeLane w = whole_lane(d, unit - d.unit_begin);
+    ResTerms<G, UF> pol;
+    pol.a = &a;
+    pol.gu = unit_base<G>(d, w);
+    const int64_t e0 = w.r0 * w.cols + w.c0;
+    pol.mu = UF ? g_as<const void>(g_as<const uint8_t>(d.m) + e0) : g_as<const void>(g_as<const float>(d.m) + e0);
+    pol.msu = d.mm + (e0 >> 8);
+    pol.rf = d.rfac + w.r0 + w.h;
+    pol.cols = w.cols;
+    pol.hcols = w.h * w.cols;
+    pol.lo = w.lo;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pol.cf[j] = d.cfac[w.c0 + 8 * w.q + j];
+    pol.clip = d.scal[0];
+    pol.rclip = 1.0 / pol.clip;
+    whole_unit_sums(pol, d, w.r0 / 256, w.c0 / 256, stage);
+}
+
 hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
     const bool uf = a.m_codec == UF8;
-    if (grad_dtype == G_BF16)
-        return uf ? launch_per_unit(came_res_kernel<G_BF16, true>, a, s)
-                  : launch_per_unit(came_res_kernel<G_BF16, false>, a, s);
-    return uf ? launch_per_unit(came_res_kernel<G_F32, true>, a, s) : launch_per_unit(came_res_kernel<G_F32, false>, a, s);
+    hipError_t e;
+    if (grad_dtype == G_BF16) {
+        if ((e = uf ? launch_per_unit(came_res_whole_kernel<G_BF16, true>, a, 0, a.whole_units, s)
+                    : launch_per_unit(came_res_whole_kernel<G_BF16, false>, a, 0, a.whole_units, s)) != hipSuccess)
+            return e;
+        return uf ? launch_per_unit(came_res_kernel<G_BF16, true>, a, a.whole_units, a.total_units, s)
+                  : launch_per_unit(came_res_kernel<G_BF16, false>, a, a.whole_units, a.total_units, s);
+    }
+    if ((e = uf ? launch_per_unit(came_res_whole_kernel<G_F32, true>, a, 0, a.whole_units, s)
+                : launch_per_unit(came_res_whole_kernel<G_F32, false>, a, 0, a.whole_units, s)) != hipSuccess)
+        return e;
+    return uf ? launch_per_unit(came_res_kernel<G_F32, true>, a, a.whole_units, a.total_units, s)
+              : launch_per_unit(came_res_kernel<G_F32, false>, a, a.whole_units, a.total_units, s);
 }
 
 // ------------------------------------------------------ CAME apply (2-D)
@@ -1313,14 +1818,114 @@ __global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) 
     }
 }
 
+// Whole units: one wavefront per 8-row chunk, as the Adafactor apply (lane
+// 32 h + q: rows 2k + h, columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3).
+// A unit row is one 256-element momentum block held by the 32 lanes of one
+// half, so its absmax is a 32-lane reduction; each lane writes its codes as
+// two 4-byte words.
+template <int G, bool UF>
+__global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = chunk / (256 / kChunkRows);
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const ChunkLane c = chunk_lane(d, unit - d.unit_begin, chunk % (256 / kChunkRows));
+    const double clip = d.scal[0], rclip = 1.0 / clip;
+    const gp<uint8_t> mc = g_as<uint8_t>(d.m);
+    const gp<float> mf = g_as<float>(d.m);
+    constexpr int NP = kChunkRows / 2;
+    float gv[NP][2][4];
+    float4 pv[NP][2], mv[UF ? 1 : NP][2];
+    uint32_t mw[UF ? NP : 1][2];
+    float ms[NP];
+    double ri[NP], si[NP];
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+        ri[k] = d.rfac[c.row0 + 2 * k];
+        si[k] = d.sr[c.row0 + 2 * k];
+        if constexpr (UF) ms[k] = d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8];
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            const int64_t e = chunk_elem(c, k, sg);
+            load_g4<G>(d.g, e, gv[k][sg]);
+            pv[k][sg] = ld_f4<true>(d.p + e);
+            if constexpr (UF)
+                mw[k][sg] = ld_u1<true>(g_as<const void>(mc + e));
+            else
+                mv[k][sg] = ld_f4<true>(mf + e);
+        }
+    }
+    double cf[2][4], sf[2][4];
+#pragma unroll
+    for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            cf[sg][j] = d.cfac[c.c0 + 128 * sg + 4 * c.q + j];
+            sf[sg][j] = d.sc[c.c0 + 128 * sg + 4 * c.q + j];
+        }
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+        float mnew[2][4];
+        const double st = UF ? div127((double)ms[k]) : 0.0;
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            float mh[4], uh[4];
+            if constexpr (UF) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[k][sg] >> (8 * j)), st);
+            } else {
+                mh[0] = mv[k][sg].x, mh[1] = mv[k][sg].y, mh[2] = mv[k][sg].z, mh[3] = mv[k][sg].w;
+            }
+            double uu[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) uu[j] = (ri[k] * cf[sg][j]) * (double)gv[k][sg][j];
+            div4_to_f32(uu, clip, rclip, uh);
+            const float pin[4] = {pv[k][sg].x, pv[k][sg].y, pv[k][sg].z, pv[k][sg].w};
+            float pout[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                mnew[sg][j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
+                const double upd = (si[k] * sf[sg][j]) * (double)mnew[sg][j];
+                pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+            }
+            const int64_t e = chunk_elem(c, k, sg);
+            st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
+            if constexpr (!UF) st_f4<true>(mf + e, make_float4(mnew[sg][0], mnew[sg][1], mnew[sg][2], mnew[sg][3]));
+        }
+        if constexpr (UF) {
+            uint32_t am = 0u;
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[sg][j]));
+            am = group_reduce<OpMax, 32>(am);  // the row's block: the 32 lanes of this half
+            const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg) {
+                uint32_t qv[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) qv[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[sg][j] * rs) & 0xFFu;
+                st_u1<true>(g_as<void>(mc + chunk_elem(c, k, sg)), qv[0] | (qv[1] << 8) | (qv[2] << 16) | (qv[3] << 24));
+            }
+            if (c.q == 0) d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8] = u2f(am);
+        }
+    }
+}
+
 hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
     const bool uf = a.m_codec == UF8;
-    hipError_t e = grad_dtype == G_BF16
-                       ? (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_BF16, true>, a, s)
-                             : launch_wave_per_unit(came_apply_unit_kernel<G_BF16, false>, a, s))
-                       : (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_F32, true>, a, s)
-                             : launch_wave_per_unit(came_apply_unit_kernel<G_F32, false>, a, s));
+    const bool bf = grad_dtype == G_BF16;
+    hipError_t e = bf ? (uf ? launch_per_chunk(came_apply_whole_kernel<G_BF16, true>, a, s)
+                            : launch_per_chunk(came_apply_whole_kernel<G_BF16, false>, a, s))
+                      : (uf ? launch_per_chunk(came_apply_whole_kernel<G_F32, true>, a, s)
+                            : launch_per_chunk(came_apply_whole_kernel<G_F32, false>, a, s));
+    if (e != hipSuccess) return e;
+    const int64_t b0 = a.whole_units, b1 = a.total_units;
+    e = bf ? (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_BF16, true>, a, b0, b1, s)
+                 : launch_wave_per_unit(came_apply_unit_kernel<G_BF16, false>, a, b0, b1, s))
+           : (uf ? launch_wave_per_unit(came_apply_unit_kernel<G_F32, true>, a, b0, b1, s)
+                 : launch_wave_per_unit(came_apply_unit_kernel<G_F32, false>, a, b0, b1, s));
     if (e != hipSuccess || a.total_chunks == 0) return e;
     const int64_t cap = int64_t(1) << 30;
     const int64_t want = (a.total_chunks + 3) / 4;
