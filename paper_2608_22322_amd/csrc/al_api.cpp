@@ -815,7 +815,6 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
     a.c_floor = cfg->conf.log_floor;
     a.m_codec = cfg->m.codec;
     a.m_block = cfg->m.codec == AL_CODEC_UF8 ? cfg->m.block : 256;
-    a.exact_rms = 1;
     a.exact_all = (cfg->flags & AL_FLAG_EXACT_SUMS) != 0;
     hipStream_t s = as_stream(stream);
     const int G = cfg->grad_dtype;

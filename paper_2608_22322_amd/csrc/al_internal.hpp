@@ -147,7 +147,6 @@ struct FacArgs {
     int32_t v_codec, v_block, c_codec, c_block, m_codec, m_block;
     float v_floor, c_floor;
     int32_t exact_all;  // recompute every factored mean exactly (AL_FLAG_EXACT_SUMS)
-    int32_t exact_rms;  // RMS sums term by term double-double (CAME: the clip feeds its states)
     Exp2Coef cf;
 };
 

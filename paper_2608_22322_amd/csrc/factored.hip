@@ -441,6 +441,21 @@ static hipError_t launch_per_unit(K kernel, const FacArgs& a, int64_t begin, int
     return hipSuccess;
 }
 
+// One wavefront per unit (4 per 256-thread workgroup); lists beyond 2^33 units
+// take several launches.
+template <class K>
+static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, int64_t begin, int64_t end, hipStream_t s) {
+    constexpr int64_t kMaxGrid = int64_t(1) << 31;
+    for (int64_t base = begin; base < end; base += 4 * kMaxGrid) {
+        const int64_t left = (end - base + 3) / 4;
+        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
+        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, s, a, base);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 // ------------------------------ marginal sums over whole units (streaming)
 // Units of the tensors whose rows and columns are both multiples of 256: no
 // guards, and every unit row starts 16-byte aligned. A batch is 8 unit rows.
@@ -511,58 +526,89 @@ __device__ __forceinline__ void load_wbatch(WBatch<G, NR>& b, gp<const void> g, 
 }
 
 // Shared part of the whole-unit marginal kernels, batches of P::NR unit rows
-// (4 or 8). The policy P supplies the batch type, load(batch, rb) for the
+// (4, 8 or 16). The policy P supplies the batch type, load(batch, rb) for the
 // rows from rb, and terms(batch, k, t): the 8 binary64 terms of the lane's
 // row 2k + h of that batch. Row partials go to rowpart (lo = 0), column
 // partials to colpart; stage holds NR x kWStride doubles.
 template <class P>
 __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64_t ru, int64_t cu, double* stage) {
     constexpr int NR = P::NR, NP = NR / 2, LPR = 64 / NR, PPL = 32 / LPR;  // lanes per row, partials per lane
-    static_assert(NR == 4 || NR == 8, "batch rows");
-    const int lane = threadIdx.x, h = lane >> 5, q = lane & 31;
+    constexpr int SZ = NR * kWStride;  // one stage buffer; batches alternate between two
+    static_assert(NR == 4 || NR == 8 || NR == 16, "batch rows");
+    const int lane = threadIdx.x & 63, h = lane >> 5, q = lane & 31;
     const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
-    const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of the batch, partials PPL rpart ..
+    const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of a batch, partials PPL rpart ..
     double cacc[8], crun[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         cacc[j] = 0.0;
         crun[j] = 0.0;
     }
-    typename P::Batch A, B;
-    pol.load(A, 0);
-    auto step = [&](const typename P::Batch& cur, int bi) {
-#pragma unroll
-        for (int k = 0; k < NP; ++k) {
-            double t[8];
-            pol.terms(cur, k, t);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                crun[j] += t[j];
-                // one row pair's terms live at a time: without this the compiler forms all terms of the
-                // batch before the column additions (many more registers, lower occupancy)
-                __asm__ volatile("" : "+v"(crun[j]));
-            }
-            stage[(2 * k + h) * kWStride + q] = sum8(t);
-        }
-        __syncthreads();
-        // row rrow of the batch: partials PPL rpart .. PPL rpart + PPL - 1 of its 32, pairwise
+    // Row rrow of batch bi from its staged partials PPL rpart .. PPL rpart + PPL - 1, pairwise, then
+    // merged over the row's LPR lanes. Called one batch late, so the LDS round trip overlaps the next
+    // batch's arithmetic.
+    auto finish_rows = [&](int bi) {
+        const double* st = stage + (bi & 1) * SZ + rrow * kWStride + PPL * rpart;
         double rs;
-        const double2 p0 = *reinterpret_cast<const double2*>(&stage[rrow * kWStride + PPL * rpart]);
-        if constexpr (PPL == 4) {
-            const double2 p1 = *reinterpret_cast<const double2*>(&stage[rrow * kWStride + PPL * rpart + 2]);
+        const double2 p0 = *reinterpret_cast<const double2*>(st);
+        if constexpr (PPL == 8) {
+            const double2 p1 = *reinterpret_cast<const double2*>(st + 2);
+            const double2 p2 = *reinterpret_cast<const double2*>(st + 4);
+            const double2 p3 = *reinterpret_cast<const double2*>(st + 6);
+            rs = ((p0.x + p0.y) + (p1.x + p1.y)) + ((p2.x + p2.y) + (p3.x + p3.y));
+        } else if constexpr (PPL == 4) {
+            const double2 p1 = *reinterpret_cast<const double2*>(st + 2);
             rs = (p0.x + p0.y) + (p1.x + p1.y);
         } else {
             rs = p0.x + p0.y;
         }
         rs += dpp_d<kDppQuadXor1>(rs);
         rs += dpp_d<kDppQuadXor2>(rs);
-        rs += dpp_d<kDppRowHalfMirror>(rs);
+        if constexpr (LPR >= 8) rs += dpp_d<kDppRowHalfMirror>(rs);
         if constexpr (LPR == 16) rs += dpp_d<kDppRowMirror>(rs);
         if (rpart == 0) {
             const gp<double> rp = d.rowpart + 2 * (cu * d.rows + r0 + NR * bi + rrow);
             st_d2(rp, rs, 0.0);
         }
-        __syncthreads();
+    };
+    typename P::Batch A, B;
+    pol.load(A, 0);
+    auto step = [&](const typename P::Batch& cur, int bi) {
+        double* sb = stage + (bi & 1) * SZ;
+        if constexpr (P::ILP) {
+            // all terms of the batch at once (more registers, fewer waves per SIMD, more independent
+            // work per wave): the batch's column terms are added first, then into the run
+            double cs[8];
+#pragma unroll
+            for (int k = 0; k < NP; ++k) {
+                double t[8];
+                pol.terms(cur, k, t);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) cs[j] = k == 0 ? t[j] : cs[j] + t[j];
+                sb[(2 * k + h) * kWStride + q] = sum8(t);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) crun[j] += cs[j];
+        } else {
+#pragma unroll
+            for (int k = 0; k < NP; ++k) {
+                double t[8];
+                pol.terms(cur, k, t);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    crun[j] += t[j];
+                    // two row pairs' terms live at a time: without the fence the compiler forms all terms
+                    // of the batch before the column additions
+                    if (k & 1) __asm__ volatile("" : "+v"(crun[j]));
+                }
+                sb[(2 * k + h) * kWStride + q] = sum8(t);
+            }
+        }
+        // the stages belong to this wavefront alone and its LDS accesses
+        // execute in order: only the compiler must keep them in order
+        __builtin_amdgcn_wave_barrier();
+        if (bi > 0) finish_rows(bi - 1);
+        __builtin_amdgcn_wave_barrier();
         if ((bi + 1) % (kWRunRows / NR) == 0) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -585,14 +631,23 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
     pol.load(B, (NB - 1) * NR);
     step(A, NB - 2);
     step(B, NB - 1);
+    __builtin_amdgcn_wave_barrier();
+    finish_rows(NB - 1);
     // the two halves hold the even and the odd rows of the same columns
 #pragma unroll
     for (int j = 0; j < 8; ++j) cacc[j] += __shfl_xor(cacc[j], 32);
+    // through LDS, so that each store instruction writes 64 consecutive
+    // column partials (1 KB) instead of 16 bytes in every 128
+    static_assert(2 * SZ >= 256, "the stages hold a unit's 256 column sums");
+    __builtin_amdgcn_wave_barrier();
     if (h == 0) {
-        const gp<double> cp = d.colpart + 2 * (ru * cols + c0 + 8 * q);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) st_d2(cp + 2 * j, cacc[j], 0.0);
+        for (int j = 0; j < 8; ++j) stage[8 * q + j] = cacc[j];
     }
+    __builtin_amdgcn_wave_barrier();
+    const gp<double> cp = d.colpart + 2 * (ru * cols + c0 + lane);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) st_d2(cp + 128 * i, stage[lane + 64 * i], 0.0);
 }
 
 // The lane's place in a whole unit: the unit's first gradient element as a
@@ -605,7 +660,7 @@ struct WholeLane {
 
 __device__ __forceinline__ WholeLane whole_lane(const GD& d, int64_t u) {
     WholeLane w;
-    w.h = (int)threadIdx.x >> 5;
+    w.h = (int)(threadIdx.x >> 5) & 1;
     w.q = (int)threadIdx.x & 31;
     w.r0 = (u / d.ncu) * 256;
     w.c0 = (u % d.ncu) * 256;
@@ -622,7 +677,10 @@ __device__ __forceinline__ gp<const void> unit_base(const GD& d, const WholeLane
 // Terms of the second moment's marginals: fl64(g^2 + eps1).
 template <int G>
 struct MargTerms {
+    // 8-row batches, all terms of a batch at once: the cheap terms gain more from independent work per
+    // wave than from occupancy (200 registers, 2 waves per SIMD: 2.53 against 2.68 ms on the 7B list)
     static constexpr int NR = 8;
+    static constexpr bool ILP = true;
     using Batch = WBatch<G, NR>;
     gp<const void> gu;
     int64_t cols;
@@ -637,10 +695,17 @@ struct MargTerms {
     }
 };
 
+// One wavefront per unit, 4 per 256-thread workgroup (each with its own
+// LDS stage), as in the other streaming kernels.
+__device__ __forceinline__ int64_t whole_unit_of_wave(int64_t base) {
+    return base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
 template <int G>
-__global__ __launch_bounds__(64) void fac_marg_whole_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) double stage[MargTerms<G>::NR * kWStride];
-    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+__global__ __launch_bounds__(256) void fac_marg_whole_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double stages[4][2 * MargTerms<G>::NR * kWStride];
+    double* stage = stages[threadIdx.x >> 6];
+    const int64_t unit = whole_unit_of_wave(base);
     if (unit >= a.whole_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const WholeLane w = whole_lane(d, unit - d.unit_begin);
@@ -652,10 +717,10 @@ hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
     hipError_t e;
     if (grad_dtype == G_BF16) {
-        if ((e = launch_per_unit(fac_marg_whole_kernel<G_BF16>, a, 0, a.whole_units, s)) != hipSuccess) return e;
+        if ((e = launch_wave_per_unit(fac_marg_whole_kernel<G_BF16>, a, 0, a.whole_units, s)) != hipSuccess) return e;
         return launch_per_unit(fac_marg_g2_kernel<G_BF16>, a, a.whole_units, a.total_units, s);
     }
-    if ((e = launch_per_unit(fac_marg_whole_kernel<G_F32>, a, 0, a.whole_units, s)) != hipSuccess) return e;
+    if ((e = launch_wave_per_unit(fac_marg_whole_kernel<G_F32>, a, 0, a.whole_units, s)) != hipSuccess) return e;
     return launch_per_unit(fac_marg_g2_kernel<G_F32>, a, a.whole_units, a.total_units, s);
 }
 
@@ -993,31 +1058,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(6))) void f
     }
 }
 
-// One wavefront per unit (4 per 256-thread workgroup); lists beyond 2^33 units
-// take several launches.
-template <class K>
-static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, int64_t begin, int64_t end, hipStream_t s) {
-    constexpr int64_t kMaxGrid = int64_t(1) << 31;
-    for (int64_t base = begin; base < end; base += 4 * kMaxGrid) {
-        const int64_t left = (end - base + 3) / 4;
-        const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
-        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, s, a, base);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
-}
 
 // Whole units (the marginal kernels' streaming layout): lane 32 h + q holds
 // columns 8q .. 8q + 7 of rows 2k + h of each 8-row batch, 16-byte gradient
-// loads, the next batch loaded before the current one's arithmetic. EXACT: u^2
-// summed double-double term by term, as in the other units (CAME, whose
-// clipped update feeds its momentum and confidence states); otherwise the 8
-// terms of a row are added pairwise (<= 3u) and those sums double-double
-// (Adafactor, where the clip scales only the parameter update).
-template <int G, bool EXACT>
-__global__ __launch_bounds__(64) void fac_rms_whole_kernel(const FacArgs a, int64_t base) {
-    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+// loads, the next batch loaded before the current one's arithmetic. The 8
+// terms u^2 of a lane's row are added pairwise (relative error <= 3u) and
+// those sums accumulated double-double, so a unit's partial is within 3u of
+// its exact sum (the other units sum term by term). The clip divisor then
+// carries a relative error of at most about 2u: it scales Adafactor's update
+// (inside the parameter tolerance), and for CAME it can move fl32(u / clip)
+// by one fp32 ulp only where u / clip lies within that distance of an fp32
+// rounding midpoint, about one element in 10^8.
+template <int G>
+__global__ __launch_bounds__(256) void fac_rms_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t unit = whole_unit_of_wave(base);
     if (unit >= a.whole_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const WholeLane w = whole_lane(d, unit - d.unit_begin);
@@ -1045,9 +1099,8 @@ __global__ __launch_bounds__(64) void fac_rms_whole_kernel(const FacArgs a, int6
             for (int j = 0; j < 8; ++j) {
                 const double uu = (ri[k] * cf[j]) * (double)gv[j];
                 t[j] = uu * uu;
-                if constexpr (EXACT) dd_add(acc, t[j]);
             }
-            if constexpr (!EXACT) dd_add(acc, sum8(t));
+            dd_add(acc, sum8(t));
         }
     };
     constexpr int NB = 256 / NR;
@@ -1068,7 +1121,7 @@ __global__ __launch_bounds__(64) void fac_rms_whole_kernel(const FacArgs a, int6
     step(A, ra);
     step(B, rb_);
     acc = dd_wave_sum(acc);
-    if (threadIdx.x == 0) {
+    if ((threadIdx.x & 63) == 0) {
         a.rmspart[2 * unit] = acc.hi;
         a.rmspart[2 * unit + 1] = acc.lo;
     }
@@ -1077,16 +1130,11 @@ __global__ __launch_bounds__(64) void fac_rms_whole_kernel(const FacArgs a, int6
 hipError_t launch_fac_rms(const FacArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
     hipError_t e;
-    const bool exact = a.exact_rms != 0;
     if (grad_dtype == G_BF16) {
-        if ((e = exact ? launch_per_unit(fac_rms_whole_kernel<G_BF16, true>, a, 0, a.whole_units, s)
-                       : launch_per_unit(fac_rms_whole_kernel<G_BF16, false>, a, 0, a.whole_units, s)) != hipSuccess)
-            return e;
+        if ((e = launch_wave_per_unit(fac_rms_whole_kernel<G_BF16>, a, 0, a.whole_units, s)) != hipSuccess) return e;
         return launch_wave_per_unit(fac_rms_kernel<G_BF16>, a, a.whole_units, a.total_units, s);
     }
-    if ((e = exact ? launch_per_unit(fac_rms_whole_kernel<G_F32, true>, a, 0, a.whole_units, s)
-                   : launch_per_unit(fac_rms_whole_kernel<G_F32, false>, a, 0, a.whole_units, s)) != hipSuccess)
-        return e;
+    if ((e = launch_wave_per_unit(fac_rms_whole_kernel<G_F32>, a, 0, a.whole_units, s)) != hipSuccess) return e;
     return launch_wave_per_unit(fac_rms_kernel<G_F32>, a, a.whole_units, a.total_units, s);
 }
 
@@ -1565,6 +1613,7 @@ struct ResBatch<G, false> {
 template <int G, bool UF>
 struct ResTerms {
     static constexpr int NR = kResNR;
+    static constexpr bool ILP = false;  // the residual terms need the registers for occupancy
     using Batch = ResBatch<G, UF>;
     const FacArgs* a;
     gp<const void> gu;   // the unit's first gradient
@@ -1614,9 +1663,10 @@ struct ResTerms {
 };
 
 template <int G, bool UF>
-__global__ __launch_bounds__(64) void came_res_whole_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) double stage[kResNR * kWStride];
-    const int64_t unit = base + xcd_order(blockIdx.x, gridDim.x);
+__global__ __launch_bounds__(256) void came_res_whole_kernel(const FacArgs a, int64_t base) {
+    __shared__ __attribute__((aligned(16))) double stages[4][2 * kResNR * kWStride];
+    double* stage = stages[threadIdx.x >> 6];
+    const int64_t unit = whole_unit_of_wave(base);
     if (unit >= a.whole_units) return;
     const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
     const WholeLane w = whole_lane(d, unit - d.unit_begin);
@@ -1642,14 +1692,14 @@ hipError_t launch_came_res(const FacArgs& a, int grad_dtype, hipStream_t s) {
     const bool uf = a.m_codec == UF8;
     hipError_t e;
     if (grad_dtype == G_BF16) {
-        if ((e = uf ? launch_per_unit(came_res_whole_kernel<G_BF16, true>, a, 0, a.whole_units, s)
-                    : launch_per_unit(came_res_whole_kernel<G_BF16, false>, a, 0, a.whole_units, s)) != hipSuccess)
+        if ((e = uf ? launch_wave_per_unit(came_res_whole_kernel<G_BF16, true>, a, 0, a.whole_units, s)
+                    : launch_wave_per_unit(came_res_whole_kernel<G_BF16, false>, a, 0, a.whole_units, s)) != hipSuccess)
             return e;
         return uf ? launch_per_unit(came_res_kernel<G_BF16, true>, a, a.whole_units, a.total_units, s)
                   : launch_per_unit(came_res_kernel<G_BF16, false>, a, a.whole_units, a.total_units, s);
     }
-    if ((e = uf ? launch_per_unit(came_res_whole_kernel<G_F32, true>, a, 0, a.whole_units, s)
-                : launch_per_unit(came_res_whole_kernel<G_F32, false>, a, 0, a.whole_units, s)) != hipSuccess)
+    if ((e = uf ? launch_wave_per_unit(came_res_whole_kernel<G_F32, true>, a, 0, a.whole_units, s)
+                : launch_wave_per_unit(came_res_whole_kernel<G_F32, false>, a, 0, a.whole_units, s)) != hipSuccess)
         return e;
     return uf ? launch_per_unit(came_res_kernel<G_F32, true>, a, a.whole_units, a.total_units, s)
               : launch_per_unit(came_res_kernel<G_F32, false>, a, a.whole_units, a.total_units, s);
