@@ -215,9 +215,38 @@ __device__ __forceinline__ float grad_at(const typename Pick<G == G_BF16, uint2,
         return f4_at(w, j);
 }
 
+// The min/max keys of two second-moment blocks (A, B: each lane's running
+// minimum of bits - 1 and maximum of bits) reduced over the wavefront by one
+// reduce-scatter: the minima travel complemented, so every step is a maximum.
+// After the two quad steps lane L holds key (L & 1 ? maximum : minimum) of
+// block (L & 2 ? B : A) over its quad; four more steps (lane xor 4, 8, 16,
+// 32) complete it over the wavefront. Lanes 4 pair .. 4 pair + 3 take the
+// result into their slot: lane 2b then holds block b's minimum (bits; 0 when
+// the block has no positive value) and 2b + 1 its maximum.
+__device__ __forceinline__ uint32_t key_pair_reduce(uint32_t amn, uint32_t amx, uint32_t bmn, uint32_t bmx, int lane,
+                                                    int pair, uint32_t slot) {
+    const bool b0 = lane & 1, b1 = lane & 2;
+    const uint32_t wa0 = ~amn, wb0 = ~bmn;
+    // step 1 (lane xor 1): keep this lane's kind (minimum / maximum) of both blocks
+    uint32_t ka = b0 ? amx : wa0, kb = b0 ? bmx : wb0;
+    const uint32_t sa = b0 ? wa0 : amx, sb = b0 ? wb0 : bmx;
+    ka = OpMax::f(ka, dpp<kDppQuadXor1>(sa));
+    kb = OpMax::f(kb, dpp<kDppQuadXor1>(sb));
+    // step 2 (lane xor 2): keep this lane's block
+    uint32_t v = b1 ? kb : ka;
+    v = OpMax::f(v, dpp<kDppQuadXor2>(b1 ? ka : kb));
+    v = OpMax::f(v, (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, kSwzXor4));
+    v = OpMax::f(v, (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, kSwzXor8));
+    v = OpMax::f(v, (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, kSwzXor16));
+    v = OpMax::f(v, (uint32_t)__shfl_xor((int)v, 32));
+    const uint32_t key = b0 ? v : ~v + 1u;
+    return (lane >> 2) == pair ? key : slot;
+}
+
 template <int G, int MC, int VC, int BV, bool FULL>
 __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG& d, int64_t e0, int64_t valid,
-                                              int lane, double* lut, double* stab, uint2* skey) {
+                                              int lane, double* lut, double* stab, uint2* skey, uint4* encp,
+                                              double2* encd) {
     using Q = Geo<MC, VC, BV>;
     constexpr int K = Q::K;
     constexpr int NB = Q::NB;
@@ -250,8 +279,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     // positive levels fl32(2^(l_min + k step)), k = 0..254, built in this
     // wavefront's LDS slice (4 levels per lane) from the block's 16 + 16
     // split factors below (32 evaluations per block instead of 255; a level is
-    // one binary64 product, within about 2.5 binary64 ulps before the fp32
-    // rounding). LDS traffic of one wavefront is ordered, so no barrier is
+    // one binary64 product, relative error about (ln 2 |E| + 2.5) 2^-53 before
+    // the fp32 rounding). LDS traffic of one wavefront is ordered, so no barrier is
     // needed between building and reading its own tables.
     // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q,
     // kept in binary64 (the fp32 value widened) for the binary64 EMA.
@@ -266,7 +295,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const float l1 = u2f(readlane_u(f2u(om.l), 32 + b1));
             const double st = lane < 32 ? st0 : st1;
             const int j = lane & 31;
-            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
+            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j - 1) * st : (double)(j - 16) * st;
             const double v = exp2_d(arg, kExp2);
             if (lane + kWave * i < NF) stab[lane + kWave * i] = v;
         }
@@ -276,19 +305,20 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int k = lane + 64 * i;
-                const uint32_t kq = k == 0 ? 0u : (uint32_t)(k - 1);
-                const float lv = (float)(t[kq >> 4] * t[16 + (kq & 15u)]);
+                const float lv = (float)(t[k >> 4] * t[16 + (k & 15)]);
                 lut[b * 256 + k] = k == 0 ? 0.0 : (double)lv;
             }
         }
     }
 
     // Blocks of 128 and 256 elements: a level table would cost one evaluation
-    // per element. Instead, with k = 16 a + b (a, b in 0..15),
-    // 2^(l_min + k step) = 2^(l_min + 16 a step) * 2^(b step): entries [0, 16)
-    // of a block's split table hold the first factor, [16, 32) the second, so a
-    // block costs 32 evaluations and an element one binary64 product (within
-    // about 2.5 binary64 ulps of 2^(l_min + k step), then rounded to fp32).
+    // per element. Instead, with the code q = 16 a + b (a, b in 0..15) of level
+    // q - 1, 2^(l_min + (q - 1) step) = 2^(l_min + (16 a - 1) step) * 2^(b step):
+    // entries [0, 16) of a block's split table hold the first factor, [16, 32)
+    // the second, so a block costs 32 evaluations and an element one binary64
+    // product indexed by the code's two nibbles (relative error about
+    // (ln 2 |E| + 2.5) 2^-53 against 2^E, then rounded to fp32; code 0 is
+    // replaced by exact zero).
     if constexpr (Q::SPLIT) {
         static_assert(NB * 32 % kWave == 0, "split tables fill whole wavefront passes");
 #pragma unroll
@@ -299,16 +329,17 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const float l1 = u2f(readlane_u(f2u(om.l), 33 + 2 * i));
             const double st = lane < 32 ? st0 : st1;
             const int j = lane & 31;
-            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j) * st : (double)(j - 16) * st;
+            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j - 1) * st : (double)(j - 16) * st;
             stab[lane + kWave * i] = exp2_d(arg, kExp2);
         }
     }
 
-    // Blocks of 64: k = 64 a + 8 b + c (a < 4, b, c < 8) and
-    // 2^(l_min + k step) = 2^(l_min + 64 a step) * 2^(8 b step) * 2^(c step):
-    // 20 entries per block ([0, 4) first factor, [4, 12) second, [12, 20)
-    // third), 5 evaluations per lane for the chunk's 16 blocks, and two binary64
-    // products per element (within about 4 binary64 ulps, then rounded to fp32).
+    // Blocks of 64: with the code q = 64 a + 8 b + c (a < 4, b, c < 8),
+    // 2^(l_min + (q - 1) step) = 2^(l_min + (64 a - 1) step) * 2^(8 b step) *
+    // 2^(c step): 20 entries per block ([0, 4) first factor, [4, 12) second,
+    // [12, 20) third), 5 evaluations per lane for the chunk's 16 blocks, and two
+    // binary64 products per element (relative error about (ln 2 |E| + 4) 2^-53,
+    // then rounded to fp32).
     if constexpr (Q::SPLIT3) {
         static_assert(NB * 20 % kWave == 0, "three-factor tables fill whole wavefront passes");
 #pragma unroll
@@ -317,7 +348,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const int b = e / 20, j = e - 20 * b;
             const double st = shfl_d(q1, 32 + b);
             const double l32 = (double)__shfl(om.l, 32 + b);
-            const double arg = j < 4 ? l32 + (double)(64 * j) * st
+            const double arg = j < 4 ? l32 + (double)(64 * j - 1) * st
                                      : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
             stab[e] = exp2_d(arg, kExp2);
         }
@@ -328,6 +359,9 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     float vk[K][4];
     uint32_t vmn[Q::NSLOT], vmx[Q::NSLOT];
     uint32_t pmn = 0xFFFFFFFFu, pmx = 0u;
+    // blocks of 256: the previous block's lane keys, and this lane's slot of
+    // the chunk's reduced keys (lane 2b: block b's minimum, 2b + 1: its maximum)
+    uint32_t qmn = 0xFFFFFFFFu, qmx = 0u, fitkey = 0u;
 #pragma unroll
     for (int s = 0; s < Q::NSLOT; ++s) {
         vmn[s] = 0xFFFFFFFFu;
@@ -361,8 +395,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const uint32_t kq = q == 0u ? 0u : q - 1u;
-                const float lv = (float)(t[kq >> 4] * t[16 + (kq & 15u)]);
+                const float lv = (float)(t[q >> 4] * t[16 + (q & 15u)]);
                 vh[j] = q == 0u ? 0.0f : lv;
             }
         } else if constexpr (Q::SPLIT3) {
@@ -370,8 +403,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const uint32_t kq = q == 0u ? 0u : q - 1u;
-                const float lv = (float)((t[kq >> 6] * t[4 + ((kq >> 3) & 7u)]) * t[12 + (kq & 7u)]);
+                const float lv = (float)((t[q >> 6] * t[4 + ((q >> 3) & 7u)]) * t[12 + (q & 7u)]);
                 vh[j] = q == 0u ? 0.0f : lv;
             }
         } else if constexpr (VQ) {
@@ -453,7 +485,18 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
                     pmn = OpMin::f(pmn, f2u(vn[j]) - 1u);
                     pmx = OpMax::f(pmx, f2u(vn[j]));
                 }
-                if ((k + 1) * kSub % BV == 0) {
+                if constexpr (BV == kSub) {
+                    // one block per sub-tile: the keys of two blocks at a time go
+                    // through one reduce-scatter (below) instead of four reductions
+                    if (k & 1) {
+                        fitkey = key_pair_reduce(qmn, qmx, pmn, pmx, lane, k >> 1, fitkey);
+                    } else {
+                        qmn = pmn;
+                        qmx = pmx;
+                    }
+                    pmn = 0xFFFFFFFFu;
+                    pmx = 0u;
+                } else if ((k + 1) * kSub % BV == 0) {
                     const int s = k * kSub / BV;
                     vmn[s] = group_reduce<OpMin, 64>(pmn) + 1u;  // back to bits; 0 when no positive
                     vmx[s] = group_reduce<OpMax, 64>(pmx);
@@ -487,7 +530,11 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
         // lanes 2b, 2b+1 hold block b's min / max key; both compute its interval.
         uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
         const int b = lane >> 1;
-        if constexpr (BV >= kSub) {
+        if constexpr (BV == kSub) {
+            const uint32_t other = dpp<kDppQuadXor1>(fitkey);
+            kmin = (lane & 1) ? other : fitkey;
+            kmax = (lane & 1) ? fitkey : other;
+        } else if constexpr (BV >= kSub) {
 #pragma unroll
             for (int s = 0; s < NB; ++s) {
                 kmin = (b == s) ? vmn[s] : kmin;
@@ -513,6 +560,16 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             *g_as<f2v>(d.vm + 2 * (e0 / BV + b)) = any ? f2v{(float)l0, (float)dl} : f2v{0.0f, 0.0f};
         }
         const double q2 = any ? (double)LEVELS / dl : 1.0;  // (L - 2) / delta
+        if constexpr (VC == AL8 && BV < kSub) {
+            // blocks inside a sub-tile: each block's encode parameters once, to LDS
+            // (lane 2b), instead of two shuffles and the derivation per element group
+            if ((lane & 1) == 0 && b < NB) {
+                const ALEnc p = al_enc_params(l0, q2);
+                encp[b] = make_uint4((uint32_t)p.I, f2u(p.fr32), f2u(p.inv32), f2u(p.guard32));
+                encd[b] = make_double2(l0, q2);
+            }
+            __builtin_amdgcn_wave_barrier();  // this wavefront's LDS accesses run in order
+        }
 
         // -------------------------------------------- 5. second-moment codes
 #pragma unroll
@@ -524,6 +581,17 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
                 const int bb = k * kSub / BV;
                 enc = al_enc_params(readlane_d(l0, 2 * bb), readlane_d(q2, 2 * bb));
                 live = FULL || (int64_t)bb * BV < valid;
+            } else if constexpr (VC == AL8) {
+                const int bb = (k * kSub + 4 * lane) / BV;
+                live = FULL || (int64_t)bb * BV < valid;
+                const uint4 pw = encp[bb];
+                uint32_t q[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    q[j] = al_encode_f32(vk[k][j], (int)pw.x, u2f(pw.y), u2f(pw.z), u2f(pw.w),
+                                         [&] { return encd[bb]; });
+                if (live) store_codes4<VC, FULL && kNtStore>(d.v, e, q);
+                continue;
             } else {
                 const int bb = (k * kSub + 4 * lane) / BV;
                 enc = al_enc_params(shfl_d(l0, 2 * bb), shfl_d(q2, 2 * bb));
@@ -531,7 +599,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             }
             uint32_t q[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = al_encode_fast<LEVELS>(vk[k][j], enc);
+            for (int j = 0; j < 4; ++j)
+                q[j] = VC == AL8 ? al_encode_f32(vk[k][j], enc) : al_encode_fast<LEVELS>(vk[k][j], enc);
             if (live) store_codes4<VC, FULL && kNtStore>(d.v, e, q);
         }
     }
@@ -576,9 +645,13 @@ void adamw_kernel(const AdamWLaunch a) {
     __shared__ double lut_all[4][NT];
     __shared__ double stab_all[4][NS];
     __shared__ uint2 skey_all[4][NK];
+    __shared__ uint4 encp_all[4][NK];     // blocks inside a sub-tile: fp32 encode parameters
+    __shared__ double2 encd_all[4][NK];   // and {l_min, (L - 2) / delta} for the binary64 recheck
     double* lut = lut_all[threadIdx.x >> 6];
     double* stab = stab_all[threadIdx.x >> 6];
     uint2* skey = skey_all[threadIdx.x >> 6];
+    uint4* encp = encp_all[threadIdx.x >> 6];
+    double2* encd = encd_all[threadIdx.x >> 6];
     if (chunk >= a.total_tiles) return;
     // the descriptor's pointers come from memory: mark them global so the
     // streams use global (not flat) loads and stores
@@ -588,9 +661,9 @@ void adamw_kernel(const AdamWLaunch a) {
     const int64_t e0 = (chunk - D[ti].tile_begin) * C;
     const int64_t valid = d.n - e0;
     if (valid >= C)
-        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut, stab, skey);
+        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut, stab, skey, encp, encd);
     else
-        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut, stab, skey);
+        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut, stab, skey, encp, encd);
 }
 
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }

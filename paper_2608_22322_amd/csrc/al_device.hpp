@@ -34,7 +34,9 @@ constexpr int kDppQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
 constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
 constexpr int kDppRowHalfMirror = 0x141;  // lane i -> 7-i within 8
 constexpr int kDppRowMirror = 0x140;      // lane i -> 15-i within 16
-// ds_swizzle bit mode: and_mask 0x1F, xor_mask 0x10 -> lane ^ 16 within 32
+// ds_swizzle bit mode: and_mask 0x1F, xor_mask m -> lane ^ m within 32
+constexpr int kSwzXor4 = 0x101F;
+constexpr int kSwzXor8 = 0x201F;
 constexpr int kSwzXor16 = 0x401F;
 
 // Every control word above reads a lane of the same row, so no lane is out of
@@ -165,13 +167,14 @@ __device__ __forceinline__ float al_decode_fast(uint32_t q, double lmin32, doubl
 constexpr double kLog2MantErr = 0x1p-21;
 
 // Per-block encode parameters: the binary64 interval start, LEVELS/delta,
-// and a guard band on the code position.
+// and a guard band on the code position (binary64 and fp32 arithmetic).
 struct ALEnc {
     double lmin;
     double inv;    // (L - 2) / delta
     double fr;     // lmin - floor(lmin), exact
     double guard;  // bound on |fast position - binary64 position|
     int I;         // floor(lmin)
+    float inv32, fr32, guard32;  // the fp32 path (AL8): fl32(inv), fl32(fr), its guard
 };
 
 __device__ __forceinline__ ALEnc al_enc_params(double lmin, double inv) {
@@ -182,6 +185,13 @@ __device__ __forceinline__ ALEnc al_enc_params(double lmin, double inv) {
     p.I = (int)I;
     p.fr = lmin - I;
     p.guard = inv * kLog2MantErr + 1e-9;
+    // fp32 path: |y32 - y| <= inv (kLog2MantErr + 2^-24 + 2^-25) + 3 * 2^-24 |y| (the mantissa log,
+    // the fp32 rounding of fr and of l - fr, and three relative roundings of at most 2^-24: d, inv, the
+    // product); only |y| <= 255 decides a code (beyond it both sides clamp), so 1.25 * 2^-21 inv +
+    // 2^-14 bounds it
+    p.inv32 = (float)inv;
+    p.fr32 = (float)p.fr;
+    p.guard32 = (float)(inv * 0x1.4p-21 + 0x1p-14);
     return p;
 }
 
@@ -204,6 +214,33 @@ __device__ __forceinline__ uint32_t al_encode_fast(float x, const ALEnc& p) {
         r = __builtin_rint(yc);
     }
     return x > 0.0f ? 1u + (uint32_t)r : 0u;
+}
+
+// AL8 code of x with the fast position in fp32 arithmetic (AL8 positions are
+// at most 254, so fp32 carries them to about 2^-16); the guard band of
+// al_enc_params covers the fp32 roundings, and positions inside it take the
+// same binary64 recheck as al_encode_fast, so every rounding decision is the
+// binary64 one.
+// SLOW() returns {lmin, inv} for the recheck (read only when it is needed).
+template <class Slow>
+__device__ __forceinline__ uint32_t al_encode_f32(float x, int I, float fr32, float inv32, float guard32, Slow slow) {
+    constexpr float L = 254.0f;
+    const float mant = __builtin_amdgcn_frexp_mantf(x);
+    const int ex = __builtin_amdgcn_frexp_expf(x);
+    const float l = __builtin_amdgcn_logf(mant);
+    const float d = (float)(ex - I) + (l - fr32);
+    float yc = __builtin_fminf(__builtin_fmaxf(d * inv32, 0.0f), L);
+    float r = __builtin_rintf(yc);
+    if (__builtin_fabsf(yc - r) > 0.5f - guard32) {
+        const double2 li = slow();
+        const double ys = (log2((double)x) - li.x) * li.y;
+        r = (float)__builtin_rint(__builtin_fmin(__builtin_fmax(ys, 0.0), 254.0));
+    }
+    return x > 0.0f ? 1u + (uint32_t)r : 0u;
+}
+
+__device__ __forceinline__ uint32_t al_encode_f32(float x, const ALEnc& p) {
+    return al_encode_f32(x, p.I, p.fr32, p.inv32, p.guard32, [&] { return make_double2(p.lmin, p.inv); });
 }
 
 // fl32(x / d) from a precomputed rd = fl64(1 / d). q = fl64(x * rd) lies
