@@ -300,6 +300,7 @@ struct ApolloPlan {
     std::vector<al::ApolloDesc> desc;
     std::vector<int> idx;  // tensor index of each descriptor (empty tensors are skipped)
     int64_t total_tiles = 0, total_chans = 0, total_units = 0;
+    int32_t any_whole = 0, any_ragged = 0;
     size_t adamw_off = 0;  // descriptor table of the AdamW launch over the projected moments
     size_t bytes = 0;
 };
@@ -346,6 +347,8 @@ al_status apollo_plan(const al_apollo_tensor* ts, int nt, const al_apollo_cfg* c
         P.total_chans += C;
         d.unit_begin = P.total_units;
         P.total_units += (int64_t)d.nru * d.ncu;
+        d.whole = t.rows % 256 == 0 && t.cols % 256 == 0;
+        (d.whole ? P.any_whole : P.any_ragged) = 1;
         P.desc.push_back(d);
         P.idx.push_back(i);
     }
@@ -623,6 +626,8 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
     a.total_tiles = P.total_tiles;
     a.total_chans = P.total_chans;
     a.total_units = P.total_units;
+    a.any_whole = P.any_whole;
+    a.any_ragged = P.any_ragged;
     a.lr = cfg->lr;
     a.decay = 1.0 - cfg->lr * cfg->weight_decay;
     a.gamma = cfg->gamma;

@@ -184,7 +184,7 @@ struct ApolloDesc {
     int64_t unit_begin;  // first 256x256 update unit
     int32_t right;       // channels are rows (rows >= cols)
     int32_t nru, ncu;
-    int32_t pad_;
+    int32_t whole;       // rows and columns multiples of 256 (the update takes the streaming chunk layout)
 };
 
 constexpr int kApolloCopyBatch = 16;
@@ -196,6 +196,7 @@ struct ApolloDescBatch {
 struct ApolloArgs {
     const ApolloDesc* D;
     int32_t nt, rank;
+    int32_t any_whole, any_ragged;  // some tensors are (are not) made of whole 256x256 units
     int64_t total_tiles, total_chans, total_units;
     double lr, decay, gamma;
     int64_t step;

@@ -11,11 +11,12 @@
 //           exact and the accumulation is binary64, so fl32 of the result is
 //           the exactly rounded value except within ~L ulps of binary64 of an
 //           fp32 midpoint. Also sums g^2 per channel and clears Rt.
-//   scale   one wavefront per channel: s_c = ||Rt_c|| / (||R_c|| + 1e-8).
+//   scale   16 lanes per channel: s_c = ||Rt_c|| / (||R_c|| + 1e-8).
 //   norm    one wavefront per tensor: ||G~||^2 = sum_c s_c^2 ||G_c||^2 and the
 //           norm-growth limiter.
-//   update  p = fl32(p (1 - lr wd) - lr g (s_c / lam)) over 256x256 units,
-//           one wavefront per unit, 4 columns per lane, rows in batches.
+//   update  p = fl32(p (1 - lr wd) - lr g (s_c / lam)): one wavefront per
+//           8-row chunk of a 256x256 unit (per unit for tensors of other
+//           shapes).
 // The projection is the one dense contraction of the path (2 r flops per
 // parameter); everything else streams.
 #include "al_device.hpp"
@@ -217,34 +218,50 @@ hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s
 
 // ------------------------------------------------------------ channel scales
 // A wavefront takes kScaleCh consecutive channels of the list (one tensor's
-// channels are consecutive, so a group may span two tensors), 4 elements per
-// lane with 16-byte loads; each channel's two sums of squares reduce over
-// the wavefront in a fixed butterfly order. Rt holds the negated direction
-// (the AdamW kernel's parameter output from zero); only squares are used.
-constexpr int kScaleCh = 4;
+// channels are consecutive, so a group may span two tensors), 4 at a time:
+// 16 lanes per channel, 16-byte loads of R and Rt covering 4 KB of each, and
+// each channel's two sums of squares merged over its 16 lanes with DPP in a
+// fixed order. Rt holds the negated direction (the AdamW kernel's parameter
+// output from zero); only squares are used.
+constexpr int kScaleCh = 16;
+
+__device__ __forceinline__ double row16_sum_d(double x) {
+    x += dpp_d<kDppQuadXor1>(x);
+    x += dpp_d<kDppQuadXor2>(x);
+    x += dpp_d<kDppRowHalfMirror>(x);
+    x += dpp_d<kDppRowMirror>(x);
+    return x;
+}
 
 __global__ __launch_bounds__(256) void apollo_scale_kernel(const ApolloArgs a) {
-    const int lane = threadIdx.x & 63;
+    const int lane = threadIdx.x & 63, sub = lane >> 4, l16 = lane & 15;
     const int64_t ch0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kScaleCh;
     const int r = a.rank;
-    for (int q = 0; q < kScaleCh; ++q) {
-        const int64_t ch = ch0 + q;
-        if (ch >= a.total_chans) return;
-        const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::chan_begin>(a.D, a.nt, ch)];
-        const int64_t c = ch - d.chan_begin;
+    for (int q = 0; q < kScaleCh; q += 4) {
+        const int64_t ch = ch0 + q + sub;  // this lane's channel
+        const bool live = ch < a.total_chans;
+        if (__builtin_amdgcn_readfirstlane(ch0 + q) >= a.total_chans) return;
         double st = 0.0, sr = 0.0;
-        for (int k = 4 * lane; k < r; k += 256) {
-            const float4 x = *reinterpret_cast<const float4*>(d.Rt + c * r + k);
-            const float4 y = *reinterpret_cast<const float4*>(d.R + c * r + k);
-            st += (double)x.x * x.x + (double)x.y * x.y + (double)x.z * x.z + (double)x.w * x.w;
-            sr += (double)y.x * y.x + (double)y.y * y.y + (double)y.z * y.z + (double)y.w * y.w;
+        int64_t c = 0;
+        const ApolloDesc* dp = nullptr;
+        if (live) {
+            dp = &a.D[apollo_locate<&ApolloDesc::chan_begin>(a.D, a.nt, ch)];
+            c = ch - dp->chan_begin;
+            const gp<const float> rt = to_g((const float*)dp->Rt) + c * r;
+            const gp<const float> rr = to_g((const float*)dp->R) + c * r;
+            for (int k = 4 * l16; k < r; k += 64) {
+                const float4 x = ld_f4<false>(rt + k);
+                const float4 y = ld_f4<false>(rr + k);
+                st += ((double)x.x * x.x + (double)x.y * x.y) + ((double)x.z * x.z + (double)x.w * x.w);
+                sr += ((double)y.x * y.x + (double)y.y * y.y) + ((double)y.z * y.z + (double)y.w * y.w);
+            }
         }
-        st = wave_sum_d(st);
-        sr = wave_sum_d(sr);
-        if (lane == 0) {
+        st = row16_sum_d(st);
+        sr = row16_sum_d(sr);
+        if (live && l16 == 0) {
             const double sc = sqrt(st) / (sqrt(sr) + 1e-8);
-            d.s[c] = sc;
-            d.sg[c] = sc * sc * d.gn2[c];
+            dp->s[c] = sc;
+            dp->sg[c] = sc * sc * dp->gn2[c];
         }
     }
 }
@@ -302,6 +319,7 @@ __global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) 
                          __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (unit >= a.total_units) return;
     const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::unit_begin>(a.D, a.nt, unit)];
+    if (d.whole) return;  // the chunk kernel's
     const int64_t u = unit - d.unit_begin;
     const int64_t ru = u / d.ncu, cu = u % d.ncu;
     const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
@@ -379,8 +397,100 @@ __global__ __launch_bounds__(256) void apollo_update_kernel(const ApolloArgs a) 
     }
 }
 
+// Tensors of whole 256x256 units: one wavefront per chunk of 8 unit rows
+// (2048 elements, 4 per 256-thread workgroup) with no loop, lane 32 h + q on
+// rows 2k + h and columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3, so every
+// access covers contiguous row segments; all loads of the chunk before its
+// stores. A chunk of another tensor returns (the unit kernel takes those).
+constexpr int kUpdChunkRows = 8;
+
+template <int G, bool RIGHT>
+__device__ __forceinline__ void apollo_update_chunk(const ApolloArgs& a, const ApolloDesc& d, int64_t row0, int64_t c0,
+                                                    int q) {
+    const int64_t cols = d.cols;
+    const double lam = d.lam[0];
+    const gp<const double> sv = to_g((const double*)d.s);
+    const gp<float> pp = to_g(d.p);
+    constexpr int NP = kUpdChunkRows / 2;
+    float4 pv[NP][2];
+    uint2 gw[NP][2];
+    float4 gf[NP][2];
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            const int64_t e = (row0 + 2 * k) * cols + c0 + 128 * sg + 4 * q;
+            pv[k][sg] = ld_f4<true>(gp<const float>(pp + e));
+            if constexpr (G == G_BF16)
+                gw[k][sg] = ld_u2<true>(g_as<const void>(to_g((const uint16_t*)d.g) + e));
+            else
+                gf[k][sg] = ld_f4<true>(to_g((const float*)d.g) + e);
+        }
+    }
+    // channel scales s_c / lambda: one per row pair (channels are rows) or per column
+    double sr[RIGHT ? NP : 1], sc[RIGHT ? 1 : 2][4];
+    if constexpr (RIGHT) {
+#pragma unroll
+        for (int k = 0; k < NP; ++k) sr[k] = sv[row0 + 2 * k] / lam;
+    } else {
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sc[sg][j] = sv[c0 + 128 * sg + 4 * q + j] / lam;
+    }
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg) {
+            float gv[4];
+            if constexpr (G == G_BF16) {
+                gv[0] = bf16_to_f32(gw[k][sg].x & 0xFFFFu), gv[1] = bf16_to_f32(gw[k][sg].x >> 16);
+                gv[2] = bf16_to_f32(gw[k][sg].y & 0xFFFFu), gv[3] = bf16_to_f32(gw[k][sg].y >> 16);
+            } else {
+                gv[0] = gf[k][sg].x, gv[1] = gf[k][sg].y, gv[2] = gf[k][sg].z, gv[3] = gf[k][sg].w;
+            }
+            const float pin[4] = {pv[k][sg].x, pv[k][sg].y, pv[k][sg].z, pv[k][sg].w};
+            float out[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const double upd = (double)gv[j] * (RIGHT ? sr[k] : sc[RIGHT ? 0 : sg][j]);
+                out[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+            }
+            const int64_t e = (row0 + 2 * k) * cols + c0 + 128 * sg + 4 * q;
+            st_f4<true>(pp + e, make_float4(out[0], out[1], out[2], out[3]));
+        }
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(256) void apollo_update_chunk_kernel(const ApolloArgs a) {
+    const int lane = threadIdx.x & 63, h = lane >> 5, q = lane & 31;
+    const int64_t chunk = xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = chunk / (256 / kUpdChunkRows);
+    if (unit >= a.total_units) return;
+    const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::unit_begin>(a.D, a.nt, unit)];
+    if (!d.whole) return;
+    const int64_t u = unit - d.unit_begin;
+    const int64_t r0 = (u / d.ncu) * 256, c0 = (u % d.ncu) * 256;
+    const int64_t row0 = r0 + (chunk % (256 / kUpdChunkRows)) * kUpdChunkRows + h;
+    if (d.right)
+        apollo_update_chunk<G, true>(a, d, row0, c0, q);
+    else
+        apollo_update_chunk<G, false>(a, d, row0, c0, q);
+}
+
 hipError_t launch_apollo_update(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_units == 0) return hipSuccess;
+    if (a.any_whole) {
+        const unsigned grid = (unsigned)((a.total_units * (256 / kUpdChunkRows) + 3) / 4);
+        if (grad_dtype == G_BF16)
+            hipLaunchKernelGGL(apollo_update_chunk_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL(apollo_update_chunk_kernel<G_F32>, dim3(grid), dim3(256), 0, s, a);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (!a.any_ragged) return hipSuccess;
     const unsigned grid = (unsigned)((a.total_units + 3) / 4);
     if (grad_dtype == G_BF16)
         hipLaunchKernelGGL(apollo_update_kernel<G_BF16>, dim3(grid), dim3(256), 0, s, a);
