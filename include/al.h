@@ -319,6 +319,16 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * the clipped updates. x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
+/* The AL8 levels of the fused AdamW step's split-table decode (section 4.1,
+ * Eq. al_dequant): for each of nblocks blocks with metadata {l_min, delta}
+ * (fp32 pairs, the AL8 layout), out[255 b + q - 1] is the binary64 value of
+ * the level of code q = 1..255 before its rounding to fp32, computed by the
+ * same device functions as the step: kind 0 = two factors (blocks of 128 and
+ * more), 1 = three factors (blocks of 64). meta, out: device, 16-byte
+ * aligned; out holds 255 nblocks doubles. For measuring the decode's error
+ * against 2^E. */
+al_status al_diag_levels(int32_t kind, const float* meta, int64_t nblocks, double* out, void* stream);
+
 /* Sums of squares behind the relative update error of section 3.2 (Eq.
  * update_error): with U = a, U_ref = b (two updates of the same n elements,
  * fp32 device arrays), writes out[0] = sum_i (a_i - b_i)^2 and out[1] =

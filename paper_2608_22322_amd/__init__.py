@@ -83,7 +83,7 @@ EXPORTS = ("al_version", "al_last_error", "al_code_bytes", "al_meta_floats", "al
            "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adamw_step_noalloc",
            "al_adafactor_workspace_bytes", "al_came_workspace_bytes",
            "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes", "al_apollo_step", "al_diag_math",
-           "al_diag_stream", "al_diff_norms", "al_synth_normal")
+           "al_diag_levels", "al_diag_stream", "al_diff_norms", "al_synth_normal")
 
 
 def lib():
@@ -118,12 +118,13 @@ def lib():
         L.al_apollo_step.argtypes = [ctypes.POINTER(ApolloTensor), i32, ctypes.POINTER(ApolloCfg), i64, vp, sz, vp]
         L.al_synth_normal.argtypes = [vp, i32, i64, u64, f, u64, u64, vp]
         L.al_diag_math.argtypes = [i32, vp, i64, vp, vp]
+        L.al_diag_levels.argtypes = [i32, vp, i64, vp, vp]
         L.al_diag_stream.argtypes = [i32, vp, vp, vp, vp, i64, vp]
         L.al_diff_norms.argtypes = [vp, vp, i64, vp, vp]
         for name in ("al_quantize", "al_dequantize", "al_adamw_workspace_bytes", "al_adamw_step", "al_adamw_step_noalloc",
                      "al_adafactor_workspace_bytes",
                      "al_came_workspace_bytes", "al_adafactor_step", "al_came_step", "al_apollo_workspace_bytes",
-                     "al_apollo_step", "al_diag_math", "al_diag_stream",
+                     "al_apollo_step", "al_diag_math", "al_diag_levels", "al_diag_stream",
                      "al_diff_norms", "al_synth_normal"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -203,6 +204,12 @@ def dequantize(codec: int, codes, meta, n: int, block: int, out, stream=None) ->
 
 def diag_math(fn: int, x, out, stream=None) -> None:
     check(lib().al_diag_math(fn, _ptr(x), x.numel(), _ptr(out), _stream(stream)))
+
+
+def diag_levels(kind: int, meta, nblocks: int, out, stream=None) -> None:
+    """Binary64 AL8 levels of codes 1..255 per block through the step's split tables (kind 0: two factors,
+    1: three factors), before the fp32 rounding."""
+    check(lib().al_diag_levels(kind, _ptr(meta), nblocks, _ptr(out), _stream(stream)))
 
 
 def diag_stream(nontemporal: bool, p, g, m, v, stream=None, wide: bool = False) -> None:

@@ -43,6 +43,32 @@ namespace al {
 // the whole chunk, next to the descriptor read from the table, and spill).
 __constant__ Exp2Coef kExp2 = AL_EXP2_TAYLOR;
 
+// Split-table decode of AL8 levels. A code q >= 1 stands for level q - 1,
+// fl32(2^(l32 + (q - 1) st)) with l32 = fl32(l_min) and st = delta32 / 254 in
+// binary64 (Eq. al_dequant). Two factors (blocks of 128+): q = 16 a + b and
+// 2^(l32 + (q - 1) st) = 2^(l32 + (16 a - 1) st) * 2^(b st), table entries
+// j < 16 the first factor, 16 + j the second. Three factors (blocks of 64):
+// q = 64 a + 8 b + c, entries [0, 4) 2^(l32 + (64 a - 1) st), [4, 12) 2^(8 b st),
+// [12, 20) 2^(c st). The binary64 value before the fp32 rounding is the
+// product; al_diag_levels evaluates the same functions.
+__device__ __forceinline__ double split2_entry(double l32, double st, int j) {
+    const double arg = j < 16 ? l32 + (double)(16 * j - 1) * st : (double)(j - 16) * st;
+    return exp2_d(arg, kExp2);
+}
+__device__ __forceinline__ double split2_product(double f1, double f2) { return f1 * f2; }
+__device__ __forceinline__ double split2_level(const double* t, uint32_t q) {
+    return split2_product(t[q >> 4], t[16 + (q & 15u)]);
+}
+__device__ __forceinline__ double split3_entry(double l32, double st, int j) {
+    const double arg = j < 4 ? l32 + (double)(64 * j - 1) * st
+                             : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
+    return exp2_d(arg, kExp2);
+}
+__device__ __forceinline__ double split3_product(double f1, double f2, double f3) { return (f1 * f2) * f3; }
+__device__ __forceinline__ double split3_level(const double* t, uint32_t q) {
+    return split3_product(t[q >> 6], t[4 + ((q >> 3) & 7u)], t[12 + (q & 7u)]);
+}
+
 // Every byte the step touches is read once and written once, so the full-chunk
 // path may mark its loads and stores non-temporal (streaming).
 constexpr bool kNtLoad = AL_ADAMW_NT_LOAD != 0;
@@ -279,8 +305,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     // positive levels fl32(2^(l_min + k step)), k = 0..254, built in this
     // wavefront's LDS slice (4 levels per lane) from the block's 16 + 16
     // split factors below (32 evaluations per block instead of 255; a level is
-    // one binary64 product, relative error about (ln 2 |E| + 2.5) 2^-53 before
-    // the fp32 rounding). LDS traffic of one wavefront is ordered, so no barrier is
+    // one binary64 product, relative error below (ln 2 (|l_min| + 3 k st) + 5)
+    // 2^-53 before the fp32 rounding). LDS traffic of one wavefront is ordered, so no barrier is
     // needed between building and reading its own tables.
     // Entry 0 holds 0.0 (code 0 is exact zero), entry q the level of code q,
     // kept in binary64 (the fp32 value widened) for the binary64 EMA.
@@ -294,9 +320,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const float l0 = u2f(readlane_u(f2u(om.l), 32 + b0));
             const float l1 = u2f(readlane_u(f2u(om.l), 32 + b1));
             const double st = lane < 32 ? st0 : st1;
-            const int j = lane & 31;
-            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j - 1) * st : (double)(j - 16) * st;
-            const double v = exp2_d(arg, kExp2);
+            const double v = split2_entry((double)(lane < 32 ? l0 : l1), st, lane & 31);
             if (lane + kWave * i < NF) stab[lane + kWave * i] = v;
         }
 #pragma unroll
@@ -305,7 +329,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int k = lane + 64 * i;
-                const float lv = (float)(t[k >> 4] * t[16 + (k & 15)]);
+                const float lv = (float)split2_level(t, (uint32_t)k);
                 lut[b * 256 + k] = k == 0 ? 0.0 : (double)lv;
             }
         }
@@ -316,9 +340,9 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     // q - 1, 2^(l_min + (q - 1) step) = 2^(l_min + (16 a - 1) step) * 2^(b step):
     // entries [0, 16) of a block's split table hold the first factor, [16, 32)
     // the second, so a block costs 32 evaluations and an element one binary64
-    // product indexed by the code's two nibbles (relative error about
-    // (ln 2 |E| + 2.5) 2^-53 against 2^E, then rounded to fp32; code 0 is
-    // replaced by exact zero).
+    // product indexed by the code's two nibbles (relative error below
+    // (ln 2 (|l_min| + 3 (q - 1) st) + 5) 2^-53 against 2^E, then rounded to
+    // fp32; code 0 is replaced by exact zero).
     if constexpr (Q::SPLIT) {
         static_assert(NB * 32 % kWave == 0, "split tables fill whole wavefront passes");
 #pragma unroll
@@ -328,9 +352,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const float l0 = u2f(readlane_u(f2u(om.l), 32 + 2 * i));
             const float l1 = u2f(readlane_u(f2u(om.l), 33 + 2 * i));
             const double st = lane < 32 ? st0 : st1;
-            const int j = lane & 31;
-            const double arg = j < 16 ? (double)(lane < 32 ? l0 : l1) + (double)(16 * j - 1) * st : (double)(j - 16) * st;
-            stab[lane + kWave * i] = exp2_d(arg, kExp2);
+            stab[lane + kWave * i] = split2_entry((double)(lane < 32 ? l0 : l1), st, lane & 31);
         }
     }
 
@@ -338,8 +360,8 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     // 2^(l_min + (q - 1) step) = 2^(l_min + (64 a - 1) step) * 2^(8 b step) *
     // 2^(c step): 20 entries per block ([0, 4) first factor, [4, 12) second,
     // [12, 20) third), 5 evaluations per lane for the chunk's 16 blocks, and two
-    // binary64 products per element (relative error about (ln 2 |E| + 4) 2^-53,
-    // then rounded to fp32).
+    // binary64 products per element (relative error below (ln 2 (|l_min| + 3 (q - 1)
+    // st) + 7) 2^-53, then rounded to fp32).
     if constexpr (Q::SPLIT3) {
         static_assert(NB * 20 % kWave == 0, "three-factor tables fill whole wavefront passes");
 #pragma unroll
@@ -348,9 +370,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const int b = e / 20, j = e - 20 * b;
             const double st = shfl_d(q1, 32 + b);
             const double l32 = (double)__shfl(om.l, 32 + b);
-            const double arg = j < 4 ? l32 + (double)(64 * j - 1) * st
-                                     : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
-            stab[e] = exp2_d(arg, kExp2);
+            stab[e] = split3_entry(l32, st, j);
         }
     }
 
@@ -395,7 +415,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const float lv = (float)(t[q >> 4] * t[16 + (q & 15u)]);
+                const float lv = (float)split2_level(t, q);
                 vh[j] = q == 0u ? 0.0f : lv;
             }
         } else if constexpr (Q::SPLIT3) {
@@ -403,7 +423,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const float lv = (float)((t[q >> 6] * t[4 + ((q >> 3) & 7u)]) * t[12 + (q & 7u)]);
+                const float lv = (float)split3_level(t, q);
                 vh[j] = q == 0u ? 0.0f : lv;
             }
         } else if constexpr (VQ) {
@@ -667,6 +687,33 @@ void adamw_kernel(const AdamWLaunch a) {
 }
 
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
+
+// al_diag_levels: every positive AL8 level of each block through the step
+// kernel's split-table functions, as the binary64 product before the fp32
+// rounding (kind 0: two factors, kind 1: three factors).
+__global__ __launch_bounds__(256) void diag_levels_kernel(int kind, const float* __restrict__ meta, int64_t nblocks,
+                                                          double* __restrict__ out) {
+    const int64_t total = nblocks * 255;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t b = i / 255;
+        const uint32_t q = 1u + (uint32_t)(i - b * 255);
+        const double l32 = (double)meta[2 * b], st = (double)meta[2 * b + 1] / 254.0;
+        if (kind == 0)
+            out[i] = split2_product(split2_entry(l32, st, (int)(q >> 4)), split2_entry(l32, st, 16 + (int)(q & 15u)));
+        else
+            out[i] = split3_product(split3_entry(l32, st, (int)(q >> 6)),
+                                    split3_entry(l32, st, 4 + (int)((q >> 3) & 7u)),
+                                    split3_entry(l32, st, 12 + (int)(q & 7u)));
+    }
+}
+
+hipError_t launch_diag_levels(int kind, const float* meta, int64_t nblocks, double* out, int grid_cap, hipStream_t s) {
+    if (nblocks == 0) return hipSuccess;
+    const int64_t want = (nblocks * 255 + 255) / 256;
+    const int grid = (int)(want < grid_cap ? want : grid_cap);
+    hipLaunchKernelGGL(diag_levels_kernel, dim3(grid), dim3(256), 0, s, kind, meta, nblocks, out);
+    return hipGetLastError();
+}
 
 // ------------------------------------------------------------ descriptor table
 struct AdamWDescBatch {

@@ -690,6 +690,17 @@ al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void
     return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_math launch");
 }
 
+al_status al_diag_levels(int32_t kind, const float* meta, int64_t nblocks, double* out, void* stream) {
+    g_err[0] = 0;
+    if (kind < 0 || kind > 1) return fail(AL_EINVAL, "al_diag_levels: kind %d", kind);
+    if (nblocks < 0 || nblocks > (int64_t(1) << 40)) return fail(AL_EINVAL, "al_diag_levels: nblocks out of range");
+    if (nblocks == 0) return AL_OK;
+    if (!meta || !out) return fail(AL_EINVAL, "al_diag_levels: NULL buffer");
+    if (!aligned16(meta) || !aligned16(out)) return fail(AL_EALIGN, "al_diag_levels: alignment");
+    hipError_t e = al::launch_diag_levels(kind, meta, nblocks, out, al::device_cu_count() * 8, as_stream(stream));
+    return e == hipSuccess ? AL_OK : hip_fail(e, "al_diag_levels launch");
+}
+
 al_status al_diff_norms(const float* a, const float* b, int64_t n, double* out, void* stream) {
     g_err[0] = 0;
     if (n < 0) return fail(AL_EINVAL, "al_diff_norms: n < 0");

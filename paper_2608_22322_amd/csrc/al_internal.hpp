@@ -150,6 +150,8 @@ struct FacArgs {
     Exp2Coef cf;
 };
 
+hipError_t launch_diag_levels(int kind, const float* meta, int64_t nblocks, double* out, int grid_cap, hipStream_t s);
+
 hipError_t fac_copy_desc(const FacDesc* host, int count, FacDesc* dev, hipStream_t s);
 hipError_t launch_fac_marg_g2(const FacArgs& a, int grad_dtype, hipStream_t s);
 hipError_t launch_fac_fin(const FacArgs& a, int role, int grad_dtype, hipStream_t s);

@@ -175,11 +175,12 @@ def _factored_run(dev, came, shapes, bf16):
                      [getattr(st, r + "_meta") for st in states for r in roles])
 
 
+@pytest.mark.parametrize("bf16", [True, False])
 @pytest.mark.parametrize("came", [False, True])
-def test_factored_bounds_and_determinism(dev, came):
-    shapes = [(300, 257), (37, 130), (256, 512), (1, 700), (513, 64)]
-    a = _factored_run(dev, came, shapes, True)
-    b = _factored_run(dev, came, shapes, True)
+def test_factored_bounds_and_determinism(dev, came, bf16):
+    shapes = [(300, 257), (37, 130), (256, 512), (1, 700), (513, 64), (512, 256)]
+    a = _factored_run(dev, came, shapes, bf16)
+    b = _factored_run(dev, came, shapes, bf16)
     assert all(np.array_equal(x, y) for x, y in zip(a, b))
     log(f"{'came' if came else 'adafactor'}: guards intact, runs identical")
 
@@ -215,7 +216,7 @@ def _apollo_run(dev, shapes, rank):
 
 
 def test_apollo_bounds_and_determinism(dev):
-    shapes = [(70, 33), (40, 300), (129, 64), (5, 700)]
+    shapes = [(70, 33), (40, 300), (256, 512), (129, 64), (5, 700), (512, 256)]
     a = _apollo_run(dev, shapes, 64)
     b = _apollo_run(dev, shapes, 64)
     assert all(np.array_equal(x, y) for x, y in zip(a, b))

@@ -1,8 +1,9 @@
 """GPU parity of the factored optimizer steps (al_adafactor_step, al_came_step)
 against the CPU oracle.
 
-* ragged tensor lists (partial 64x64 tiles, odd column counts, 1-D tensors)
-  over codec / block combinations, bf16 and fp32 grads, 3 steps;
+* ragged tensor lists (partial 64x64 tiles, odd column counts, 1-D tensors,
+  and tensors of whole 256x256 units) over codec / block combinations, bf16
+  and fp32 grads, 3 steps;
 * 50-step trajectories on TinyLlama-shaped tensors (AL8 B256 Adafactor;
   AL16 B128 + UF8 CAME);
 * the full TinyLlama-1.1B list stepped on the GPU in one call, with whole
@@ -142,8 +143,11 @@ def _cmp_state(codes, meta, hs, tag):
     return near
 
 
-RAGGED = [Shape("a", 5, 7), Shape("b", 64, 256), Shape("c", 130, 513), Shape("d", 300, 66), Shape("e", 2, 1030),
-          Shape("f", 1, 1), Shape("g", 1, 777), Shape("h", 257, 3), Shape("i", 1, 2048)]
+# ragged shapes (partial units, odd widths, 1-D) and two tensors of whole 256x256 units (w, x: the
+# streaming kernels), so every codec combination and both gradient types cover both kernel families
+RAGGED = [Shape("a", 5, 7), Shape("b", 64, 256), Shape("w", 256, 512), Shape("c", 130, 513), Shape("d", 300, 66),
+          Shape("e", 2, 1030), Shape("f", 1, 1), Shape("x", 512, 256), Shape("g", 1, 777), Shape("h", 257, 3),
+          Shape("i", 1, 2048)]
 
 
 @pytest.mark.parametrize("grad_bf16", [True, False])
