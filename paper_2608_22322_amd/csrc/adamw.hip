@@ -481,7 +481,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             const double rr = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
             uint32_t q[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mn[j] * rr) & 0xFFu;
+            for (int j = 0; j < 4; ++j) q[j] = rint_low_bits((double)mn[j] * rr) & 0xFFu;
             if (FULL || k * kSub < valid) {
                 store_codes4<UF8, FULL && kNtStore>(d.m, e, q);
                 if (lane == 0) d.ms[e0 / kSub + k] = u2f(am);

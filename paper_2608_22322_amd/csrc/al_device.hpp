@@ -246,14 +246,15 @@ __device__ __forceinline__ uint32_t al_encode_f32(float x, const ALEnc& p) {
 // fl32(x / d) from a precomputed rd = fl64(1 / d). q = fl64(x * rd) lies
 // within 2.5 binary64 ulps of fl64(x / d), so the two round to the same fp32
 // value unless q is that close to an fp32 rounding midpoint (its 29 low
-// mantissa bits near 2^28) or fl32(q) leaves the normal range (subnormal
+// mantissa bits near 2^28) or |fl32(q)| is not above FLT_MIN (subnormal
 // results round on a coarser grid; FLT_MIN itself may be the rounding of a
-// subnormal-range q); those rare cases take the binary64 division. The
-// conditions combine as lane masks, with no short-circuit branches.
+// subnormal-range q); those rare cases take the binary64 division. An
+// infinite fl32(q) passes: the overflow threshold is the midpoint above
+// FLT_MAX, which the low-bit test catches; a NaN fails. The conditions
+// combine as lane masks, with no short-circuit branches.
 __device__ __forceinline__ bool quotient_ok(double q, float f) {
     const uint32_t low = (uint32_t)__builtin_bit_cast(uint64_t, q) & 0x1FFFFFFFu;
-    const bool normal = __builtin_amdgcn_classf(f, 0x108) & (__builtin_fabsf(f) != 0x1p-126f);  // +-normal
-    return (q == 0.0) | (normal & (low - 0x0FFFFFF8u > 16u));
+    return (q == 0.0) | ((__builtin_fabsf(f) > 0x1p-126f) & (low - 0x0FFFFFF8u > 16u));
 }
 
 __device__ __forceinline__ float div_to_f32(double x, double d, double rd) {
@@ -347,6 +348,14 @@ __device__ __forceinline__ DD dd_wave_sum(DD a) {
 }
 
 // ----------------------------------------------------------------- UF8 code
+// The low byte of rint(y) in two's complement, for |y| <= 2^51: adding
+// 1.5 2^52 rounds y to an integer in the sum's last place (to nearest even,
+// as rint does), and the sum's low word is then 2^51 + rint(y). One binary64
+// addition in place of a rounding and a conversion.
+__device__ __forceinline__ uint32_t rint_low_bits(double y) {
+    return (uint32_t)__builtin_bit_cast(uint64_t, y + 0x1.8p52);
+}
+
 // Encode with r = 127 / absmax (binary64), y = x * r, round to nearest even,
 // clamp to [-127, 127].
 __device__ __forceinline__ int32_t uf8_encode(float x, double r) {

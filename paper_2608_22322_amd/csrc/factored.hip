@@ -1791,7 +1791,7 @@ __global__ __launch_bounds__(256) void came_apply_unit_kernel(const FacArgs a, i
                 const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
                 uint32_t q[4];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) q[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[j] * rs) & 0xFFu;
+                for (int j = 0; j < 4; ++j) q[j] = rint_low_bits((double)mnew[j] * rs) & 0xFFu;
                 const uint32_t w = (q[0] & 0xFFu) | ((q[1] & 0xFFu) << 8) | ((q[2] & 0xFFu) << 16) | (q[3] << 24);
                 st_u1<true>(g_as<void>(g_as<uint8_t>(d.m) + e), w);
                 if (lane == 0) d.mm[(e - c) / 256] = u2f(am);
@@ -1872,7 +1872,10 @@ __global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) 
 // 32 h + q: rows 2k + h, columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3).
 // A unit row is one 256-element momentum block held by the 32 lanes of one
 // half, so its absmax is a 32-lane reduction; each lane writes its codes as
-// two 4-byte words.
+// two 4-byte words. The kernel takes one row pair at a time (loads, then
+// stores): 90 registers, five waves per SIMD; loading all four pairs first
+// (152 registers, three waves) measured the same.
+constexpr int kCameApplyPairs = 1;
 template <int G, bool UF>
 __global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, int64_t base) {
     const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1883,28 +1886,6 @@ __global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, 
     const double clip = d.scal[0], rclip = 1.0 / clip;
     const gp<uint8_t> mc = g_as<uint8_t>(d.m);
     const gp<float> mf = g_as<float>(d.m);
-    constexpr int NP = kChunkRows / 2;
-    float gv[NP][2][4];
-    float4 pv[NP][2], mv[UF ? 1 : NP][2];
-    uint32_t mw[UF ? NP : 1][2];
-    float ms[NP];
-    double ri[NP], si[NP];
-#pragma unroll
-    for (int k = 0; k < NP; ++k) {
-        ri[k] = d.rfac[c.row0 + 2 * k];
-        si[k] = d.sr[c.row0 + 2 * k];
-        if constexpr (UF) ms[k] = d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8];
-#pragma unroll
-        for (int sg = 0; sg < 2; ++sg) {
-            const int64_t e = chunk_elem(c, k, sg);
-            load_g4<G>(d.g, e, gv[k][sg]);
-            pv[k][sg] = ld_f4<true>(d.p + e);
-            if constexpr (UF)
-                mw[k][sg] = ld_u1<true>(g_as<const void>(mc + e));
-            else
-                mv[k][sg] = ld_f4<true>(mf + e);
-        }
-    }
     double cf[2][4], sf[2][4];
 #pragma unroll
     for (int sg = 0; sg < 2; ++sg)
@@ -1913,51 +1894,79 @@ __global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, 
             cf[sg][j] = d.cfac[c.c0 + 128 * sg + 4 * c.q + j];
             sf[sg][j] = d.sc[c.c0 + 128 * sg + 4 * c.q + j];
         }
+    constexpr int NP = kCameApplyPairs;  // row pairs loaded together
 #pragma unroll
-    for (int k = 0; k < NP; ++k) {
-        float mnew[2][4];
-        const double st = UF ? div127((double)ms[k]) : 0.0;
+    for (int k0 = 0; k0 < kChunkRows / 2; k0 += NP) {
+        float gv[NP][2][4];
+        float4 pv[NP][2], mv[UF ? 1 : NP][2];
+        uint32_t mw[UF ? NP : 1][2];
+        float ms[NP];
+        double ri[NP], si[NP];
 #pragma unroll
-        for (int sg = 0; sg < 2; ++sg) {
-            float mh[4], uh[4];
-            if constexpr (UF) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[k][sg] >> (8 * j)), st);
-            } else {
-                mh[0] = mv[k][sg].x, mh[1] = mv[k][sg].y, mh[2] = mv[k][sg].z, mh[3] = mv[k][sg].w;
-            }
-            double uu[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) uu[j] = (ri[k] * cf[sg][j]) * (double)gv[k][sg][j];
-            div4_to_f32(uu, clip, rclip, uh);
-            const float pin[4] = {pv[k][sg].x, pv[k][sg].y, pv[k][sg].z, pv[k][sg].w};
-            float pout[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                mnew[sg][j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
-                const double upd = (si[k] * sf[sg][j]) * (double)mnew[sg][j];
-                pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
-            }
-            const int64_t e = chunk_elem(c, k, sg);
-            st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
-            if constexpr (!UF) st_f4<true>(mf + e, make_float4(mnew[sg][0], mnew[sg][1], mnew[sg][2], mnew[sg][3]));
-        }
-        if constexpr (UF) {
-            uint32_t am = 0u;
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[sg][j]));
-            am = group_reduce<OpMax, 32>(am);  // the row's block: the 32 lanes of this half
-            const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
+        for (int kk = 0; kk < NP; ++kk) {
+            const int k = k0 + kk;
+            ri[kk] = d.rfac[c.row0 + 2 * k];
+            si[kk] = d.sr[c.row0 + 2 * k];
+            if constexpr (UF) ms[kk] = d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8];
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg) {
-                uint32_t qv[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) qv[j] = (uint32_t)(int32_t)__builtin_rint((double)mnew[sg][j] * rs) & 0xFFu;
-                st_u1<true>(g_as<void>(mc + chunk_elem(c, k, sg)), qv[0] | (qv[1] << 8) | (qv[2] << 16) | (qv[3] << 24));
+                const int64_t e = chunk_elem(c, k, sg);
+                load_g4<G>(d.g, e, gv[kk][sg]);
+                pv[kk][sg] = ld_f4<true>(d.p + e);
+                if constexpr (UF)
+                    mw[kk][sg] = ld_u1<true>(g_as<const void>(mc + e));
+                else
+                    mv[kk][sg] = ld_f4<true>(mf + e);
             }
-            if (c.q == 0) d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8] = u2f(am);
+        }
+#pragma unroll
+        for (int kk = 0; kk < NP; ++kk) {
+            const int k = k0 + kk;
+            float mnew[2][4];
+            const double st = UF ? div127((double)ms[kk]) : 0.0;
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg) {
+                float mh[4], uh[4];
+                if constexpr (UF) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[kk][sg] >> (8 * j)), st);
+                } else {
+                    mh[0] = mv[kk][sg].x, mh[1] = mv[kk][sg].y, mh[2] = mv[kk][sg].z, mh[3] = mv[kk][sg].w;
+                }
+                double uu[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) uu[j] = (ri[kk] * cf[sg][j]) * (double)gv[kk][sg][j];
+                div4_to_f32(uu, clip, rclip, uh);
+                const float pin[4] = {pv[kk][sg].x, pv[kk][sg].y, pv[kk][sg].z, pv[kk][sg].w};
+                float pout[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    mnew[sg][j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
+                    const double upd = (si[kk] * sf[sg][j]) * (double)mnew[sg][j];
+                    pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+                }
+                const int64_t e = chunk_elem(c, k, sg);
+                st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
+                if constexpr (!UF) st_f4<true>(mf + e, make_float4(mnew[sg][0], mnew[sg][1], mnew[sg][2], mnew[sg][3]));
+            }
+            if constexpr (UF) {
+                uint32_t am = 0u;
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[sg][j]));
+                am = group_reduce<OpMax, 32>(am);  // the row's block: the 32 lanes of this half
+                const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg) {
+                    uint32_t qv[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) qv[j] = rint_low_bits((double)mnew[sg][j] * rs) & 0xFFu;
+                    st_u1<true>(g_as<void>(mc + chunk_elem(c, k, sg)), qv[0] | (qv[1] << 8) | (qv[2] << 16) | (qv[3] << 24));
+                }
+                if (c.q == 0) d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8] = u2f(am);
+            }
         }
     }
 }
