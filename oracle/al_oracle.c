@@ -22,10 +22,12 @@
  * Pin status (the CPU tests hold each function to something other than
  * itself): the codes to worked examples, invariants and brute force; AdamW
  * to torch.optim.AdamW; Adafactor to Hugging Face's Adafactor. CAME's
- * official implementation is not available: the CAME step is pinned only
- * through closed forms (beta1 = 0, uniform and rank-1 gradients, the
- * second-moment path at t = 1); multi-step CAME with beta1 > 0 is parity
- * unpinned beyond them.
+ * official implementation is not available: the CAME step is pinned through
+ * closed forms (beta1 = 0 against the clipped update, the second-moment path
+ * at t = 1, and 20 steps with beta1 = 0.9 for constant uniform and rank-1
+ * gradients, sign flips at one step or at element-specific steps, and a
+ * rows == 1 tensor); against CAME itself it stays parity unpinned for
+ * gradients of varying magnitude with beta1 > 0 beyond those structures.
  */
 #include "al_oracle.h"
 
