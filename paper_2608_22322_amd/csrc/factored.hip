@@ -1227,37 +1227,13 @@ __global__ __launch_bounds__(256) void ada_apply_kernel(const FacArgs a, int64_t
     }
 }
 
-// Whole units, one wavefront per chunk of 8 unit rows (2048 elements, 32 per
-// unit, 4 per 256-thread workgroup) with no loop: the grid itself streams,
-// as in the AdamW step. Lane 32 h + q takes rows 2k + h (k < 4) of the chunk
-// and columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3, so every load and
-// store instruction covers whole contiguous row segments (a half-wave 512
-// bytes of parameters, 256 of gradients). All loads of the chunk are issued
-// before its arithmetic and stores; 16-byte non-temporal parameter accesses.
-constexpr int kChunkRows = 8;
-
-struct ChunkLane {
-    int64_t r0, c0, cols, row0;  // row0: the lane's first row (within the tensor)
-    int h, q, rb;                // rb: the chunk's first row within the unit
-};
-
-__device__ __forceinline__ ChunkLane chunk_lane(const GD& d, int64_t u, int64_t chunk_in_unit) {
-    ChunkLane c;
-    c.h = (int)(threadIdx.x >> 5) & 1;
-    c.q = (int)threadIdx.x & 31;
-    c.r0 = (u / d.ncu) * 256;
-    c.c0 = (u % d.ncu) * 256;
-    c.cols = d.cols;
-    c.rb = (int)chunk_in_unit * kChunkRows;
-    c.row0 = c.r0 + c.rb + c.h;
-    return c;
-}
-
-// Element index of (row pair k, column group s) of the lane: row row0 + 2k,
-// column c0 + 128 s + 4 q.
-__device__ __forceinline__ int64_t chunk_elem(const ChunkLane& c, int k, int s) {
-    return (c.row0 + 2 * k) * c.cols + c.c0 + 128 * s + 4 * c.q;
-}
+// Whole units, one wavefront per chunk of 2048 elements (32 per unit, 4 per
+// 256-thread workgroup) with no loop: the grid itself streams, as in the
+// AdamW step. Lanes take 4 consecutive columns of each 256-column row
+// segment, so every load and store instruction covers a contiguous 1 KB of
+// parameters (512 bytes of bf16 gradients); 16-byte non-temporal parameter
+// accesses.
+constexpr int kChunksPerUnit = 32;
 
 template <int G>
 __device__ __forceinline__ void load_g4(gp<const void> g, int64_t e, float gv[4]) {
@@ -1270,36 +1246,64 @@ __device__ __forceinline__ void load_g4(gp<const void> g, int64_t e, float gv[4]
     }
 }
 
-template <int G>
-__global__ __launch_bounds__(256) void ada_apply_whole_kernel(const FacArgs a, int64_t base) {
-    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t unit = chunk / (256 / kChunkRows);
-    if (unit >= a.whole_units) return;
-    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
-    const ChunkLane c = chunk_lane(d, unit - d.unit_begin, chunk % (256 / kChunkRows));
+// A whole-unit chunk as rows and columns: 8 / W rows from row0, 256 W
+// columns from col0 (W units side by side; the unit columns left over in a
+// unit row, ncu mod W, take W = 1: 8 rows x 256). A unit row holds 32 ncu
+// chunks.
+struct RowChunk {
+    int64_t row0, col0;
+    bool full;  // W units (else one)
+};
+
+template <int W>
+__device__ __forceinline__ RowChunk row_chunk(const GD& d, int64_t chunk) {
+    const int64_t t_ch = chunk - d.unit_begin * kChunksPerUnit;
+    const int64_t cpr = (int64_t)d.ncu * kChunksPerUnit;  // chunks per unit row
+    const int64_t ur = t_ch / cpr, r = t_ch - ur * cpr;
+    const int64_t ng = d.ncu / W;             // groups of W units in a unit row
+    RowChunk c;
+    c.full = r < ng * W * kChunksPerUnit;
+    if (c.full) {
+        const int64_t grp = r / (W * kChunksPerUnit), ci = r - grp * (W * kChunksPerUnit);
+        c.row0 = ur * 256 + ci * (8 / W);
+        c.col0 = grp * (256 * W);
+    } else {
+        const int64_t x = r - ng * W * kChunksPerUnit;
+        c.row0 = ur * 256 + (x % kChunksPerUnit) * 8;
+        c.col0 = (ng * W + x / kChunksPerUnit) * 256;
+    }
+    return c;
+}
+
+// Adafactor apply over a row chunk (lane l: columns 4l .. 4l + 3 of each
+// 256-column segment): every load of the chunk is issued before the
+// arithmetic.
+template <int G, int W>
+__device__ __forceinline__ void ada_apply_rows(const FacArgs& a, const GD& d, int64_t row0, int64_t col0) {
+    constexpr int R = 8 / W;
+    const int64_t cb = col0 + 4 * (threadIdx.x & 63);
     const double rclip = 1.0 / d.scal[0], lr = a.lr, decay = a.decay;
-    constexpr int NP = kChunkRows / 2;
-    float gv[NP][2][4];
-    float4 pv[NP][2];
-    double ri[NP], cf[2][4];
+    float gv[R][W][4];
+    float4 pv[R][W];
+    double ri[R], cf[W][4];
 #pragma unroll
-    for (int k = 0; k < NP; ++k) {
-        ri[k] = d.rfac[c.row0 + 2 * k];
+    for (int k = 0; k < R; ++k) {
+        ri[k] = d.rfac[row0 + k];
 #pragma unroll
-        for (int sg = 0; sg < 2; ++sg) {
-            const int64_t e = chunk_elem(c, k, sg);
+        for (int sg = 0; sg < W; ++sg) {
+            const int64_t e = (row0 + k) * d.cols + cb + 256 * sg;
             load_g4<G>(d.g, e, gv[k][sg]);
             pv[k][sg] = ld_f4<true>(d.p + e);
         }
     }
 #pragma unroll
-    for (int sg = 0; sg < 2; ++sg)
+    for (int sg = 0; sg < W; ++sg)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) cf[sg][j] = d.cfac[c.c0 + 128 * sg + 4 * c.q + j];
+        for (int j = 0; j < 4; ++j) cf[sg][j] = d.cfac[cb + 256 * sg + j];
 #pragma unroll
-    for (int k = 0; k < NP; ++k) {
+    for (int k = 0; k < R; ++k) {
 #pragma unroll
-        for (int sg = 0; sg < 2; ++sg) {
+        for (int sg = 0; sg < W; ++sg) {
             const float pin[4] = {pv[k][sg].x, pv[k][sg].y, pv[k][sg].z, pv[k][sg].w};
             float out[4];
 #pragma unroll
@@ -1308,9 +1312,24 @@ __global__ __launch_bounds__(256) void ada_apply_whole_kernel(const FacArgs a, i
                 const double pd = (double)pin[j] * decay;
                 out[j] = (float)(pd - lr * (uu * rclip));  // p carries a tolerance: multiply by 1 / clip
             }
-            st_f4<true>(d.p + chunk_elem(c, k, sg), make_float4(out[0], out[1], out[2], out[3]));
+            st_f4<true>(d.p + (row0 + k) * d.cols + cb + 256 * sg, make_float4(out[0], out[1], out[2], out[3]));
         }
     }
+}
+
+constexpr int kAdaApplyW = 2;
+
+template <int G>
+__global__ __launch_bounds__(256) void ada_apply_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = chunk / kChunksPerUnit;
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const RowChunk c = row_chunk<kAdaApplyW>(d, chunk);
+    if (c.full)
+        ada_apply_rows<G, kAdaApplyW>(a, d, c.row0, c.col0);
+    else
+        ada_apply_rows<G, 1>(a, d, c.row0, c.col0);
 }
 
 // One wavefront per whole-unit chunk, 4 per 256-thread workgroup; grids
@@ -1318,7 +1337,7 @@ __global__ __launch_bounds__(256) void ada_apply_whole_kernel(const FacArgs a, i
 template <class K>
 static hipError_t launch_per_chunk(K kernel, const FacArgs& a, hipStream_t s) {
     constexpr int64_t kMaxGrid = int64_t(1) << 31;
-    const int64_t end = a.whole_units * (256 / kChunkRows);
+    const int64_t end = a.whole_units * kChunksPerUnit;
     for (int64_t base = 0; base < end; base += 4 * kMaxGrid) {
         const int64_t left = (end - base + 3) / 4;
         const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
@@ -1868,107 +1887,105 @@ __global__ __launch_bounds__(256) void came_apply_chunk_kernel(const FacArgs a) 
     }
 }
 
-// Whole units: one wavefront per 8-row chunk, as the Adafactor apply (lane
-// 32 h + q: rows 2k + h, columns 4q .. 4q + 3 and 128 + 4q .. 128 + 4q + 3).
-// A unit row is one 256-element momentum block held by the 32 lanes of one
-// half, so its absmax is a 32-lane reduction; each lane writes its codes as
-// two 4-byte words. The kernel takes one row pair at a time (loads, then
-// stores): 90 registers, five waves per SIMD; loading all four pairs first
-// (152 registers, three waves) measured the same.
-constexpr int kCameApplyPairs = 1;
-template <int G, bool UF>
-__global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, int64_t base) {
-    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t unit = chunk / (256 / kChunkRows);
-    if (unit >= a.whole_units) return;
-    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
-    const ChunkLane c = chunk_lane(d, unit - d.unit_begin, chunk % (256 / kChunkRows));
+// Whole units: a wavefront takes a chunk of 8 / W rows x 256 W columns, W
+// units side by side (lane l: columns 4l .. 4l + 3 of each 256-column
+// segment), one row at a time: each row is one contiguous segment of 256 W
+// elements. A unit row holds 32 chunks' worth of the unit columns; the unit
+// columns left over in a row (ncu mod W) take W = 1 (8 rows x 256). Each
+// 256-column segment of a row is one momentum block over all 64 lanes.
+// W = 2 (2 KB parameter segments, 88 registers) measured 1.8% faster than
+// 8 rows x 256 columns in two 32-lane halves; W = 1 and 4 no faster, W = 8
+// (232 registers) 21% slower.
+constexpr int kCameApplyW = 2;
+template <int G, bool UF, int W>
+__device__ __forceinline__ void came_apply_rows(const FacArgs& a, const GD& d, int64_t row0, int64_t col0) {
+    constexpr int R = 8 / W;
+    const int lane = threadIdx.x & 63;
+    const int64_t cb = col0 + 4 * lane;
+    const int64_t cols = d.cols;
     const double clip = d.scal[0], rclip = 1.0 / clip;
     const gp<uint8_t> mc = g_as<uint8_t>(d.m);
     const gp<float> mf = g_as<float>(d.m);
-    double cf[2][4], sf[2][4];
+    double cf[W][4], sf[W][4];
 #pragma unroll
-    for (int sg = 0; sg < 2; ++sg)
+    for (int sg = 0; sg < W; ++sg)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            cf[sg][j] = d.cfac[c.c0 + 128 * sg + 4 * c.q + j];
-            sf[sg][j] = d.sc[c.c0 + 128 * sg + 4 * c.q + j];
+            cf[sg][j] = d.cfac[cb + 256 * sg + j];
+            sf[sg][j] = d.sc[cb + 256 * sg + j];
         }
-    constexpr int NP = kCameApplyPairs;  // row pairs loaded together
+#pragma unroll 1
+    for (int k = 0; k < R; ++k) {
+        const int64_t row = row0 + k;
+        const double ri = d.rfac[row], si = d.sr[row];
+        float gv[W][4], ms[W];
+        float4 pv[W], mv[UF ? 1 : W];
+        uint32_t mw[W];
 #pragma unroll
-    for (int k0 = 0; k0 < kChunkRows / 2; k0 += NP) {
-        float gv[NP][2][4];
-        float4 pv[NP][2], mv[UF ? 1 : NP][2];
-        uint32_t mw[UF ? NP : 1][2];
-        float ms[NP];
-        double ri[NP], si[NP];
-#pragma unroll
-        for (int kk = 0; kk < NP; ++kk) {
-            const int k = k0 + kk;
-            ri[kk] = d.rfac[c.row0 + 2 * k];
-            si[kk] = d.sr[c.row0 + 2 * k];
-            if constexpr (UF) ms[kk] = d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8];
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg) {
-                const int64_t e = chunk_elem(c, k, sg);
-                load_g4<G>(d.g, e, gv[kk][sg]);
-                pv[kk][sg] = ld_f4<true>(d.p + e);
-                if constexpr (UF)
-                    mw[kk][sg] = ld_u1<true>(g_as<const void>(mc + e));
-                else
-                    mv[kk][sg] = ld_f4<true>(mf + e);
+        for (int sg = 0; sg < W; ++sg) {
+            const int64_t e = row * cols + cb + 256 * sg;
+            load_g4<G>(d.g, e, gv[sg]);
+            pv[sg] = ld_f4<true>(d.p + e);
+            if constexpr (UF) {
+                mw[sg] = ld_u1<true>(g_as<const void>(mc + e));
+                ms[sg] = d.mm[e >> 8];
+            } else {
+                mv[sg] = ld_f4<true>(mf + e);
             }
         }
 #pragma unroll
-        for (int kk = 0; kk < NP; ++kk) {
-            const int k = k0 + kk;
-            float mnew[2][4];
-            const double st = UF ? div127((double)ms[kk]) : 0.0;
+        for (int sg = 0; sg < W; ++sg) {
+            const int64_t e = row * cols + cb + 256 * sg;
+            float mh[4], uh[4], mnew[4];
+            if constexpr (UF) {
+                const double st = div127((double)ms[sg]);
 #pragma unroll
-            for (int sg = 0; sg < 2; ++sg) {
-                float mh[4], uh[4];
-                if constexpr (UF) {
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[kk][sg] >> (8 * j)), st);
-                } else {
-                    mh[0] = mv[kk][sg].x, mh[1] = mv[kk][sg].y, mh[2] = mv[kk][sg].z, mh[3] = mv[kk][sg].w;
-                }
-                double uu[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) uu[j] = (ri[kk] * cf[sg][j]) * (double)gv[kk][sg][j];
-                div4_to_f32(uu, clip, rclip, uh);
-                const float pin[4] = {pv[kk][sg].x, pv[kk][sg].y, pv[kk][sg].z, pv[kk][sg].w};
-                float pout[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    mnew[sg][j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
-                    const double upd = (si[kk] * sf[sg][j]) * (double)mnew[sg][j];
-                    pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
-                }
-                const int64_t e = chunk_elem(c, k, sg);
-                st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
-                if constexpr (!UF) st_f4<true>(mf + e, make_float4(mnew[sg][0], mnew[sg][1], mnew[sg][2], mnew[sg][3]));
+                for (int j = 0; j < 4; ++j) mh[j] = uf8_decode((int32_t)(int8_t)(uint8_t)(mw[sg] >> (8 * j)), st);
+            } else {
+                mh[0] = mv[sg].x, mh[1] = mv[sg].y, mh[2] = mv[sg].z, mh[3] = mv[sg].w;
             }
+            double uu[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) uu[j] = (ri * cf[sg][j]) * (double)gv[sg][j];
+            div4_to_f32(uu, clip, rclip, uh);
+            const float pin[4] = {pv[sg].x, pv[sg].y, pv[sg].z, pv[sg].w};
+            float pout[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
+                const double upd = (si * sf[sg][j]) * (double)mnew[j];
+                pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+            }
+            st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
             if constexpr (UF) {
                 uint32_t am = 0u;
 #pragma unroll
-                for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[sg][j]));
-                am = group_reduce<OpMax, 32>(am);  // the row's block: the 32 lanes of this half
+                for (int j = 0; j < 4; ++j) am = OpMax::f(am, abs_bits(mnew[j]));
+                am = group_reduce<OpMax, 64>(am);
                 const double rs = am != 0u ? rdiv127((double)u2f(am)) : 0.0;
+                uint32_t qv[4];
 #pragma unroll
-                for (int sg = 0; sg < 2; ++sg) {
-                    uint32_t qv[4];
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) qv[j] = rint_low_bits((double)mnew[sg][j] * rs) & 0xFFu;
-                    st_u1<true>(g_as<void>(mc + chunk_elem(c, k, sg)), qv[0] | (qv[1] << 8) | (qv[2] << 16) | (qv[3] << 24));
-                }
-                if (c.q == 0) d.mm[((c.row0 + 2 * k) * c.cols + c.c0) >> 8] = u2f(am);
+                for (int j = 0; j < 4; ++j) qv[j] = rint_low_bits((double)mnew[j] * rs) & 0xFFu;
+                st_u1<true>(g_as<void>(mc + e), qv[0] | (qv[1] << 8) | (qv[2] << 16) | (qv[3] << 24));
+                if (lane == 0) d.mm[e >> 8] = u2f(am);
+            } else {
+                st_f4<true>(mf + e, make_float4(mnew[0], mnew[1], mnew[2], mnew[3]));
             }
         }
     }
+}
+
+template <int G, bool UF>
+__global__ __launch_bounds__(256) void came_apply_whole_kernel(const FacArgs a, int64_t base) {
+    const int64_t chunk = base + xcd_order(blockIdx.x, gridDim.x) * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t unit = chunk / kChunksPerUnit;
+    if (unit >= a.whole_units) return;
+    const GD d = gview(a.D[locate_unit(a.D, a.n2, unit)]);
+    const RowChunk c = row_chunk<kCameApplyW>(d, chunk);
+    if (c.full)
+        came_apply_rows<G, UF, kCameApplyW>(a, d, c.row0, c.col0);
+    else
+        came_apply_rows<G, UF, 1>(a, d, c.row0, c.col0);
 }
 
 hipError_t launch_came_apply(const FacArgs& a, int grad_dtype, hipStream_t s) {
