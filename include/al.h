@@ -316,7 +316,8 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * (factored second-moment reconstruction), 5 = x / 127 and 6 = 127 / x by
  * the division-free sequences of the UF8 code (exact for x a finite fp32
  * value, x > 0 for 6), 7 = fl32(x / 3) by the multiply-and-check quotient of
- * the clipped updates. x, out: n doubles (device). */
+ * the clipped updates, 8 = the binary64 log2 of (float)x that fits the AdamW
+ * step's second-moment blocks (x > 0). x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
 /* The AL8 levels of the fused AdamW step's split-table decode (section 4.1,

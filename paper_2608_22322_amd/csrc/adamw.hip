@@ -567,7 +567,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
         }
         const bool any = kmax != 0u && b < NB;
         const uint32_t key = (lane & 1) ? kmax : kmin;
-        const double lg = log2((double)(any ? u2f(key) : 1.0f));
+        const double lg = fit_log2(any ? u2f(key) : 1.0f);
         const double lg_other = __shfl_xor(lg, 1);
         const double lo = (lane & 1) ? lg_other : lg;
         const double hi = (lane & 1) ? lg : lg_other;

@@ -166,6 +166,57 @@ __device__ __forceinline__ float al_decode_fast(uint32_t q, double lmin32, doubl
 // which requires the measured maximum to stay below a quarter of this).
 constexpr double kLog2MantErr = 0x1p-21;
 
+// log2 x in binary64 for x a positive fp32 value (the block endpoints of the
+// second-moment codes), in well under half the instructions of the general
+// binary64 log2: x = 2^e m with m in [sqrt(1/2), sqrt(2)), s = (m - 1) / (m + 1)
+// (m - 1 and m + 1 exact; the quotient by a refined reciprocal and one
+// remainder correction, its residual carried as s_lo), and
+// ln m = 2 atanh s = 2 s (1 + z Q(z)), z = s^2, Q(z) = 1/3 + z/5 + ... + z^9/21
+// (|s| <= 0.1716: the first omitted term is below 2^-57 relative). With
+// K = 2 / ln 2 = Kh + Kl, log2 x = e + K s (1 + z Q): the leading product
+// Kh s and its sum with e are carried exactly (FMA product error, Fast2Sum),
+// the small remainder terms (Kl s, Kh s_lo, Kh s z Q) are added to the error
+// terms, and the result is rounded once: correctly rounded except within a
+// few hundredths of an ulp of a rounding midpoint. The device test holds it to
+// the host's log2 on every fp32 significand of three binades and on random
+// fp32 values.
+__device__ __forceinline__ double fit_log2(float xf) {
+    const double x = (double)xf;
+    double m = __builtin_amdgcn_frexp_mant(x);  // [1/2, 1)
+    int e = __builtin_amdgcn_frexp_exp(x);
+    const bool lo = m < 0x1.6a09e667f3bcdp-1;
+    m = lo ? 2.0 * m : m;
+    e = lo ? e - 1 : e;
+    const double num = m - 1.0, den = m + 1.0;
+    double r = __builtin_amdgcn_rcp(den);
+    r = __builtin_fma(__builtin_fma(-den, r, 1.0), r, r);
+    r = __builtin_fma(__builtin_fma(-den, r, 1.0), r, r);
+    const double s0 = num * r;
+    const double s = __builtin_fma(__builtin_fma(-den, s0, num), r, s0);
+    const double s_lo = __builtin_fma(-den, s, num) * r;  // num / den - s, to first order
+    const double z = s * s;
+    double q = 1.0 / 21.0;
+    q = __builtin_fma(q, z, 1.0 / 19.0);
+    q = __builtin_fma(q, z, 1.0 / 17.0);
+    q = __builtin_fma(q, z, 1.0 / 15.0);
+    q = __builtin_fma(q, z, 1.0 / 13.0);
+    q = __builtin_fma(q, z, 1.0 / 11.0);
+    q = __builtin_fma(q, z, 1.0 / 9.0);
+    q = __builtin_fma(q, z, 1.0 / 7.0);
+    q = __builtin_fma(q, z, 1.0 / 5.0);
+    q = __builtin_fma(q, z, 1.0 / 3.0);
+    constexpr double kKh = 0x1.71547652b82fep+1;   // 2 / ln 2 rounded to binary64
+    constexpr double kKl = 0x1.777d0ffda0d24p-55;  // 2 / ln 2 - kKh
+    const double hi = s * kKh;
+    double tail = __builtin_fma(s, kKh, -hi);  // exact error of hi
+    tail += __builtin_fma(s_lo, kKh, s * kKl);
+    tail = __builtin_fma(hi, z * q, tail);
+    const double ed = (double)e;
+    const double sum = ed + hi;
+    const double err = (ed - sum) + hi;  // Fast2Sum: |e| >= |hi| or e = 0
+    return sum + (err + tail);
+}
+
 // Per-block encode parameters: the binary64 interval start, LEVELS/delta,
 // and a guard band on the code position (binary64 and fp32 arithmetic).
 struct ALEnc {

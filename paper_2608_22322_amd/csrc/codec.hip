@@ -77,7 +77,9 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
 
 // Device math primitives the codes rely on, evaluated elementwise so a test
 // can compare them with the host: 0 = hardware fp32 log2, 1 = the binary64
-// exp2 polynomial, 2 = binary64 log2, 3 = binary64 sqrt, 4 = 1 / sqrt(x).
+// exp2 polynomial, 2 = binary64 log2, 3 = binary64 sqrt, 4 = 1 / sqrt(x),
+// 5 / 6 = the UF8 quotients, 7 = the clipped-update quotient, 8 = the block
+// endpoint log2 of an fp32 value.
 __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __restrict__ x, int64_t n,
                                                          double* __restrict__ out, const Exp2Coef cf) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -93,6 +95,7 @@ __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __
             case 5: r = div127(v); break;
             case 6: r = rdiv127(v); break;
             case 7: r = (double)div_to_f32(v, 3.0, 1.0 / 3.0); break;
+            case 8: r = fit_log2((float)v); break;
         }
         out[i] = r;
     }

@@ -66,6 +66,33 @@ def test_log2_sqrt_rsqrt():
     assert np.array_equal(_run(4, x), 1.0 / np.sqrt(x))
 
 
+def test_fit_log2_matches_host_log2():
+    """The block-endpoint log2 of an fp32 value (fn 8) against the host libm log2 (the oracle's):
+    every fp32 significand of the binade [2^-20, 2^-19), every significand of [1/2, 2) (results
+    near 0), 2^20 random positive finite fp32 values (subnormals included) and powers of two. Bound:
+    one ulp of the result plus 1.5 2^-53 (the small term's roundings); the fp32 roundings, which the
+    stored metadata takes, must agree everywhere."""
+    require_gpu()
+    import math
+
+    sig = (np.arange(1 << 23, dtype=np.uint32) | np.uint32(0x3F800000)).view(np.float32).astype(np.float64)
+    rng = np.random.default_rng(8)
+    bits = rng.integers(1, 0x7F800000, 1 << 20, dtype=np.uint32)
+    x = np.concatenate([sig * 2.0**-20, sig * 0.5, sig, bits.view(np.float32).astype(np.float64),
+                        np.exp2(np.arange(-149.0, 128.0))])
+    got = _run(8, x)
+    ref = np.array([math.log2(v) for v in x])
+    err = np.abs(got - ref)
+    bound = np.spacing(np.abs(ref)) + 1.5 * 2.0**-53
+    worst = float((err / bound).max())
+    ndiff = int(np.count_nonzero(got != ref))
+    log(f"fit log2: {ndiff} of {x.size:,} differ from the host's (largest error {worst:.3f} of the bound)")
+    assert worst <= 1.0
+    assert np.array_equal(got.astype(np.float32), ref.astype(np.float32))
+    p2 = np.exp2(np.arange(-149.0, 128.0))
+    assert np.array_equal(_run(8, p2), np.arange(-149.0, 128.0))  # exact at powers of two
+
+
 def _fp32_cover():
     """Every fp32 significand (x in [1, 2)), the same significands at the ends of the fp32 range
     (subnormals included, as values), and 2^20 random positive finite fp32 bit patterns."""
