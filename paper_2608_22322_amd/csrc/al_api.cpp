@@ -232,6 +232,7 @@ al_status fac_plan(const al_tensor* ts, int nt, bool came, const al_state_spec& 
         d.cc = t.cc;
         d.ccm = t.cc_meta;
         if (fac) {
+            // (hi, lo) pairs per unit and column / row; whole-unit tensors use the first half
             d.colpart = reinterpret_cast<double*>(take((size_t)d.nru * t.cols * 16));
             d.rowpart = reinterpret_cast<double*>(take((size_t)d.ncu * t.rows * 16));
             d.rfac = reinterpret_cast<double*>(take((size_t)t.rows * 8));

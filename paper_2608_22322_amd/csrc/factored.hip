@@ -528,8 +528,9 @@ __device__ __forceinline__ void load_wbatch(WBatch<G, NR>& b, gp<const void> g, 
 // Shared part of the whole-unit marginal kernels, batches of P::NR unit rows
 // (4, 8 or 16). The policy P supplies the batch type, load(batch, rb) for the
 // rows from rb, and terms(batch, k, t): the 8 binary64 terms of the lane's
-// row 2k + h of that batch. Row partials go to rowpart (lo = 0), column
-// partials to colpart; stage holds NR x kWStride doubles.
+// row 2k + h of that batch. Row partials go to rowpart, column partials to
+// colpart, one binary64 sum each (the other tensors' partials are (hi, lo)
+// pairs); stage holds NR x kWStride doubles.
 template <class P>
 __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64_t ru, int64_t cu, double* stage) {
     constexpr int NR = P::NR, NP = NR / 2, LPR = 64 / NR, PPL = 32 / LPR;  // lanes per row, partials per lane
@@ -566,10 +567,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         rs += dpp_d<kDppQuadXor2>(rs);
         if constexpr (LPR >= 8) rs += dpp_d<kDppRowHalfMirror>(rs);
         if constexpr (LPR == 16) rs += dpp_d<kDppRowMirror>(rs);
-        if (rpart == 0) {
-            const gp<double> rp = d.rowpart + 2 * (cu * d.rows + r0 + NR * bi + rrow);
-            st_d2(rp, rs, 0.0);
-        }
+        if (rpart == 0) d.rowpart[cu * d.rows + r0 + NR * bi + rrow] = rs;
     };
     typename P::Batch A, B;
     pol.load(A, 0);
@@ -637,7 +635,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
 #pragma unroll
     for (int j = 0; j < 8; ++j) cacc[j] += __shfl_xor(cacc[j], 32);
     // through LDS, so that each store instruction writes 64 consecutive
-    // column partials (1 KB) instead of 16 bytes in every 128
+    // column partials (512 bytes) instead of 8 bytes in every 64
     static_assert(2 * SZ >= 256, "the stages hold a unit's 256 column sums");
     __builtin_amdgcn_wave_barrier();
     if (h == 0) {
@@ -645,9 +643,9 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         for (int j = 0; j < 8; ++j) stage[8 * q + j] = cacc[j];
     }
     __builtin_amdgcn_wave_barrier();
-    const gp<double> cp = d.colpart + 2 * (ru * cols + c0 + lane);
+    const gp<double> cp = d.colpart + (ru * cols + c0 + lane);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) st_d2(cp + 128 * i, stage[lane + 64 * i], 0.0);
+    for (int i = 0; i < 4; ++i) cp[64 * i] = stage[lane + 64 * i];
 }
 
 // The lane's place in a whole unit: the unit's first gradient element as a
@@ -848,6 +846,7 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
     float* meta = isrow ? R.rm : R.cm;
     float* x = isrow ? d.rtmp : d.ctmp;
     const double cnt = (double)(isrow ? d.cols : d.rows);
+    const bool whole = d.unit_begin < a.whole_units;  // the tensor's units are all whole
     // 1. EMA of the means (each lane handles the elements it encodes). The
     // marginal kernels' partials are within 3u of the exact sums; where that
     // could change the fp32 rounding of the EMA (or with exact_all), the
@@ -862,17 +861,19 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
             DD acc{0.0, 0.0};
             // the partials' loads do not depend on the running sum: unrolled, they are issued ahead
             // (the embedding's column blocks merge 125 row-unit partials per element)
+            // whole-unit tensors' partials are single binary64 sums, the others' (hi, lo) pairs
+            const int st = whole ? 1 : 2;
             if (isrow) {
 #pragma unroll 8
                 for (int cu = 0; cu < d.ncu; ++cu) {
-                    const double* rp = d.rowpart + 2 * ((int64_t)cu * d.rows + i);
-                    acc = dd_merge(acc, DD{rp[0], rp[1]});
+                    const double* rp = d.rowpart + st * ((int64_t)cu * d.rows + i);
+                    acc = dd_merge(acc, DD{rp[0], whole ? 0.0 : rp[1]});
                 }
             } else {
 #pragma unroll 8
                 for (int ru = 0; ru < d.nru; ++ru) {
-                    const double* cp = d.colpart + 2 * ((int64_t)ru * d.cols + i);
-                    acc = dd_merge(acc, DD{cp[0], cp[1]});
+                    const double* cp = d.colpart + st * ((int64_t)ru * d.cols + i);
+                    acc = dd_merge(acc, DD{cp[0], whole ? 0.0 : cp[1]});
                 }
             }
             old = vec_decode(R.codec, R.B, codes, meta, i, a.cf);
