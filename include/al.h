@@ -317,7 +317,10 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * the division-free sequences of the UF8 code (exact for x a finite fp32
  * value, x > 0 for 6), 7 = fl32(x / 3) by the multiply-and-check quotient of
  * the clipped updates, 8 = the binary64 log2 of (float)x that fits the AdamW
- * step's second-moment blocks (x > 0). x, out: n doubles (device). */
+ * step's second-moment blocks (x > 0), 9 = the clipped update of the CAME
+ * passes, fl32(fl64(fl64(r c) x) / d) for fixed binary64 r, c, d from the
+ * quotient with fl64(1 / d) folded into r and the decision test over eight
+ * consecutive inputs (n a multiple of 8). x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
 /* The AL8 levels of the fused AdamW step's split-table decode (section 4.1,

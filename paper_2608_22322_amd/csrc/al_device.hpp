@@ -331,6 +331,39 @@ __device__ __forceinline__ void div4_to_f32(const double x[4], double d, double 
     }
 }
 
+// fp32 roundings of N approximate quotients. Each q_j lies within 8 binary64
+// ulps of the binary64 quotient fl64(x_j / d) whose fp32 rounding is wanted
+// (q_j = fl64(fl64(fl64(r * fl64(1 / d)) * c_j) * g_j) against x_j =
+// fl64(fl64(r * c_j) * g_j): four roundings against three, 7 ulps). f_j =
+// fl32(q_j), and the result is true when every f_j is that rounding: bits
+// 0..28 of q_j (the ones the fp32 rounding drops) are more than kQuotW from
+// the halfway pattern 2^28, and |q_j| is at least 2^-126 (1 + 2^-20) (the fp32
+// normal range with a margin) or below the binary64 normal range (zero, or a
+// quotient that rounds to zero either way). Both tests are unsigned minima
+// over the N quotients (v_min3 chains), one compare each, with no per-element
+// lane masks. Infinities pass (the overflow threshold is the midpoint above
+// FLT_MAX, caught by the first test), NaNs pass and stay NaN.
+constexpr uint32_t kQuotW = 32;
+__device__ __forceinline__ uint32_t umin32(uint32_t a, uint32_t b) { return a < b ? a : b; }
+template <int N>
+__device__ __forceinline__ bool f32_roundings_decided(const double q[N], float f[N]) {
+    uint32_t mk = 0xFFFFFFFFu, mz = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+        f[j] = (float)q[j];
+        const uint2 b = __builtin_bit_cast(uint2, q[j]);  // (low word, high word)
+        // ((bits 0..28) - (2^28 - W)) mod 2^29, times 8: at most 16 W iff within W of 2^28
+        mk = umin32(mk, (b.x << 3) - ((0x10000000u - kQuotW) << 3));
+        // 2 |high word| - 1: 2^32 - 1 for a zero high word; above 0x70200000 iff |q| >= 2^-126 (1 + 2^-20).
+        // Written as the instruction: from C the compiler sees bits 32..63 of q shifted, and emits a
+        // 64-bit funnel shift, a mask and an add.
+        uint32_t z;
+        __asm__("v_lshl_add_u32 %0, %1, 1, -1" : "=v"(z) : "v"(b.y));
+        mz = umin32(mz, z);
+    }
+    return (mk > 16u * kQuotW) & (mz > 0x70200000u);
+}
+
 // Cross-lane moves of 64-bit values.
 __device__ __forceinline__ double shfl_d(double v, int src) { return __shfl(v, src); }
 __device__ __forceinline__ double readlane_d(double v, int lane) {

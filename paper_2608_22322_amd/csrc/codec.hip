@@ -79,10 +79,30 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
 // can compare them with the host: 0 = hardware fp32 log2, 1 = the binary64
 // exp2 polynomial, 2 = binary64 log2, 3 = binary64 sqrt, 4 = 1 / sqrt(x),
 // 5 / 6 = the UF8 quotients, 7 = the clipped-update quotient, 8 = the block
-// endpoint log2 of an fp32 value.
+// endpoint log2 of an fp32 value, 9 = the clipped update of the CAME passes
+// with 1 / clip folded into the row factor: fl32(fl64(fl64(r c) x) / d) for
+// r, c, d below, eight consecutive inputs per decision as in the kernels (n a
+// multiple of 8).
+constexpr double kDiagR = 0.7310585786300049, kDiagC = 1234.5678901234567, kDiagD = 3.0000000000000004;
 __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __restrict__ x, int64_t n,
                                                          double* __restrict__ out, const Exp2Coef cf) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if (fn == 9) {
+        const double rk = kDiagR * (1.0 / kDiagD);
+        for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; 8 * g + 8 <= n; g += stride) {
+            double q[8];
+            float f[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) q[j] = (rk * kDiagC) * x[8 * g + j];
+            if (!f32_roundings_decided<8>(q, f)) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) f[j] = (float)(((kDiagR * kDiagC) * x[8 * g + j]) / kDiagD);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) out[8 * g + j] = (double)f[j];
+        }
+        return;
+    }
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         const double v = x[i];
         double r = 0.0;

@@ -107,6 +107,13 @@ __device__ __forceinline__ double res_term(const FacArgs& a, float mh, float uh)
     return df * df + a.eps2;
 }
 
+// uhat - m of the same term (exact in binary64): the whole-unit residual pass
+// accumulates its square with fused multiply-adds and adds eps2 to the mean.
+__device__ __forceinline__ double res_diff(const FacArgs& a, float mh, float uh) {
+    const float m = (float)(a.beta1 * (double)mh + a.omb1 * (double)uh);
+    return (double)uh - (double)m;
+}
+
 template <int G>
 __device__ __forceinline__ float grad1(const void* g, int64_t e) {
     if constexpr (G == G_BF16)
@@ -466,11 +473,17 @@ static hipError_t launch_wave_per_unit(K kernel, const FacArgs& a, int64_t begin
 // for non-negative terms) and stages that partial in LDS; 8 lanes then finish
 // each row from 4 partials apiece (pairwise, then a quad and a half-row DPP
 // merge), so a row's partial over the unit has relative error <= 8u and needs
-// no further merge inside the unit. Columns: the loading lanes add their terms
-// in plain runs over 16 of their rows (<= 15u) and add the 8 runs of the unit
-// (<= 7u more); the even- and odd-row halves merge at the end (1u): a column
-// partial has relative error <= 23u. The finalize step's robustness margin
-// covers these bounds.
+// no further merge inside the unit. Columns: with all terms of a batch formed
+// at once (the second moment's terms), the loading lanes add them in plain runs
+// over 16 of their rows (<= 15u) and add the 8 runs of the unit (<= 7u more).
+// CAME's residual terms (uhat - m)^2 + eps2 are formed one row pair at a time
+// (they need the registers) and summed without eps2: each lane accumulates the
+// squares of its 128 rows' differences by fused multiply-adds (<= 128u, one
+// rounding per term) and its row partials likewise (8 terms), and the finalize
+// adds eps2 to the mean; the oracle's terms fl64(fl64(d^2) + eps2) are within
+// 2u of d^2 + eps2. The even- and odd-row halves merge at the end (1u): a
+// column partial has relative error <= 23u or <= 131u against the exact sum
+// of the terms. The finalize step's robustness margin covers these bounds.
 constexpr int kWStride = 34;  // LDS stride of a staged row, in doubles (16-byte aligned rows)
 constexpr int kWRunRows = 32; // unit rows per plain column run (16 rows of each lane)
 
@@ -528,9 +541,12 @@ __device__ __forceinline__ void load_wbatch(WBatch<G, NR>& b, gp<const void> g, 
 // Shared part of the whole-unit marginal kernels, batches of P::NR unit rows
 // (4, 8 or 16). The policy P supplies the batch type, load(batch, rb) for the
 // rows from rb, and terms(batch, k, t): the 8 binary64 terms of the lane's
-// row 2k + h of that batch. Row partials go to rowpart, column partials to
-// colpart, one binary64 sum each (the other tensors' partials are (hi, lo)
-// pairs); stage holds NR x kWStride doubles.
+// row 2k + h of that batch (with P::SQUARES, 8 values whose squares are the
+// terms, summed by fused multiply-adds); P::DEPTH batches are in flight (2: the next
+// batch's loads are issued before the current batch's arithmetic; 3: the
+// next two). Row partials go to rowpart, column partials to colpart, one
+// binary64 sum each (the other tensors' partials are (hi, lo) pairs); stage
+// holds NR x kWStride doubles.
 template <class P>
 __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64_t ru, int64_t cu, double* stage) {
     constexpr int NR = P::NR, NP = NR / 2, LPR = 64 / NR, PPL = 32 / LPR;  // lanes per row, partials per lane
@@ -539,6 +555,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
     const int lane = threadIdx.x & 63, h = lane >> 5, q = lane & 31;
     const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
     const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of a batch, partials PPL rpart ..
+    // column sums: runs in crun added into cacc (all terms of a batch at once), else one plain sum in cacc
     double cacc[8], crun[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -587,6 +604,22 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
             }
 #pragma unroll
             for (int j = 0; j < 8; ++j) crun[j] += cs[j];
+        } else if constexpr (P::SQUARES) {
+            // column sums and the lane's row partial take the squares by fused multiply-adds (one
+            // rounding per term)
+#pragma unroll
+            for (int k = 0; k < NP; ++k) {
+                double t[8];
+                pol.terms(cur, k, t);
+                double rs = t[0] * t[0];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    cacc[j] = __builtin_fma(t[j], t[j], cacc[j]);
+                    if (j > 0) rs = __builtin_fma(t[j], t[j], rs);
+                    if (k & 1) __asm__ volatile("" : "+v"(cacc[j]));
+                }
+                sb[(2 * k + h) * kWStride + q] = rs;
+            }
         } else {
 #pragma unroll
             for (int k = 0; k < NP; ++k) {
@@ -594,10 +627,10 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
                 pol.terms(cur, k, t);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    crun[j] += t[j];
+                    cacc[j] += t[j];
                     // two row pairs' terms live at a time: without the fence the compiler forms all terms
                     // of the batch before the column additions
-                    if (k & 1) __asm__ volatile("" : "+v"(crun[j]));
+                    if (k & 1) __asm__ volatile("" : "+v"(cacc[j]));
                 }
                 sb[(2 * k + h) * kWStride + q] = sum8(t);
             }
@@ -607,7 +640,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         __builtin_amdgcn_wave_barrier();
         if (bi > 0) finish_rows(bi - 1);
         __builtin_amdgcn_wave_barrier();
-        if ((bi + 1) % (kWRunRows / NR) == 0) {
+        if (P::ILP && (bi + 1) % (kWRunRows / NR) == 0) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 cacc[j] += crun[j];
@@ -619,16 +652,38 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
     // loop the compiler's wait counts would have to hold for both paths, and
     // every odd batch would wait for the next even batch's loads.
     constexpr int NB = 256 / NR;
+    if constexpr (P::DEPTH == 2) {
 #pragma unroll 1
-    for (int bi = 0; bi < NB - 2; bi += 2) {
-        pol.load(B, (bi + 1) * NR);
-        step(A, bi);
-        pol.load(A, (bi + 2) * NR);
-        step(B, bi + 1);
+        for (int bi = 0; bi < NB - 2; bi += 2) {
+            pol.load(B, (bi + 1) * NR);
+            step(A, bi);
+            pol.load(A, (bi + 2) * NR);
+            step(B, bi + 1);
+        }
+        pol.load(B, (NB - 1) * NR);
+        step(A, NB - 2);
+        step(B, NB - 1);
+    } else {
+        // three batches rotate, two in flight ahead of the one being formed
+        static_assert(P::DEPTH == 3 && NB % 3 == 1, "three-deep rotation over NB = 1 mod 3 batches");
+        typename P::Batch C;
+        pol.load(B, NR);
+#pragma unroll 1
+        for (int bi = 0; bi < NB - 4; bi += 3) {
+            pol.load(C, (bi + 2) * NR);
+            step(A, bi);
+            pol.load(A, (bi + 3) * NR);
+            step(B, bi + 1);
+            pol.load(B, (bi + 4) * NR);
+            step(C, bi + 2);
+        }
+        pol.load(C, (NB - 2) * NR);
+        step(A, NB - 4);
+        pol.load(A, (NB - 1) * NR);
+        step(B, NB - 3);
+        step(C, NB - 2);
+        step(A, NB - 1);
     }
-    pol.load(B, (NB - 1) * NR);
-    step(A, NB - 2);
-    step(B, NB - 1);
     __builtin_amdgcn_wave_barrier();
     finish_rows(NB - 1);
     // the two halves hold the even and the odd rows of the same columns
@@ -679,6 +734,8 @@ struct MargTerms {
     // wave than from occupancy (200 registers, 2 waves per SIMD: 2.53 against 2.68 ms on the 7B list)
     static constexpr int NR = 8;
     static constexpr bool ILP = true;
+    static constexpr bool SQUARES = false;
+    static constexpr int DEPTH = 2;
     using Batch = WBatch<G, NR>;
     gp<const void> gu;
     int64_t cols;
@@ -821,13 +878,17 @@ __device__ DD exact_line_sum(const FacArgs& a, const FacDesc& d, int role, bool 
 
 // Relative distance from an fp32 rounding midpoint below which the EMA value
 // from the fast partial sums may round differently from the one from the exact
-// sum. A partial is within 23u (u = 2^-53) of its exact sum: the whole-unit
-// kernels' column partials (plain runs of 16 binary64 additions of
-// non-negative terms, 8 runs added, two halves merged; their row partials:
-// 8u), the other units' runs of at most 4 (3u) accumulated double-double; the
-// partials are merged double-double, and the mean and the EMA add at most 4u.
-// 32u bounds the total.
-constexpr double kRobustTol = 32.0 * 0x1p-53;
+// sum. A partial is within 131u (u = 2^-53) of its exact sum: the whole-unit
+// kernels' column partials (the second moment's: plain runs of 16 binary64
+// additions of non-negative terms, 8 runs added, two halves merged, 23u;
+// CAME's residual: fused multiply-add sums of 128 squared differences per
+// lane, two halves merged, eps2 added to the mean, 131u against the sum of
+// the oracle's terms; their row partials: 16u), the other units' runs of at
+// most 4 (3u) accumulated double-double; the partials are merged
+// double-double, and the mean, eps2 and the EMA add at most 5u. 160u bounds
+// the total; an EMA value that close to a midpoint is about one in a million
+// (the exact sum of its line is then taken).
+constexpr double kRobustTol = 160.0 * 0x1p-53;
 
 template <int G>
 __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int role) {
@@ -877,7 +938,9 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
                 }
             }
             old = vec_decode(R.codec, R.B, codes, meta, i, a.cf);
-            y = R.beta * (double)old + R.omb * (dd_value(acc) / cnt);
+            // whole-unit residual partials sum (uhat - m)^2 alone: eps2 joins the mean
+            const double mean = role == 1 && whole ? dd_value(acc) / cnt + a.eps2 : dd_value(acc) / cnt;
+            y = R.beta * (double)old + R.omb * mean;
         }
         const bool robust = !act || (!a.exact_all && f32_round_robust(y, kRobustTol * y));
         uint64_t pend = __ballot(!robust);
@@ -1634,6 +1697,10 @@ template <int G, bool UF>
 struct ResTerms {
     static constexpr int NR = kResNR;
     static constexpr bool ILP = false;  // the residual terms need the registers for occupancy
+    // terms() gives uhat - m; the sums take its square (eps2 is added to the means in the finalize)
+    static constexpr bool SQUARES = true;
+    // the registers the single column sum frees (against runs) hold a third batch: 3 waves per SIMD either way
+    static constexpr int DEPTH = 3;
     using Batch = ResBatch<G, UF>;
     const FacArgs* a;
     gp<const void> gu;   // the unit's first gradient
@@ -1672,18 +1739,23 @@ struct ResTerms {
             mh[0] = b.ma[k].x, mh[1] = b.ma[k].y, mh[2] = b.ma[k].z, mh[3] = b.ma[k].w;
             mh[4] = b.mb[k].x, mh[5] = b.mb[k].y, mh[6] = b.mb[k].z, mh[7] = b.mb[k].w;
         }
-        double uu[8];
+        // uhat = fl32(u / clip), u = fl64(fl64(r c) g): from the quotient with 1 / clip folded into the
+        // row factor (two multiplications), the exact division where its rounding is not decided
+        const double rk = b.ri[k] * rclip;
+        double qv[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) uu[j] = (b.ri[k] * cf[j]) * (double)gv[j];
-        div4_to_f32(uu, clip, rclip, uh);
-        div4_to_f32(uu + 4, clip, rclip, uh + 4);
+        for (int j = 0; j < 8; ++j) qv[j] = (rk * cf[j]) * (double)gv[j];
+        if (__builtin_expect(!f32_roundings_decided<8>(qv, uh), 0)) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) t[j] = res_term(*a, mh[j], uh[j]);
+            for (int j = 0; j < 8; ++j) uh[j] = (float)(((b.ri[k] * cf[j]) * (double)gv[j]) / clip);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t[j] = res_diff(*a, mh[j], uh[j]);
     }
 };
 
 template <int G, bool UF>
-__global__ __launch_bounds__(256) void came_res_whole_kernel(const FacArgs a, int64_t base) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void came_res_whole_kernel(const FacArgs a, int64_t base) {
     __shared__ __attribute__((aligned(16))) double stages[4][2 * kResNR * kWStride];
     double* stage = stages[threadIdx.x >> 6];
     const int64_t unit = whole_unit_of_wave(base);
@@ -1918,7 +1990,7 @@ __device__ __forceinline__ void came_apply_rows(const FacArgs& a, const GD& d, i
 #pragma unroll 1
     for (int k = 0; k < R; ++k) {
         const int64_t row = row0 + k;
-        const double ri = d.rfac[row], si = d.sr[row];
+        const double ri = d.rfac[row], si = d.sr[row], rk = ri * rclip;
         float gv[W][4], ms[W];
         float4 pv[W], mv[UF ? 1 : W];
         uint32_t mw[W];
@@ -1945,10 +2017,13 @@ __device__ __forceinline__ void came_apply_rows(const FacArgs& a, const GD& d, i
             } else {
                 mh[0] = mv[sg].x, mh[1] = mv[sg].y, mh[2] = mv[sg].z, mh[3] = mv[sg].w;
             }
-            double uu[4];
+            double qv[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) uu[j] = (ri * cf[sg][j]) * (double)gv[sg][j];
-            div4_to_f32(uu, clip, rclip, uh);
+            for (int j = 0; j < 4; ++j) qv[j] = (rk * cf[sg][j]) * (double)gv[sg][j];
+            if (__builtin_expect(!f32_roundings_decided<4>(qv, uh), 0)) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) uh[j] = (float)(((ri * cf[sg][j]) * (double)gv[sg][j]) / clip);
+            }
             const float pin[4] = {pv[sg].x, pv[sg].y, pv[sg].z, pv[sg].w};
             float pout[4];
 #pragma unroll

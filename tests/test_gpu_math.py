@@ -138,3 +138,38 @@ def test_clipped_quotient_matches_division():
     bad = np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32))
     log(f"clipped quotient: {x.size:,} inputs, {bad} differences")
     assert bad == 0
+
+
+def test_folded_clipped_quotient_matches_division():
+    """The CAME passes' clipped update: q = fl64(fl64(fl64(r * fl64(1/d)) * c) * x) with the decision test over
+    eight quotients at a time (two unsigned minima) and the exact fl32(fl64(fl64(r c) x) / d) for the whole
+    group when any rounding is undecided, against that division on the host bit for bit. Groups of eight
+    normal-range quotients (the fast path), groups with one quotient on or beside an fp32 rounding midpoint
+    among seven normal ones, and groups of random magnitudes across the fp32 range (subnormal, underflowing
+    and overflowing quotients) with zeros of both signs."""
+    require_gpu()
+    r, c, d = 0.7310585786300049, 1234.5678901234567, 3.0000000000000004  # the kernel's constants
+    rc = r * c
+    rng = np.random.default_rng(9)
+
+    def normal(k):
+        return np.exp2(rng.uniform(-100.0, 100.0, k)) * rng.choice([-1.0, 1.0], k) * d / rc
+
+    plain = normal(1 << 20)
+    f = rng.integers(0x00800000, 0x7F000000, 3 << 16, dtype=np.uint32).view(np.float32).astype(np.float64)
+    nxt = np.nextafter(f.astype(np.float32), np.float32(np.inf)).astype(np.float64)
+    xm = (f + nxt) / 2.0 * d / rc  # quotients within a few binary64 ulps of a midpoint
+    near = np.concatenate([xm[: 1 << 16], np.nextafter(xm[1 << 16: 2 << 16], np.inf),
+                           np.nextafter(xm[2 << 16:], -np.inf)])
+    mixed = normal(8 * near.size).reshape(-1, 8)
+    mixed[np.arange(near.size), rng.integers(0, 8, near.size)] = near
+    wide = np.exp2(rng.uniform(-170.0, 130.0, 1 << 18)) * rng.choice([-1.0, 1.0], 1 << 18) * d / rc
+    edge = np.array([0.0, -0.0, 2.0**-126 * d / rc, -(2.0**-150) * d / rc, 2.0**128 * d / rc, 1e-320, -1e-310,
+                     2.0**-126 * (1 + 2.0**-20) * d / rc])
+    x = np.concatenate([plain, mixed.reshape(-1), wide, edge])
+    got = _run(9, x).astype(np.float32)
+    with np.errstate(over="ignore", under="ignore"):
+        ref = ((rc * x) / d).astype(np.float32)
+    bad = np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32))
+    log(f"folded clipped quotient: {x.size:,} inputs, {bad} differences")
+    assert bad == 0
