@@ -1979,18 +1979,23 @@ __device__ __forceinline__ void came_apply_rows(const FacArgs& a, const GD& d, i
     const double clip = d.scal[0], rclip = 1.0 / clip;
     const gp<uint8_t> mc = g_as<uint8_t>(d.m);
     const gp<float> mf = g_as<float>(d.m);
-    double cf[W][4], sf[W][4];
+    // The parameter update runs in fp32 (the states never depend on p, which is held to a relative
+    // tolerance): p' = fma(-lr, (s_i s_j) m, p (1 - lr wd)) on the fp32 roundings of the factors.
+    const float lrf = (float)a.lr, decayf = (float)a.decay;
+    double cf[W][4];
+    float sf[W][4];
 #pragma unroll
     for (int sg = 0; sg < W; ++sg)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             cf[sg][j] = d.cfac[cb + 256 * sg + j];
-            sf[sg][j] = d.sc[cb + 256 * sg + j];
+            sf[sg][j] = (float)d.sc[cb + 256 * sg + j];
         }
 #pragma unroll 1
     for (int k = 0; k < R; ++k) {
         const int64_t row = row0 + k;
-        const double ri = d.rfac[row], si = d.sr[row], rk = ri * rclip;
+        const double ri = d.rfac[row], rk = ri * rclip;
+        const float si = (float)d.sr[row];
         float gv[W][4], ms[W];
         float4 pv[W], mv[UF ? 1 : W];
         uint32_t mw[W];
@@ -2029,8 +2034,8 @@ __device__ __forceinline__ void came_apply_rows(const FacArgs& a, const GD& d, i
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 mnew[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * (double)uh[j]);
-                const double upd = (si * sf[sg][j]) * (double)mnew[j];
-                pout[j] = (float)((double)pin[j] * a.decay - a.lr * upd);
+                const float upd = (si * sf[sg][j]) * mnew[j];
+                pout[j] = __builtin_fmaf(-lrf, upd, pin[j] * decayf);
             }
             st_f4<true>(d.p + e, make_float4(pout[0], pout[1], pout[2], pout[3]));
             if constexpr (UF) {
