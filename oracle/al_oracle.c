@@ -26,8 +26,12 @@
  * closed forms (beta1 = 0 against the clipped update, the second-moment path
  * at t = 1, and 20 steps with beta1 = 0.9 for constant uniform and rank-1
  * gradients, sign flips at one step or at element-specific steps, and a
- * rows == 1 tensor); against CAME itself it stays parity unpinned for
- * gradients of varying magnitude with beta1 > 0 beyond those structures.
+ * rows == 1 tensor) and, for gradients whose row and column magnitudes
+ * vary from step to step, by symmetries its definition implies over 20 steps
+ * with beta1 = 0.9 (row and column permutations and negation commute with
+ * the step bit for bit, scaling the gradient by 2 leaves the update unchanged,
+ * transposition swaps the factors); against CAME's own implementation the
+ * values for such gradients stay parity unpinned.
  */
 #include "al_oracle.h"
 

@@ -180,3 +180,38 @@ def test_transpose_symmetry():
         assert np.array_equal(oa["R"], ob["R"]) and np.array_equal(oa["s"], ob["s"])
     assert np.array_equal(a_p.reshape(rows, cols), b_p.reshape(cols, rows).T)
     assert np.array_equal(a_m.codes, b_m.codes) and np.array_equal(a_v.codes, b_v.codes)
+
+
+@pytest.mark.parametrize("shape", [(24, 16), (16, 24)])
+def test_channel_permutation_equivariance(shape):
+    """Permuting the channels of the gradient and the parameter (rows when rows >= cols, else columns)
+    with the projection fixed permutes R, both moments, the direction and the channel scales, and leaves
+    the limiter's norm unchanged (its sum is exact), so 5 steps give the permuted parameter bit for bit:
+    each channel's scale reads only its own row of R and of the direction."""
+    rows, cols = shape
+    r = 8
+    right, C, L = oap.layout(rows, cols)
+    rng = np.random.default_rng(71)
+    perm = rng.permutation(C)
+    P = synth.proj_matrix(71, 0, L, r)
+    p0 = _g(rows, cols, synth.param_key(71), 0.02).reshape(rows, cols)
+
+    def chan(x):  # x: rows x cols
+        return x[perm] if right else x[:, perm]
+
+    a_p, b_p = p0.ravel().copy(), np.ascontiguousarray(chan(p0)).ravel()
+    a_m, a_v = _states(C, r)
+    b_m, b_v = _states(C, r)
+    a_prev, b_prev = np.zeros(1, np.float32), np.zeros(1, np.float32)
+    for t in range(1, 6):
+        g = _g(rows, cols, synth.grad_key(72, t), zero_frac=0.05).reshape(rows, cols)
+        sc = np.exp2(rng.integers(-2, 3, C)).astype(np.float32)  # channel magnitudes that vary by step
+        g = g * (sc[:, None] if right else sc[None, :])
+        oa = oap.apollo_step(a_p, g.ravel(), rows, cols, P, a_m, a_v, t, a_prev)
+        ob = oap.apollo_step(b_p, np.ascontiguousarray(chan(g)).ravel(), rows, cols, P, b_m, b_v, t, b_prev)
+        assert np.array_equal(oa["R"][perm], ob["R"]) and np.array_equal(oa["s"][perm], ob["s"]), t
+        assert a_prev[0] == b_prev[0], t
+    assert np.array_equal(chan(a_p.reshape(rows, cols)), b_p.reshape(rows, cols))
+    for a, b in ((a_m, b_m), (a_v, b_v)):
+        assert np.array_equal(a.codes.reshape(C, r)[perm], b.codes.reshape(C, r))
+    assert np.ptp(oa["s"]) > 0.1 * np.abs(oa["s"]).mean()  # the scales differ by channel

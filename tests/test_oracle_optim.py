@@ -6,8 +6,11 @@
   the paper's reference path uses), plus the rank-1 closed form.
 * CAME: the official implementation is not available here, so the CAME oracle
   is pinned by closed forms (beta1 = 0; a uniform gradient; a rank-1
-  gradient) and by its second-moment path against the (HF-pinned) Adafactor
-  oracle at t = 1.
+  gradient; 20 steps with beta1 = 0.9 for constant gradients and sign flips),
+  by its second-moment path against the (HF-pinned) Adafactor oracle at t = 1,
+  and, for gradients of varying magnitude over 20 steps, by the symmetries its
+  definition implies (row / column permutation, negation, scaling by 2,
+  transposition).
 * Dormant entries (exact zeros) keep code 0 and a pure weight-decay
   trajectory, as the exact-zero invariant (section 4.2) implies.
 """
@@ -416,3 +419,101 @@ def test_came_staggered_sign_flips_closed_form():
         atol = 2 * ulp + lr * t * 2.0**-23 / np.sqrt(S.min())
         np.testing.assert_allclose(before.astype(np.float64) - p, want.reshape(-1), rtol=tol, atol=atol,
                                    err_msg=f"update at t={t}")
+
+
+# -------------------------------------- CAME over many steps: symmetries that hold for any gradient
+# Constant gradients give closed forms; for gradients that vary in magnitude from step to step the step
+# is pinned by what the method's definition implies for every input. With FP32 states and exact sums,
+# the step commutes with permuting rows or columns (the factors, the means, the clip's RMS and the
+# confidence are sums over rows / columns) and with negating the gradient (uhat, m and the update change
+# sign; V, the residual and the confidence do not), bit for bit; scaling the gradient by 2 (eps1 = 0)
+# leaves uhat, m, the confidence and the update unchanged and scales V by exactly 4; transposing the
+# gradient swaps the roles of rows and columns (equal up to the fp32 roundings of the factor means). A
+# factor indexed by the wrong side, a residual against the previous momentum, a missing normalisation or
+# a sign slip breaks one of them.
+
+def _came_run(g_steps, rows, cols, p0, **kw):
+    st = _came_states(rows, cols, codec=FP32, mcodec=FP32)
+    p = p0.copy()
+    for t, g in enumerate(g_steps, 1):
+        oracle.came_step(p, g, rows, cols, t=t, **kw, **st)
+    return p, st
+
+
+def _varying_grads(rows, cols, T, seed):
+    """Gradients whose row and column scales change from step to step (so the factors, the clip and the
+    confidence are far from uniform), with exact zeros."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for t in range(1, T + 1):
+        a = np.exp2(rng.uniform(-3, 3, rows))[:, None]
+        b = np.exp2(rng.uniform(-3, 3, cols))[None, :]
+        g = (rng.standard_normal((rows, cols)) * a * b * 1e-3).astype(np.float32)
+        g[rng.random((rows, cols)) < 0.03] = 0.0
+        out.append(g)
+    return out
+
+
+def test_came_multistep_permutation_equivariance():
+    rows, cols, T = 24, 40, 20
+    rng = np.random.default_rng(51)
+    gs = _varying_grads(rows, cols, T, 52)
+    p0 = _param(rows * cols, 53).reshape(rows, cols)
+    pr, pc = rng.permutation(rows), rng.permutation(cols)
+    kw = dict(beta1=0.9, lr=1e-4)
+    p, st = _came_run([g.ravel() for g in gs], rows, cols, p0.ravel(), **kw)
+    q, sq = _came_run([np.ascontiguousarray(g[pr][:, pc]).ravel() for g in gs], rows, cols,
+                      np.ascontiguousarray(p0[pr][:, pc]).ravel(), **kw)
+    assert np.array_equal(p.reshape(rows, cols)[pr][:, pc], q.reshape(rows, cols))
+    assert np.array_equal(st["m"].codes.reshape(rows, cols)[pr][:, pc], sq["m"].codes.reshape(rows, cols))
+    for key, perm in (("vr", pr), ("cr", pr), ("vc", pc), ("cc", pc)):
+        assert np.array_equal(st[key].codes[perm], sq[key].codes), key
+    # the factors are far from uniform: the test sees the indexing
+    assert np.ptp(st["cr"].codes) > 0.1 * st["cr"].codes.mean() and np.ptp(st["vc"].codes) > st["vc"].codes.mean()
+
+
+def test_came_multistep_sign_equivariance():
+    rows, cols, T = 24, 40, 20
+    gs = _varying_grads(rows, cols, T, 54)
+    zero = np.zeros(rows * cols, np.float32)
+    kw = dict(beta1=0.9, lr=1e-4)
+    p, st = _came_run([g.ravel() for g in gs], rows, cols, zero, **kw)
+    q, sq = _came_run([(-g).ravel() for g in gs], rows, cols, zero, **kw)
+    assert np.array_equal(q, -p) and np.abs(p).max() > 0
+    assert np.array_equal(sq["m"].codes, -st["m"].codes)
+    for key in ("vr", "vc", "cr", "cc"):
+        assert np.array_equal(st[key].codes, sq[key].codes), key
+
+
+def test_came_multistep_scale_invariance():
+    rows, cols, T = 24, 40, 20
+    gs = _varying_grads(rows, cols, T, 55)
+    for g in gs:  # eps1 = 0: a zero row or column would divide by zero
+        g[g == 0] = np.float32(1e-4)
+    p0 = _param(rows * cols, 56)
+    kw = dict(beta1=0.9, lr=1e-4, eps1=0.0)
+    p, st = _came_run([g.ravel() for g in gs], rows, cols, p0, **kw)
+    q, sq = _came_run([(2 * g).ravel() for g in gs], rows, cols, p0, **kw)
+    assert np.array_equal(p, q) and np.array_equal(st["m"].codes, sq["m"].codes)
+    for key in ("cr", "cc"):
+        assert np.array_equal(st[key].codes, sq[key].codes), key
+    for key in ("vr", "vc"):
+        assert np.array_equal(4 * st[key].codes, sq[key].codes), key
+
+
+def test_came_multistep_transposition():
+    rows, cols, T = 24, 40, 20
+    gs = _varying_grads(rows, cols, T, 57)
+    p0 = _param(rows * cols, 58).reshape(rows, cols)
+    kw = dict(beta1=0.9, lr=1e-4)
+    p, st = _came_run([g.ravel() for g in gs], rows, cols, p0.ravel(), **kw)
+    q, sq = _came_run([np.ascontiguousarray(g.T).ravel() for g in gs], cols, rows,
+                      np.ascontiguousarray(p0.T).ravel(), **kw)
+    # V and the confidence of one side are the other's, up to fp32 roundings propagated over 20 steps
+    for a, b in (("vr", "vc"), ("cr", "cc"), ("vc", "vr"), ("cc", "cr")):
+        np.testing.assert_allclose(st[a].codes, sq[b].codes, rtol=1e-5, err_msg=a)
+    np.testing.assert_allclose(st["m"].codes.reshape(rows, cols), sq["m"].codes.reshape(cols, rows).T,
+                               rtol=1e-4, atol=1e-6)
+    upd_p = p0.astype(np.float64) - p.reshape(rows, cols)
+    upd_q = p0.astype(np.float64) - q.reshape(cols, rows).T
+    np.testing.assert_allclose(upd_q, upd_p, rtol=1e-3, atol=1e-3 * np.abs(upd_p).max())
