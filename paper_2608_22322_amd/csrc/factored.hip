@@ -885,10 +885,11 @@ __device__ DD exact_line_sum(const FacArgs& a, const FacDesc& d, int role, bool 
 // lane, two halves merged, eps2 added to the mean, 131u against the sum of
 // the oracle's terms; their row partials: 16u), the other units' runs of at
 // most 4 (3u) accumulated double-double; the partials are merged
-// double-double, and the mean, eps2 and the EMA add at most 5u. 160u bounds
-// the total; an EMA value that close to a midpoint is about one in a million
-// (the exact sum of its line is then taken).
-constexpr double kRobustTol = 160.0 * 0x1p-53;
+// double-double, and the mean, eps2 and the EMA add at most 5u. 32u bounds
+// the second moment's total (role 0), 160u CAME's confidence (role 1); an EMA
+// value that close to a midpoint is about one in ten million (one in a
+// million) of the elements (the exact sum of its line is then taken).
+constexpr double kRobustTol[2] = {32.0 * 0x1p-53, 160.0 * 0x1p-53};
 
 template <int G>
 __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int role) {
@@ -942,7 +943,7 @@ __global__ __launch_bounds__(256) void fac_fin_block_kernel(const FacArgs a, int
             const double mean = role == 1 && whole ? dd_value(acc) / cnt + a.eps2 : dd_value(acc) / cnt;
             y = R.beta * (double)old + R.omb * mean;
         }
-        const bool robust = !act || (!a.exact_all && f32_round_robust(y, kRobustTol * y));
+        const bool robust = !act || (!a.exact_all && f32_round_robust(y, kRobustTol[role] * y));
         uint64_t pend = __ballot(!robust);
         while (pend) {
             const int src = __builtin_ctzll(pend);
