@@ -146,6 +146,8 @@ struct DescG {
     gp<uint8_t> v;
     gp<float> vm;
     int64_t n;
+    gp<double> cs, csg;   // APOLLO: channel scales and s_c^2 gn2_c (rank 256: one channel per sub-tile)
+    gp<const double> cg2;  // APOLLO: per-channel sums of g^2
 };
 
 // The table is read-only during the step, so it is read through the constant
@@ -156,12 +158,12 @@ using cp = __attribute__((address_space(4))) T*;
 
 __device__ __forceinline__ DescG gview(cp<const AdamWDesc> D, int i) {
     return DescG{to_g(D[i].p), (gp<const uint8_t>)to_g(D[i].g), (gp<uint8_t>)to_g(D[i].m), to_g(D[i].ms),
-                 (gp<uint8_t>)to_g(D[i].v), to_g(D[i].vm), D[i].n};
+                 (gp<uint8_t>)to_g(D[i].v), to_g(D[i].vm), D[i].n, nullptr, nullptr, nullptr};
 }
 
 typedef float f2v __attribute__((ext_vector_type(2)));
 
-template <int G, int MC, int VC, int BV, bool FULL>
+template <int G, int MC, int VC, int BV, bool FULL, bool APO>
 __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const DescG& d, int64_t e0, int64_t valid,
                                          int lane, int ph) {
     using R = Raw<G, MC, VC, BV>;
@@ -169,8 +171,9 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const DescG& d, 
     for (int k = 0; k < R::P; ++k) {
         const int rel = (ph * R::P + k) * kSub + 4 * lane;
         const int64_t e = e0 + rel;
+        if constexpr (APO) r.p[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);  // no parameter stream
         if constexpr (FULL) {
-            r.p[k] = ld_f4<kNtLoad>(d.p + e);
+            if constexpr (!APO) r.p[k] = ld_f4<kNtLoad>(d.p + e);
             if constexpr (G == G_BF16)
                 r.g[k] = ld_u2<kNtLoad>(g_as<const uint16_t>(d.g) + e);
             else
@@ -192,7 +195,7 @@ __device__ __forceinline__ void load_raw(Raw<G, MC, VC, BV>& r, const DescG& d, 
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const bool ok = rel + j < valid;
-                pp[j] = ok ? d.p[e + j] : 0.0f;
+                pp[j] = (ok && !APO) ? d.p[e + j] : 0.0f;
                 if constexpr (G == G_BF16) gb[j] = ok ? g_as<const uint16_t>(d.g)[e + j] : 0u;
                 else gf[j] = ok ? g_as<const float>(d.g)[e + j] : 0.0f;
                 if constexpr (MC == UF8) mb[j] = ok ? g_as<const uint8_t>(d.m)[e + j] : 0u;
@@ -269,10 +272,26 @@ __device__ __forceinline__ uint32_t key_pair_reduce(uint32_t amn, uint32_t amx, 
     return (lane >> 2) == pair ? key : slot;
 }
 
-template <int G, int MC, int VC, int BV, bool FULL>
+// A binary64 sum over each row of 16 lanes in a fixed order (DPP); every lane
+// of the row gets it.
+__device__ __forceinline__ double row16_sum(double x) {
+    x += dpp_d<kDppQuadXor1>(x);
+    x += dpp_d<kDppQuadXor2>(x);
+    x += dpp_d<kDppRowHalfMirror>(x);
+    x += dpp_d<kDppRowMirror>(x);
+    return x;
+}
+
+// APO: APOLLO's moments on the projected gradient R (rank 256): the parameter
+// stream is absent (a zero parameter, lr 1: the output would be the negated
+// direction Rt), and each sub-tile -- one channel of 256 -- reduces sum Rt^2
+// and sum R^2 over its rows of 16 lanes into LDS (csum); after the last
+// sub-tile, lane k adds its channel's four row sums and forms the channel
+// scale.
+template <int G, int MC, int VC, int BV, bool FULL, bool APO>
 __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG& d, int64_t e0, int64_t valid,
                                               int lane, double* lut, double* stab, uint2* skey, uint4* encp,
-                                              double2* encd) {
+                                              double2* encd, double2* csum) {
     using Q = Geo<MC, VC, BV>;
     constexpr int K = Q::K;
     constexpr int NB = Q::NB;
@@ -282,7 +301,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
     using R = Raw<G, MC, VC, BV>;
     // first load phase and the old metadata are issued before any arithmetic
     R r;
-    load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, 0);
+    load_raw<G, MC, VC, BV, FULL, APO>(r, d, e0, valid, lane, 0);
     const OldMeta om = load_meta<MC, VC, BV, FULL>(d, e0, valid, lane);
 
     // ------------------------------------------------ 1. decode steps of the old metadata, one block per lane
@@ -394,10 +413,11 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
         const int kk = k % R::P;  // slot of this sub-tile in the current load phase
         if (k > 0 && kk == 0) {
             __builtin_amdgcn_sched_barrier(0);  // keep the next phase's loads after this phase's arithmetic
-            load_raw<G, MC, VC, BV, FULL>(r, d, e0, valid, lane, k / R::P);
+            load_raw<G, MC, VC, BV, FULL, APO>(r, d, e0, valid, lane, k / R::P);
         }
         float mh[4], vh[4], mn[4], vn[4], pn[4];
         double vhd[4];  // the decoded second moment, widened for the EMA
+        double r2 = 0.0;  // APO: this lane's sum of R^2
         if constexpr (MC == UF8) {
             const double mstep = readlane_d(q1, k);
 #pragma unroll
@@ -453,6 +473,7 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const double gd = (double)grad_at<G>(r.g[kk], j);
+            if constexpr (APO) r2 += gd * gd;
             mn[j] = (float)(a.beta1 * (double)mh[j] + a.omb1 * gd);
             if constexpr (!Q::LUT) vhd[j] = (double)vh[j];
             vn[j] = (float)(a.beta2 * vhd[j] + a.omb2 * (gd * gd));
@@ -465,7 +486,16 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
             for (int j = 0; j < 4; ++j)
                 if (rel + j >= valid) mn[j] = vn[j] = 0.0f;  // absent: no state, no reduction input
         }
-        if constexpr (FULL) {
+        if constexpr (APO) {
+            // the channel of this sub-tile: sums of Rt^2 (Rt the fp32 direction) and R^2 per row of 16
+            // lanes (absent elements have R = 0 and a zero direction)
+            double t2 = 0.0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) t2 += (double)pn[j] * (double)pn[j];
+            t2 = row16_sum(t2);
+            r2 = row16_sum(r2);
+            if ((lane & 15) == 0) csum[4 * k + (lane >> 4)] = make_double2(t2, r2);
+        } else if constexpr (FULL) {
             st_f4<kNtStore>(d.p + e, make_float4(pn[0], pn[1], pn[2], pn[3]));
         } else {
 #pragma unroll
@@ -543,6 +573,19 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 if (rel + j < valid) g_as<float>(d.v)[e + j] = vn[j];
+        }
+    }
+    if constexpr (APO) {
+        // ||Rt_c|| / (||R_c|| + 1e-8) and s_c^2 gn2_c of the chunk's K channels, lane k channel k
+        __builtin_amdgcn_wave_barrier();  // this wavefront's LDS accesses run in order
+        if (lane < K && (FULL || lane * kSub < valid)) {
+            const double2 q0 = csum[4 * lane], q1 = csum[4 * lane + 1], q2 = csum[4 * lane + 2],
+                          q3 = csum[4 * lane + 3];
+            const double st = (q0.x + q1.x) + (q2.x + q3.x), sr = (q0.y + q1.y) + (q2.y + q3.y);
+            const int64_t c = (e0 + lane * kSub) / kSub;
+            const double sc = sqrt(st) / (sqrt(sr) + 1e-8);
+            d.cs[c] = sc;
+            d.csg[c] = sc * sc * d.cg2[c];
         }
     }
     if constexpr (VQ) {
@@ -653,7 +696,7 @@ __device__ __forceinline__ int locate(cp<const int64_t> tb, int nt, int64_t chun
 // One chunk per wave; each wave issues the loads of up to 4 sub-tiles
 // (packed, 8 registers per sub-tile for bf16/UF8/AL8) before it computes on
 // them. A chunk that ends a tensor takes the guarded path.
-template <int G, int MC, int VC, int BV>
+template <int G, int MC, int VC, int BV, bool APO>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(adamw_waves_per_eu<MC, VC, BV>())))
 void adamw_kernel(const AdamWLaunch a) {
     constexpr int C = Geo<MC, VC, BV>::C;
@@ -667,23 +710,30 @@ void adamw_kernel(const AdamWLaunch a) {
     __shared__ uint2 skey_all[4][NK];
     __shared__ uint4 encp_all[4][NK];     // blocks inside a sub-tile: fp32 encode parameters
     __shared__ double2 encd_all[4][NK];   // and {l_min, (L - 2) / delta} for the binary64 recheck
+    __shared__ double2 csum_all[4][APO ? 4 * C / kSub : 1];  // APO: row sums of each channel
     double* lut = lut_all[threadIdx.x >> 6];
     double* stab = stab_all[threadIdx.x >> 6];
     uint2* skey = skey_all[threadIdx.x >> 6];
     uint4* encp = encp_all[threadIdx.x >> 6];
     double2* encd = encd_all[threadIdx.x >> 6];
+    double2* csum = csum_all[threadIdx.x >> 6];
     if (chunk >= a.total_tiles) return;
     // the descriptor's pointers come from memory: mark them global so the
     // streams use global (not flat) loads and stores
     const cp<const AdamWDesc> D = (cp<const AdamWDesc>)a.D;
     const int ti = locate((cp<const int64_t>)a.tb, a.nt, chunk);
-    const DescG d = gview(D, ti);
+    DescG d = gview(D, ti);
+    if constexpr (APO) {
+        d.cs = to_g(a.apollo[ti].s);
+        d.csg = to_g(a.apollo[ti].sg);
+        d.cg2 = to_g((const double*)a.apollo[ti].gn2);
+    }
     const int64_t e0 = (chunk - D[ti].tile_begin) * C;
     const int64_t valid = d.n - e0;
     if (valid >= C)
-        adamw_compute<G, MC, VC, BV, true>(a, d, e0, C, lane, lut, stab, skey, encp, encd);
+        adamw_compute<G, MC, VC, BV, true, APO>(a, d, e0, C, lane, lut, stab, skey, encp, encd, csum);
     else
-        adamw_compute<G, MC, VC, BV, false>(a, d, e0, valid, lane, lut, stab, skey, encp, encd);
+        adamw_compute<G, MC, VC, BV, false, APO>(a, d, e0, valid, lane, lut, stab, skey, encp, encd, csum);
 }
 
 int adamw_tile_elems(int v_codec, int v_block) { return chunk_elems(v_codec, v_block); }
@@ -800,59 +850,66 @@ hipError_t adamw_static_table(void** table) {
 // sized by occupancy moves the same byte mix about 6% slower on gfx950, and a
 // chunk loop lets the compiler hoist per-chunk constants into spilled
 // registers.) Lists beyond 2^32 chunks take several launches.
-template <int G, int MC, int VC, int BV>
+template <int G, int MC, int VC, int BV, bool APO>
 static hipError_t launch_t(const AdamWLaunch& a, hipStream_t s) {
     constexpr int64_t kMaxGrid = int64_t(1) << 30;  // workgroups (4 waves each) per launch
     AdamWLaunch b = a;
     for (b.chunk_base = 0; b.chunk_base < a.total_tiles; b.chunk_base += 4 * kMaxGrid) {
         const int64_t left = (a.total_tiles - b.chunk_base + 3) / 4;
         const int64_t grid = left < kMaxGrid ? left : kMaxGrid;
-        hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV>), dim3((unsigned)grid), dim3(256), 0, s, b);
+        hipLaunchKernelGGL((adamw_kernel<G, MC, VC, BV, APO>), dim3((unsigned)grid), dim3(256), 0, s, b);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-template <int G, int MC, int VC>
+template <int G, int MC, int VC, bool APO>
 static hipError_t launch_bv(const AdamWLaunch& a, int bv, hipStream_t s) {
     if constexpr (VC == FP32) {
-        return launch_t<G, MC, VC, 256>(a, s);
+        return launch_t<G, MC, VC, 256, APO>(a, s);
     } else {
         switch (bv) {
-            case 64: return launch_t<G, MC, VC, 64>(a, s);
-            case 128: return launch_t<G, MC, VC, 128>(a, s);
-            case 256: return launch_t<G, MC, VC, 256>(a, s);
-            case 512: return launch_t<G, MC, VC, 512>(a, s);
-            case 1024: return launch_t<G, MC, VC, 1024>(a, s);
-            case 2048: return launch_t<G, MC, VC, 2048>(a, s);
+            case 64: return launch_t<G, MC, VC, 64, APO>(a, s);
+            case 128: return launch_t<G, MC, VC, 128, APO>(a, s);
+            case 256: return launch_t<G, MC, VC, 256, APO>(a, s);
+            case 512: return launch_t<G, MC, VC, 512, APO>(a, s);
+            case 1024: return launch_t<G, MC, VC, 1024, APO>(a, s);
+            case 2048: return launch_t<G, MC, VC, 2048, APO>(a, s);
         }
         return hipErrorInvalidValue;
     }
 }
 
-template <int G, int MC>
+template <int G, int MC, bool APO>
 static hipError_t launch_vc(const AdamWLaunch& a, int vc, int bv, hipStream_t s) {
     switch (vc) {
-        case AL8: return launch_bv<G, MC, AL8>(a, bv, s);
-        case AL16: return launch_bv<G, MC, AL16>(a, bv, s);
-        case FP32: return launch_bv<G, MC, FP32>(a, bv, s);
+        case AL8: return launch_bv<G, MC, AL8, APO>(a, bv, s);
+        case AL16: return launch_bv<G, MC, AL16, APO>(a, bv, s);
+        case FP32: return launch_bv<G, MC, FP32, APO>(a, bv, s);
     }
     return hipErrorInvalidValue;
 }
 
-template <int G>
+template <int G, bool APO>
 static hipError_t launch_mc(const AdamWLaunch& a, int mc, int vc, int bv, hipStream_t s) {
     switch (mc) {
-        case UF8: return launch_vc<G, UF8>(a, vc, bv, s);
-        case FP32: return launch_vc<G, FP32>(a, vc, bv, s);
+        case UF8: return launch_vc<G, UF8, APO>(a, vc, bv, s);
+        case FP32: return launch_vc<G, FP32, APO>(a, vc, bv, s);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block, hipStream_t s) {
-    if (grad_dtype == G_BF16) return launch_mc<G_BF16>(a, m_codec, v_codec, v_block, s);
-    return launch_mc<G_F32>(a, m_codec, v_codec, v_block, s);
+// apollo: APOLLO's projected moments at rank 256 (fp32 gradient R, no parameter
+// stream, channel scales out; see AdamWLaunch::apollo).
+hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block, hipStream_t s,
+                        bool apollo) {
+    if (apollo) {
+        if (grad_dtype != G_F32 || !a.apollo) return hipErrorInvalidValue;
+        return launch_mc<G_F32, true>(a, m_codec, v_codec, v_block, s);
+    }
+    if (grad_dtype == G_BF16) return launch_mc<G_BF16, false>(a, m_codec, v_codec, v_block, s);
+    return launch_mc<G_F32, false>(a, m_codec, v_codec, v_block, s);
 }
 
 }  // namespace al

@@ -307,7 +307,13 @@ struct ApolloPlan {
 };
 
 // Validate the list and lay out the workspace: descriptor table, then per
-// tensor R, Rt (C x rank fp32), gn2, s, sg (C doubles) and the limiter slot.
+// tensor R, Rt (C x rank fp32; no Rt at rank 256, where the AdamW step on R
+// reduces the direction into the channel scales itself), gn2, s, sg (C
+// doubles) and the limiter slot.
+// At rank 256 a channel of R is one 256-element sub-tile of the AdamW step,
+// which then forms the channel scales itself (no Rt, no scale pass).
+bool apollo_fused(int64_t rank) { return rank == 256; }
+
 al_status apollo_plan(const al_apollo_tensor* ts, int nt, const al_apollo_cfg* cfg, char* ws, ApolloPlan& P) {
     if (nt < 0) return fail(AL_EINVAL, "apollo: nt < 0");
     if (nt > 0 && !ts) return fail(AL_EINVAL, "apollo: tensors is NULL");
@@ -364,7 +370,7 @@ al_status apollo_plan(const al_apollo_tensor* ts, int nt, const al_apollo_cfg* c
     };
     for (auto& d : P.desc) {
         d.R = reinterpret_cast<float*>(take((size_t)(d.C * r) * 4));
-        d.Rt = reinterpret_cast<float*>(take((size_t)(d.C * r) * 4));
+        d.Rt = apollo_fused(r) ? nullptr : reinterpret_cast<float*>(take((size_t)(d.C * r) * 4));
         d.gn2 = reinterpret_cast<double*>(take((size_t)d.C * 8));
         d.s = reinterpret_cast<double*>(take((size_t)d.C * 8));
         d.sg = reinterpret_cast<double*>(take((size_t)d.C * 8));
@@ -635,7 +641,9 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
     a.step = step;
 
     // the fused AdamW step over the projected moments: gradient R, parameter Rt
-    // (cleared by the projection), lr 1, no weight decay -> Rt = -direction
+    // (cleared by the projection), lr 1, no weight decay -> Rt = -direction;
+    // at rank 256 no parameter stream: the step writes the channel scales
+    const bool fused = apollo_fused(cfg->rank);
     al::AdamWLaunch w;
     std::memset(&w, 0, sizeof(w));
     const double bc1 = 1.0 - std::pow(cfg->beta1, (double)step);
@@ -649,6 +657,7 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
     w.eps = (float)cfg->eps;
     w.decay = 1.0f;
     w.v_floor = cfg->v.log_floor;
+    w.apollo = fused ? a.D : nullptr;  // descriptor i of the AdamW table is projected tensor i
     const int T = al::adamw_tile_elems(cfg->v.codec, cfg->v.block);
     std::vector<al::AdamWDesc> wd(P.desc.size());
     for (size_t k = 0; k < P.desc.size(); ++k) {
@@ -672,10 +681,10 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
         (e = al::launch_apollo_proj(a, cfg->grad_dtype, s)) != hipSuccess ||
         (e = al::adamw_write_table(wd.data(), (int)wd.size(), static_cast<char*>(ws) + P.adamw_off, w, s)) !=
             hipSuccess ||
-        (e = al::launch_adamw(w, AL_DTYPE_F32, cfg->m.codec, cfg->v.codec, cfg->v.block, s)) != hipSuccess)
+        (e = al::launch_adamw(w, AL_DTYPE_F32, cfg->m.codec, cfg->v.codec, cfg->v.block, s, fused)) != hipSuccess)
         return hip_fail(e, "al_apollo_step launch");
-    if ((e = al::launch_apollo_scale(a, s)) != hipSuccess || (e = al::launch_apollo_norm(a, s)) != hipSuccess ||
-        (e = al::launch_apollo_update(a, cfg->grad_dtype, s)) != hipSuccess)
+    if ((!fused && (e = al::launch_apollo_scale(a, s)) != hipSuccess) ||
+        (e = al::launch_apollo_norm(a, s)) != hipSuccess || (e = al::launch_apollo_update(a, cfg->grad_dtype, s)) != hipSuccess)
         return hip_fail(e, "al_apollo_step launch");
     return AL_OK;
 }

@@ -24,6 +24,8 @@ struct AdamWDesc {
     int64_t tile_begin;  // first chunk of this tensor within the launch
 };
 
+struct ApolloDesc;
+
 struct AdamWLaunch {
     double beta1, omb1, beta2, omb2;  // state EMA coefficients (binary64)
     float step_size;                  // lr / (1 - beta1^t)
@@ -36,6 +38,13 @@ struct AdamWLaunch {
     int32_t nt;
     int64_t total_tiles;
     int64_t chunk_base;  // first chunk of this launch (one wave per chunk)
+    // APOLLO's moments on the projected gradient at rank 256 (launch_adamw with
+    // apollo set): descriptor i is the projected tensor of apollo[i]; there is
+    // no parameter stream, and each 256-element sub-tile (one channel) yields
+    // the channel scale ||Rt_c|| / (||R_c|| + 1e-8) into apollo[i].s and
+    // s_c^2 gn2_c into apollo[i].sg, Rt being the step's direction (the
+    // parameter output from zero with lr 1)
+    const ApolloDesc* apollo;
 };
 
 // Descriptors per copy launch: 60 x 64 bytes keep the argument segment under
@@ -66,7 +75,7 @@ hipError_t adamw_static_table(void** table);
 // Elements per tile: max(block of v, 256).
 int adamw_tile_elems(int v_codec, int v_block);
 hipError_t launch_adamw(const AdamWLaunch& a, int grad_dtype, int m_codec, int v_codec, int v_block,
-                        hipStream_t s);
+                        hipStream_t s, bool apollo = false);
 
 // ------------------------------------------------------------------ codec
 hipError_t launch_quantize(int codec, const float* x, int64_t n, int block, float log_floor, void* codes,

@@ -10,8 +10,11 @@
 //           slices of 16 inputs and widened to binary64; the products are
 //           exact and the accumulation is binary64, so fl32 of the result is
 //           the exactly rounded value except within ~L ulps of binary64 of an
-//           fp32 midpoint. Also sums g^2 per channel and clears Rt.
-//   scale   16 lanes per channel: s_c = ||Rt_c|| / (||R_c|| + 1e-8).
+//           fp32 midpoint. Also sums g^2 per channel and clears Rt (below
+//           rank 256).
+//   scale   16 lanes per channel: s_c = ||Rt_c|| / (||R_c|| + 1e-8) (below rank
+//           256; at rank 256 a channel is one sub-tile of the AdamW step, which
+//           forms s_c itself and never writes Rt).
 //   norm    one wavefront per tensor: ||G~||^2 = sum_c s_c^2 ||G_c||^2 and the
 //           norm-growth limiter.
 //   update  p = fl32(p (1 - lr wd) - lr g (s_c / lam)): one wavefront per
@@ -189,6 +192,8 @@ void apollo_proj_kernel(const ApolloArgs a) {
         }
         __syncthreads();
     }
+    // Rt exists below rank 256 only (it is then the AdamW step's parameter, cleared here)
+    const bool clear_rt = d.Rt != nullptr;
     if (active) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -200,7 +205,7 @@ void apollo_proj_kernel(const ApolloArgs a) {
                     const int k = kProjCW * w + 16 * j + (lane & 15);
                     if (c < C) {
                         d.R[c * r + k] = (float)acc[i][j][v];
-                        d.Rt[c * r + k] = 0.0f;
+                        if (clear_rt) d.Rt[c * r + k] = 0.0f;
                     }
                 }
     }
