@@ -177,12 +177,15 @@ def test_came_ragged_lists(dev, grad_bf16, mc, vc, vb, cc, cb):
         pair.compare(t, 1e-5 * t)
 
 
-TL_SUBSET = [Shape("k", 256, 2048), Shape("attn_norm", 1, 2048), Shape("down_slab", 96, 5632)]
+# a q projection (8 x 8 whole units: column sums merged over unit rows), a k projection (one unit row), a
+# norm (1-D) and a ragged slab (the per-unit kernels)
+TL_SUBSET = [Shape("q", 2048, 2048), Shape("k", 256, 2048), Shape("attn_norm", 1, 2048),
+             Shape("down_slab", 96, 5632)]
 
 
 def test_adafactor_100_steps(dev):
     """Independent 100-step trajectories (the TinyLlama Adafactor configuration's length) on a
-    subset of its shapes: states and parameters compared along the way."""
+    subset of its shapes, a full q projection among them: states and parameters compared along the way."""
     import paper_2608_22322_amd as al
 
     w = Workload("tl-subset", TL_SUBSET, zero_frac=0.0, steps=100)
