@@ -364,6 +364,21 @@ __device__ __forceinline__ bool f32_roundings_decided(const double q[N], float f
     return (mk > 16u * kQuotW) & (mz > 0x70200000u);
 }
 
+// As f32_roundings_decided, with the range test known to pass for every q_j
+// (each q_j zero or at least 2^-126 (1 + 2^-20) in magnitude): the midpoint
+// test alone.
+template <int N>
+__device__ __forceinline__ bool f32_midpoints_decided(const double q[N], float f[N]) {
+    uint32_t mk = 0xFFFFFFFFu;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+        f[j] = (float)q[j];
+        const uint2 b = __builtin_bit_cast(uint2, q[j]);
+        mk = umin32(mk, (b.x << 3) - ((0x10000000u - kQuotW) << 3));
+    }
+    return mk > 16u * kQuotW;
+}
+
 // Cross-lane moves of 64-bit values.
 __device__ __forceinline__ double shfl_d(double v, int src) { return __shfl(v, src); }
 __device__ __forceinline__ double readlane_d(double v, int lane) {

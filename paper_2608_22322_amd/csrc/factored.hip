@@ -549,12 +549,15 @@ __device__ __forceinline__ void load_wbatch(WBatch<G, NR>& b, gp<const void> g, 
 // holds NR x kWStride doubles.
 template <class P>
 __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64_t ru, int64_t cu, double* stage) {
-    constexpr int NR = P::NR, NP = NR / 2, LPR = 64 / NR, PPL = 32 / LPR;  // lanes per row, partials per lane
-    constexpr int SZ = NR * kWStride;  // one stage buffer; batches alternate between two
+    // row partials are finished P::FR rows (FB batches) at a time
+    constexpr int NR = P::NR, NP = NR / 2, FR = P::FR, FB = FR / NR;
+    constexpr int LPR = 64 / FR, PPL = 32 / LPR;  // lanes per finished row, partials per lane
+    constexpr int SZ = FR * kWStride;  // one stage buffer; finish groups alternate between two
     static_assert(NR == 4 || NR == 8 || NR == 16, "batch rows");
+    static_assert(FR % NR == 0 && (FR == 4 || FR == 8 || FR == 16), "finish group rows");
     const int lane = threadIdx.x & 63, h = lane >> 5, q = lane & 31;
     const int64_t r0 = ru * 256, c0 = cu * 256, cols = d.cols;
-    const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of a batch, partials PPL rpart ..
+    const int rrow = lane / LPR, rpart = lane % LPR;  // row finishing: row rrow of a group, partials PPL rpart ..
     // column sums: runs in crun added into cacc (all terms of a batch at once), else one plain sum in cacc
     double cacc[8], crun[8];
 #pragma unroll
@@ -562,11 +565,11 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         cacc[j] = 0.0;
         crun[j] = 0.0;
     }
-    // Row rrow of batch bi from its staged partials PPL rpart .. PPL rpart + PPL - 1, pairwise, then
-    // merged over the row's LPR lanes. Called one batch late, so the LDS round trip overlaps the next
-    // batch's arithmetic.
-    auto finish_rows = [&](int bi) {
-        const double* st = stage + (bi & 1) * SZ + rrow * kWStride + PPL * rpart;
+    // Row rrow of finish group gi from its staged partials PPL rpart .. PPL rpart + PPL - 1, pairwise,
+    // then merged over the row's LPR lanes. Called one batch late (with the next group's first batch),
+    // so the LDS round trip overlaps that batch's arithmetic.
+    auto finish_rows = [&](int gi) {
+        const double* st = stage + (gi & 1) * SZ + rrow * kWStride + PPL * rpart;
         double rs;
         const double2 p0 = *reinterpret_cast<const double2*>(st);
         if constexpr (PPL == 8) {
@@ -584,12 +587,12 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         rs += dpp_d<kDppQuadXor2>(rs);
         if constexpr (LPR >= 8) rs += dpp_d<kDppRowHalfMirror>(rs);
         if constexpr (LPR == 16) rs += dpp_d<kDppRowMirror>(rs);
-        if (rpart == 0) d.rowpart[cu * d.rows + r0 + NR * bi + rrow] = rs;
+        if (rpart == 0) d.rowpart[cu * d.rows + r0 + FR * gi + rrow] = rs;
     };
     typename P::Batch A, B;
     pol.load(A, 0);
     auto step = [&](const typename P::Batch& cur, int bi) {
-        double* sb = stage + (bi & 1) * SZ;
+        double* sb = stage + ((bi / FB) & 1) * SZ + (bi % FB) * NR * kWStride;
         if constexpr (P::ILP) {
             // all terms of the batch at once (more registers, fewer waves per SIMD, more independent
             // work per wave): the batch's column terms are added first, then into the run
@@ -638,7 +641,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         // the stages belong to this wavefront alone and its LDS accesses
         // execute in order: only the compiler must keep them in order
         __builtin_amdgcn_wave_barrier();
-        if (bi > 0) finish_rows(bi - 1);
+        if (bi > 0 && bi % FB == 0) finish_rows(bi / FB - 1);
         __builtin_amdgcn_wave_barrier();
         if (P::ILP && (bi + 1) % (kWRunRows / NR) == 0) {
 #pragma unroll
@@ -685,7 +688,7 @@ __device__ __forceinline__ void whole_unit_sums(const P& pol, const GD& d, int64
         step(A, NB - 1);
     }
     __builtin_amdgcn_wave_barrier();
-    finish_rows(NB - 1);
+    finish_rows(NB / FB - 1);
     // the two halves hold the even and the odd rows of the same columns
 #pragma unroll
     for (int j = 0; j < 8; ++j) cacc[j] += __shfl_xor(cacc[j], 32);
@@ -733,6 +736,7 @@ struct MargTerms {
     // 8-row batches, all terms of a batch at once: the cheap terms gain more from independent work per
     // wave than from occupancy (200 registers, 2 waves per SIMD: 2.53 against 2.68 ms on the 7B list)
     static constexpr int NR = 8;
+    static constexpr int FR = NR;
     static constexpr bool ILP = true;
     static constexpr bool SQUARES = false;
     static constexpr int DEPTH = 2;
@@ -1697,6 +1701,7 @@ struct ResBatch<G, false> {
 template <int G, bool UF>
 struct ResTerms {
     static constexpr int NR = kResNR;
+    static constexpr int FR = 16;  // row partials finished 16 rows at a time (4 batches)
     static constexpr bool ILP = false;  // the residual terms need the registers for occupancy
     // terms() gives uhat - m; the sums take its square (eps2 is added to the means in the finalize)
     static constexpr bool SQUARES = true;
@@ -1711,6 +1716,7 @@ struct ResTerms {
     int64_t cols, hcols;  // hcols = h * cols: the lane's row within a pair
     uint32_t lo;
     double cf[8];
+    double cfmin;  // the smallest of the lane's column factors
     double clip, rclip;
     __device__ void load(Batch& b, int rb) const {
         load_wbatch<G, NR>(b.g, gu, rb, cols, lo);
@@ -1746,7 +1752,15 @@ struct ResTerms {
         double qv[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) qv[j] = (rk * cf[j]) * (double)gv[j];
-        if (__builtin_expect(!f32_roundings_decided<8>(qv, uh), 0)) {
+        // A nonzero bf16 gradient has |g| >= 2^-133, so when rk * min_j c_j >= 2^7 (1 + 2^-18) on every
+        // lane each q_j is zero or above 2^-126 (1 + 2^-19) (three roundings of at most u each): only the
+        // midpoint test remains. The condition is taken wave-wide, so the branch is uniform.
+        bool ok;
+        if (G == G_BF16 && __builtin_expect(__all(rk * cfmin >= 0x1.00004p7), 1))
+            ok = f32_midpoints_decided<8>(qv, uh);
+        else
+            ok = f32_roundings_decided<8>(qv, uh);
+        if (__builtin_expect(!ok, 0)) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) uh[j] = (float)(((b.ri[k] * cf[j]) * (double)gv[j]) / clip);
         }
@@ -1757,7 +1771,7 @@ struct ResTerms {
 
 template <int G, bool UF>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void came_res_whole_kernel(const FacArgs a, int64_t base) {
-    __shared__ __attribute__((aligned(16))) double stages[4][2 * kResNR * kWStride];
+    __shared__ __attribute__((aligned(16))) double stages[4][2 * ResTerms<G, UF>::FR * kWStride];
     double* stage = stages[threadIdx.x >> 6];
     const int64_t unit = whole_unit_of_wave(base);
     if (unit >= a.whole_units) return;
@@ -1775,6 +1789,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void c
     pol.lo = w.lo;
 #pragma unroll
     for (int j = 0; j < 8; ++j) pol.cf[j] = d.cfac[w.c0 + 8 * w.q + j];
+    pol.cfmin = pol.cf[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) pol.cfmin = pol.cf[j] < pol.cfmin ? pol.cf[j] : pol.cfmin;
     pol.clip = d.scal[0];
     pol.rclip = 1.0 / pol.clip;
     whole_unit_sums(pol, d, w.r0 / 256, w.c0 / 256, stage);
