@@ -320,7 +320,9 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
  * step's second-moment blocks (x > 0), 9 = the clipped update of the CAME
  * passes, fl32(fl64(fl64(r c) x) / d) for fixed binary64 r, c, d from the
  * quotient with fl64(1 / d) folded into r and the decision test over eight
- * consecutive inputs (n a multiple of 8). x, out: n doubles (device). */
+ * consecutive inputs (n a multiple of 8), 10 = the same for bf16 values x with
+ * r = d = 1 and c = 0x1.00008c3a4f91dp7 (about 2^7 (1 + 2^-17)), where the residual pass's range test is
+ * known to pass and only the midpoint test runs. x, out: n doubles (device). */
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream);
 
 /* The AL8 levels of the fused AdamW step's split-table decode (section 4.1,

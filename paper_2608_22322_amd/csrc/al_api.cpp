@@ -691,9 +691,9 @@ al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_a
 
 al_status al_diag_math(int32_t fn, const double* x, int64_t n, double* out, void* stream) {
     g_err[0] = 0;
-    if (fn < 0 || fn > 9) return fail(AL_EINVAL, "al_diag_math: fn %d", fn);
+    if (fn < 0 || fn > 10) return fail(AL_EINVAL, "al_diag_math: fn %d", fn);
     if (n < 0) return fail(AL_EINVAL, "al_diag_math: n < 0");
-    if (fn == 9 && n % 8 != 0) return fail(AL_EINVAL, "al_diag_math: fn 9 takes groups of 8 inputs");
+    if (fn >= 9 && n % 8 != 0) return fail(AL_EINVAL, "al_diag_math: fn 9 and 10 take groups of 8 inputs");
     if (n == 0) return AL_OK;
     if (!x || !out) return fail(AL_EINVAL, "al_diag_math: NULL buffer");
     if (!aligned16(x) || !aligned16(out)) return fail(AL_EALIGN, "al_diag_math: alignment");

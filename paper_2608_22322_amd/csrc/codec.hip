@@ -82,11 +82,30 @@ __global__ __launch_bounds__(256) void dequantize_kernel(const void* __restrict_
 // endpoint log2 of an fp32 value, 9 = the clipped update of the CAME passes
 // with 1 / clip folded into the row factor: fl32(fl64(fl64(r c) x) / d) for
 // r, c, d below, eight consecutive inputs per decision as in the kernels (n a
-// multiple of 8).
+// multiple of 8), 10 = the same for bf16 inputs (x a bf16 value) with r = d = 1
+// and c = 0x1.00008c3a4f91dp7 (about 2^7 (1 + 2^-17)), just above the factor at which the CAME residual
+// pass drops the range test: the midpoint test alone.
 constexpr double kDiagR = 0.7310585786300049, kDiagC = 1234.5678901234567, kDiagD = 3.0000000000000004;
 __global__ __launch_bounds__(256) void diag_math_kernel(int fn, const double* __restrict__ x, int64_t n,
                                                          double* __restrict__ out, const Exp2Coef cf) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if (fn == 10) {
+        constexpr double c = 0x1.00008c3a4f91dp7;  // r * c / d with r = d = 1: the row-safe threshold holds
+        static_assert(c >= 0x1.00004p7, "above the row-safe factor");
+        for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; 8 * g + 8 <= n; g += stride) {
+            double q[8];
+            float f[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) q[j] = (1.0 * c) * x[8 * g + j];
+            if (!f32_midpoints_decided<8>(q, f)) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) f[j] = (float)(((1.0 * c) * x[8 * g + j]) / 1.0);
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) out[8 * g + j] = (double)f[j];
+        }
+        return;
+    }
     if (fn == 9) {
         const double rk = kDiagR * (1.0 / kDiagD);
         for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; 8 * g + 8 <= n; g += stride) {

@@ -173,3 +173,24 @@ def test_folded_clipped_quotient_matches_division():
     bad = np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32))
     log(f"folded clipped quotient: {x.size:,} inputs, {bad} differences")
     assert bad == 0
+
+
+def test_bf16_quotient_midpoint_test_alone():
+    """The CAME residual pass with bf16 gradients drops the range test when r_i / clip * min_j c_j >=
+    2^7 (1 + 2^-18): every nonzero bf16 has |g| >= 2^-133, so each quotient is zero or in the fp32 normal
+    range. At a factor just above that bound (about 2^7 (1 + 2^-17)), every bf16 value (subnormal ones, whose
+    quotients land just above FLT_MIN, included), in groups of eight, against the host division bit for
+    bit."""
+    require_gpu()
+    c = float.fromhex("0x1.00008c3a4f91dp7")  # the kernel's constant, about 2^7 (1 + 2^-17)
+    bits = np.arange(1 << 16, dtype=np.uint32)
+    x = (bits << 16).view(np.float32).astype(np.float64)
+    x = x[np.isfinite(x)]
+    x = np.concatenate([x, np.zeros((-x.size) % 8)])
+    got = _run(10, x).astype(np.float32)
+    with np.errstate(over="ignore"):
+        ref = ((1.0 * c) * x / 1.0).astype(np.float32)
+    assert np.all(np.abs(ref[x != 0]) >= np.float32(2.0**-126))  # the bound the pass relies on
+    bad = np.count_nonzero(got.view(np.uint32) != ref.view(np.uint32))
+    log(f"bf16 quotients, midpoint test alone: {x.size:,} inputs, {bad} differences")
+    assert bad == 0
