@@ -184,8 +184,8 @@ def test_bf16_quotient_midpoint_test_alone():
     require_gpu()
     c = float.fromhex("0x1.00008c3a4f91dp7")  # the kernel's constant, about 2^7 (1 + 2^-17)
     bits = np.arange(1 << 16, dtype=np.uint32)
-    x = (bits << 16).view(np.float32).astype(np.float64)
-    x = x[np.isfinite(x)]
+    xf = (bits << 16).view(np.float32)
+    x = xf[np.isfinite(xf)].astype(np.float64)
     x = np.concatenate([x, np.zeros((-x.size) % 8)])
     got = _run(10, x).astype(np.float32)
     with np.errstate(over="ignore"):
