@@ -59,10 +59,15 @@ __device__ __forceinline__ double split2_product(double f1, double f2) { return 
 __device__ __forceinline__ double split2_level(const double* t, uint32_t q) {
     return split2_product(t[q >> 4], t[16 + (q & 15u)]);
 }
+// The three-factor entries' arguments share one conversion, product and sum
+// (the lanes of one pass take different entry kinds): base + fl64(m st) with
+// base = l32 for the first factor and +0.0 otherwise, which adds exactly
+// (m st >= 0); 1% faster at B_V 64. (The same form for the two-factor
+// entries raised the B_V 256 kernel's spills and ran 1% slower there.)
 __device__ __forceinline__ double split3_entry(double l32, double st, int j) {
-    const double arg = j < 4 ? l32 + (double)(64 * j - 1) * st
-                             : (j < 12 ? (double)(8 * (j - 4)) * st : (double)(j - 12) * st);
-    return exp2_d(arg, kExp2);
+    const int m = j < 4 ? 64 * j - 1 : (j < 12 ? 8 * (j - 4) : j - 12);
+    const double base = j < 4 ? l32 : 0.0;
+    return exp2_d(base + (double)m * st, kExp2);
 }
 __device__ __forceinline__ double split3_product(double f1, double f2, double f3) { return (f1 * f2) * f3; }
 __device__ __forceinline__ double split3_level(const double* t, uint32_t q) {
