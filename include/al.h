@@ -293,18 +293,21 @@ al_status al_came_step(const al_tensor* tensors, int32_t nt, const al_came_cfg* 
                        int64_t step, void* ws, size_t ws_bytes, void* stream);
 
 /* Workspace size (bytes) that al_apollo_step needs for this list and config:
- * per tensor R and Rt (rank * C floats each) and per-channel binary64 sums,
- * and the descriptor tables of the step's launches. */
+ * per tensor R (rank * C floats), below rank 256 also Rt (as many floats),
+ * per-channel binary64 sums, and the descriptor tables of the step's
+ * launches. */
 al_status al_apollo_workspace_bytes(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg,
                                     size_t* bytes);
 
 /* One APOLLO step over nt projected tensors (rows, cols >= 1). Kernels, in
  * stream order: the binary64 projection on the matrix cores (also sums of
  * squares per channel of G), the fused AdamW step over the projected moments
- * (fp32 R as its gradient, Rt in the workspace as its parameter, lr 1, no
- * weight decay), the channel scales, the limiter per tensor, and the
- * parameter update. ws: device workspace of at least the queried size,
- * 256-byte aligned. */
+ * (fp32 R as its gradient, lr 1, no weight decay; at rank 256 it forms the
+ * channel scales itself, one channel per 256-element sub-tile, from the
+ * direction it computes; below rank 256 it writes the direction as its
+ * parameter Rt in the workspace and a separate pass forms the channel
+ * scales), the limiter per tensor, and the parameter update. ws: device
+ * workspace of at least the queried size, 256-byte aligned. */
 al_status al_apollo_step(const al_apollo_tensor* tensors, int32_t nt, const al_apollo_cfg* cfg, int64_t step,
                          void* ws, size_t ws_bytes, void* stream);
 
