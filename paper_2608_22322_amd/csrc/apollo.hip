@@ -85,104 +85,159 @@ constexpr int kLK = 16;  // inputs per LDS slice
 
 // One workgroup of 8 wavefronts per tile of 64 channels; wave w computes output
 // columns [32 w, 32 w + 32) of the tile (4 x 2 MFMA tiles of 16 x 16, eight
-// binary64 accumulators: 124 VGPRs, 4 waves per SIMD) when 32 w < r. (Four
-// wavefronts of 64 x 64 outputs -- 16 accumulators, 230 VGPRs, 2 waves per SIMD
-// -- ran the projection 14% slower.) The next slice's global loads are issued
-// into registers before the matrix work on the current slice (software
-// prefetch; one LDS buffer, two barriers per slice). MFMA f64 16x16x4 operand
-// layout: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]; result
-// register v of lane l is D[l / 16 + 4 v][l % 16].
+// binary64 accumulators, 4 waves per SIMD) when 32 w < r. (Four wavefronts of
+// 64 x 64 outputs -- 16 accumulators, 230 VGPRs, 2 waves per SIMD -- ran the
+// projection 14% slower.) Slices of 16 inputs are double-buffered in LDS with
+// one barrier per slice: while the matrix cores work on slice n, slice n + 1 of
+// Pi is copied straight from global memory into the other buffer (LDS DMA, one
+// 1 KB row of Pi per wavefront instruction; rows past L repeat row L - 1, whose
+// products meet zero inputs) and slice n + 1 of A is loaded into registers, then
+// stored to the other buffer after the matrix work. A stays fp32 in LDS (row
+// pitch 20 floats: the 64 lanes of an operand read hit 64 distinct banks) and
+// is widened to binary64 with Pi when the operands are read; the four 4-input
+// steps of a slice are unrolled so their reads run ahead of the matrix work.
+// MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
 constexpr int kProjWaves = 8;                                     // wavefronts per workgroup
 constexpr int kProjThreads = 64 * kProjWaves;
 constexpr int kProjCW = 256 / kProjWaves;                         // output columns per wavefront
 constexpr int kProjJT = kProjCW / 16;                             // 16-column MFMA tiles per wavefront
 constexpr int kAPer = kApolloTileCh * kLK / kProjThreads;         // A values per thread and slice
-constexpr int kBPer = kLK * 256 / 4 / kProjThreads;               // Pi float4 per thread and slice at rank 256
+constexpr int kAsPitch = 20;                                      // A row pitch in LDS (floats)
+constexpr int kBsPitch = 256 + 16;                                // Pi row pitch in LDS (floats)
+static_assert(kLK == 2 * kProjWaves, "each wavefront copies two rows of Pi per slice");
+
+// Where one tile's inputs live: the descriptor's fields, read once into
+// registers (read through the descriptor, they are fetched again every slice
+// and those fetches wait for the slice's copies in flight).
+struct ProjSrc {
+    const void* g;
+    int64_t cols, C, L, c0;
+    bool right;
+};
+
+// Slice l0 of A: thread e holds input (c, l) of the tile as raw bits, loaded
+// from a clamped (always valid) address without branches, so the wait for it
+// falls after the matrix work; proj_store_a zeroes what lies outside the tensor.
+template <int G>
+__device__ __forceinline__ void proj_tile_pos(const ProjSrc& s, int tid, int q, int& c, int& l) {
+    const int e = tid + kProjThreads * q;
+    c = s.right ? e / kLK : e % kApolloTileCh;
+    l = s.right ? e % kLK : e / kApolloTileCh;
+}
 
 template <int G>
-__device__ __forceinline__ void proj_fetch(const ApolloDesc& d, int64_t c0, int64_t l0, int r4, bool right, int tid,
-                                           float (&ra)[kAPer], float4 (&rb)[kBPer]) {
+__device__ __forceinline__ void proj_fetch_a(const ProjSrc& s, int64_t l0, int tid, uint32_t (&ra)[kAPer]) {
+    const gp<const uint16_t> gh = to_g(reinterpret_cast<const uint16_t*>(s.g));
+    const gp<const uint32_t> gf = to_g(reinterpret_cast<const uint32_t*>(s.g));
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
-        const int e = tid + kProjThreads * q;
-        const int c = right ? e / kLK : e % kApolloTileCh;
-        const int l = right ? e % kLK : e / kApolloTileCh;
-        float x = 0.0f;
-        if (c0 + c < d.C && l0 + l < d.L) {
-            const int64_t idx = right ? (c0 + c) * d.cols + (l0 + l) : (l0 + l) * d.cols + (c0 + c);
-            if constexpr (G == G_BF16)
-                x = bf16_to_f32(reinterpret_cast<const uint16_t*>(d.g)[idx]);
-            else
-                x = reinterpret_cast<const float*>(d.g)[idx];
-        }
-        ra[q] = x;
+        int c, l;
+        proj_tile_pos<G>(s, tid, q, c, l);
+        const int64_t cc = s.c0 + c < s.C ? s.c0 + c : s.C - 1;
+        const int64_t ll = l0 + l < s.L ? l0 + l : s.L - 1;
+        const int64_t idx = s.right ? cc * s.cols + ll : ll * s.cols + cc;
+        if constexpr (G == G_BF16)
+            ra[q] = gh[idx];
+        else
+            ra[q] = gf[idx];
     }
+}
+
+template <int G>
+__device__ __forceinline__ void proj_store_a(const ProjSrc& s, int64_t l0, float (*As)[kAsPitch], int tid,
+                                             const uint32_t (&ra)[kAPer]) {
 #pragma unroll
-    for (int q = 0; q < kBPer; ++q) {
-        const int e = tid + kProjThreads * q;
-        const int l = e / r4, k4 = e - l * r4;
-        float4 x = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        if (e < kLK * r4 && l0 + l < d.L) x = *reinterpret_cast<const float4*>(d.proj + (l0 + l) * (4 * r4) + 4 * k4);
-        rb[q] = x;
+    for (int q = 0; q < kAPer; ++q) {
+        int c, l;
+        proj_tile_pos<G>(s, tid, q, c, l);
+        const float x = G == G_BF16 ? __uint_as_float(ra[q] << 16) : __uint_as_float(ra[q]);
+        As[c][l] = (s.c0 + c < s.C && l0 + l < s.L) ? x : 0.0f;
+    }
+}
+
+// Rows l0 + 2 w and l0 + 2 w + 1 of Pi (r floats each, lanes < r / 4 copy 16 B)
+// into rows 2 w, 2 w + 1 of the LDS buffer; completion is counted by vmcnt.
+__device__ __forceinline__ void proj_copy_pi(const float* proj, int64_t L, int64_t l0, int r, int w, int lane,
+                                             float (*Bs)[kBsPitch]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        int64_t row = l0 + 2 * w + t;
+        row = row < L ? row : L - 1;
+        if (4 * lane < r)
+            __builtin_amdgcn_global_load_lds(proj + row * r + 4 * lane, &Bs[2 * w + t][0], 16, 0, 0);
     }
 }
 
 template <int G>
 __global__ __launch_bounds__(kProjThreads) __attribute__((amdgpu_waves_per_eu(4)))
 void apollo_proj_kernel(const ApolloArgs a) {
-    __shared__ double As[kApolloTileCh][kLK + 1];
-    __shared__ __attribute__((aligned(16))) float Bs[kLK][256];
+    // Two buffers of each operand as four separate LDS objects, named statically
+    // in each half of the unrolled slice loop: the compiler then knows that the
+    // copy into one buffer does not alias the reads of the other and does not
+    // wait for the copy before the matrix work.
+    __shared__ __attribute__((aligned(16))) float As0[kApolloTileCh][kAsPitch];
+    __shared__ __attribute__((aligned(16))) float As1[kApolloTileCh][kAsPitch];
+    __shared__ __attribute__((aligned(16))) float Bs0[kLK][kBsPitch];
+    __shared__ __attribute__((aligned(16))) float Bs1[kLK][kBsPitch];
     const int64_t tile = blockIdx.x;
     const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::tile_begin>(a.D, a.nt, tile)];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int r = a.rank, r4 = a.rank / 4;
-    const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
-    const int64_t C = d.C, L = d.L;
-    const bool right = d.right != 0;
+    const int l16 = lane & 15, l4 = lane >> 4;
+    const int r = a.rank;
+    ProjSrc src;
+    src.g = d.g;
+    src.cols = d.cols;
+    src.C = d.C;
+    src.L = d.L;
+    src.c0 = (tile - d.tile_begin) * kApolloTileCh;
+    src.right = d.right != 0;
+    const float* proj = d.proj;
+    float* const Rp = d.R;
+    float* const Rtp = d.Rt;
+    double* const gn2 = d.gn2;
+    const int64_t c0 = src.c0, C = src.C, L = src.L;
     const bool active = kProjCW * w < r;
     d4v acc[4][kProjJT];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < kProjJT; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
-    double gsum = 0.0;
-    float ra[kAPer];
-    float4 rb[kBPer];
-    proj_fetch<G>(d, c0, 0, r4, right, tid, ra, rb);
-    for (int64_t l0 = 0; l0 < L; l0 += kLK) {
-#pragma unroll
-        for (int q = 0; q < kAPer; ++q) {
-            const int e = tid + kProjThreads * q;
-            const int c = right ? e / kLK : e % kApolloTileCh;
-            const int l = right ? e % kLK : e / kApolloTileCh;
-            As[c][l] = (double)ra[q];
-        }
-#pragma unroll
-        for (int q = 0; q < kBPer; ++q) {
-            const int e = tid + kProjThreads * q;
-            if (e < kLK * r4) {
-                const int l = e / r4, k4 = e - l * r4;
-                *reinterpret_cast<float4*>(&Bs[l][4 * k4]) = rb[q];
-            }
-        }
-        __syncthreads();
-        if (l0 + kLK < L) proj_fetch<G>(d, c0, l0 + kLK, r4, right, tid, ra, rb);
-        if (tid < kApolloTileCh) {
-#pragma unroll 8
-            for (int l = 0; l < kLK; ++l) {
-                const double x = As[tid][l];
-                gsum += x * x;
-            }
+    double gs[4] = {0.0, 0.0, 0.0, 0.0};  // wavefront 0: sum of g^2 of channel 16 i + lane % 16, inputs = lane / 16 mod 4
+    uint32_t ra[kAPer];
+    const int64_t ns = (L + kLK - 1) / kLK;
+    // Slice n from (Ac, Bc) while slice n + 1 is brought into (An, Bn).
+    auto slice = [&](int64_t n, float (*Ac)[kAsPitch], float (*Bc)[kBsPitch], float (*An)[kAsPitch],
+                     float (*Bn)[kBsPitch]) {
+        const bool more = n + 1 < ns;
+        if (more) {
+            proj_copy_pi(proj, L, (n + 1) * kLK, r, w, lane, Bn);
+            proj_fetch_a<G>(src, (n + 1) * kLK, tid, ra);
         }
         if (active) {
-#pragma unroll 2
+            // the operands of step kk + 4 are read before the matrix work of step kk
+            float xa[2][4], xb[2][kProjJT];
+            auto rd = [&](int st, int kk) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xa[st][i] = Ac[16 * i + l16][kk + l4];
+#pragma unroll
+                for (int j = 0; j < kProjJT; ++j) xb[st][j] = Bc[kk + l4][kProjCW * w + 16 * j + l16];
+            };
+            rd(0, 0);
+#pragma unroll
             for (int kk = 0; kk < kLK; kk += 4) {
+                const int st = (kk >> 2) & 1;
+                if (kk + 4 < kLK) rd(st ^ 1, kk + 4);
                 double af[4], bf[kProjJT];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) af[i] = As[16 * i + (lane & 15)][kk + (lane >> 4)];
+                for (int i = 0; i < 4; ++i) af[i] = (double)xa[st][i];
 #pragma unroll
-                for (int j = 0; j < kProjJT; ++j)
-                    bf[j] = (double)Bs[kk + (lane >> 4)][kProjCW * w + 16 * j + (lane & 15)];
+                for (int j = 0; j < kProjJT; ++j) bf[j] = (double)xb[st][j];
+                // wavefront 0 reads every input of the slice once: the channel sums of g^2
+                if (w == 0) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) gs[i] = __builtin_fma(af[i], af[i], gs[i]);
+                }
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -190,10 +245,26 @@ void apollo_proj_kernel(const ApolloArgs a) {
                         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
             }
         }
+        if (more) proj_store_a<G>(src, (n + 1) * kLK, An, tid, ra);
+        // the copies into the other buffers have landed and every read of these is done
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+    };
+    if (ns > 0) {
+        proj_copy_pi(proj, L, 0, r, w, lane, Bs0);
+        proj_fetch_a<G>(src, 0, tid, ra);
+        proj_store_a<G>(src, 0, As0, tid, ra);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
+    for (int64_t n = 0; n < ns; n += 2) {
+        slice(n, As0, Bs0, As1, Bs1);
+        if (n + 1 < ns) slice(n + 1, As1, Bs1, As0, Bs0);
+    }
     // Rt exists below rank 256 only (it is then the AdamW step's parameter, cleared here)
-    const bool clear_rt = d.Rt != nullptr;
+    const bool clear_rt = Rtp != nullptr;
+    const gp<float> Rg = to_g(Rp);
+    const gp<float> Rtg = to_g(Rtp);
     if (active) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -201,15 +272,25 @@ void apollo_proj_kernel(const ApolloArgs a) {
             for (int j = 0; j < kProjJT; ++j)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int64_t c = c0 + 16 * i + (lane >> 4) + 4 * v;
-                    const int k = kProjCW * w + 16 * j + (lane & 15);
+                    const int64_t c = c0 + 16 * i + l4 + 4 * v;
+                    const int k = kProjCW * w + 16 * j + l16;
                     if (c < C) {
-                        d.R[c * r + k] = (float)acc[i][j][v];
-                        if (clear_rt) d.Rt[c * r + k] = 0.0f;
+                        Rg[c * r + k] = (float)acc[i][j][v];
+                        if (clear_rt) Rtg[c * r + k] = 0.0f;
                     }
                 }
     }
-    if (tid < kApolloTileCh && c0 + tid < C) d.gn2[c0 + tid] = gsum;
+    if (w == 0) {
+        const gp<double> gn = to_g(gn2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            double x = gs[i];
+            x += __shfl_xor(x, 16);
+            x += __shfl_xor(x, 32);
+            const int64_t c = c0 + 16 * i + lane;
+            if (lane < 16 && c < C) gn[c] = x;
+        }
+    }
 }
 
 hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
