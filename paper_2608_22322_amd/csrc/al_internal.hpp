@@ -177,7 +177,7 @@ hipError_t launch_came_vec1d(const FacArgs& a, int grad_dtype, hipStream_t s);
 // tensor has C channels of L inputs (A = G or G^T as C x L) and rank r; its
 // workspace regions hold R and Rt (C x r fp32, channel-major) and per-channel
 // binary64 sums.
-constexpr int kApolloTileCh = 64;  // channels per projection workgroup
+constexpr int kApolloTileCh = 32;  // channels per projection workgroup
 struct ApolloDesc {
     float* p;
     const void* g;

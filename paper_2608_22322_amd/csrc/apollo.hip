@@ -83,89 +83,109 @@ hipError_t apollo_copy_desc(const ApolloDesc* host, int count, ApolloDesc* dev, 
 // ---------------------------------------------------------------- projection
 constexpr int kLK = 16;  // inputs per LDS slice
 
-// One workgroup of 8 wavefronts per tile of 64 channels; wave w computes output
-// columns [32 w, 32 w + 32) of the tile (4 x 2 MFMA tiles of 16 x 16, eight
-// binary64 accumulators, 4 waves per SIMD) when 32 w < r. (Four wavefronts of
-// 64 x 64 outputs -- 16 accumulators, 230 VGPRs, 2 waves per SIMD -- ran the
-// projection 14% slower.) Slices of 16 inputs are double-buffered in LDS with
-// one barrier per slice: while the matrix cores work on slice n, slice n + 1 of
-// Pi is copied straight from global memory into the other buffer (LDS DMA, one
-// 1 KB row of Pi per wavefront instruction; rows past L repeat row L - 1, whose
-// products meet zero inputs) and slice n + 1 of A is loaded into registers, then
-// stored to the other buffer after the matrix work. A stays fp32 in LDS (row
-// pitch 20 floats: the 64 lanes of an operand read hit 64 distinct banks) and
-// is widened to binary64 with Pi when the operands are read; the four 4-input
-// steps of a slice are unrolled so their reads run ahead of the matrix work.
-// MFMA f64 16x16x4 operand layout: lane l supplies A[l % 16][l / 16] and
-// B[l / 16][l % 16]; result register v of lane l is D[l / 16 + 4 v][l % 16].
-constexpr int kProjWaves = 8;                                     // wavefronts per workgroup
+// One workgroup of 4 wavefronts per tile of 32 channels; wave w computes output
+// columns [64 w, 64 w + 64) of the tile (2 x 4 MFMA tiles of 16 x 16, eight
+// binary64 accumulators) when 64 w < r. Four such workgroups share a CU (one
+// wavefront of each per SIMD), so one workgroup's barrier leaves three to feed
+// the matrix cores. (Eight wavefronts on 64 channels: 2 workgroups per CU,
+// projection 5% slower; four wavefronts of 64 x 64 outputs -- 16 accumulators,
+// 230 VGPRs, 2 waves per SIMD -- 14% slower.) Slices of 16 inputs are
+// double-buffered in LDS with one barrier per slice: while the matrix cores
+// work on slice n, slice n + 1 of Pi is copied straight from global memory into
+// the other buffer (LDS DMA, one row of Pi per wavefront instruction; rows past
+// L repeat row L - 1, whose products meet zero inputs) and slice n + 1 of A is
+// loaded into registers, then stored to the other buffer after the matrix work.
+// A stays fp32 in LDS (row pitch 20 floats: the 64 lanes of an operand read hit
+// 64 distinct banks) and is widened to binary64 with Pi when the operands are
+// read; the four 4-input steps of a slice are unrolled, each step's operands
+// read before the previous step's matrix work. MFMA f64 16x16x4 operand
+// layout: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]; result
+// register v of lane l is D[l / 16 + 4 v][l % 16].
+constexpr int kProjWaves = 4;                                     // wavefronts per workgroup
 constexpr int kProjThreads = 64 * kProjWaves;
+constexpr int kProjIT = kApolloTileCh / 16;                       // 16-channel MFMA tiles per wavefront
 constexpr int kProjCW = 256 / kProjWaves;                         // output columns per wavefront
 constexpr int kProjJT = kProjCW / 16;                             // 16-column MFMA tiles per wavefront
+constexpr int kProjRows = kLK / kProjWaves;                       // rows of Pi each wavefront copies per slice
 constexpr int kAPer = kApolloTileCh * kLK / kProjThreads;         // A values per thread and slice
 constexpr int kAsPitch = 20;                                      // A row pitch in LDS (floats)
 constexpr int kBsPitch = 256 + 16;                                // Pi row pitch in LDS (floats)
-static_assert(kLK == 2 * kProjWaves, "each wavefront copies two rows of Pi per slice");
+static_assert(kProjIT * kProjJT == 8 && kLK % kProjWaves == 0 && kAPer * kProjThreads == kApolloTileCh * kLK,
+              "projection tiling");
 
-// Where one tile's inputs live: the descriptor's fields, read once into
-// registers (read through the descriptor, they are fetched again every slice
-// and those fetches wait for the slice's copies in flight).
-struct ProjSrc {
-    const void* g;
-    int64_t cols, C, L, c0;
-    bool right;
+// One thread's share of the A slices of a tile, fixed for the whole tile:
+// value q of every slice is input (c_q, l0 + l_q), stored at As[c_q][l_q].
+// Slices that lie wholly inside the tensor load from base_q + l0 * stride with
+// no clamping; only a ragged last slice clamps l to L - 1 (and zeroes it).
+template <int G>
+struct ProjA {
+    using T = typename std::conditional<G == G_BF16, uint16_t, uint32_t>::type;
+    gp<const T> base[kAPer];  // element (c_q clamped to C - 1, l_q) of slice 0
+    int l[kAPer];             // l_q
+    int slot[kAPer];          // c_q * kAsPitch + l_q
+    bool cval[kAPer];         // c_q inside the tensor
+    int64_t stride;           // distance between consecutive inputs of a channel
 };
 
-// Slice l0 of A: thread e holds input (c, l) of the tile as raw bits, loaded
-// from a clamped (always valid) address without branches, so the wait for it
-// falls after the matrix work; proj_store_a zeroes what lies outside the tensor.
 template <int G>
-__device__ __forceinline__ void proj_tile_pos(const ProjSrc& s, int tid, int q, int& c, int& l) {
-    const int e = tid + kProjThreads * q;
-    c = s.right ? e / kLK : e % kApolloTileCh;
-    l = s.right ? e % kLK : e / kApolloTileCh;
-}
-
-template <int G>
-__device__ __forceinline__ void proj_fetch_a(const ProjSrc& s, int64_t l0, int tid, uint32_t (&ra)[kAPer]) {
-    const gp<const uint16_t> gh = to_g(reinterpret_cast<const uint16_t*>(s.g));
-    const gp<const uint32_t> gf = to_g(reinterpret_cast<const uint32_t*>(s.g));
+__device__ __forceinline__ void proj_a_setup(ProjA<G>& A, const void* g, int64_t cols, int64_t C, int64_t c0,
+                                             bool right, int tid) {
+    const gp<const typename ProjA<G>::T> gt = to_g(reinterpret_cast<const typename ProjA<G>::T*>(g));
+    A.stride = right ? 1 : cols;
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
-        int c, l;
-        proj_tile_pos<G>(s, tid, q, c, l);
-        const int64_t cc = s.c0 + c < s.C ? s.c0 + c : s.C - 1;
-        const int64_t ll = l0 + l < s.L ? l0 + l : s.L - 1;
-        const int64_t idx = s.right ? cc * s.cols + ll : ll * s.cols + cc;
-        if constexpr (G == G_BF16)
-            ra[q] = gh[idx];
-        else
-            ra[q] = gf[idx];
+        const int e = tid + kProjThreads * q;
+        const int c = right ? e / kLK : e % kApolloTileCh;
+        const int l = right ? e % kLK : e / kApolloTileCh;
+        const int64_t cc = c0 + c < C ? c0 + c : C - 1;
+        A.base[q] = gt + (right ? cc * cols : cc) + l * A.stride;
+        A.l[q] = l;
+        A.slot[q] = c * kAsPitch + l;
+        A.cval[q] = c0 + c < C;
     }
 }
 
+// Slice l0 of A as raw bits into registers (the wait for them falls after the
+// matrix work, where proj_store_a consumes them).
 template <int G>
-__device__ __forceinline__ void proj_store_a(const ProjSrc& s, int64_t l0, float (*As)[kAsPitch], int tid,
-                                             const uint32_t (&ra)[kAPer]) {
+__device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int64_t l0, int64_t L, uint32_t (&ra)[kAPer]) {
+    if (l0 + kLK <= L) {
+#pragma unroll
+        for (int q = 0; q < kAPer; ++q) ra[q] = A.base[q][l0 * A.stride];
+    } else {
+#pragma unroll
+        for (int q = 0; q < kAPer; ++q) {
+            const int64_t ll = l0 + A.l[q] < L ? l0 : L - 1 - A.l[q];
+            ra[q] = A.base[q][ll * A.stride];
+        }
+    }
+}
+
+// The slice into LDS as fp32, inputs outside the tensor as zero; each thread
+// also accumulates the squares of the values it stores (binary64, exact products).
+template <int G>
+__device__ __forceinline__ void proj_store_a(const ProjA<G>& A, int64_t l0, int64_t L, float* As,
+                                             const uint32_t (&ra)[kAPer], double (&gq)[kAPer]) {
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
-        int c, l;
-        proj_tile_pos<G>(s, tid, q, c, l);
         const float x = G == G_BF16 ? __uint_as_float(ra[q] << 16) : __uint_as_float(ra[q]);
-        As[c][l] = (s.c0 + c < s.C && l0 + l < s.L) ? x : 0.0f;
+        const float v = (A.cval[q] && l0 + A.l[q] < L) ? x : 0.0f;
+        As[A.slot[q]] = v;
+        gq[q] = __builtin_fma((double)v, (double)v, gq[q]);
     }
 }
 
-// Rows l0 + 2 w and l0 + 2 w + 1 of Pi (r floats each, lanes < r / 4 copy 16 B)
-// into rows 2 w, 2 w + 1 of the LDS buffer; completion is counted by vmcnt.
+// Rows l0 + kProjRows w + t of Pi (r floats each, lanes < r / 4 copy 16 B) into
+// the same rows of the LDS buffer; rows past L repeat row L - 1. w is uniform,
+// so the row addresses are scalar. Completion is counted by vmcnt.
 __device__ __forceinline__ void proj_copy_pi(const float* proj, int64_t L, int64_t l0, int r, int w, int lane,
                                              float (*Bs)[kBsPitch]) {
+    if (4 * lane >= r) return;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        int64_t row = l0 + 2 * w + t;
+    for (int t = 0; t < kProjRows; ++t) {
+        int64_t row = l0 + kProjRows * w + t;
         row = row < L ? row : L - 1;
-        if (4 * lane < r)
-            __builtin_amdgcn_global_load_lds(proj + row * r + 4 * lane, &Bs[2 * w + t][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(proj + row * r + 4 * lane, &Bs[kProjRows * w + t][0], 16, 0, 0);
     }
 }
 
@@ -182,28 +202,30 @@ void apollo_proj_kernel(const ApolloArgs a) {
     __shared__ __attribute__((aligned(16))) float Bs1[kLK][kBsPitch];
     const int64_t tile = blockIdx.x;
     const ApolloDesc& d = a.D[apollo_locate<&ApolloDesc::tile_begin>(a.D, a.nt, tile)];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, l4 = lane >> 4;
     const int r = a.rank;
-    ProjSrc src;
-    src.g = d.g;
-    src.cols = d.cols;
-    src.C = d.C;
-    src.L = d.L;
-    src.c0 = (tile - d.tile_begin) * kApolloTileCh;
-    src.right = d.right != 0;
+    // the descriptor's fields, read once (read through the descriptor they are
+    // fetched again every slice, and those fetches wait for the copies in flight)
+    const int64_t C = d.C, L = d.L;
+    const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
     const float* proj = d.proj;
     float* const Rp = d.R;
     float* const Rtp = d.Rt;
     double* const gn2 = d.gn2;
-    const int64_t c0 = src.c0, C = src.C, L = src.L;
+    const bool right = d.right != 0;
+    ProjA<G> A;
+    proj_a_setup<G>(A, d.g, d.cols, C, c0, right, tid);
     const bool active = kProjCW * w < r;
-    d4v acc[4][kProjJT];
+    d4v acc[kProjIT][kProjJT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kProjIT; ++i)
 #pragma unroll
         for (int j = 0; j < kProjJT; ++j) acc[i][j] = d4v{0.0, 0.0, 0.0, 0.0};
-    double gs[4] = {0.0, 0.0, 0.0, 0.0};  // wavefront 0: sum of g^2 of channel 16 i + lane % 16, inputs = lane / 16 mod 4
+    double gq[kAPer];  // this thread's sums of squares, value q of every slice
+#pragma unroll
+    for (int q = 0; q < kAPer; ++q) gq[q] = 0.0;
     uint32_t ra[kAPer];
     const int64_t ns = (L + kLK - 1) / kLK;
     // Slice n from (Ac, Bc) while slice n + 1 is brought into (An, Bn).
@@ -212,14 +234,14 @@ void apollo_proj_kernel(const ApolloArgs a) {
         const bool more = n + 1 < ns;
         if (more) {
             proj_copy_pi(proj, L, (n + 1) * kLK, r, w, lane, Bn);
-            proj_fetch_a<G>(src, (n + 1) * kLK, tid, ra);
+            proj_fetch_a<G>(A, (n + 1) * kLK, L, ra);
         }
         if (active) {
             // the operands of step kk + 4 are read before the matrix work of step kk
-            float xa[2][4], xb[2][kProjJT];
+            float xa[2][kProjIT], xb[2][kProjJT];
             auto rd = [&](int st, int kk) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) xa[st][i] = Ac[16 * i + l16][kk + l4];
+                for (int i = 0; i < kProjIT; ++i) xa[st][i] = Ac[16 * i + l16][kk + l4];
 #pragma unroll
                 for (int j = 0; j < kProjJT; ++j) xb[st][j] = Bc[kk + l4][kProjCW * w + 16 * j + l16];
             };
@@ -228,32 +250,27 @@ void apollo_proj_kernel(const ApolloArgs a) {
             for (int kk = 0; kk < kLK; kk += 4) {
                 const int st = (kk >> 2) & 1;
                 if (kk + 4 < kLK) rd(st ^ 1, kk + 4);
-                double af[4], bf[kProjJT];
+                double af[kProjIT], bf[kProjJT];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) af[i] = (double)xa[st][i];
+                for (int i = 0; i < kProjIT; ++i) af[i] = (double)xa[st][i];
 #pragma unroll
                 for (int j = 0; j < kProjJT; ++j) bf[j] = (double)xb[st][j];
-                // wavefront 0 reads every input of the slice once: the channel sums of g^2
-                if (w == 0) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) gs[i] = __builtin_fma(af[i], af[i], gs[i]);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < kProjIT; ++i)
 #pragma unroll
                     for (int j = 0; j < kProjJT; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
             }
         }
-        if (more) proj_store_a<G>(src, (n + 1) * kLK, An, tid, ra);
+        if (more) proj_store_a<G>(A, (n + 1) * kLK, L, &An[0][0], ra, gq);
         // the copies into the other buffers have landed and every read of these is done
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     };
     if (ns > 0) {
         proj_copy_pi(proj, L, 0, r, w, lane, Bs0);
-        proj_fetch_a<G>(src, 0, tid, ra);
-        proj_store_a<G>(src, 0, As0, tid, ra);
+        proj_fetch_a<G>(A, 0, L, ra);
+        proj_store_a<G>(A, 0, L, &As0[0][0], ra, gq);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
@@ -261,13 +278,34 @@ void apollo_proj_kernel(const ApolloArgs a) {
         slice(n, As0, Bs0, As1, Bs1);
         if (n + 1 < ns) slice(n + 1, As1, Bs1, As0, Bs0);
     }
+    // Channel sums of g^2 in a fixed order: the per-thread sums go to LDS (the
+    // first Pi buffer, free after the last barrier), then thread c adds the 16
+    // of channel c -- value q of threads c + 32 m (channels along the rows of g)
+    // or value c / 16 of threads 16 (c % 16) + m (channels along the columns).
+    static_assert(kApolloTileCh == 32 && kAPer == 2 && kProjThreads == 256 && kLK == 16,
+                  "the reduction below assumes 32-channel tiles, 2 values per thread");
+    double* red = reinterpret_cast<double*>(&Bs0[0][0]);
+#pragma unroll
+    for (int q = 0; q < kAPer; ++q) red[q * kProjThreads + tid] = gq[q];
+    __syncthreads();
+    if (tid < kApolloTileCh && c0 + tid < C) {
+        double x = 0.0;
+        if (right) {
+            const int q = tid / 16, t0 = 16 * (tid % 16);
+            for (int m = 0; m < 16; ++m) x += red[q * kProjThreads + t0 + m];
+        } else {
+            for (int q = 0; q < kAPer; ++q)
+                for (int m = 0; m < kProjThreads / kApolloTileCh; ++m) x += red[q * kProjThreads + tid + 32 * m];
+        }
+        to_g(gn2)[c0 + tid] = x;
+    }
     // Rt exists below rank 256 only (it is then the AdamW step's parameter, cleared here)
     const bool clear_rt = Rtp != nullptr;
     const gp<float> Rg = to_g(Rp);
     const gp<float> Rtg = to_g(Rtp);
     if (active) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kProjIT; ++i)
 #pragma unroll
             for (int j = 0; j < kProjJT; ++j)
 #pragma unroll
@@ -279,17 +317,6 @@ void apollo_proj_kernel(const ApolloArgs a) {
                         if (clear_rt) Rtg[c * r + k] = 0.0f;
                     }
                 }
-    }
-    if (w == 0) {
-        const gp<double> gn = to_g(gn2);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            double x = gs[i];
-            x += __shfl_xor(x, 16);
-            x += __shfl_xor(x, 32);
-            const int64_t c = c0 + 16 * i + lane;
-            if (lane < 16 && c < C) gn[c] = x;
-        }
     }
 }
 
