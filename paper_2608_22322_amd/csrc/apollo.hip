@@ -95,9 +95,9 @@ constexpr int kLK = 16;  // inputs per LDS slice
 // the other buffer (LDS DMA, one row of Pi per wavefront instruction; rows past
 // L repeat row L - 1, whose products meet zero inputs) and slice n + 1 of A is
 // loaded into registers, then stored to the other buffer after the matrix work.
-// A stays fp32 in LDS (row pitch 20 floats: the 64 lanes of an operand read hit
-// 64 distinct banks) and is widened to binary64 with Pi when the operands are
-// read; the four 4-input steps of a slice are unrolled, each step's operands
+// A stays fp32 in LDS (row pitch 18 floats: each half-wavefront of an operand
+// read hits 32 distinct banks; pitch 20, distinct over 64 banks, measured 1%
+// slower) and is widened to binary64 with Pi when the operands are read; the four 4-input steps of a slice are unrolled, each step's operands
 // read before the previous step's matrix work. MFMA f64 16x16x4 operand
 // layout: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]; result
 // register v of lane l is D[l / 16 + 4 v][l % 16].
@@ -108,7 +108,7 @@ constexpr int kProjCW = 256 / kProjWaves;                         // output colu
 constexpr int kProjJT = kProjCW / 16;                             // 16-column MFMA tiles per wavefront
 constexpr int kProjRows = kLK / kProjWaves;                       // rows of Pi each wavefront copies per slice
 constexpr int kAPer = kApolloTileCh * kLK / kProjThreads;         // A values per thread and slice
-constexpr int kAsPitch = 20;                                      // A row pitch in LDS (floats)
+constexpr int kAsPitch = 18;                                      // A row pitch in LDS (floats)
 constexpr int kBsPitch = 256 + 16;                                // Pi row pitch in LDS (floats)
 static_assert(kProjIT * kProjJT == 8 && kLK % kProjWaves == 0 && kAPer * kProjThreads == kApolloTileCh * kLK,
               "projection tiling");
@@ -280,10 +280,13 @@ void apollo_proj_kernel(const ApolloArgs a) {
     }
     // Channel sums of g^2 in a fixed order: the per-thread sums go to LDS (the
     // first Pi buffer, free after the last barrier), then thread c adds the 16
-    // of channel c -- value q of threads c + 32 m (channels along the rows of g)
-    // or value c / 16 of threads 16 (c % 16) + m (channels along the columns).
-    static_assert(kApolloTileCh == 32 && kAPer == 2 && kProjThreads == 256 && kLK == 16,
-                  "the reduction below assumes 32-channel tiles, 2 values per thread");
+    // of channel c -- value q of threads c + kApolloTileCh m (channels along the
+    // rows of g) or value c / G16 of threads 16 (c % G16) + m, G16 = threads / 16
+    // (channels along the columns).
+    constexpr int kG16 = kProjThreads / 16;
+    static_assert(kAPer * kProjThreads / kApolloTileCh == 16 && kProjThreads % kApolloTileCh == 0 &&
+                      kAPer * kProjThreads * 8 <= (int)sizeof(Bs0),
+                  "the reduction below takes 16 values per channel");
     double* red = reinterpret_cast<double*>(&Bs0[0][0]);
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) red[q * kProjThreads + tid] = gq[q];
@@ -291,11 +294,12 @@ void apollo_proj_kernel(const ApolloArgs a) {
     if (tid < kApolloTileCh && c0 + tid < C) {
         double x = 0.0;
         if (right) {
-            const int q = tid / 16, t0 = 16 * (tid % 16);
+            const int q = tid / kG16, t0 = 16 * (tid % kG16);
             for (int m = 0; m < 16; ++m) x += red[q * kProjThreads + t0 + m];
         } else {
             for (int q = 0; q < kAPer; ++q)
-                for (int m = 0; m < kProjThreads / kApolloTileCh; ++m) x += red[q * kProjThreads + tid + 32 * m];
+                for (int m = 0; m < kProjThreads / kApolloTileCh; ++m)
+                    x += red[q * kProjThreads + tid + kApolloTileCh * m];
         }
         to_g(gn2)[c0 + tid] = x;
     }
