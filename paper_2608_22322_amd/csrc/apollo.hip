@@ -88,7 +88,7 @@ constexpr int kLK = 16;  // inputs per LDS slice
 // binary64 accumulators) when 64 w < r. Four such workgroups share a CU (one
 // wavefront of each per SIMD), so one workgroup's barrier leaves three to feed
 // the matrix cores. (Eight wavefronts on 64 channels: 2 workgroups per CU,
-// projection 5% slower; four wavefronts of 64 x 64 outputs -- 16 accumulators,
+// projection 2% slower; four wavefronts of 64 x 64 outputs -- 16 accumulators,
 // 230 VGPRs, 2 waves per SIMD -- 14% slower.) Slices of 16 inputs are
 // double-buffered in LDS with one barrier per slice: while the matrix cores
 // work on slice n, slice n + 1 of Pi is copied straight from global memory into
