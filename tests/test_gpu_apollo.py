@@ -2,9 +2,11 @@
 (oracle/apollo.py).
 
 * ragged tensor lists on both projection sides (rows >= cols: channels are rows; rows < cols:
-  channels are columns), partial 64-channel projection tiles, partial 256x256 update units,
+  channels are columns), partial 32-channel projection tiles, partial 256x256 update units,
   projected lengths below and above the rank;
-* ranks 64 and 256, bf16 and fp32 gradients, UF8 + AL8 B2048 codes and FP32 states;
+* the projection's slice and tile edges: projected lengths of one 16-input slice, one slice and
+  one input, an odd number of slices, and channel counts one past a tile, at every rank;
+* ranks 64, 128 and 256, bf16 and fp32 gradients, UF8 + AL8 B2048 codes and FP32 states;
 * three steps with the norm-growth limiter on, an all-zero gradient channel;
 * the ApolloStep driver over a small named list (projected and full-AdamW tensors).
 
@@ -111,10 +113,20 @@ def _run(dev, shapes, rank, bf16, coded, steps=3, gamma=1.01, zero_channel=None)
 RAGGED = [(70, 33), (40, 300), (300, 40), (256, 256), (5, 700), (129, 64)]
 
 
-@pytest.mark.parametrize("rank", [64, 256])
+@pytest.mark.parametrize("rank", [64, 128, 256])
 @pytest.mark.parametrize("bf16", [True, False])
 def test_apollo_coded_ragged(dev, rank, bf16):
     _run(dev, RAGGED, rank, bf16, coded=True)
+
+
+# (rows, cols) -> (channels, projected length): (33, 16) 33 x 16, (32, 17) 32 x 17, (64, 32) 64 x 32,
+# (65, 48) 65 x 48, (16, 100) 100 x 16, (17, 96) 96 x 17, (31, 48) 48 x 31
+EDGES = [(33, 16), (32, 17), (64, 32), (65, 48), (16, 100), (17, 96), (31, 48)]
+
+
+@pytest.mark.parametrize("rank", [64, 128, 256])
+def test_apollo_projection_slice_and_tile_edges(dev, rank):
+    _run(dev, EDGES, rank, True, coded=True, steps=2)
 
 
 def test_apollo_fp32_states(dev):
