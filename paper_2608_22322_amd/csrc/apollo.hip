@@ -4,10 +4,11 @@
 //
 // Kernel sequence of one step (the fused AdamW step over the projected
 // moments runs between proj and scale, launched by the C ABI):
-//   proj    R = fl32(A Pi) for a tile of 64 channels and all r columns, in
+//   proj    R = fl32(A Pi) for a tile of 32 channels and all r columns, in
 //           binary64 on the matrix cores (v_mfma_f64_16x16x4f64): A (bf16 or
 //           fp32 gradient, as C x L) and Pi (fp32) are staged through LDS in
-//           slices of 16 inputs and widened to binary64; the products are
+//           slices of 16 inputs (Pi by LDS DMA) and widened to binary64 as the
+//           operands are read; the products are
 //           exact and the accumulation is binary64, so fl32 of the result is
 //           the exactly rounded value except within ~L ulps of binary64 of an
 //           fp32 midpoint. Also sums g^2 per channel and clears Rt (below
