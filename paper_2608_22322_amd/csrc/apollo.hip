@@ -327,6 +327,8 @@ void apollo_proj_kernel(const ApolloArgs a) {
 
 hipError_t launch_apollo_proj(const ApolloArgs& a, int grad_dtype, hipStream_t s) {
     if (a.total_tiles == 0) return hipSuccess;
+    // an active wavefront stores all kProjCW of its columns, and Pi rows are copied 16 B per lane
+    if (a.rank <= 0 || a.rank > 256 || a.rank % kProjCW != 0) return hipErrorInvalidValue;
     if (grad_dtype == G_BF16)
         hipLaunchKernelGGL(apollo_proj_kernel<G_BF16>, dim3((unsigned)a.total_tiles), dim3(kProjThreads), 0, s, a);
     else
