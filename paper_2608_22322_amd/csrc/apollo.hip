@@ -261,6 +261,13 @@ void apollo_proj_kernel(const ApolloArgs a) {
 #pragma unroll
                     for (int j = 0; j < kProjJT; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(af[i], bf[j], acc[i][j], 0, 0, 0);
+                // issue order: one matrix instruction, then one read of the next step's operands
+#pragma unroll
+                for (int x = 0; x < kProjIT + kProjJT; ++x) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, kProjIT * kProjJT - kProjIT - kProjJT, 0);
             }
         }
         if (more) proj_store_a<G>(A, (n + 1) * kLK, L, &An[0][0], ra, gq);
