@@ -98,8 +98,10 @@ constexpr int kLK = 16;  // inputs per LDS slice
 // loaded into registers, then stored to the other buffer after the matrix work.
 // A stays fp32 in LDS (row pitch 18 floats: each half-wavefront of an operand
 // read hits 32 distinct banks; pitch 20, distinct over 64 banks, measured 1%
-// slower) and is widened to binary64 with Pi when the operands are read; the four 4-input steps of a slice are unrolled, each step's operands
-// read before the previous step's matrix work. MFMA f64 16x16x4 operand
+// slower) and is widened to binary64 with Pi when the operands are read; the
+// four 4-input steps of a slice are unrolled, each step's operands read during
+// the previous step's matrix work, one read per matrix instruction (scheduling
+// groups: 0.7% faster than the compiler's own order). MFMA f64 16x16x4 operand
 // layout: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16]; result
 // register v of lane l is D[l / 16 + 4 v][l % 16].
 constexpr int kProjWaves = 4;                                     // wavefronts per workgroup
