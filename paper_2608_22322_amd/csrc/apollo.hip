@@ -151,15 +151,15 @@ __device__ __forceinline__ void proj_a_setup(ProjA<G>& A, const void* g, int64_t
 // Slice l0 of A as raw bits into registers (the wait for them falls after the
 // matrix work, where proj_store_a consumes them).
 template <int G>
-__device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int64_t l0, int64_t L, uint32_t (&ra)[kAPer]) {
+__device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int l0, int L, uint32_t (&ra)[kAPer]) {
     if (l0 + kLK <= L) {
 #pragma unroll
-        for (int q = 0; q < kAPer; ++q) ra[q] = A.base[q][l0 * A.stride];
+        for (int q = 0; q < kAPer; ++q) ra[q] = A.base[q][(int64_t)l0 * A.stride];
     } else {
 #pragma unroll
         for (int q = 0; q < kAPer; ++q) {
-            const int64_t ll = l0 + A.l[q] < L ? l0 : L - 1 - A.l[q];
-            ra[q] = A.base[q][ll * A.stride];
+            const int ll = l0 + A.l[q] < L ? l0 : L - 1 - A.l[q];
+            ra[q] = A.base[q][(int64_t)ll * A.stride];
         }
     }
 }
@@ -167,7 +167,7 @@ __device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int64_t l0, int6
 // The slice into LDS as fp32, inputs outside the tensor as zero; each thread
 // also accumulates the squares of the values it stores (binary64, exact products).
 template <int G>
-__device__ __forceinline__ void proj_store_a(const ProjA<G>& A, int64_t l0, int64_t L, float* As,
+__device__ __forceinline__ void proj_store_a(const ProjA<G>& A, int l0, int L, float* As,
                                              const uint32_t (&ra)[kAPer], double (&gq)[kAPer]) {
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
@@ -180,15 +180,16 @@ __device__ __forceinline__ void proj_store_a(const ProjA<G>& A, int64_t l0, int6
 
 // Rows l0 + kProjRows w + t of Pi (r floats each, lanes < r / 4 copy 16 B) into
 // the same rows of the LDS buffer; rows past L repeat row L - 1. w is uniform,
-// so the row addresses are scalar. Completion is counted by vmcnt.
-__device__ __forceinline__ void proj_copy_pi(const float* proj, int64_t L, int64_t l0, int r, int w, int lane,
+// so the row addresses are scalar (32-bit row arithmetic: a 64-bit compare has no
+// scalar form). Completion is counted by vmcnt.
+__device__ __forceinline__ void proj_copy_pi(const float* proj, int L, int l0, int r, int w, int lane,
                                              float (*Bs)[kBsPitch]) {
     if (4 * lane >= r) return;
 #pragma unroll
     for (int t = 0; t < kProjRows; ++t) {
-        int64_t row = l0 + kProjRows * w + t;
+        int row = l0 + kProjRows * w + t;
         row = row < L ? row : L - 1;
-        __builtin_amdgcn_global_load_lds(proj + row * r + 4 * lane, &Bs[kProjRows * w + t][0], 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(proj + (int64_t)row * r + 4 * lane, &Bs[kProjRows * w + t][0], 16, 0, 0);
     }
 }
 
@@ -211,7 +212,10 @@ void apollo_proj_kernel(const ApolloArgs a) {
     const int r = a.rank;
     // the descriptor's fields, read once (read through the descriptor they are
     // fetched again every slice, and those fetches wait for the copies in flight)
-    const int64_t C = d.C, L = d.L;
+    const int64_t C = d.C;
+    // the projected length is at most 2^20 (rows * cols <= 2^40): slice arithmetic in
+    // 32 bits and uniform, so its compares are scalar
+    const int L = __builtin_amdgcn_readfirstlane((int)d.L);
     const int64_t c0 = (tile - d.tile_begin) * kApolloTileCh;
     const float* proj = d.proj;
     float* const Rp = d.R;
@@ -230,9 +234,9 @@ void apollo_proj_kernel(const ApolloArgs a) {
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) gq[q] = 0.0;
     uint32_t ra[kAPer];
-    const int64_t ns = (L + kLK - 1) / kLK;
+    const int ns = (L + kLK - 1) / kLK;
     // Slice n from (Ac, Bc) while slice n + 1 is brought into (An, Bn).
-    auto slice = [&](int64_t n, float (*Ac)[kAsPitch], float (*Bc)[kBsPitch], float (*An)[kAsPitch],
+    auto slice = [&](int n, float (*Ac)[kAsPitch], float (*Bc)[kBsPitch], float (*An)[kAsPitch],
                      float (*Bn)[kBsPitch]) {
         const bool more = n + 1 < ns;
         if (more) {
@@ -284,7 +288,7 @@ void apollo_proj_kernel(const ApolloArgs a) {
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
-    for (int64_t n = 0; n < ns; n += 2) {
+    for (int n = 0; n < ns; n += 2) {
         slice(n, As0, Bs0, As1, Bs1);
         if (n + 1 < ns) slice(n + 1, As1, Bs1, As0, Bs0);
     }
