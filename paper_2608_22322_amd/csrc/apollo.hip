@@ -116,32 +116,52 @@ constexpr int kBsPitch = 256 + 16;                                // Pi row pitc
 static_assert(kProjIT * kProjJT == 8 && kLK % kProjWaves == 0 && kAPer * kProjThreads == kApolloTileCh * kLK,
               "projection tiling");
 
+// A pointer known to be the same on every lane, made scalar, so that a load
+// from it plus a 32-bit lane offset needs no vector address arithmetic.
+template <class P>
+__device__ __forceinline__ P uniform_ptr(P p) {
+    const uint64_t v = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (P)(((uint64_t)hi << 32) | lo);
+}
+
 // One thread's share of the A slices of a tile, fixed for the whole tile:
 // value q of every slice is input (c_q, l0 + l_q), stored at As[c_q][l_q].
-// Slices that lie wholly inside the tensor load from base_q + l0 * stride with
-// no clamping; only a ragged last slice clamps l to L - 1 (and zeroes it).
+// Every slice loads from a uniform slice base plus a fixed 32-bit byte offset
+// per value (no vector address work): one offset for slices wholly inside the
+// tensor, one for a ragged last slice, which clamps l to L - 1 (and zeroes it).
 template <int G>
 struct ProjA {
     using T = typename std::conditional<G == G_BF16, uint16_t, uint32_t>::type;
-    gp<const T> base[kAPer];  // element (c_q clamped to C - 1, l_q) of slice 0
-    int l[kAPer];             // l_q
-    int slot[kAPer];          // c_q * kAsPitch + l_q
-    bool cval[kAPer];         // c_q inside the tensor
-    int64_t stride;           // distance between consecutive inputs of a channel
+    gp<const T> tile;       // element (c0, 0): the tile's first channel, first input
+    int64_t stride;         // distance between consecutive inputs of a channel
+    uint32_t off[kAPer];    // bytes from the slice base to (c_q clamped to C - 1, l_q)
+    uint32_t offt[kAPer];   // the same in the last slice, l_q clamped to L - 1
+    int l[kAPer];           // l_q
+    int slot[kAPer];        // c_q * kAsPitch + l_q
+    bool cval[kAPer];       // c_q inside the tensor
+    bool cfull;             // every channel of the tile inside the tensor (uniform)
 };
 
 template <int G>
 __device__ __forceinline__ void proj_a_setup(ProjA<G>& A, const void* g, int64_t cols, int64_t C, int64_t c0,
-                                             bool right, int tid) {
-    const gp<const typename ProjA<G>::T> gt = to_g(reinterpret_cast<const typename ProjA<G>::T*>(g));
+                                             int L, bool right, int tid) {
+    using T = typename ProjA<G>::T;
     A.stride = right ? 1 : cols;
+    A.tile = to_g(reinterpret_cast<const T*>(g)) + (right ? c0 * cols : c0);
+    A.cfull = c0 + kApolloTileCh <= C;
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
         const int e = tid + kProjThreads * q;
         const int c = right ? e / kLK : e % kApolloTileCh;
         const int l = right ? e % kLK : e / kApolloTileCh;
-        const int64_t cc = c0 + c < C ? c0 + c : C - 1;
-        A.base[q] = gt + (right ? cc * cols : cc) + l * A.stride;
+        const int64_t cc = c0 + c < C ? c : C - 1 - c0;
+        const int64_t coff = right ? cc * cols : cc;
+        const int llast = ((L - 1) / kLK) * kLK;  // first input of the last slice
+        const int lt = llast + l < L ? l : L - 1 - llast;
+        A.off[q] = (uint32_t)((coff + l * A.stride) * (int64_t)sizeof(T));
+        A.offt[q] = (uint32_t)((coff + lt * A.stride) * (int64_t)sizeof(T));
         A.l[q] = l;
         A.slot[q] = c * kAsPitch + l;
         A.cval[q] = c0 + c < C;
@@ -152,16 +172,11 @@ __device__ __forceinline__ void proj_a_setup(ProjA<G>& A, const void* g, int64_t
 // matrix work, where proj_store_a consumes them).
 template <int G>
 __device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int l0, int L, uint32_t (&ra)[kAPer]) {
-    if (l0 + kLK <= L) {
+    using T = typename ProjA<G>::T;
+    const bool inside = l0 + kLK <= L;  // otherwise the last slice
+    const gp<const char> sb = uniform_ptr(g_as<const char>(A.tile + (int64_t)l0 * A.stride));
 #pragma unroll
-        for (int q = 0; q < kAPer; ++q) ra[q] = A.base[q][(int64_t)l0 * A.stride];
-    } else {
-#pragma unroll
-        for (int q = 0; q < kAPer; ++q) {
-            const int ll = l0 + A.l[q] < L ? l0 : L - 1 - A.l[q];
-            ra[q] = A.base[q][(int64_t)ll * A.stride];
-        }
-    }
+    for (int q = 0; q < kAPer; ++q) ra[q] = *g_as<const T>(sb + (inside ? A.off[q] : A.offt[q]));
 }
 
 // The slice into LDS as fp32, inputs outside the tensor as zero; each thread
@@ -169,10 +184,11 @@ __device__ __forceinline__ void proj_fetch_a(const ProjA<G>& A, int l0, int L, u
 template <int G>
 __device__ __forceinline__ void proj_store_a(const ProjA<G>& A, int l0, int L, float* As,
                                              const uint32_t (&ra)[kAPer], double (&gq)[kAPer]) {
+    const bool full = A.cfull && l0 + kLK <= L;
 #pragma unroll
     for (int q = 0; q < kAPer; ++q) {
         const float x = G == G_BF16 ? __uint_as_float(ra[q] << 16) : __uint_as_float(ra[q]);
-        const float v = (A.cval[q] && l0 + A.l[q] < L) ? x : 0.0f;
+        const float v = (full || (A.cval[q] && l0 + A.l[q] < L)) ? x : 0.0f;
         As[A.slot[q]] = v;
         gq[q] = __builtin_fma((double)v, (double)v, gq[q]);
     }
@@ -189,7 +205,8 @@ __device__ __forceinline__ void proj_copy_pi(const float* proj, int L, int l0, i
     for (int t = 0; t < kProjRows; ++t) {
         int row = l0 + kProjRows * w + t;
         row = row < L ? row : L - 1;
-        __builtin_amdgcn_global_load_lds(proj + (int64_t)row * r + 4 * lane, &Bs[kProjRows * w + t][0], 16, 0, 0);
+        const float* rp = uniform_ptr(proj + (int64_t)row * r);
+        __builtin_amdgcn_global_load_lds(rp + 4 * lane, &Bs[kProjRows * w + t][0], 16, 0, 0);
     }
 }
 
@@ -223,7 +240,7 @@ void apollo_proj_kernel(const ApolloArgs a) {
     double* const gn2 = d.gn2;
     const bool right = d.right != 0;
     ProjA<G> A;
-    proj_a_setup<G>(A, d.g, d.cols, C, c0, right, tid);
+    proj_a_setup<G>(A, d.g, d.cols, C, c0, L, right, tid);
     const bool active = kProjCW * w < r;
     d4v acc[kProjIT][kProjJT];
 #pragma unroll
