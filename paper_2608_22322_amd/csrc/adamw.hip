@@ -55,6 +55,8 @@ __device__ __forceinline__ double split2_entry(double l32, double st, int j) {
     const double arg = j < 16 ? l32 + (double)(16 * j - 1) * st : (double)(j - 16) * st;
     return exp2_d(arg, kExp2);
 }
+// An empty register constraint: the compiler cannot move work across it.
+__device__ __forceinline__ void opaque_f(float& x) { asm volatile("" : "+v"(x)); }
 __device__ __forceinline__ double split2_product(double f1, double f2) { return f1 * f2; }
 __device__ __forceinline__ double split2_level(const double* t, uint32_t q) {
     return split2_product(t[q >> 4], t[16 + (q & 15u)]);
@@ -440,16 +442,20 @@ __device__ __forceinline__ void adamw_compute(const AdamWLaunch& a, const DescG&
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const float lv = (float)split2_level(t, q);
-                vh[j] = q == 0u ? 0.0f : lv;
+                float lv = (float)split2_level(t, q);
+                lv = q == 0u ? 0.0f : lv;
+                opaque_f(lv);  // the code-0 select stays on the fp32 value (one select, not two after widening)
+                vh[j] = lv;
             }
         } else if constexpr (Q::SPLIT3) {
             const double* t = stab + ((k * kSub + 4 * lane) / BV) * 20;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t q = (r.v[kk] >> (8 * j)) & 0xFFu;
-                const float lv = (float)split3_level(t, q);
-                vh[j] = q == 0u ? 0.0f : lv;
+                float lv = (float)split3_level(t, q);
+                lv = q == 0u ? 0.0f : lv;
+                opaque_f(lv);  // the code-0 select stays on the fp32 value (one select, not two after widening)
+                vh[j] = lv;
             }
         } else if constexpr (VQ) {
             double vstep, vl32;
