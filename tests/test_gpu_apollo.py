@@ -125,8 +125,9 @@ EDGES = [(33, 16), (32, 17), (64, 32), (65, 48), (16, 100), (17, 96), (31, 48)]
 
 
 @pytest.mark.parametrize("rank", [64, 128, 256])
-def test_apollo_projection_slice_and_tile_edges(dev, rank):
-    _run(dev, EDGES, rank, True, coded=True, steps=2)
+@pytest.mark.parametrize("bf16", [True, False])
+def test_apollo_projection_slice_and_tile_edges(dev, rank, bf16):
+    _run(dev, EDGES, rank, bf16, coded=True, steps=2)
 
 
 def test_apollo_fp32_states(dev):
